@@ -1,0 +1,242 @@
+/*
+ * eao.h -- CPU oracle for the KV-offload data path (TEST INFRASTRUCTURE ONLY).
+ *
+ * This library is the plain, slow, single-threaded definition of what the
+ * offload path computes, written from "EfficientAgent: What Makes KV Cache
+ * Offloading Work for Concurrent Agents?" (arXiv 2609.33762).  It exists so the
+ * tests can check the GPU library bit for bit.  Only the test suite, the smoke
+ * check and the CPU-baseline leg of the benchmark may load it; the product
+ * path never does.  It shares no code, header, table or constant with the GPU
+ * library: the SHA-256 round constants and initial hash value are derived here
+ * from their definition (FIPS 180-4, 4.2.2 and 5.3.3) at run time.
+ *
+ * Everything is host memory.  The "GPU cache" is a host byte array with the
+ * same logical layout the GPU library uses:
+ *
+ *   cache  : [L][P][2][T][H][D] elements of elem_bytes  (one (layer, page)
+ *            "piece" of 2*T*H*D*elem_bytes bytes is contiguous)
+ *   scales : optional [L][P][2] float32 (K scale, V scale), copied as bytes
+ *   tier   : [S][slot_bytes]; a slot holds one page of every layer,
+ *            [L][2][T][H][D] bytes, followed (when scales exist) by an
+ *            [L][2] float32 trailer padded to a multiple of 256 bytes.
+ *
+ * Status codes mirror the product library: 0 ok, negative on error, and on
+ * error nothing is written.
+ */
+#ifndef EAO_H
+#define EAO_H
+
+#include <stdint.h>
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  EAO_OK = 0,
+  EAO_EINVAL = -1,
+  EAO_ENOMEM = -2,
+  EAO_ENOSPC = -3,
+  EAO_ENOTSUP = -5
+};
+
+/* ---------------------------------------------------------------- SHA-256 */
+
+/* SHA-256 of an arbitrary byte string, FIPS 180-4 sections 5.1.1 (padding),
+ * 5.2.1 (parsing), 6.2.2 (hash computation). */
+void eao_sha256(const uint8_t *msg, uint64_t len, uint8_t digest[32]);
+
+/* The 64 round constants K and the initial hash value H(0), computed from
+ * their definition: first 32 bits of the fractional parts of the cube roots
+ * of the first 64 primes (4.2.2) and of the square roots of the first 8
+ * primes (5.3.3). */
+void eao_sha256_constants(uint32_t k[64], uint32_t h0[8]);
+
+/* ------------------------------------------------------ footprint (Eq. 1) */
+
+/* KV bytes per token on one tensor-parallel rank,
+ * beta_rank = 2 * L * d * s * max(1, ceil(H_kv / TP))  (section 2, Eq. 1). */
+int64_t eao_beta_rank(int64_t layers, int64_t head_dim, int64_t elem_bytes,
+                      int64_t kv_heads, int64_t tp);
+
+/* Reuse working-set scale C_reuse = (A - 1) * Nbar * beta_rank in bytes
+ * (section 3.2, Eq. 5). */
+double eao_working_set_bytes(double active_pool, double mean_prompt_tokens,
+                             double beta_rank);
+
+/* Host tier capacity in chunks, K_H = floor(C_H / (b * beta_rank))
+ * (section 4, "Which writes a tier can decline"; survival bound of Eq. 4). */
+int64_t eao_tier_chunks(int64_t capacity_bytes, int64_t block_tokens,
+                        int64_t beta_rank);
+
+/* ------------------------------------------------------------------ layout */
+
+typedef struct {
+  int32_t num_pages;    /* P: pages in the GPU cache                        */
+  int32_t num_layers;   /* L                                                 */
+  int32_t page_tokens;  /* T: tokens per page (= hash block size b)          */
+  int32_t num_kv_heads; /* H: KV heads held by this rank                     */
+  int32_t head_dim;     /* D                                                 */
+  int32_t elem_bytes;   /* s: bytes per element (2 for bf16, 1 for fp8)      */
+  int32_t has_scales;   /* 1 when a [L][P][2] float32 scale plane exists     */
+} eao_shape;
+
+int64_t eao_piece_bytes(const eao_shape *sh);  /* 2*T*H*D*s                 */
+int64_t eao_page_bytes(const eao_shape *sh);   /* L * piece                 */
+int64_t eao_trailer_bytes(const eao_shape *sh);/* L*2*4 rounded up to 256, or 0 */
+int64_t eao_slot_bytes(const eao_shape *sh);   /* page + trailer            */
+int64_t eao_cache_bytes(const eao_shape *sh);  /* L * P * piece             */
+int64_t eao_scale_bytes(const eao_shape *sh);  /* L * P * 8, or 0           */
+
+/* ------------------------------------------------------- chained hashing */
+
+/* Chained prefix-block keys (section 2 "Exact-prefix reuse"; section 3.2:
+ * each full chunk's key depends on its entire prefix).
+ *
+ * Sequence s is tokens[seq_offsets[s] .. seq_offsets[s+1]).  With
+ * b = block_tokens and key_{-1} = parents[s] (32 zero bytes when parents is
+ * NULL), for every FULL block i:
+ *     key_i = SHA-256( LE32(tok[i*b]) || ... || LE32(tok[i*b+b-1]) || key_{i-1} )
+ * A trailing partial block gets no key.  Keys of sequence s are written to
+ * keys_out[key_offsets_out[s] ..], key_offsets_out has n_seqs+1 entries and
+ * key_offsets_out[0] = 0.  A token is hashed as the little-endian bytes of
+ * its 32-bit two's-complement value; b >= 1. */
+int eao_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
+                    int32_t n_seqs, int32_t block_tokens,
+                    const uint8_t *parents, uint8_t *keys_out,
+                    int64_t *key_offsets_out);
+
+/* ------------------------------------------------------------------ copies */
+
+/* Store (host write, "KV copied from GPU to host", section 2): for every i
+ * with mask[i] != 0 (mask NULL = all), slot host_slots[i] receives page
+ * block_ids[i] of every layer (K and V) and, with scales, the page's
+ * [L][2] scales as the slot trailer.  Nothing else changes.  Admitted slots
+ * must be distinct; ids and slots must be in range. */
+int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
+                     const uint8_t *scales, uint8_t *tier, int64_t num_slots,
+                     const int32_t *block_ids, const int64_t *host_slots,
+                     const uint8_t *mask, int32_t n);
+
+/* Load (host restore, section 3.1): page dst_pages[i] of every layer
+ * receives slot host_slots[i] (and its scale trailer).  Destination pages
+ * must be distinct. */
+int eao_load_blocks(const eao_shape *sh, const uint8_t *tier,
+                    int64_t num_slots, uint8_t *cache, uint8_t *scales,
+                    const int64_t *host_slots, const int32_t *dst_pages,
+                    int32_t n);
+
+/* The part of the load that touches one layer: after it has run for every
+ * layer the state equals eao_load_blocks'. */
+int eao_load_layer(const eao_shape *sh, const uint8_t *tier,
+                   int64_t num_slots, uint8_t *cache, uint8_t *scales,
+                   const int64_t *host_slots, const int32_t *dst_pages,
+                   int32_t n, int32_t layer);
+
+/* ---------------------------------------------------- host tier metadata */
+
+/* Slot states. */
+enum { EAO_SLOT_FREE = 0, EAO_SLOT_PENDING = 1, EAO_SLOT_RESIDENT = 2 };
+
+/* Admission modes: the conditioned rule of Eq. 6 and its two endpoints
+ * (section 4: offload without admission is p = 0, fixed admission p = 1). */
+enum { EAO_ADMIT_CONDITIONED = 0, EAO_ADMIT_ALWAYS = 1, EAO_ADMIT_FIXED = 2 };
+
+typedef struct {
+  int64_t theta_ppm;        /* occupancy threshold in parts per million
+                               (950000 = 0.95); full when
+                               registered * 1e6 >= theta_ppm * K_H            */
+  int64_t kappa;            /* write threshold in full blocks                 */
+  int64_t block_tokens;     /* b                                              */
+  int64_t beta_rank;        /* bytes per token per rank for C_reuse           */
+  int64_t activity_window;  /* window for A_t and e_t, in caller clock units:
+                               an event at time t counts when t > now - W     */
+  int32_t length_window;    /* N_t = mean of the last this-many first lookups */
+  int32_t mode;             /* EAO_ADMIT_*                                    */
+  int32_t telemetry;        /* 1: the tier's state is a fresh report;
+                               0: no report, the estimate alone decides       */
+  int32_t _pad;
+} eao_policy;
+
+typedef struct {
+  int64_t n_tokens;  /* n: prompt tokens                                      */
+  int64_t h_tokens;  /* h: prompt tokens the host tier already holds          */
+  int64_t task_id;   /* agent/task identity for A_t                           */
+  int64_t now;       /* caller clock (e.g. microseconds or turns), never
+                        smaller than the previous request's                   */
+  int32_t decided;   /* -1: first lookup, decide now; 0/1: keep earlier save  */
+  int32_t _pad;
+} eao_request;
+
+typedef struct {
+  int64_t capacity_slots;   /* K_H                                            */
+  int64_t registered;       /* pending + resident slots                       */
+  int64_t resident;
+  int64_t pinned;           /* slots with a pin count > 0                     */
+  int64_t evictions_total;  /* evictions made to allocate                     */
+  int64_t evictions_window; /* of those, within the activity window at clock  */
+  int64_t clock;            /* last request clock                             */
+  int64_t active_tasks;     /* A_t at the last decision                       */
+  double  mean_prompt;      /* N_t at the last decision (display only)        */
+  double  working_set;      /* C_reuse at the last decision (display only)    */
+  int32_t last_pressure;    /* p_t at the last decision                       */
+  int32_t last_save;
+} eao_tier_stats;
+
+typedef struct eao_tier eao_tier;
+
+/* K_H = floor(capacity_bytes / slot_bytes); fails with EAO_EINVAL if K_H < 1.
+ * capacity_bytes is also the C_H that the admission rule compares the
+ * working-set estimate with. */
+int eao_tier_create(const eao_shape *sh, int64_t capacity_bytes,
+                    eao_tier **out);
+int eao_tier_destroy(eao_tier *t);
+int64_t eao_tier_capacity(const eao_tier *t);
+
+/* Consecutive-prefix lookup (section 3.2; App. "Prefix coverage"): the hit
+ * count is the largest k with key_0..key_{k-1} all resident; a lookup stops
+ * at the first absent key, and a key whose slot is still PENDING (allocated,
+ * store not yet issued) counts as absent.  Hits are moved to the most-recent end in
+ * increasing position order and pinned (one pin each).  slots_out[i] for
+ * i < hit count gets the slot. */
+int eao_tier_lookup(eao_tier *t, const uint8_t *keys, int64_t n,
+                    int64_t *hit_blocks, int64_t *slots_out);
+
+/* Write admission (section 4, Eq. 6; App. "Runtime Admission Details",
+ * Eq. 10) plus copy-time deduplication: save_out gets save(r), and
+ * mask_out[i] = save && key_i is not registered in the tier. */
+int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
+                       const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                       int32_t *save_out);
+
+/* Allocate a slot for every i with mask[i] != 0 whose key is not already
+ * registered: the lowest-numbered free slot, else the least-recent resident
+ * unpinned slot (an eviction).  New slots are PENDING, registered under the
+ * key, placed at the most-recent end in increasing position order, and
+ * pinned.  slots_out[i] = -1 where nothing was allocated; once no victim is
+ * left, every later admitted block gets -1.  *allocated gets the count. */
+int eao_tier_alloc(eao_tier *t, const uint8_t *keys, const uint8_t *mask,
+                   int64_t n, int64_t *slots_out, int64_t *allocated);
+
+/* Metadata effect of a store issued to these slots: PENDING slots become
+ * RESIDENT (entries with mask 0 are skipped; mask NULL = all). */
+int eao_tier_mark_stored(eao_tier *t, const int64_t *slots,
+                         const uint8_t *mask, int64_t n);
+
+/* Drop one pin from each slot; a PENDING slot whose last pin goes away is
+ * abandoned: its key is unregistered and the slot becomes free. */
+int eao_tier_unpin(eao_tier *t, const int64_t *slots, int64_t n);
+
+int eao_tier_stats_get(const eao_tier *t, eao_tier_stats *s);
+
+/* Full metadata image for bit-exact comparison: for every slot its state,
+ * pin count and key (zeros when free), and the resident/pending slots from
+ * least-recent to most-recent in lru_out (*n_lru entries). */
+int eao_tier_export(const eao_tier *t, uint8_t *state_out, int32_t *pins_out,
+                    uint8_t *keys_out, int64_t *lru_out, int64_t *n_lru);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EAO_H */
