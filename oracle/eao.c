@@ -253,9 +253,12 @@ int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
       memcpy(slot + l * piece, cache + ((int64_t)l * P + block_ids[i]) * piece,
              (size_t)piece);
     if (sh->has_scales) {
+      /* trailer: 8 bytes of scales per layer, then zero padding */
       uint8_t *trailer = slot + eao_page_bytes(sh);
       for (int32_t l = 0; l < sh->num_layers; ++l)
         memcpy(trailer + 8 * l, scales + ((int64_t)l * P + block_ids[i]) * 8, 8);
+      memset(trailer + 8 * (int64_t)sh->num_layers, 0,
+             (size_t)(eao_trailer_bytes(sh) - 8 * (int64_t)sh->num_layers));
     }
   }
   return EAO_OK;

@@ -18,7 +18,9 @@
  *   scales : optional [L][P][2] float32 (K scale, V scale), copied as bytes
  *   tier   : [S][slot_bytes]; a slot holds one page of every layer,
  *            [L][2][T][H][D] bytes, followed (when scales exist) by an
- *            [L][2] float32 trailer padded to a multiple of 256 bytes.
+ *            [L][2] float32 trailer padded with zeros to a multiple of 256
+ *            bytes (a store writes the padding too, so a stored slot is a
+ *            complete image).
  *
  * Status codes mirror the product library: 0 ok, negative on error, and on
  * error nothing is written.
@@ -112,7 +114,8 @@ int eao_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
 /* Store (host write, "KV copied from GPU to host", section 2): for every i
  * with mask[i] != 0 (mask NULL = all), slot host_slots[i] receives page
  * block_ids[i] of every layer (K and V) and, with scales, the page's
- * [L][2] scales as the slot trailer.  Nothing else changes.  Admitted slots
+ * [L][2] scales plus zero padding as the slot trailer.  Nothing else
+ * changes.  Admitted slots
  * must be distinct; ids and slots must be in range. */
 int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
                      const uint8_t *scales, uint8_t *tier, int64_t num_slots,

@@ -25,6 +25,7 @@ def _np_store(sh, sz, cache, sc, tier, ids, slots):
         out[s, :sz["page"]] = c[:, p, :].reshape(-1)
         if sc is not None:
             out[s, sz["page"]:sz["page"] + 8 * L] = sc.reshape(L, P, 8)[:, p, :].reshape(-1)
+            out[s, sz["page"] + 8 * L:] = 0
     return out
 
 
@@ -104,11 +105,14 @@ def test_fp8_nan_patterns_survive():
     assert np.array_equal(out_sc.reshape(2, 4, 8)[:, [1, 3]], sc.reshape(2, 4, 8)[:, [1, 3]])
 
 
-def test_trailer_padding_is_not_written():
+def test_trailer_padding_is_zeroed_in_stored_slots_only():
     sh, sz, rng, cache, sc, tier = _setup(5, scales=True)
-    pad_before = tier[:, sz["page"] + 8 * sh.num_layers:].copy()
+    pad = slice(sz["page"] + 8 * sh.num_layers, sz["slot"])
+    assert sz["slot"] - pad.start > 0
+    before = tier.copy()
     oracle.store_blocks(sh, cache, sc, tier, np.array([0, 1], np.int32), np.array([0, 1]))
-    assert np.array_equal(tier[:, sz["page"] + 8 * sh.num_layers:], pad_before)
+    assert not tier[:2, pad].any()
+    assert np.array_equal(tier[2:], before[2:])
 
 
 @pytest.mark.parametrize("bad", ["id_high", "id_neg", "slot_high", "dup_slot"])
