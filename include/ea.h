@@ -1,0 +1,321 @@
+/*
+ * ea.h -- C ABI of the MI355X KV-offload library (libea.so).
+ *
+ * The library moves KV cache state between a paged GPU cache in HBM and a
+ * pinned host-memory tier, as described in "EfficientAgent: What Makes KV
+ * Cache Offloading Work for Concurrent Agents?" (arXiv 2609.33762): host
+ * writes and restores are KV copied from GPU to host and back (section 2, "A
+ * closed-loop workload"); reusable prefixes are found through chained
+ * content keys of full blocks (section 2 "Exact-prefix reuse", section 3.2);
+ * and a write-admission rule decides, once per request, whether its new KV
+ * enters the tier (section 4, Eq. 6; App. "Runtime Admission Details",
+ * Eq. 10), with copy-time deduplication.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Return value: EA_OK (0) or a negative EA_E* code.  ea_strerror() gives
+ *    text; ea_last_hip_error() gives the HIP error behind EA_EHIP on this
+ *    thread.
+ *  - Arguments are validated before anything is enqueued: on any error no
+ *    byte moves and no tier metadata changes.
+ *  - Index arrays (block ids, slots, masks, keys) are HOST pointers and are
+ *    read before the call returns; the caller may reuse them at once.
+ *  - Copies are asynchronous on the caller's HIP stream and ordered with the
+ *    caller's other work on that stream.  A store or load that touches a host
+ *    slot that an earlier call on another stream still transfers waits for
+ *    that transfer on the device (no host blocking).
+ *  - GPU cache layout (caller-owned device memory): element array
+ *    [L][P][2][T][H][D] of elem_bytes each, so the K and V data of one
+ *    (layer, page) form one contiguous "piece" of 2*T*H*D*elem_bytes bytes.
+ *    The optional scale plane is a caller-owned float32 array [L][P][2]
+ *    (K scale, V scale of each layer and page), moved as opaque bytes.
+ *  - Host slot layout (library-owned pinned memory): slot s holds one page of
+ *    every layer, [L][2][T][H][D], followed when scales exist by an [L][2]
+ *    float32 trailer padded to a multiple of 256 bytes.  The tier holds
+ *    K_H = floor(capacity_bytes / slot_bytes) slots.
+ *  - A tier is internally locked; one tier may be used from several threads.
+ *    Calls are bound to the device that was current when the cache or tier
+ *    was created.
+ */
+#ifndef EA_H
+#define EA_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  EA_OK = 0,
+  EA_EINVAL = -1,  /* bad argument: null pointer, out-of-range id or slot,
+                      duplicate destination, unsupported shape               */
+  EA_ENOMEM = -2,  /* host or device allocation failed                      */
+  EA_ENOSPC = -3,  /* reserved: no tier call fails for lack of space; a full
+                      tier reports unallocated blocks instead                */
+  EA_EHIP = -4,    /* a HIP call failed; see ea_last_hip_error()            */
+  EA_ENOTSUP = -5  /* valid request this build does not implement           */
+};
+
+const char *ea_strerror(int code);
+int ea_last_hip_error(void);
+
+/* ------------------------------------------------------------------ cache */
+
+typedef struct {
+  void *base;           /* device pointer, [L][P][2][T][H][D], 16-B aligned  */
+  void *scale_base;     /* device pointer to [L][P][2] float32, or NULL      */
+  int32_t num_pages;    /* P                                                  */
+  int32_t num_layers;   /* L                                                  */
+  int32_t page_tokens;  /* T, tokens per page (one hash block)               */
+  int32_t num_kv_heads; /* H, KV heads held by this rank                     */
+  int32_t head_dim;     /* D                                                  */
+  int32_t elem_bytes;   /* bytes per element: 2 for bf16, 1 for fp8          */
+} ea_cache_desc;
+
+typedef struct ea_cache ea_cache;
+
+/* Describe a caller-owned paged KV cache (KV footprint of Eq. 1: a page of
+ * T tokens holds T * 2 * L * D * elem_bytes * H bytes).  The piece size
+ * 2*T*H*D*elem_bytes must be a multiple of 16 bytes (EA_EINVAL otherwise).
+ * The library never frees base or scale_base. */
+int ea_cache_create(const ea_cache_desc *desc, ea_cache **out);
+int ea_cache_destroy(ea_cache *cache);
+
+/* ------------------------------------------------------------------- tier */
+
+typedef struct ea_tier ea_tier;
+
+typedef struct {
+  int64_t capacity_slots; /* K_H                                              */
+  int64_t slot_bytes;
+  int64_t piece_bytes;
+  int64_t page_bytes;     /* data bytes of a slot (trailer excluded)          */
+  int64_t trailer_bytes;
+  int64_t capacity_bytes; /* C_H as given at creation                         */
+  void *host_base;        /* host address of slot 0 (pinned, mapped)          */
+  void *device_base;      /* the same memory as seen by kernels               */
+} ea_tier_info;
+
+/* Create the host tier: K_H = floor(capacity_bytes / slot_bytes) slots of
+ * pinned, device-mapped host memory, OWNED by the library (freed by
+ * ea_tier_destroy).  `shape` supplies the slot layout (the tier can serve
+ * any cache of the same shape).  numa_node >= 0 binds the allocation to that
+ * NUMA node; -1 uses the runtime's default placement.  capacity_bytes is also
+ * the C_H the write rule compares the working-set estimate with.  Fails with
+ * EA_EINVAL if K_H < 1, EA_ENOMEM if the pinned allocation fails. */
+int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes,
+                   int numa_node, ea_tier **out);
+
+/* Waits for every transfer the library issued on this tier, then frees it. */
+int ea_tier_destroy(ea_tier *tier);
+
+int ea_tier_get_info(const ea_tier *tier, ea_tier_info *info);
+
+/* --------------------------------------------------------- chained hashing */
+
+/* Chained prefix-block keys (section 2 "Exact-prefix reuse"; section 3.2: a
+ * full chunk's key depends on its entire prefix, so equal text after a
+ * different prefix gets a different key and an early edit rekeys every later
+ * chunk).  For sequence s = tokens[seq_offsets[s] .. seq_offsets[s+1]) and
+ * b = block_tokens, with key_{-1} = parents[s] (32 zero bytes if parents is
+ * NULL), every FULL block i gets
+ *     key_i = SHA-256( LE32(tok[i*b]) || ... || LE32(tok[i*b+b-1]) || key_{i-1} )
+ * (FIPS 180-4 SHA-256; a token is its 32-bit two's-complement value).  A
+ * trailing partial block gets no key.
+ *
+ * Host pointers: tokens int32[seq_offsets[n_seqs]] (only the ranges named by
+ * seq_offsets are read), seq_offsets int64[n_seqs+1] non-decreasing from
+ * >= 0, parents uint8[n_seqs][32] or NULL; outputs keys_out
+ * uint8[sum floor(len_s/b)][32] and key_offsets_out int64[n_seqs+1]
+ * (key_offsets_out[0] = 0).  Runs on `stream` and returns when the keys are
+ * in keys_out (the scheduler needs them at once, App. "Runtime Admission
+ * Details").  block_tokens must be a positive multiple of 16 (EA_ENOTSUP
+ * otherwise: the GPU splits each key into 4*b/64 parallel message blocks and
+ * one chained block). */
+int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
+                   int32_t n_seqs, int32_t block_tokens,
+                   const uint8_t *parents, uint8_t *keys_out,
+                   int64_t *key_offsets_out, hipStream_t stream);
+
+/* The same keys from DEVICE-resident tokens: d_tokens (device int32),
+ * seq_offsets (HOST int64[n_seqs+1]), d_parents (device uint8[n_seqs][32] or
+ * NULL), d_keys_out (device uint8[...][32]) and key_offsets_out (HOST
+ * int64[n_seqs+1], filled before return).  Asynchronous: the keys are valid
+ * once the work enqueued on `stream` completes. */
+int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,
+                          int32_t n_seqs, int32_t block_tokens,
+                          const uint8_t *d_parents, uint8_t *d_keys_out,
+                          int64_t *key_offsets_out, hipStream_t stream);
+
+/* ------------------------------------------------- lookup and admission */
+
+/* Consecutive-prefix lookup (section 3.2; App. "Prefix coverage from a
+ * reference stream"): *hit_blocks = largest k such that keys 0..k-1 are all
+ * resident; a lookup stops at the first absent key (a key whose store has
+ * not been issued yet counts as absent).  The hits move to the most-recent
+ * end of the LRU order in increasing position order (App. "Recency order of
+ * the host tier") and each gets one pin, so it cannot be evicted before the
+ * caller's load is issued; release with ea_tier_unpin.  slots_out[i] gets the
+ * slot of key i for i < *hit_blocks.  keys: host uint8[n][32]. */
+int ea_tier_lookup(ea_tier *tier, const uint8_t *keys, int64_t n,
+                   int64_t *hit_blocks, int64_t *slots_out);
+
+enum { EA_ADMIT_CONDITIONED = 0, /* Eq. 6 with the pressure signal p_t       */
+       EA_ADMIT_ALWAYS = 1,      /* p_t = 0: offload without write admission */
+       EA_ADMIT_FIXED = 2 };     /* p_t = 1: fixed write admission           */
+
+typedef struct {
+  int64_t theta_ppm;       /* occupancy threshold theta in parts per million
+                              (950000 = 0.95): full when
+                              registered * 10^6 >= theta_ppm * K_H            */
+  int64_t kappa;           /* write threshold in full blocks (u > kappa)      */
+  int64_t block_tokens;    /* b                                               */
+  int64_t beta_rank;       /* KV bytes per token per rank (Eq. 1)             */
+  int64_t activity_window; /* window of A_t and e_t in caller clock units; an
+                              event at time t counts when t > now - window    */
+  int32_t length_window;   /* N_t = mean n of the last this-many first lookups*/
+  int32_t mode;            /* EA_ADMIT_*                                      */
+  int32_t telemetry;       /* 1: the tier's own state is a fresh report;
+                              0: no report, the estimate alone decides        */
+  int32_t _pad;
+} ea_policy;
+
+typedef struct {
+  int64_t n_tokens; /* n, prompt tokens                                       */
+  int64_t h_tokens; /* h, prompt tokens the host tier already holds           */
+  int64_t task_id;  /* agent / task identity (for A_t)                        */
+  int64_t now;      /* caller clock; not below the previous first lookup's    */
+  int32_t decided;  /* -1: first lookup, decide now and enter the windows;
+                       0 or 1: a later lookup of the same request keeps that
+                       earlier decision (App. "Runtime Admission Details")    */
+  int32_t _pad;
+} ea_request;
+
+/* Write admission and copy-time deduplication (section 4, Eq. 6; Eq. 10).
+ * With u = floor(n/b) - floor(h/b), A_t = distinct task_ids of the first
+ * lookups inside the window (this one included), N_t = mean n of the last
+ * length_window first lookups, C_reuse = (A_t - 1) * N_t * beta_rank (Eq. 5)
+ * compared exactly with C_H = the tier's capacity_bytes:
+ *   p_t  = [C_reuse > C_H] and [registered >= theta K_H and e_t > 0]
+ *          (the second factor is dropped when telemetry == 0),
+ *   save = not (p_t and u > kappa),
+ *   mask_out[i] = save and key i is not registered in the tier.
+ * e_t counts evictions made to allocate inside the window.  n_keys must be
+ * floor(n/b); keys host uint8[n_keys][32]; mask_out host uint8[n_keys]. */
+int ea_admission_fill(ea_tier *tier, const ea_policy *policy,
+                      const ea_request *request, const uint8_t *keys,
+                      int64_t n_keys, uint8_t *mask_out, int32_t *save_out);
+
+/* Allocate host slots for the keys with mask[i] != 0 (mask NULL = all) that
+ * are not already registered: the lowest-numbered free slot, else the
+ * least-recent resident slot that no lookup, allocation or transfer pins (an
+ * eviction inside allocation, App. "Runtime Admission Details").  New slots
+ * are registered under their key, go to the most-recent end in increasing
+ * position order, and carry one pin; they become visible to lookups once
+ * ea_store_blocks has been issued for them.  slots_out[i] = -1 where no slot
+ * was allocated; once no victim is left every later block gets -1 (not an
+ * error).  *allocated gets the number of slots allocated. */
+int ea_tier_alloc(ea_tier *tier, const uint8_t *keys, const uint8_t *mask,
+                  int64_t n, int64_t *slots_out, int64_t *allocated);
+
+/* Drop one pin from each listed slot (pins from ea_tier_lookup or
+ * ea_tier_alloc).  A slot allocated but never stored whose last pin goes away
+ * is released.  EA_EINVAL (and no change) if any slot would drop below zero. */
+int ea_tier_unpin(ea_tier *tier, const int64_t *slots, int64_t n);
+
+typedef struct {
+  int64_t capacity_slots;   /* K_H                                          */
+  int64_t registered;       /* allocated + resident slots                   */
+  int64_t resident;
+  int64_t pinned;           /* slots with at least one pin                  */
+  int64_t evictions_total;  /* evictions made to allocate                   */
+  int64_t evictions_window; /* of those, inside the last decision's window  */
+  int64_t clock;            /* last first-lookup clock                      */
+  int64_t active_tasks;     /* A_t of the last decision                     */
+  double mean_prompt;       /* N_t of the last decision (report only)       */
+  double working_set;       /* C_reuse of the last decision (report only)   */
+  int32_t last_pressure;    /* p_t of the last decision                     */
+  int32_t last_save;
+  int64_t bytes_stored;     /* bytes enqueued host-ward by ea_store_blocks  */
+  int64_t bytes_loaded;     /* bytes enqueued device-ward by loads          */
+  int64_t store_calls;
+  int64_t load_calls;
+} ea_tier_stats;
+
+/* Tier telemetry (App. "Runtime Admission Details": registered chunks, K_H,
+ * evictions in the window). */
+int ea_tier_stats_get(const ea_tier *tier, ea_tier_stats *stats);
+
+enum { EA_SLOT_FREE = 0, EA_SLOT_PENDING = 1, EA_SLOT_RESIDENT = 2 };
+
+/* Full metadata image: per slot its state, pin count and key (zeros when
+ * free), and the registered slots from least to most recent in lru_out
+ * (*n_lru entries).  Host arrays of K_H entries. */
+int ea_tier_export(const ea_tier *tier, uint8_t *state_out, int32_t *pins_out,
+                   uint8_t *keys_out, int64_t *lru_out, int64_t *n_lru);
+
+/* ---------------------------------------------------------------- copies */
+
+/* Store ("KV copied from GPU to host", section 2): for every i with
+ * admit_mask[i] != 0 (NULL = all), host slot host_slots[i] receives page
+ * block_ids[i] of every layer (K and V) and, with scales, the page's [L][2]
+ * scales as its trailer.  Admitted slots must be distinct and in [0, K_H);
+ * ids in [0, P).  Slots allocated by ea_tier_alloc become resident.  The
+ * cache must have the tier's shape. */
+int ea_store_blocks(ea_cache *cache, ea_tier *tier, const int32_t *block_ids,
+                    const int64_t *host_slots, const uint8_t *admit_mask,
+                    int32_t n, hipStream_t stream);
+
+/* Load (host restore, the T_load of Eq. 2): page dst_pages[i] of every layer
+ * receives host slot host_slots[i] (and its scales).  Destination pages must
+ * be distinct; sources may repeat. */
+int ea_load_blocks(ea_tier *tier, ea_cache *cache, const int64_t *host_slots,
+                   const int32_t *dst_pages, int32_t n, hipStream_t stream);
+
+/* Layer-pipelined load: the same end state as ea_load_blocks, issued one
+ * layer at a time on copy_stream; after layer l's copy the library records
+ * layer_done[l] (caller-created events, num_layers of them) on copy_stream,
+ * so a consumer stream can hipStreamWaitEvent(layer_done[l]) and use layer l
+ * of every destination page while later layers are still in flight. */
+int ea_load_blocks_layered(ea_tier *tier, ea_cache *cache,
+                           const int64_t *host_slots, const int32_t *dst_pages,
+                           int32_t n, hipStream_t copy_stream,
+                           hipEvent_t *layer_done);
+
+/* Paged gather / scatter between the cache and a DEVICE buffer in slot
+ * layout (the HBM half of a staged transfer, also usable on its own):
+ * gather writes page block_ids[i] (with scales) to d_dst + i*slot_bytes;
+ * scatter writes d_src + i*slot_bytes into page dst_pages[i] (destinations
+ * distinct).  slot_bytes is the tier's (ea_tier_info) for the same shape. */
+int ea_gather_blocks(ea_cache *cache, const int32_t *block_ids, int32_t n,
+                     void *d_dst, hipStream_t stream);
+int ea_scatter_blocks(ea_cache *cache, const void *d_src,
+                      const int32_t *dst_pages, int32_t n, hipStream_t stream);
+
+/* How stores and loads cross the host link:
+ *  EA_PLAN_DIRECT: one kernel reads/writes the mapped pinned slots;
+ *  EA_PLAN_STAGED: gather/scatter through an HBM staging buffer plus DMA
+ *                  copies (hipMemcpyAsync) of runs of consecutive slots;
+ *  EA_PLAN_AUTO:   the library's measured default per direction.
+ * The environment variable EA_TRANSFER=direct|staged overrides AUTO. */
+enum { EA_PLAN_AUTO = 0, EA_PLAN_DIRECT = 1, EA_PLAN_STAGED = 2 };
+enum { EA_DIR_STORE = 0, EA_DIR_LOAD = 1, EA_DIR_BOTH = 2 };
+int ea_tier_set_plan(ea_tier *tier, int direction, int plan);
+int ea_tier_get_plan(const ea_tier *tier, int direction, int *plan);
+
+/* Pinned-copy peak of the host link: hipMemcpyAsync of `bytes` contiguous
+ * bytes between d_buf (device, >= bytes; for EA_DIR_BOTH >= 2*bytes) and the
+ * tier's pinned memory, best of `reps`, in GB/s (1e9 bytes/s).  direction:
+ * EA_DIR_STORE (device to host), EA_DIR_LOAD (host to device) or EA_DIR_BOTH
+ * (both at once on two streams; total bytes over the slower one).  Overwrites
+ * the first bytes (2*bytes for BOTH) of the tier's slots: use it on a tier
+ * that holds nothing yet. */
+int ea_peak_probe(ea_tier *tier, void *d_buf, int64_t bytes, int direction,
+                  int reps, double *gbps);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EA_H */

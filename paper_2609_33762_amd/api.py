@@ -1,0 +1,247 @@
+"""Python binding of libea: thin wrappers that pass torch device pointers,
+numpy host arrays and HIP stream handles to the C ABI (include/ea.h).
+
+Nothing here computes any part of the offload path; it marshals arguments
+and raises EAError on a negative status.
+"""
+import ctypes as C
+
+import numpy as np
+
+from . import _native as N
+from ._native import EAError  # noqa: F401
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _i64(a):
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _u8(a):
+    return np.ascontiguousarray(a, dtype=np.uint8)
+
+
+def current_stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _stream(s):
+    if s is None:
+        return current_stream()
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+class Cache:
+    """A caller-owned paged KV cache: `kv` is a CUDA tensor holding
+    [L][P][2][T][H][D] elements of elem_bytes each (any dtype, contiguous);
+    `scales` an optional contiguous CUDA float32 tensor [L][P][2]."""
+
+    def __init__(self, kv, num_pages, num_layers, page_tokens, num_kv_heads,
+                 head_dim, elem_bytes, scales=None):
+        lib = N.load()
+        assert kv.is_cuda and kv.is_contiguous()
+        piece = 2 * page_tokens * num_kv_heads * head_dim * elem_bytes
+        if kv.numel() * kv.element_size() < num_layers * num_pages * piece:
+            raise ValueError("kv tensor is smaller than the described cache")
+        if scales is not None:
+            assert scales.is_cuda and scales.is_contiguous()
+            if scales.numel() * scales.element_size() < num_layers * num_pages * 8:
+                raise ValueError("scale tensor is smaller than [L][P][2] float32")
+        self.kv, self.scales = kv, scales
+        self.desc = N.CacheDesc(kv.data_ptr(), scales.data_ptr() if scales is not None else None,
+                                num_pages, num_layers, page_tokens, num_kv_heads,
+                                head_dim, elem_bytes)
+        self.num_pages, self.num_layers = num_pages, num_layers
+        self.piece_bytes = piece
+        self._h = C.c_void_p()
+        N.check("ea_cache_create", lib.ea_cache_create(C.byref(self.desc), C.byref(self._h)))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h:
+            N.load().ea_cache_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def gather(self, block_ids, dst, stream=None):
+        ids = _i32(block_ids)
+        N.check("ea_gather_blocks", N.load().ea_gather_blocks(
+            self._h, _ptr(ids), len(ids), dst.data_ptr(), _stream(stream)))
+
+    def scatter(self, src, dst_pages, stream=None):
+        d = _i32(dst_pages)
+        N.check("ea_scatter_blocks", N.load().ea_scatter_blocks(
+            self._h, src.data_ptr(), _ptr(d), len(d), _stream(stream)))
+
+
+def make_policy(kappa, block_tokens, beta_rank, theta_ppm=950000, activity_window=64,
+                length_window=256, mode=N.EA_ADMIT_CONDITIONED, telemetry=1):
+    return N.Policy(theta_ppm, kappa, block_tokens, beta_rank, activity_window,
+                    length_window, mode, telemetry, 0)
+
+
+class Tier:
+    """Library-owned pinned host tier shaped like `cache`."""
+
+    def __init__(self, cache, capacity_bytes, numa_node=-1):
+        lib = N.load()
+        self._h = C.c_void_p()
+        N.check("ea_tier_create", lib.ea_tier_create(cache.handle, capacity_bytes, numa_node,
+                                                     C.byref(self._h)))
+        info = N.TierInfo()
+        N.check("ea_tier_get_info", lib.ea_tier_get_info(self._h, C.byref(info)))
+        self.info = {f: getattr(info, f) for f, _ in N.TierInfo._fields_}
+        self.capacity = info.capacity_slots
+        self.slot_bytes = info.slot_bytes
+
+    def close(self):
+        if self._h:
+            N.load().ea_tier_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def host_view(self):
+        """numpy uint8 [K_H, slot_bytes] view of the pinned slots (no copy)."""
+        n = self.capacity * self.slot_bytes
+        buf = (C.c_uint8 * n).from_address(self.info["host_base"])
+        return np.frombuffer(buf, dtype=np.uint8).reshape(self.capacity, self.slot_bytes)
+
+    # -------------------------------------------------- metadata / policy
+    def lookup(self, keys):
+        keys = _u8(keys).reshape(-1, 32)
+        n = keys.shape[0]
+        hit = C.c_int64()
+        slots = np.full(max(n, 1), -1, np.int64)
+        N.check("ea_tier_lookup", N.load().ea_tier_lookup(
+            self._h, _ptr(keys) if n else None, n, C.byref(hit), _ptr(slots)))
+        return hit.value, slots[:hit.value].copy()
+
+    def admission(self, policy, n_tokens, h_tokens, task_id, now, keys, decided=-1):
+        keys = _u8(keys).reshape(-1, 32)
+        n = keys.shape[0]
+        req = N.Request(n_tokens, h_tokens, task_id, now, decided, 0)
+        mask = np.zeros(max(n, 1), np.uint8)
+        save = C.c_int32()
+        N.check("ea_admission_fill", N.load().ea_admission_fill(
+            self._h, C.byref(policy), C.byref(req), _ptr(keys) if n else None, n,
+            _ptr(mask), C.byref(save)))
+        return save.value, mask[:n].copy()
+
+    def alloc(self, keys, mask=None):
+        keys = _u8(keys).reshape(-1, 32)
+        n = keys.shape[0]
+        mask = None if mask is None else _u8(mask)
+        slots = np.full(max(n, 1), -1, np.int64)
+        count = C.c_int64()
+        N.check("ea_tier_alloc", N.load().ea_tier_alloc(
+            self._h, _ptr(keys) if n else None, _ptr(mask), n, _ptr(slots), C.byref(count)))
+        return count.value, slots[:n].copy()
+
+    def unpin(self, slots):
+        slots = _i64(slots)
+        N.check("ea_tier_unpin", N.load().ea_tier_unpin(self._h, _ptr(slots), len(slots)))
+
+    def stats(self):
+        s = N.TierStats()
+        N.check("ea_tier_stats_get", N.load().ea_tier_stats_get(self._h, C.byref(s)))
+        return {f: getattr(s, f) for f, _ in N.TierStats._fields_}
+
+    def export(self):
+        K = self.capacity
+        state = np.zeros(K, np.uint8)
+        pins = np.zeros(K, np.int32)
+        keys = np.zeros((K, 32), np.uint8)
+        lru = np.zeros(K, np.int64)
+        m = C.c_int64()
+        N.check("ea_tier_export", N.load().ea_tier_export(
+            self._h, _ptr(state), _ptr(pins), _ptr(keys), _ptr(lru), C.byref(m)))
+        return dict(state=state, pins=pins, keys=keys, lru=lru[:m.value].copy())
+
+    def set_plan(self, direction, plan):
+        N.check("ea_tier_set_plan", N.load().ea_tier_set_plan(self._h, direction, plan))
+
+    def get_plan(self, direction):
+        p = C.c_int()
+        N.check("ea_tier_get_plan", N.load().ea_tier_get_plan(self._h, direction, C.byref(p)))
+        return p.value
+
+    # -------------------------------------------------------------- copies
+    def store(self, cache, block_ids, host_slots, mask=None, stream=None):
+        ids, slots = _i32(block_ids), _i64(host_slots)
+        mask = None if mask is None else _u8(mask)
+        N.check("ea_store_blocks", N.load().ea_store_blocks(
+            cache.handle, self._h, _ptr(ids), _ptr(slots), _ptr(mask), len(ids),
+            _stream(stream)))
+
+    def load(self, cache, host_slots, dst_pages, stream=None):
+        slots, dst = _i64(host_slots), _i32(dst_pages)
+        N.check("ea_load_blocks", N.load().ea_load_blocks(
+            self._h, cache.handle, _ptr(slots), _ptr(dst), len(dst), _stream(stream)))
+
+    def load_layered(self, cache, host_slots, dst_pages, copy_stream, layer_events):
+        """layer_events: torch.cuda.Event objects, one per layer."""
+        slots, dst = _i64(host_slots), _i32(dst_pages)
+        for e in layer_events:
+            if not e.cuda_event:  # torch creates the HIP event at its first record
+                e.record(copy_stream)
+        evs = (C.c_void_p * len(layer_events))(*[e.cuda_event for e in layer_events])
+        N.check("ea_load_blocks_layered", N.load().ea_load_blocks_layered(
+            self._h, cache.handle, _ptr(slots), _ptr(dst), len(dst),
+            _stream(copy_stream), evs))
+
+    def peak_probe(self, dev_buf, nbytes, direction, reps=10):
+        g = C.c_double()
+        N.check("ea_peak_probe", N.load().ea_peak_probe(
+            self._h, dev_buf.data_ptr(), nbytes, direction, reps, C.byref(g)))
+        return g.value
+
+
+def hash_blocks(tokens, seq_offsets, block_tokens, parents=None, stream=None):
+    """Chained keys of every full block, computed on the GPU.  Host in, host
+    out; returns (keys uint8 [K, 32], key_offsets int64 [n_seqs + 1])."""
+    tokens, offs = _i32(tokens), _i64(seq_offsets)
+    n_seqs = len(offs) - 1
+    total = int(np.sum(np.diff(offs) // block_tokens)) if n_seqs > 0 and block_tokens > 0 else 0
+    keys = np.zeros((max(total, 1), 32), np.uint8)
+    koffs = np.zeros(n_seqs + 1, np.int64)
+    par = None if parents is None else _u8(parents).reshape(n_seqs, 32)
+    N.check("ea_hash_blocks", N.load().ea_hash_blocks(
+        _ptr(tokens) if tokens.size else None, _ptr(offs), n_seqs, block_tokens,
+        _ptr(par), _ptr(keys), _ptr(koffs), _stream(stream)))
+    return keys[:total], koffs
+
+
+def hash_blocks_device(d_tokens, seq_offsets, block_tokens, d_keys_out, d_parents=None,
+                       stream=None):
+    """Asynchronous variant on device tensors; returns key_offsets."""
+    offs = _i64(seq_offsets)
+    n_seqs = len(offs) - 1
+    koffs = np.zeros(n_seqs + 1, np.int64)
+    N.check("ea_hash_blocks_device", N.load().ea_hash_blocks_device(
+        d_tokens.data_ptr(), _ptr(offs), n_seqs, block_tokens,
+        None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),
+        _ptr(koffs), _stream(stream)))
+    return koffs

@@ -1,0 +1,195 @@
+// Hash entry points of libea: chained prefix-block keys on the GPU.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "ea.h"
+#include "ea_internal.hpp"
+
+namespace {
+
+#define HS_HIP(expr)               \
+  do {                             \
+    hipError_t e_ = (expr);        \
+    if (e_ != hipSuccess) {        \
+      ea::set_last_hip((int)e_);   \
+      return EA_EHIP;              \
+    }                              \
+  } while (0)
+
+// Grow-only device/pinned buffers for hashing on the current device.
+struct HashWs {
+  int device = -1;
+  hipEvent_t done = nullptr;  // end of the last call's use of the buffers
+  bool used = false;
+  // pinned host
+  uint8_t *h_tok = nullptr;  int64_t cap_tok = 0;   // bytes
+  uint8_t *h_meta = nullptr; int64_t cap_meta = 0;  // offsets + parents
+  uint8_t *h_keys = nullptr; int64_t cap_keys = 0;  // bytes
+  // device
+  uint8_t *d_tok = nullptr;
+  uint8_t *d_meta = nullptr;
+  uint8_t *d_keys = nullptr;
+  uint32_t *d_mid = nullptr; int64_t cap_mid = 0;   // keys
+};
+
+HashWs g_ws;
+std::mutex g_ws_mu;
+
+int grow_pair(uint8_t **h, uint8_t **d, int64_t *cap, int64_t need) {
+  if (need <= *cap) return EA_OK;
+  if (*h) (void)hipHostFree(*h);
+  if (d && *d) (void)hipFree(*d);
+  *h = nullptr;
+  if (d) *d = nullptr;
+  *cap = 0;
+  const int64_t c = std::max<int64_t>(need, 1 << 16);
+  HS_HIP(hipHostMalloc((void **)h, (size_t)c, hipHostMallocDefault));
+  if (d) HS_HIP(hipMalloc((void **)d, (size_t)c));
+  *cap = c;
+  return EA_OK;
+}
+
+int prepare(HashWs &w) {
+  int dev;
+  HS_HIP(hipGetDevice(&dev));
+  if (w.used) HS_HIP(hipEventSynchronize(w.done));
+  if (w.device != dev) {
+    // buffers belong to one device; drop them when the caller switches
+    if (w.h_tok) (void)hipHostFree(w.h_tok);
+    if (w.h_meta) (void)hipHostFree(w.h_meta);
+    if (w.h_keys) (void)hipHostFree(w.h_keys);
+    if (w.d_tok) (void)hipFree(w.d_tok);
+    if (w.d_meta) (void)hipFree(w.d_meta);
+    if (w.d_keys) (void)hipFree(w.d_keys);
+    if (w.d_mid) (void)hipFree(w.d_mid);
+    if (w.done) (void)hipEventDestroy(w.done);
+    w = HashWs();
+    w.device = dev;
+  }
+  if (!w.done) HS_HIP(hipEventCreateWithFlags(&w.done, hipEventDisableTiming));
+  return EA_OK;
+}
+
+int validate(const int64_t *seq_offsets, int32_t n_seqs, int32_t block_tokens,
+             int64_t *key_offsets_out, int64_t *total_keys) {
+  if (n_seqs < 0 || !key_offsets_out) return EA_EINVAL;
+  if (n_seqs > 0 && !seq_offsets) return EA_EINVAL;
+  if (block_tokens < 1 || block_tokens > (1 << 20)) return EA_EINVAL;
+  if (block_tokens % 16 != 0) return EA_ENOTSUP;
+  int64_t k = 0;
+  for (int32_t s = 0; s < n_seqs; ++s) {
+    if (seq_offsets[s] < 0 || seq_offsets[s + 1] < seq_offsets[s]) return EA_EINVAL;
+    k += (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
+  }
+  *total_keys = k;
+  return EA_OK;
+}
+
+int ensure_mid(HashWs &w, int64_t keys) {
+  if (keys <= w.cap_mid) return EA_OK;
+  if (w.d_mid) (void)hipFree(w.d_mid);
+  w.d_mid = nullptr;
+  w.cap_mid = 0;
+  const int64_t c = std::max<int64_t>(keys, 4096);
+  HS_HIP(hipMalloc((void **)&w.d_mid, (size_t)c * 32));
+  w.cap_mid = c;
+  return EA_OK;
+}
+
+}  // namespace
+
+extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
+                              int32_t n_seqs, int32_t block_tokens,
+                              const uint8_t *parents, uint8_t *keys_out,
+                              int64_t *key_offsets_out, hipStream_t stream) {
+  int64_t total = 0;
+  int rc = validate(seq_offsets, n_seqs, block_tokens, key_offsets_out, &total);
+  if (rc != EA_OK) return rc;
+  if (total > 0 && (!tokens || !keys_out)) return EA_EINVAL;
+  key_offsets_out[0] = 0;
+  for (int32_t s = 0; s < n_seqs; ++s)
+    key_offsets_out[s + 1] =
+        key_offsets_out[s] + (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
+  if (total == 0) return EA_OK;
+
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  HashWs &w = g_ws;
+  if ((rc = prepare(w)) != EA_OK) return rc;
+  // pack the full-block tokens of every sequence contiguously
+  const int64_t tok_bytes = total * block_tokens * 4;
+  const int64_t meta_bytes = (2 * (int64_t)n_seqs + 1) * 8 + (parents ? 32 * (int64_t)n_seqs : 0);
+  if ((rc = grow_pair(&w.h_tok, &w.d_tok, &w.cap_tok, tok_bytes)) != EA_OK) return rc;
+  if ((rc = grow_pair(&w.h_meta, &w.d_meta, &w.cap_meta, meta_bytes)) != EA_OK) return rc;
+  if ((rc = grow_pair(&w.h_keys, &w.d_keys, &w.cap_keys, total * 32)) != EA_OK) return rc;
+  if ((rc = ensure_mid(w, total)) != EA_OK) return rc;
+
+  int64_t *koff = reinterpret_cast<int64_t *>(w.h_meta);
+  int64_t *toff = koff + n_seqs + 1;
+  uint8_t *par = reinterpret_cast<uint8_t *>(toff + n_seqs);
+  int64_t packed = 0;
+  for (int32_t s = 0; s < n_seqs; ++s) {
+    koff[s] = key_offsets_out[s];
+    toff[s] = packed;
+    const int64_t nt = (key_offsets_out[s + 1] - key_offsets_out[s]) * block_tokens;
+    std::memcpy(w.h_tok + packed * 4, tokens + seq_offsets[s], (size_t)nt * 4);
+    packed += nt;
+  }
+  koff[n_seqs] = key_offsets_out[n_seqs];
+  if (parents) std::memcpy(par, parents, (size_t)n_seqs * 32);
+
+  HS_HIP(hipMemcpyAsync(w.d_tok, w.h_tok, (size_t)tok_bytes, hipMemcpyHostToDevice, stream));
+  HS_HIP(hipMemcpyAsync(w.d_meta, w.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
+  const int64_t *d_koff = reinterpret_cast<const int64_t *>(w.d_meta);
+  const int64_t *d_toff = d_koff + n_seqs + 1;
+  const uint8_t *d_par = parents ? reinterpret_cast<const uint8_t *>(d_toff + n_seqs) : nullptr;
+  HS_HIP(ea::launch_sha256_midstates(reinterpret_cast<const int32_t *>(w.d_tok), d_koff,
+                                     d_toff, n_seqs, total, block_tokens, w.d_mid, stream));
+  HS_HIP(ea::launch_sha256_chain(w.d_mid, d_koff, n_seqs, block_tokens, d_par, w.d_keys,
+                                 stream));
+  HS_HIP(hipMemcpyAsync(w.h_keys, w.d_keys, (size_t)total * 32, hipMemcpyDeviceToHost, stream));
+  HS_HIP(hipEventRecord(w.done, stream));
+  w.used = true;
+  HS_HIP(hipEventSynchronize(w.done));
+  std::memcpy(keys_out, w.h_keys, (size_t)total * 32);
+  return EA_OK;
+}
+
+extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,
+                                     int32_t n_seqs, int32_t block_tokens,
+                                     const uint8_t *d_parents, uint8_t *d_keys_out,
+                                     int64_t *key_offsets_out, hipStream_t stream) {
+  int64_t total = 0;
+  int rc = validate(seq_offsets, n_seqs, block_tokens, key_offsets_out, &total);
+  if (rc != EA_OK) return rc;
+  if (total > 0 && (!d_tokens || !d_keys_out)) return EA_EINVAL;
+  if (d_keys_out && ((uintptr_t)d_keys_out & 15) != 0) return EA_EINVAL;
+  key_offsets_out[0] = 0;
+  for (int32_t s = 0; s < n_seqs; ++s)
+    key_offsets_out[s + 1] =
+        key_offsets_out[s] + (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
+  if (total == 0) return EA_OK;
+
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  HashWs &w = g_ws;
+  if ((rc = prepare(w)) != EA_OK) return rc;
+  const int64_t meta_bytes = (2 * (int64_t)n_seqs + 1) * 8;
+  if ((rc = grow_pair(&w.h_meta, &w.d_meta, &w.cap_meta, meta_bytes)) != EA_OK) return rc;
+  if ((rc = ensure_mid(w, total)) != EA_OK) return rc;
+  int64_t *koff = reinterpret_cast<int64_t *>(w.h_meta);
+  int64_t *toff = koff + n_seqs + 1;
+  for (int32_t s = 0; s <= n_seqs; ++s) koff[s] = key_offsets_out[s];
+  for (int32_t s = 0; s < n_seqs; ++s) toff[s] = seq_offsets[s];
+  HS_HIP(hipMemcpyAsync(w.d_meta, w.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
+  const int64_t *d_koff = reinterpret_cast<const int64_t *>(w.d_meta);
+  HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_koff + n_seqs + 1, n_seqs, total,
+                                     block_tokens, w.d_mid, stream));
+  HS_HIP(ea::launch_sha256_chain(w.d_mid, d_koff, n_seqs, block_tokens, d_parents,
+                                 d_keys_out, stream));
+  HS_HIP(hipEventRecord(w.done, stream));
+  w.used = true;
+  return EA_OK;
+}

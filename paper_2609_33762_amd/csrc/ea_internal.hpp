@@ -1,0 +1,60 @@
+// Internal declarations shared by the host side of libea and its kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace ea {
+
+// Direction of a piece copy: cache pages -> slot-layout buffer (store,
+// gather) or slot-layout buffer -> cache pages (load, scatter).
+enum CopyDir : int { kToSlots = 0, kToPages = 1 };
+
+// Up to this many entries travel inside the kernel arguments instead of a
+// device index array (the small-batch latency path).
+constexpr int kInlineMax = 32;
+
+struct PieceCopy {
+  uint8_t *cache;            // [L][P][piece] bytes
+  uint8_t *scales;           // [L][P][8] bytes or nullptr
+  uint8_t *slots;            // slot-layout buffer (host mapping or HBM staging)
+  const int32_t *pages;      // device [n] or nullptr when inline
+  const int64_t *slot_idx;   // device [n] or nullptr when inline / identity
+  int64_t n;                 // entries
+  int64_t num_pages;         // P
+  int64_t piece_bytes;       // multiple of 16
+  int64_t slot_bytes;
+  int64_t page_bytes;        // offset of the scale trailer inside a slot
+  int32_t num_layers;        // L (the trailer holds 8 bytes per layer)
+  int32_t layer_begin;
+  int32_t layer_count;
+  int32_t identity_slots;    // slot index of entry i is i (staging buffers)
+};
+
+struct InlineIdx {
+  int32_t pages[kInlineMax];
+  int64_t slots[kInlineMax];
+};
+
+// Remember the HIP error behind an EA_EHIP return on this thread.
+void set_last_hip(int err);
+
+// Launch one piece-copy kernel.  grid_cap bounds the workgroups (0 = auto).
+hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir,
+                             int grid_cap, hipStream_t stream);
+
+// SHA-256 chained keys.
+//  mid:  device [n_keys][8] words scratch
+//  key_seq_begin: device int64[n_seqs+1] key offsets; tok_begin: device
+//  int64[n_seqs] token offset of each sequence.
+hipError_t launch_sha256_midstates(const int32_t *d_tokens,
+                                   const int64_t *d_key_offsets,
+                                   const int64_t *d_tok_offsets, int32_t n_seqs,
+                                   int64_t n_keys, int32_t block_tokens,
+                                   uint32_t *d_mid, hipStream_t stream);
+hipError_t launch_sha256_chain(const uint32_t *d_mid,
+                               const int64_t *d_key_offsets, int32_t n_seqs,
+                               int32_t block_tokens, const uint8_t *d_parents,
+                               uint8_t *d_keys, hipStream_t stream);
+
+}  // namespace ea

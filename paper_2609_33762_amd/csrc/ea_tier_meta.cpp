@@ -1,0 +1,240 @@
+// Host-tier metadata and write admission (see ea_tier_meta.hpp).
+//
+// Recency follows the LRU host tier the paper describes (App. "Runtime
+// Admission Details", "Recency order of the host tier"): insertions go to the
+// most-recent end, a lookup hit moves the matched prefix there, and eviction
+// happens only inside allocation, from the least-recent end, skipping chunks
+// that a pending lookup, an allocation or a transfer pins.
+#include "ea_tier_meta.hpp"
+
+#include <unordered_set>
+
+namespace ea {
+
+TierMeta::TierMeta(int64_t slots, int64_t capacity_bytes)
+    : K_(slots),
+      capacity_bytes_(capacity_bytes),
+      state_(slots, EA_SLOT_FREE),
+      pins_(slots, 0),
+      keys_(slots, Key{{0, 0, 0, 0}}),
+      prev_(slots, -1),
+      next_(slots, -1) {
+  map_.reserve((size_t)slots * 2);
+}
+
+void TierMeta::lru_remove(int64_t s) {
+  const int64_t p = prev_[s], n = next_[s];
+  if (p >= 0) next_[p] = n; else lru_head_ = n;
+  if (n >= 0) prev_[n] = p; else lru_tail_ = p;
+  prev_[s] = next_[s] = -1;
+}
+
+void TierMeta::lru_append(int64_t s) {
+  prev_[s] = lru_tail_;
+  next_[s] = -1;
+  if (lru_tail_ >= 0) next_[lru_tail_] = s; else lru_head_ = s;
+  lru_tail_ = s;
+}
+
+int64_t TierMeta::take_free_slot() {
+  if (!returned_.empty()) {
+    const int64_t s = returned_.top();
+    returned_.pop();
+    return s;
+  }
+  if (fresh_ < K_) return fresh_++;
+  return -1;
+}
+
+void TierMeta::release_slot(int64_t s) {
+  map_.erase(keys_[s]);
+  lru_remove(s);
+  state_[s] = EA_SLOT_FREE;
+  keys_[s] = Key{{0, 0, 0, 0}};
+  registered_ -= 1;
+  returned_.push(s);
+}
+
+int TierMeta::lookup(const uint8_t *keys, int64_t n, int64_t *hit,
+                     int64_t *slots_out) {
+  int64_t h = 0;
+  for (; h < n; ++h) {
+    auto it = map_.find(Key::from(keys + 32 * h));
+    if (it == map_.end() || state_[it->second] != EA_SLOT_RESIDENT) break;
+    slots_out[h] = it->second;
+  }
+  for (int64_t i = 0; i < h; ++i) {
+    const int64_t s = slots_out[i];
+    lru_remove(s);
+    lru_append(s);
+    pins_[s] += 1;
+  }
+  *hit = h;
+  return EA_OK;
+}
+
+int TierMeta::admission(const ea_policy &p, const ea_request &r,
+                        const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                        int32_t *save_out) {
+  if (p.block_tokens < 1 || p.kappa < 0 || p.beta_rank < 0 ||
+      p.activity_window < 0 || p.length_window < 1 || p.theta_ppm < 0 ||
+      p.mode < EA_ADMIT_CONDITIONED || p.mode > EA_ADMIT_FIXED ||
+      (p.telemetry != 0 && p.telemetry != 1))
+    return EA_EINVAL;
+  if (r.n_tokens < 0 || r.h_tokens < 0 || r.h_tokens > r.n_tokens) return EA_EINVAL;
+  if (n_keys != r.n_tokens / p.block_tokens) return EA_EINVAL;
+  if (r.decided < -1 || r.decided > 1) return EA_EINVAL;
+  if (r.decided == -1 && have_clock_ && r.now < clock_) return EA_EINVAL;
+
+  // new full chunks the request needs (section 4)
+  const int64_t u = r.n_tokens / p.block_tokens - r.h_tokens / p.block_tokens;
+  int32_t save;
+  if (r.decided >= 0) {
+    save = r.decided;  // a later lookup of the request keeps the first choice
+  } else {
+    log_.push_back(Lookup{r.now, r.task_id, r.n_tokens});
+    clock_ = r.now;
+    have_clock_ = true;
+    const int64_t horizon = r.now - p.activity_window;
+
+    // A_t: distinct tasks whose first lookup falls inside the window
+    std::unordered_set<int64_t> tasks;
+    for (auto it = log_.rbegin(); it != log_.rend() && it->time > horizon; ++it)
+      tasks.insert(it->task);
+    const int64_t active = (int64_t)tasks.size();
+
+    // N_t: mean prompt length of the last length_window first lookups
+    int64_t cnt = 0, sum = 0;
+    for (auto it = log_.rbegin(); it != log_.rend() && cnt < p.length_window; ++it) {
+      sum += it->n;
+      ++cnt;
+    }
+
+    // [C_reuse > C_H], C_reuse = (A_t - 1) * (sum / cnt) * beta (Eq. 5),
+    // compared exactly as (A_t - 1) * sum * beta > C_H * cnt
+    using u128 = unsigned __int128;
+    const u128 lhs = active > 1 ? (u128)(active - 1) * (u128)sum * (u128)p.beta_rank : 0;
+    const u128 rhs = (u128)capacity_bytes_ * (u128)cnt;
+    const bool over = lhs > rhs;
+
+    bool pressure;
+    if (p.telemetry) {
+      // tier full and evicting: o_t >= theta and e_t > 0 (Eq. 10)
+      const bool full = (u128)registered_ * 1000000u >= (u128)p.theta_ppm * (u128)K_;
+      const bool evicting = !evict_stamps_.empty() && evict_stamps_.back() > horizon;
+      pressure = over && full && evicting;
+    } else {
+      pressure = over;  // no fresh report: the estimate alone decides
+    }
+    if (p.mode == EA_ADMIT_ALWAYS) pressure = false;
+    if (p.mode == EA_ADMIT_FIXED) pressure = true;
+
+    save = !(pressure && u > p.kappa);  // Eq. 6
+
+    last_window_ = p.activity_window;
+    last_active_ = active;
+    last_mean_ = cnt ? (double)sum / (double)cnt : 0.0;
+    last_ws_ = (double)(active - 1) * last_mean_ * (double)p.beta_rank;
+    last_pressure_ = pressure ? 1 : 0;
+    last_save_ = save;
+  }
+  // copy-time deduplication: chunks the tier already holds are not copied
+  for (int64_t i = 0; i < n_keys; ++i)
+    mask_out[i] = (uint8_t)(save && !registered(Key::from(keys + 32 * i)));
+  *save_out = save;
+  return EA_OK;
+}
+
+int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
+                    int64_t *slots_out, int64_t *allocated) {
+  int64_t count = 0;
+  bool exhausted = false;
+  for (int64_t i = 0; i < n; ++i) {
+    slots_out[i] = -1;
+    if ((mask && !mask[i]) || exhausted) continue;
+    const Key k = Key::from(keys + 32 * i);
+    if (registered(k)) continue;
+    int64_t s = take_free_slot();
+    if (s < 0) {
+      // evict the least-recent resident chunk nothing pins
+      int64_t v = lru_head_;
+      while (v >= 0 && !(state_[v] == EA_SLOT_RESIDENT && pins_[v] == 0)) v = next_[v];
+      if (v < 0) {
+        exhausted = true;
+        continue;
+      }
+      evict_stamps_.push_back(clock_);
+      map_.erase(keys_[v]);
+      lru_remove(v);
+      state_[v] = EA_SLOT_FREE;
+      registered_ -= 1;
+      resident_ -= 1;
+      s = v;
+    }
+    keys_[s] = k;
+    state_[s] = EA_SLOT_PENDING;
+    pins_[s] += 1;
+    map_.emplace(k, s);
+    lru_append(s);
+    registered_ += 1;
+    slots_out[i] = s;
+    ++count;
+  }
+  *allocated = count;
+  return EA_OK;
+}
+
+void TierMeta::mark_stored(int64_t slot) {
+  if (state_[slot] == EA_SLOT_PENDING) {
+    state_[slot] = EA_SLOT_RESIDENT;
+    resident_ += 1;
+  }
+}
+
+int TierMeta::unpin(const int64_t *slots, int64_t n) {
+  std::unordered_map<int64_t, int32_t> drop;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t s = slots[i];
+    if (s < 0 || s >= K_) return EA_EINVAL;
+    if (++drop[s] > pins_[s]) return EA_EINVAL;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t s = slots[i];
+    pins_[s] -= 1;
+    if (pins_[s] == 0 && state_[s] == EA_SLOT_PENDING) release_slot(s);  // abandoned
+  }
+  return EA_OK;
+}
+
+void TierMeta::stats(ea_tier_stats *s) const {
+  s->capacity_slots = K_;
+  s->registered = registered_;
+  s->resident = resident_;
+  int64_t pinned = 0;
+  for (int32_t p : pins_) pinned += p > 0;
+  s->pinned = pinned;
+  s->evictions_total = (int64_t)evict_stamps_.size();
+  int64_t in_window = 0;
+  for (auto it = evict_stamps_.rbegin();
+       it != evict_stamps_.rend() && *it > clock_ - last_window_; ++it)
+    ++in_window;
+  s->evictions_window = in_window;
+  s->clock = clock_;
+  s->active_tasks = last_active_;
+  s->mean_prompt = last_mean_;
+  s->working_set = last_ws_;
+  s->last_pressure = last_pressure_;
+  s->last_save = last_save_;
+}
+
+void TierMeta::export_state(uint8_t *state, int32_t *pins, uint8_t *keys,
+                            int64_t *lru, int64_t *n_lru) const {
+  std::memcpy(state, state_.data(), (size_t)K_);
+  std::memcpy(pins, pins_.data(), (size_t)K_ * sizeof(int32_t));
+  for (int64_t s = 0; s < K_; ++s) std::memcpy(keys + 32 * s, keys_[s].w, 32);
+  int64_t m = 0;
+  for (int64_t s = lru_head_; s >= 0; s = next_[s]) lru[m++] = s;
+  *n_lru = m;
+}
+
+}  // namespace ea

@@ -1,0 +1,85 @@
+// Host-tier metadata: key -> slot map, LRU recency, pins, free slots, and
+// the working-set-aware write admission rule.  Pure CPU code; the caller
+// holds the tier lock.
+#pragma once
+
+#include <stdint.h>
+
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <unordered_map>
+#include <vector>
+
+#include "ea.h"
+
+namespace ea {
+
+struct Key {
+  uint64_t w[4];
+  bool operator==(const Key &o) const {
+    return w[0] == o.w[0] && w[1] == o.w[1] && w[2] == o.w[2] && w[3] == o.w[3];
+  }
+  static Key from(const uint8_t *p) {
+    Key k;
+    std::memcpy(k.w, p, 32);
+    return k;
+  }
+};
+
+struct KeyHash {
+  // keys are SHA-256 digests: their first 8 bytes are already uniform
+  size_t operator()(const Key &k) const { return (size_t)k.w[0]; }
+};
+
+class TierMeta {
+ public:
+  TierMeta(int64_t slots, int64_t capacity_bytes);
+
+  int64_t capacity() const { return K_; }
+
+  int lookup(const uint8_t *keys, int64_t n, int64_t *hit, int64_t *slots_out);
+  int admission(const ea_policy &p, const ea_request &r, const uint8_t *keys,
+                int64_t n_keys, uint8_t *mask_out, int32_t *save_out);
+  int alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
+            int64_t *slots_out, int64_t *allocated);
+  // A store was issued to `slot`: an allocated slot becomes resident.
+  void mark_stored(int64_t slot);
+  int unpin(const int64_t *slots, int64_t n);
+  void stats(ea_tier_stats *s) const;
+  void export_state(uint8_t *state, int32_t *pins, uint8_t *keys, int64_t *lru,
+                    int64_t *n_lru) const;
+
+ private:
+  bool registered(const Key &k) const { return map_.find(k) != map_.end(); }
+  int64_t take_free_slot();
+  void release_slot(int64_t s);
+  void lru_remove(int64_t s);
+  void lru_append(int64_t s);
+
+  int64_t K_;
+  int64_t capacity_bytes_;
+  std::vector<uint8_t> state_;
+  std::vector<int32_t> pins_;
+  std::vector<Key> keys_;
+  std::vector<int64_t> prev_, next_;
+  int64_t lru_head_ = -1, lru_tail_ = -1;  // head = least recent
+  std::unordered_map<Key, int64_t, KeyHash> map_;
+  // free slots: every slot >= fresh_ was never used; returned_ holds freed
+  // slots below fresh_, so the lowest free slot is returned_.top() or fresh_
+  int64_t fresh_ = 0;
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> returned_;
+  int64_t registered_ = 0, resident_ = 0;
+  std::vector<int64_t> evict_stamps_;
+  struct Lookup {
+    int64_t time, task, n;
+  };
+  std::vector<Lookup> log_;
+  int64_t clock_ = 0;
+  bool have_clock_ = false;
+  int64_t last_window_ = 0, last_active_ = 0;
+  double last_mean_ = 0.0, last_ws_ = 0.0;
+  int32_t last_pressure_ = 0, last_save_ = 0;
+};
+
+}  // namespace ea

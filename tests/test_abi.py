@@ -1,0 +1,108 @@
+"""CPU checks of the C ABI: libea.so loads, exports every function that
+include/ea.h declares, binds only HIP symbols that torch's bundled runtime
+also exports, and rejects bad arguments before touching the GPU."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_33762_amd import _native as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ea.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ea_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(N.LIB_PATH):
+        pytest.fail("libea.so is not built; run __graft_entry__.build()")
+    return N.load()
+
+
+def test_header_declares_the_boundary():
+    fns = declared_functions()
+    for f in ["ea_hash_blocks", "ea_store_blocks", "ea_load_blocks", "ea_load_blocks_layered",
+              "ea_admission_fill", "ea_tier_lookup", "ea_tier_alloc", "ea_tier_create"]:
+        assert f in fns
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", N.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    missing = [f for f in declared_functions() if f not in exported]
+    assert not missing, missing
+    for f in declared_functions():
+        assert hasattr(lib, f)
+
+
+def test_binding_covers_every_declared_function():
+    assert sorted(N.SIGNATURES) == declared_functions()
+
+
+def test_hip_imports_exist_in_torchs_runtime():
+    torch = pytest.importorskip("torch")
+    rt = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+    if not os.path.exists(rt):
+        pytest.skip("torch bundles no HIP runtime")
+    und = subprocess.run(["nm", "-D", "--undefined-only", N.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    need = {ln.split()[-1].split("@")[0] for ln in und.splitlines() if "hip" in ln.lower()}
+    have_out = subprocess.run(["nm", "-D", "--defined-only", rt], capture_output=True,
+                              text=True, check=True).stdout
+    have = {ln.split()[-1].split("@")[0] for ln in have_out.splitlines()}
+    assert need and not (need - have), sorted(need - have)
+
+
+def test_no_oracle_in_the_product_library():
+    out = subprocess.run(["nm", "-D", N.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    assert "eao_" not in out
+    ldd = subprocess.run(["ldd", N.LIB_PATH], capture_output=True, text=True).stdout
+    assert "libeao" not in ldd
+
+
+def test_argument_errors_need_no_gpu(lib):
+    assert lib.ea_strerror(N.EA_EINVAL).decode() == "invalid argument"
+    out = C.c_void_p()
+    assert lib.ea_cache_create(None, C.byref(out)) == N.EA_EINVAL
+    d = N.CacheDesc(None, None, 4, 1, 16, 1, 64, 2)
+    assert lib.ea_cache_create(C.byref(d), C.byref(out)) == N.EA_EINVAL  # null base
+    d = N.CacheDesc(0x1000, None, 4, 1, 1, 1, 3, 1)  # 6-byte pieces
+    assert lib.ea_cache_create(C.byref(d), C.byref(out)) == N.EA_EINVAL
+    d = N.CacheDesc(0x1001, None, 4, 1, 16, 1, 64, 2)  # misaligned base
+    assert lib.ea_cache_create(C.byref(d), C.byref(out)) == N.EA_EINVAL
+    assert lib.ea_tier_create(None, 1 << 20, -1, C.byref(out)) == N.EA_EINVAL
+    assert lib.ea_store_blocks(None, None, None, None, None, 0, None) == N.EA_EINVAL
+    assert lib.ea_load_blocks(None, None, None, None, 0, None) == N.EA_EINVAL
+    koffs = (C.c_int64 * 2)()
+    offs = (C.c_int64 * 2)(0, 32)
+    # block sizes that are not multiples of 16 are not supported on the GPU
+    assert lib.ea_hash_blocks(None, offs, 1, 8, None, None, koffs, None) == N.EA_ENOTSUP
+    assert lib.ea_hash_blocks(None, offs, 1, 0, None, None, koffs, None) == N.EA_EINVAL
+    bad = (C.c_int64 * 2)(5, 3)
+    assert lib.ea_hash_blocks(None, bad, 1, 16, None, None, koffs, None) == N.EA_EINVAL
+    # empty input: no GPU work, offsets still written
+    empty = (C.c_int64 * 2)(0, 7)
+    assert lib.ea_hash_blocks(None, empty, 1, 16, None, None, koffs, None) == N.EA_OK
+    assert list(koffs) == [0, 0]
+
+
+def test_kernel_source_sha_constants_match_the_oracles_derivation():
+    # the GPU kernels carry the FIPS 180-4 table typed in; the oracle derives
+    # it from primes: they must agree
+    import oracle
+    src = open(os.path.join(ROOT, "paper_2609_33762_amd", "csrc",
+                            "ea_sha256_kernels.hip")).read()
+    k = [int(x, 16) for x in re.findall(r"0x([0-9a-f]{8})u", src.split("kRound[64] = {")[1].split("};")[0])]
+    h = [int(x, 16) for x in re.findall(r"0x([0-9a-f]{8})u", src.split("kInit[8] = {")[1].split("};")[0])]
+    K, H = oracle.sha256_constants()
+    assert k == list(K) and h == list(H)

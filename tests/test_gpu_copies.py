@@ -1,0 +1,191 @@
+"""GPU parity of store / load / layered load / gather / scatter against the
+oracle, byte for byte on the full cache and tier images of small caches
+(several pieces per page, ragged batches, both transfer plans, fp8 with
+scales, masks, error paths, cross-stream hazards)."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_33762_amd import _native as N
+from paper_2609_33762_amd import workloads as W
+
+from gpu_common import Pair, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+PLANS = {"direct": N.EA_PLAN_DIRECT, "staged": N.EA_PLAN_STAGED}
+
+
+def tiny_pair(**kw):
+    sh = W.TINY
+    return Pair(sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                sh.elem_bytes, kw.pop("slots", W.TINY_TIER_SLOTS), **kw)
+
+
+@pytest.mark.parametrize("plan", list(PLANS))
+def test_tiny_config_store_then_load(plan):
+    # Tiny workload: 32 random pages stored, loaded into 32 other free pages
+    p = tiny_pair(seed=11)
+    p.tier.set_plan(N.EA_DIR_BOTH, PLANS[plan])
+    r = W.rng(W.SEED_IDS)
+    src = W.distinct(r, W.TINY.num_pages, 32)
+    dst = W.distinct(r, W.TINY.num_pages, 32, exclude=src)
+    slots = W.distinct(r, p.tier.capacity, 32)
+    p.tier.store(p.cache, src, slots)
+    p.o_store(src, slots)
+    p.assert_equal("store")
+    p.tier.load(p.cache, slots, dst)
+    p.o_load(slots, dst)
+    p.assert_equal("load")
+    # round trip: the destination pages now hold the source pages
+    kv = p.kv.cpu().numpy().reshape(W.TINY.num_layers, W.TINY.num_pages, -1)
+    assert np.array_equal(kv[:, dst], kv[:, src])
+    p.close()
+
+
+@pytest.mark.parametrize("plan", list(PLANS))
+@pytest.mark.parametrize("n", [1, 31, 32, 33, 100, 200])
+def test_ragged_batches_and_masks(plan, n):
+    # n <= 32 travels in kernel arguments, larger batches through index upload
+    os.environ["EA_STAGING_MB"] = "1"  # 32 slots per staging half: several chunks
+    try:
+        p = tiny_pair(seed=20 + n, slots=256)
+    finally:
+        os.environ.pop("EA_STAGING_MB")
+    p.tier.set_plan(N.EA_DIR_BOTH, PLANS[plan])
+    r = W.rng(1000 + n)
+    src = W.distinct(r, W.TINY.num_pages, n)
+    slots = W.distinct(r, p.tier.capacity, n)
+    if n > 40:  # a run of 40 consecutive slots for the DMA coalescing
+        rest = W.distinct(r, p.tier.capacity, n - 40, exclude=np.arange(100, 140))
+        slots = np.concatenate([np.arange(100, 140), rest])
+    mask = (r.random(n) < 0.8).astype(np.uint8)
+    mask[0] = 1
+    p.tier.store(p.cache, src, slots, mask)
+    p.o_store(src, slots, mask)
+    p.assert_equal("masked store")
+    keep = mask == 1
+    dst = W.distinct(r, W.TINY.num_pages, int(keep.sum()))
+    p.tier.load(p.cache, slots[keep], dst)
+    p.o_load(slots[keep], dst)
+    p.assert_equal("load")
+    p.close()
+
+
+@pytest.mark.parametrize("plan", list(PLANS))
+def test_fp8_with_scales_and_duplicate_sources(plan):
+    p = Pair(48, 3, 16, 2, 64, 1, 40, scales=True, seed=5)
+    p.tier.set_plan(N.EA_DIR_BOTH, PLANS[plan])
+    r = W.rng(7)
+    src = W.distinct(r, 48, 36)
+    slots = W.distinct(r, 40, 36)
+    p.tier.store(p.cache, src, slots)
+    p.o_store(src, slots)
+    p.assert_equal("fp8 store")
+    # the same slot may feed several destination pages
+    lslots = np.concatenate([slots[:20], slots[:5]])
+    dst = W.distinct(r, 48, 25)
+    p.tier.load(p.cache, lslots, dst)
+    p.o_load(lslots, dst)
+    p.assert_equal("fp8 load")
+    p.close()
+
+
+def test_errors_move_nothing():
+    p = tiny_pair(seed=3)
+    before_tier = p.tier.host_view().copy()
+    before = p.kv.cpu().numpy()
+    cases = [
+        ("store", dict(ids=[0, 1], slots=[0, 0])),               # duplicate destination slot
+        ("store", dict(ids=[0, W.TINY.num_pages], slots=[0, 1])),
+        ("store", dict(ids=[0, 1], slots=[0, p.tier.capacity])),
+        ("load", dict(slots=[0, 1], dst=[5, 5])),                 # duplicate destination page
+        ("load", dict(slots=[-1, 1], dst=[5, 6])),
+        ("load", dict(slots=[0, 1], dst=[5, W.TINY.num_pages])),
+    ]
+    for op, a in cases:
+        with pytest.raises(N.EAError) as e:
+            if op == "store":
+                p.tier.store(p.cache, a["ids"], a["slots"])
+            else:
+                p.tier.load(p.cache, a["slots"], a["dst"])
+        assert e.value.code == N.EA_EINVAL
+    p.torch.cuda.synchronize()
+    assert np.array_equal(p.tier.host_view(), before_tier)
+    assert np.array_equal(p.kv.cpu().numpy(), before)
+    st = p.tier.stats()
+    assert st["store_calls"] == 0 and st["load_calls"] == 0
+    p.close()
+
+
+def test_load_on_another_stream_waits_for_the_store():
+    torch = need_gpu()
+    p = tiny_pair(seed=9, slots=256)
+    r = W.rng(9)
+    src = W.distinct(r, W.TINY.num_pages, 120)
+    slots = W.distinct(r, p.tier.capacity, 120)
+    dst = W.distinct(r, W.TINY.num_pages, 120, exclude=src)
+    a, b = torch.cuda.Stream(), torch.cuda.Stream()
+    # a long store on stream a, the load of the same slots on stream b at once
+    p.tier.store(p.cache, src, slots, stream=a)
+    p.tier.load(p.cache, slots, dst, stream=b)
+    p.o_store(src, slots)
+    p.o_load(slots, dst)
+    p.assert_equal("cross-stream")
+    p.close()
+
+
+@pytest.mark.parametrize("n", [20, 300])
+def test_layered_load_events_mark_finished_layers(n):
+    torch = need_gpu()
+    L, P = 6, 700
+    p = Pair(P, L, 16, 2, 64, 1, 320, scales=True, seed=31)
+    r = W.rng(31)
+    src = W.distinct(r, P, n)
+    slots = W.distinct(r, 320, n)
+    p.tier.store(p.cache, src, slots)
+    p.o_store(src, slots)
+    dst = W.distinct(r, P, n, exclude=src)
+    # poison the destination pages so a premature event would show
+    kv3 = p.kv.view(L, P, -1)
+    kv3[:, torch.as_tensor(dst, device="cuda")] = 0xA5
+    p.snapshot()
+    copy_s, cons_s = torch.cuda.Stream(), torch.cuda.Stream()
+    events = [torch.cuda.Event() for _ in range(L)]
+    p.tier.load_layered(p.cache, slots, dst, copy_s, events)
+    snaps = []
+    d = torch.as_tensor(dst, device="cuda")
+    with torch.cuda.stream(cons_s):
+        for l in range(L):
+            cons_s.wait_event(events[l])
+            snaps.append(kv3[l].index_select(0, d).clone())
+    torch.cuda.synchronize()
+    p.o_load(slots, dst)
+    p.assert_equal("layered end state")
+    want = p.o_cache.reshape(L, P, -1)
+    for l in range(L):
+        assert np.array_equal(snaps[l].cpu().numpy(), want[l][dst]), l
+    p.close()
+
+
+@pytest.mark.parametrize("n", [7, 150])
+def test_gather_scatter_through_device_buffer(n):
+    torch = need_gpu()
+    p = Pair(256, 4, 16, 2, 64, 2, 8, scales=True, seed=41)
+    slot = p.sizes["slot"]
+    r = W.rng(41)
+    src = W.distinct(r, 256, n)
+    dst = W.distinct(r, 256, n, exclude=src if n < 128 else None)
+    buf = torch.full((n * slot,), 0x5A, dtype=torch.uint8, device="cuda")
+    p.cache.gather(src, buf)
+    # oracle: the gather buffer is a tier whose slot i holds entry i
+    want = np.full((n, slot), 0x5A, np.uint8)
+    oracle.store_blocks(p.oshape, p.o_cache, p.o_sc, want, src, np.arange(n))
+    torch.cuda.synchronize()
+    assert np.array_equal(buf.cpu().numpy().reshape(n, slot), want)
+    p.cache.scatter(buf, dst)
+    oracle.load_blocks(p.oshape, want, p.o_cache, p.o_sc, np.arange(n), dst)
+    p.assert_equal("scatter")
+    p.close()

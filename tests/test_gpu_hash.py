@@ -1,0 +1,75 @@
+"""GPU parity of the chained prefix-block keys against the oracle: ragged
+sequences, several block sizes, parents, many chains at once, the workload
+sizes (tiny, one Qwen3 agent turn, the 64k-token layered prefix) and the
+device-pointer variant."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_33762_amd import api
+from paper_2609_33762_amd import workloads as W
+
+from gpu_common import need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def check(lengths, b, parents=False, seed=0):
+    need_gpu()
+    toks, offs = W.sequences(seed, lengths)
+    par = W.host_bytes(seed + 1, 32 * len(lengths)).reshape(-1, 32) if parents else None
+    keys, koffs = api.hash_blocks(toks, offs, b, par)
+    okeys, okoffs = oracle.hash_blocks(toks, offs, b, par)
+    assert np.array_equal(koffs, okoffs)
+    if not np.array_equal(keys, okeys):
+        bad = np.nonzero((keys != okeys).any(axis=1))[0]
+        raise AssertionError(f"{len(bad)} keys differ, first {bad[:8]}")
+    return keys, koffs
+
+
+def test_tiny_workload():
+    check([512] * 4, 16, seed=W.SEED_TOKENS)
+
+
+@pytest.mark.parametrize("b", [16, 32, 1024])
+def test_ragged_lengths_and_parents(b):
+    lengths = [0, b - 1, b, b + 1, 7 * b + 3, 1, 3 * b]
+    check(lengths, b, seed=b)
+    check(lengths, b, parents=True, seed=b + 1)
+
+
+def test_many_chains_span_several_waves():
+    r = W.rng(5)
+    check(list(r.integers(0, 900, size=300)), 16, parents=True, seed=5)
+
+
+def test_one_qwen3_turn():
+    # the store refill (32k tokens) and the cached prefix (24k) of one turn
+    check([32000, 24000], 16, seed=W.SEED_TOKENS)
+
+
+def test_64k_prefix_chain():
+    keys, _ = check([65536], 16, seed=9)
+    assert keys.shape == (4096, 32)
+
+
+def test_device_variant():
+    torch = need_gpu()
+    toks, offs = W.sequences(3, [100, 0, 513, 1024])
+    d_tok = torch.as_tensor(toks, device="cuda")
+    okeys, okoffs = oracle.hash_blocks(toks, offs, 16)
+    out = torch.zeros((len(okeys), 32), dtype=torch.uint8, device="cuda")
+    koffs = api.hash_blocks_device(d_tok, offs, 16, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(koffs, okoffs)
+    assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+def test_incremental_hash_from_cached_parent():
+    # a prompt that repeats an earlier one hashes only its new blocks
+    toks, offs = W.sequences(4, [4096])
+    full, _ = oracle.hash_blocks(toks, offs, 16)
+    k = 200
+    tail, _ = api.hash_blocks(toks[16 * k:], np.array([0, 4096 - 16 * k]), 16,
+                              parents=full[k - 1].reshape(1, 32))
+    assert np.array_equal(tail, full[k:])

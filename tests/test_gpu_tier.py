@@ -1,0 +1,87 @@
+"""Parity of the library's host-tier metadata and write admission with the
+oracle: random request streams through lookup / admission / alloc / store /
+unpin, compared state for state (slot states, pins, keys, LRU order,
+telemetry) after every step."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_33762_amd import api
+from paper_2609_33762_amd import _native as N
+from paper_2609_33762_amd import workloads as W
+
+from gpu_common import Pair
+
+pytestmark = pytest.mark.gpu
+
+STAT_KEYS = ["capacity_slots", "registered", "resident", "pinned", "evictions_total",
+             "evictions_window", "clock", "active_tasks", "last_pressure", "last_save"]
+
+
+def compare(prod, orc, where):
+    a, b = prod.export(), orc.export()
+    for k in ("state", "pins", "keys", "lru"):
+        assert np.array_equal(a[k], b[k]), f"{where}: {k}"
+    sa, sb = prod.stats(), orc.stats()
+    for k in STAT_KEYS:
+        assert sa[k] == sb[k], f"{where}: {k} {sa[k]} != {sb[k]}"
+
+
+@pytest.mark.parametrize("mode,telemetry,seed", [
+    (N.EA_ADMIT_CONDITIONED, 1, 0), (N.EA_ADMIT_CONDITIONED, 0, 1),
+    (N.EA_ADMIT_ALWAYS, 1, 2), (N.EA_ADMIT_FIXED, 1, 3), (N.EA_ADMIT_CONDITIONED, 1, 4)])
+def test_random_request_streams(mode, telemetry, seed):
+    K = 48
+    p = Pair(64, 2, 16, 1, 32, 2, K, seed=seed)  # 4 KiB slots
+    beta = 2 * 2 * 32 * 2  # bytes per token of this shape
+    ot = oracle.Tier(p.oshape, K * p.sizes["slot"])
+    pol_p = api.make_policy(kappa=3, block_tokens=16, beta_rank=beta, activity_window=12,
+                            length_window=16, mode=mode, telemetry=telemetry)
+    pol_o = oracle.make_policy(kappa=3, block_tokens=16, beta=beta, activity_window=12,
+                               length_window=16, mode=mode, telemetry=telemetry)
+    r = W.rng(100 + seed)
+    agents = [W.tokens(1000 * seed + a, 16 * 40) for a in range(6)]
+    lengths = [int(r.integers(2, 10)) * 16 for _ in range(6)]
+    for turn in range(60):
+        a = int(r.integers(0, 6))
+        lengths[a] = min(lengths[a] + int(r.integers(0, 5)) * 16 + int(r.integers(0, 16)), 16 * 40)
+        if r.random() < 0.1:  # an early edit rekeys the rest of the prompt
+            agents[a] = agents[a].copy()
+            agents[a][int(r.integers(0, lengths[a]))] += 1
+        toks = agents[a][:lengths[a]]
+        keys, _ = api.hash_blocks(toks, np.array([0, len(toks)]), 16)
+        h, hs = p.tier.lookup(keys)
+        oh, ohs = ot.lookup(keys)
+        assert h == oh and np.array_equal(hs, ohs)
+        compare(p.tier, ot, f"turn {turn} lookup")
+        save, mask = p.tier.admission(pol_p, len(toks), 16 * h, a, turn, keys)
+        osave, omask = ot.admission(pol_o, len(toks), 16 * h, a, turn, keys)
+        assert save == osave and np.array_equal(mask, omask), turn
+        cnt, slots = p.tier.alloc(keys, mask)
+        ocnt, oslots = ot.alloc(keys, mask)
+        assert cnt == ocnt and np.array_equal(slots, oslots), turn
+        got = slots >= 0
+        if got.any():
+            pages = W.distinct(r, 64, int(got.sum()))
+            if r.random() < 0.9:
+                p.tier.store(p.cache, pages, slots[got])
+                ot.mark_stored(slots[got])
+            rel = slots[got]
+            p.tier.unpin(rel)
+            ot.unpin(rel)
+        if h and r.random() < 0.8:
+            p.tier.unpin(hs)
+            ot.unpin(ohs)
+        compare(p.tier, ot, f"turn {turn}")
+    p.close()
+
+
+def test_all_pinned_tier_reports_unallocated_blocks():
+    p = Pair(16, 1, 16, 1, 32, 2, 4, seed=1)
+    keys = np.stack([np.frombuffer(int(i + 1).to_bytes(32, "little"), np.uint8) for i in range(6)])
+    cnt, slots = p.tier.alloc(keys)
+    assert cnt == 4 and list(slots) == [0, 1, 2, 3, -1, -1]
+    assert p.tier.stats()["evictions_total"] == 0
+    with pytest.raises(N.EAError):
+        p.tier.unpin([0, 0])
+    p.close()
