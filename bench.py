@@ -17,8 +17,16 @@ Every step hashes and stores a fresh refill (new tokens), so the tier fills
 and starts evicting after five steps, as a serving run would.
 
 Prints one JSON line; details go to stderr and gpurun_out/bench_detail.json.
+
+Other modes:
+  --isolated-only          set-up plus the isolated kernel measurements only
+                           (what the rocprofv3 runs profile)
+  --summarize-profiles D   turn rocprofv3 CSVs under D into the summaries in
+                           profiles/
 """
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -31,10 +39,18 @@ sys.path.insert(0, ROOT)
 
 GB = 1e9
 HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_33762_amd", "csrc", "ea_copy_kernels.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_hbm_bytes.md")
+TRACE_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_kernel_trace.md")
+N_ISO = {"store": 5, "load": 5, "gather": 20, "scatter": 20}
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
 
 
 def event_ms(torch, fn, stream, reps):
@@ -49,25 +65,22 @@ def event_ms(torch, fn, stream, reps):
     return float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
 
 
-def cpu_baseline(W, store_pages, load_pages, prefix_tokens, refill_tokens):
+def cpu_baseline(W, n_s, n_l, prefix_tokens, refill_tokens):
     """The oracle (single thread, pinned to one core) running one full step of
     the same workload on host arrays: hash both sequences, store 2,000 pages,
     load 1,500 pages.  Cache and tier are sampled down to the pages touched."""
     import oracle
     sh = W.QWEN3
-    n_s, n_l = len(store_pages), len(load_pages)
     P = n_s + n_l
     oshape = oracle.make_shape(P, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
                                sh.head_dim, sh.elem_bytes)
     sz = oracle.sizes(oshape)
-    pattern = W.host_bytes(W.SEED_DATA, sz["piece"])
-    cache = np.tile(pattern, sh.num_layers * P)
+    cache = np.tile(W.host_bytes(W.SEED_DATA, sz["piece"]), sh.num_layers * P)
     tier = np.zeros((P, sz["slot"]), np.uint8)
     toks = np.concatenate([prefix_tokens, refill_tokens])
     offs = np.array([0, len(prefix_tokens), len(toks)], np.int64)
     prev = os.sched_getaffinity(0)
-    core = sorted(prev)[0]
-    os.sched_setaffinity(0, {core})
+    os.sched_setaffinity(0, {sorted(prev)[0]})
     reps, times = 3, []
     try:
         for _ in range(reps):
@@ -88,100 +101,104 @@ def cpu_baseline(W, store_pages, load_pages, prefix_tokens, refill_tokens):
             "ms_per_step": round(t * 1e3, 1)}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--plan", choices=["auto", "direct", "staged"], default="auto")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
-              "no exchange between ranks, and only single-GPU runs are part of this build "
-              "(use --gpus 1)", file=sys.stderr)
-        sys.exit(2)
+def committed_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when it is missing or was taken on another version of the kernels."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    vals, src = {}, None
+    for line in open(TRAFFIC_SUMMARY):
+        if line.startswith("kernel_source_sha256:"):
+            src = line.split(":", 1)[1].strip()
+        if line.startswith("traffic_bytes_per_launch:"):
+            for kv in line.split(":", 1)[1].split():
+                k, v = kv.split("=")
+                vals[k] = int(v)
+    if src != kernel_source_hash():
+        return None
+    return vals
 
+
+def setup(args):
     import torch
     from paper_2609_33762_amd import api, _native as N, workloads as W
-
     torch.cuda.set_device(0)
     sh = W.QWEN3
     dev = torch.device("cuda", 0)
-    t_setup = time.perf_counter()
+    t0 = time.perf_counter()
     kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device=dev)
     W.fill_bf16_normal(kv, W.SEED_DATA)
     cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
                       sh.head_dim, sh.elem_bytes)
     tier = api.Tier(cache, W.QWEN3_TIER_BYTES)
-    plan = {"auto": N.EA_PLAN_AUTO, "direct": N.EA_PLAN_DIRECT, "staged": N.EA_PLAN_STAGED}[args.plan]
-    tier.set_plan(N.EA_DIR_BOTH, plan)
-    page = tier.info["page_bytes"]
-    slot = tier.slot_bytes
-    log(f"setup: cache {sh.cache_bytes / 2**30:.2f} GiB, tier {tier.capacity} slots of {slot} B "
-        f"in {time.perf_counter() - t_setup:.1f} s")
-
-    # ---- pinned-copy peak of the host link (1 GiB contiguous, best of 10)
+    plan = {"auto": N.EA_PLAN_AUTO, "direct": N.EA_PLAN_DIRECT, "staged": N.EA_PLAN_STAGED}
+    tier.set_plan(N.EA_DIR_BOTH, plan[args.plan])
+    log(f"setup: cache {sh.cache_bytes / 2**30:.2f} GiB, tier {tier.capacity} slots of "
+        f"{tier.slot_bytes} B in {time.perf_counter() - t0:.1f} s")
+    ctx = dict(torch=torch, api=api, N=N, W=W, sh=sh, dev=dev, kv=kv, cache=cache, tier=tier,
+               page=tier.info["page_bytes"], slot=tier.slot_bytes,
+               n_load=W.QWEN3_LOAD_PAGES, n_store=W.QWEN3_STORE_PAGES, r=W.rng(W.SEED_WORKLOAD))
+    # pinned-copy peak of the host link (1 GiB contiguous, best of 10), taken
+    # while the tier is still empty
     probe = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
-    peak = {
-        "d2h": tier.peak_probe(probe, 1 << 30, N.EA_DIR_STORE, 10),
-        "h2d": tier.peak_probe(probe, 1 << 30, N.EA_DIR_LOAD, 10),
-        "bidir": tier.peak_probe(probe, 1 << 30, N.EA_DIR_BOTH, 10),
-    }
+    ctx["peak"] = {"d2h": tier.peak_probe(probe, 1 << 30, N.EA_DIR_STORE, 10),
+                   "h2d": tier.peak_probe(probe, 1 << 30, N.EA_DIR_LOAD, 10),
+                   "bidir": tier.peak_probe(probe, 1 << 30, N.EA_DIR_BOTH, 10)}
     del probe
-    log(f"pinned-copy peak GB/s: {peak}")
-
-    # ---- set-up of the turn: the cached prefix is already in the tier
-    r = W.rng(W.SEED_WORKLOAD)
-    n_load, n_store = W.QWEN3_LOAD_PAGES, W.QWEN3_STORE_PAGES
+    log(f"pinned-copy peak GB/s: { {k: round(v, 2) for k, v in ctx['peak'].items()} }")
+    # the cached prefix of the turn is already in the tier
     b = sh.page_tokens
-    prefix = W.tokens(W.SEED_TOKENS, n_load * b)
-    pkeys, _ = api.hash_blocks(prefix, np.array([0, len(prefix)]), b)
-    prefix_pages = W.distinct(r, sh.num_pages, n_load)
+    ctx["prefix"] = W.tokens(W.SEED_TOKENS, ctx["n_load"] * b)
+    pkeys, _ = api.hash_blocks(ctx["prefix"], np.array([0, len(ctx["prefix"])]), b)
+    prefix_pages = W.distinct(ctx["r"], sh.num_pages, ctx["n_load"])
     cnt, pslots = tier.alloc(pkeys)
-    assert cnt == n_load
+    assert cnt == ctx["n_load"]
     tier.store(cache, prefix_pages, pslots)
     tier.unpin(pslots)
     torch.cuda.synchronize()
-    policy = api.make_policy(kappa=256, block_tokens=b, beta_rank=sh.num_layers * sh.piece_bytes // b)
+    ctx["pslots"] = pslots
+    return ctx
 
-    steps_total = args.warmup + args.steps
-    refills = [W.tokens(W.SEED_TOKENS + 100 + k, n_store * b) for k in range(steps_total)]
+
+def run_steps(ctx, args):
+    torch, api, W, sh, tier, cache = (ctx[k] for k in ("torch", "api", "W", "sh", "tier", "cache"))
+    n_load, n_store, r, b = ctx["n_load"], ctx["n_store"], ctx["r"], sh.page_tokens
+    policy = api.make_policy(kappa=256, block_tokens=b,
+                             beta_rank=sh.num_layers * sh.piece_bytes // b)
+    total = args.warmup + args.steps
+    refills = [W.tokens(W.SEED_TOKENS + 100 + k, n_store * b) for k in range(total)]
     store_pages, load_dst = [], []
-    for k in range(steps_total):
+    for k in range(total):
         sp = W.distinct(r, sh.num_pages, n_store)
         store_pages.append(sp)
         load_dst.append(W.distinct(r, sh.num_pages, n_load, exclude=sp))
-    seqs = [np.concatenate([prefix, refills[k]]) for k in range(steps_total)]
-    offs = np.array([0, len(prefix), len(prefix) + n_store * b], np.int64)
+    seqs = [np.concatenate([ctx["prefix"], refills[k]]) for k in range(total)]
+    offs = np.array([0, n_load * b, (n_load + n_store) * b], np.int64)
     s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
-    ev = {k: [] for k in ("store0", "store1", "load0", "load1")}
+    ev = {k: [] for k in ("s0", "s1", "l0", "l1")}
 
     def step(k, timed):
-        keys, koffs = api.hash_blocks(seqs[k], offs, b)
+        keys, _ = api.hash_blocks(seqs[k], offs, b)
         h, hslots = tier.lookup(keys[:n_load])
         assert h == n_load, h
         if timed:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(s_load)
+            ev["l0"].append(torch.cuda.Event(enable_timing=True))
+            ev["l0"][-1].record(s_load)
         tier.load(cache, hslots, load_dst[k], stream=s_load)
         if timed:
-            e1.record(s_load)
-            ev["load0"].append(e0)
-            ev["load1"].append(e1)
+            ev["l1"].append(torch.cuda.Event(enable_timing=True))
+            ev["l1"][-1].record(s_load)
         rkeys = keys[n_load:]
-        save, mask = tier.admission(policy, len(refills[k]), 0, 1, k, rkeys)
-        cnt, slots = tier.alloc(rkeys, mask)
+        _, mask = tier.admission(policy, len(refills[k]), 0, 1, k, rkeys)
+        _, slots = tier.alloc(rkeys, mask)
         ok = slots >= 0
         if timed:
-            e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e2.record(s_store)
+            ev["s0"].append(torch.cuda.Event(enable_timing=True))
+            ev["s0"][-1].record(s_store)
         tier.store(cache, store_pages[k][ok], slots[ok], stream=s_store)
         if timed:
-            e3.record(s_store)
-            ev["store0"].append(e2)
-            ev["store1"].append(e3)
+            ev["s1"].append(torch.cuda.Event(enable_timing=True))
+            ev["s1"][-1].record(s_store)
         tier.unpin(slots[ok])
         tier.unpin(hslots)
         return int(ok.sum())
@@ -191,96 +208,254 @@ def main():
     torch.cuda.synchronize()
     stored = 0
     t0 = time.perf_counter()
-    for k in range(args.warmup, steps_total):
+    for k in range(args.warmup, total):
         stored += step(k, True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ms = elapsed / args.steps * 1e3
-    moved = (stored + args.steps * n_load) * page
-    value = moved / elapsed / GB
-    st = tier.stats()
-    store_ms = float(np.mean([a.elapsed_time(b_) for a, b_ in zip(ev["store0"], ev["store1"])]))
-    load_ms = float(np.mean([a.elapsed_time(b_) for a, b_ in zip(ev["load0"], ev["load1"])]))
-    log(f"step {ms:.2f} ms, {value:.1f} GB/s over the link; store {store_ms:.2f} ms, "
-        f"load {load_ms:.2f} ms (in-step, overlapped); evictions {st['evictions_total']}")
+    res = {"ms": elapsed / args.steps * 1e3,
+           "gbs": (stored + args.steps * n_load) * ctx["page"] / elapsed / GB,
+           "store_ms": float(np.mean([a.elapsed_time(c) for a, c in zip(ev["s0"], ev["s1"])])),
+           "load_ms": float(np.mean([a.elapsed_time(c) for a, c in zip(ev["l0"], ev["l1"])])),
+           "tier": tier.stats()}
+    ctx["last_store_pages"], ctx["last_load_dst"], ctx["last_refill"] = (
+        store_pages[-1], load_dst[-1], refills[-1])
+    log(f"step {res['ms']:.2f} ms, {res['gbs']:.1f} GB/s over the link; in-step store "
+        f"{res['store_ms']:.2f} ms, load {res['load_ms']:.2f} ms; evictions "
+        f"{res['tier']['evictions_total']}")
+    return res
 
-    # ---- each direction alone, and the HBM gather/scatter kernels isolated
-    torch.cuda.synchronize()
-    sp = store_pages[-1]
-    # raw stores to random slots: the step loop is over, tier contents no
-    # longer matter
-    iso_slots = W.distinct(r, tier.capacity, n_store)
+
+def isolated(ctx):
+    """Each direction alone (2,000 pages stored to the consecutive slots a
+    fresh allocation hands out, the 1,500-page prefix loaded from its slots),
+    the same with random slots, and the HBM gather/scatter kernels; ends with
+    a plain 1 GiB device copy that calibrates the HBM byte counters."""
+    torch, W, sh, tier, cache, dev = (ctx[k] for k in ("torch", "W", "sh", "tier", "cache", "dev"))
+    n_store, n_load, page, slot, r = ctx["n_store"], ctx["n_load"], ctx["page"], ctx["slot"], ctx["r"]
+    sp = ctx.get("last_store_pages")
+    if sp is None:
+        sp = W.distinct(r, sh.num_pages, n_store)
+    dst = ctx.get("last_load_dst")
+    if dst is None:
+        dst = W.distinct(r, sh.num_pages, n_load, exclude=sp)
     cur = torch.cuda.current_stream()
-    st_ms = event_ms(torch, lambda: tier.store(cache, sp, iso_slots, stream=cur), cur, 5)
-    ld_ms = event_ms(torch, lambda: tier.load(cache, iso_slots[:n_load], load_dst[-1], stream=cur),
-                     cur, 5)
+    torch.cuda.synchronize()
+    # raw stores: from here on the tier's contents no longer matter
+    # random slots first, so that the last launches of each kernel are the
+    # consecutive-slot ones the profile summaries pick out
+    out = {}
+    rnd = W.distinct(r, tier.capacity, n_store)
+    out["store_rnd_ms"] = event_ms(torch, lambda: tier.store(cache, sp, rnd, stream=cur), cur, 3)
+    out["load_rnd_ms"] = event_ms(torch, lambda: tier.load(cache, rnd[:n_load], dst, stream=cur),
+                                  cur, 3)
+    slots = np.arange(n_store, dtype=np.int64)
+    out["store_ms"] = event_ms(torch, lambda: tier.store(cache, sp, slots, stream=cur), cur,
+                               N_ISO["store"])
+    out["load_ms"] = event_ms(torch, lambda: tier.load(cache, ctx["pslots"], dst, stream=cur), cur,
+                              N_ISO["load"])
     staging = torch.empty(n_store * slot, dtype=torch.uint8, device=dev)
-    g_ms = event_ms(torch, lambda: cache.gather(sp, staging, stream=cur), cur, 10)
-    s_ms = event_ms(torch, lambda: cache.scatter(staging, sp, stream=cur), cur, 10)
-    del staging
-    store_gbs = n_store * page / (st_ms * 1e-3) / GB
-    load_gbs = n_load * page / (ld_ms * 1e-3) / GB
-    gather_gbs = 2 * n_store * page / (g_ms * 1e-3) / GB
-    scatter_gbs = 2 * n_store * page / (s_ms * 1e-3) / GB
-    log(f"alone: store {store_gbs:.1f} GB/s ({store_gbs / peak['d2h']:.1%} of pinned D2H), "
-        f"load {load_gbs:.1f} GB/s ({load_gbs / peak['h2d']:.1%} of pinned H2D); "
-        f"HBM gather {gather_gbs:.0f} GB/s, scatter {scatter_gbs:.0f} GB/s")
+    out["gather_ms"] = event_ms(torch, lambda: cache.gather(sp, staging, stream=cur), cur,
+                                N_ISO["gather"])
+    out["scatter_ms"] = event_ms(torch, lambda: cache.scatter(staging, sp, stream=cur), cur,
+                                 N_ISO["scatter"])
+    calib = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    calib.copy_(staging[: 1 << 30])
+    torch.cuda.synchronize()
+    del staging, calib
+    out["store_gbs"] = n_store * page / (out["store_ms"] * 1e-3) / GB
+    out["load_gbs"] = n_load * page / (out["load_ms"] * 1e-3) / GB
+    out["store_rnd_gbs"] = n_store * page / (out["store_rnd_ms"] * 1e-3) / GB
+    out["load_rnd_gbs"] = n_load * page / (out["load_rnd_ms"] * 1e-3) / GB
+    out["gather_gbs"] = 2 * n_store * slot / (out["gather_ms"] * 1e-3) / GB
+    out["scatter_gbs"] = 2 * n_store * slot / (out["scatter_ms"] * 1e-3) / GB
+    pk = ctx["peak"]
+    log(f"alone: store {out['store_gbs']:.1f} GB/s ({out['store_gbs'] / pk['d2h']:.1%} of pinned "
+        f"D2H), load {out['load_gbs']:.1f} GB/s ({out['load_gbs'] / pk['h2d']:.1%} of pinned H2D); "
+        f"random slots {out['store_rnd_gbs']:.1f} / {out['load_rnd_gbs']:.1f}; HBM gather "
+        f"{out['gather_gbs']:.0f} GB/s, scatter {out['scatter_gbs']:.0f} GB/s")
+    return out
 
-    plan_store = tier.get_plan(N.EA_DIR_STORE)
-    plan_load = tier.get_plan(N.EA_DIR_LOAD)
+
+# ------------------------------------------------------------ profiles
+
+def _short(name):
+    for key, short in (("copy_host_link<0", "store"), ("copy_host_link<1", "load"),
+                       ("copy_hbm<0", "gather"), ("copy_hbm<1", "scatter"),
+                       ("sha256_chain", "sha256_chain"), ("sha256_midstates", "sha256_midstates"),
+                       ("copyBuffer", "rocclr_copyBuffer")):
+        if key in name:
+            return short
+    return None
+
+
+def summarize_profiles(d):
+    """Write the committed rocprofv3 summaries from the CSVs of the three
+    --isolated-only runs under directory d."""
+    cmd_trace = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_trace "
+                 "-o trace -- python3 bench.py --isolated-only --detail "
+                 "gpurun_out/bench_detail_trace.json")
+    cmd_pmc = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{l} -o {l} -- python3 "
+               "bench.py --isolated-only --detail gpurun_out/bench_detail_{l}.json")
+    detail = json.load(open(os.path.join(d, "bench_detail_trace.json")))["isolated"]
+    rows = list(csv.DictReader(open(os.path.join(d, "prof_trace", "trace_kernel_trace.csv"))))
+    disp = {}
+    for x in rows:
+        s = _short(x["Kernel_Name"])
+        if s:
+            disp.setdefault(s, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e6)
+    # the isolated phase: the last N_ISO launches of each copy kernel
+    n_store, n_load, page, slot = 2000, 1500, 1572864, 1572864
+    alg = {"store": n_store * page, "load": n_load * page,
+           "gather": 2 * n_store * slot, "scatter": 2 * n_store * slot}
+    lines = ["# Kernel durations: piece copies, Qwen3-30B-A3B turn (2,000 stored / 1,500 loaded "
+             "pages of 1.5 MiB)", "",
+             "Command (from the repository root on the MI355X):", "", f"    {cmd_trace}",
+             "    python3 bench.py --summarize-profiles gpurun_out", "",
+             f"kernel_source_sha256: {kernel_source_hash()}", "",
+             "| kernel | launches | rocprof avg ms | HIP-event avg ms (same run) | algorithmic "
+             "GB/s (rocprof) |", "|---|---|---|---|---|"]
+    ev_key = {"store": "store_ms", "load": "load_ms", "gather": "gather_ms", "scatter": "scatter_ms"}
+    for k in ("store", "load", "gather", "scatter"):
+        ds = disp.get(k, [])[-N_ISO[k]:]
+        avg = float(np.mean(ds)) if ds else float("nan")
+        lines.append(f"| {k} | {len(ds)} | {avg:.4f} | {detail[ev_key[k]]:.4f} | "
+                     f"{alg[k] / (avg * 1e-3) / GB:.1f} |")
+    for k in ("sha256_midstates", "sha256_chain"):
+        ds = disp.get(k, [])
+        if ds:
+            lines.append(f"| {k} | {len(ds)} | {np.mean(ds):.4f} | - | - |")
+    open(TRACE_SUMMARY, "w").write("\n".join(lines) + "\n")
+
+    counters = {}
+    for label, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        rows = list(csv.DictReader(open(os.path.join(d, f"prof_{label}",
+                                                     f"{label}_counter_collection.csv"))))
+        per = {}
+        for x in rows:
+            s = _short(x["Kernel_Name"])
+            if s and x["Counter_Name"] == ctr:
+                per.setdefault(s, []).append(float(x["Counter_Value"]))
+        counters[ctr] = per
+    # calibration: the last rocclr copy is the plain 1 GiB device copy
+    cal_f = counters["FETCH_SIZE"]["rocclr_copyBuffer"][-1]
+    cal_w = counters["WRITE_SIZE"]["rocclr_copyBuffer"][-1]
+    kib = (1 << 30) / 1024
+    f_fac, w_fac = kib / cal_f, kib / cal_w
+    traffic = {}
+    lines = ["# HBM bytes per launch: piece copies, Qwen3-30B-A3B turn", "",
+             "Commands (from the repository root on the MI355X):", "",
+             "    " + cmd_pmc.format(c="FETCH_SIZE", l="fetch"),
+             "    " + cmd_pmc.format(c="WRITE_SIZE", l="write"),
+             "    python3 bench.py --summarize-profiles gpurun_out", "",
+             f"kernel_source_sha256: {kernel_source_hash()}", "",
+             f"Calibration: a plain 1 GiB device copy (rocclr copyBuffer) reads FETCH_SIZE "
+             f"{cal_f:.0f} KiB and WRITE_SIZE {cal_w:.0f} KiB for 1,048,576 KiB each way, so "
+             f"FETCH_SIZE is scaled by {f_fac:.3f} and WRITE_SIZE by {w_fac:.3f}.  Reads and "
+             "writes of the mapped pinned host slots count in the same counters.", "",
+             "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes | algorithmic bytes | "
+             "ratio |", "|---|---|---|---|---|---|"]
+    for k in ("store", "load", "gather", "scatter"):
+        fv = counters["FETCH_SIZE"].get(k, [])[-N_ISO[k]:]
+        wv = counters["WRITE_SIZE"].get(k, [])[-N_ISO[k]:]
+        if not fv or not wv:
+            continue
+        fk, wk = float(np.mean(fv)), float(np.mean(wv))
+        tb = int((fk * f_fac + wk * w_fac) * 1024)
+        a2 = 2 * alg[k] if k in ("store", "load") else alg[k]
+        traffic[k] = tb
+        lines.append(f"| {k} | {fk:.0f} | {wk:.0f} | {tb} | {a2} | {tb / a2:.4f} |")
+    lines += ["", "Algorithmic bytes count each moved byte once read and once written.", "",
+              "traffic_bytes_per_launch: " + " ".join(f"{k}={v}" for k, v in traffic.items())]
+    open(TRAFFIC_SUMMARY, "w").write("\n".join(lines) + "\n")
+    print(open(TRACE_SUMMARY).read())
+    print(open(TRAFFIC_SUMMARY).read())
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--plan", choices=["auto", "direct", "staged"], default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--isolated-only", action="store_true")
+    ap.add_argument("--summarize-profiles", metavar="DIR")
+    ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
+    args = ap.parse_args()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
+              "no exchange between ranks, and only single-GPU runs are part of this build "
+              "(use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    ctx = setup(args)
+    N = ctx["N"]
+    os.makedirs(os.path.dirname(args.detail), exist_ok=True)
+    if args.isolated_only:
+        iso = isolated(ctx)
+        json.dump({"isolated": iso, "peak": ctx["peak"]}, open(args.detail, "w"), indent=1)
+        ctx["tier"].close()
+        ctx["cache"].close()
+        return
+
+    steps = run_steps(ctx, args)
+    iso = isolated(ctx)
+    tier = ctx["tier"]
     plan_name = {N.EA_PLAN_DIRECT: "direct", N.EA_PLAN_STAGED: "staged"}
-    detail = {
-        "peak_gbs": peak, "step_ms": ms, "link_gbs": value,
-        "store_alone": {"ms": st_ms, "gbs": store_gbs, "frac_of_pinned_d2h": store_gbs / peak["d2h"]},
-        "load_alone": {"ms": ld_ms, "gbs": load_gbs, "frac_of_pinned_h2d": load_gbs / peak["h2d"]},
-        "in_step": {"store_ms": store_ms, "load_ms": load_ms},
-        "gather": {"ms": g_ms, "gbs": gather_gbs, "frac_of_hbm": gather_gbs / HBM_PEAK_GBS},
-        "scatter": {"ms": s_ms, "gbs": scatter_gbs, "frac_of_hbm": scatter_gbs / HBM_PEAK_GBS},
-        "plans": {"store": plan_name[plan_store], "load": plan_name[plan_load]},
-        "tier": st, "us_per_token_load": ld_ms * 1e3 / (n_load * b),
-    }
-
+    plans = {"store": plan_name[tier.get_plan(N.EA_DIR_STORE)],
+             "load": plan_name[tier.get_plan(N.EA_DIR_LOAD)]}
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle, one core) ...")
-        cpu = cpu_baseline(W, store_pages[-1], load_dst[-1], prefix, refills[-1])
+        cpu = cpu_baseline(ctx["W"], ctx["n_store"], ctx["n_load"], ctx["prefix"],
+                           ctx["last_refill"])
         log(f"cpu baseline: {cpu}")
     tier.close()
-    cache.close()
+    ctx["cache"].close()
 
-    # dominant kernel of the step: the store (2,000 pages) on the host link
+    peak = ctx["peak"]
+    traffic = committed_traffic() or {}
+    # the dominant kernel of the step is the store (2,000 pages over the link)
     roofline = {
-        "bound": "host-link", "kernel": f"store ({plan_name[plan_store]})",
-        "achieved": round(store_gbs, 2), "peak": round(peak["d2h"], 2),
-        "peak_kind": "measured pinned hipMemcpyAsync D2H, 1 GiB, best of 10",
-        "unit": "GB/s", "frac": round(store_gbs / peak["d2h"], 4), "traffic": None,
+        "bound": "host-link", "kernel": f"copy_host_link<store> ({plans['store']} plan, "
+                                        f"2,000 pages)",
+        "achieved": round(iso["store_gbs"], 2), "peak": round(peak["d2h"], 2),
+        "peak_kind": "measured pinned hipMemcpyAsync device-to-host, 1 GiB, best of 10",
+        "unit": "GB/s", "frac": round(iso["store_gbs"] / peak["d2h"], 4),
+        "traffic": traffic.get("store"),
     }
     roofline_hbm = {
-        "bound": "hbm", "kernel": "gather_blocks (paged gather, 2,000 pages)",
-        "achieved": round(gather_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(gather_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-        "scatter": {"achieved": round(scatter_gbs, 1), "frac": round(scatter_gbs / HBM_PEAK_GBS, 4)},
+        "bound": "hbm", "kernel": "copy_hbm<gather> (paged gather of 2,000 pages to HBM)",
+        "achieved": round(iso["gather_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(iso["gather_gbs"] / HBM_PEAK_GBS, 4), "traffic": traffic.get("gather"),
+        "scatter": {"achieved": round(iso["scatter_gbs"], 1),
+                    "frac": round(iso["scatter_gbs"] / HBM_PEAK_GBS, 4),
+                    "traffic": traffic.get("scatter")},
     }
     out = {
         "metric": "host-link GB/s for KV block store/load; HBM GB/s of paged gather/scatter",
-        "value": round(value, 3), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "value": round(steps["gbs"], 3), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(steps["ms"], 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
         "config": {"workload": "qwen3_30b_a3b_turn: store 2,000 + load 1,500 pages of 1.5 MiB, "
                                "hash 56,000 tokens, 20,000-page cache, 16 GiB tier",
-                   "page_bytes": page, "store_pages": n_store, "load_pages": n_load,
-                   "plans": detail["plans"]},
+                   "page_bytes": ctx["page"], "store_pages": ctx["n_store"],
+                   "load_pages": ctx["n_load"], "plans": plans},
         "roofline": roofline, "roofline_hbm": roofline_hbm,
-        "host_link": {"store_gbs": round(store_gbs, 2), "load_gbs": round(load_gbs, 2),
+        "host_link": {"store_gbs": round(iso["store_gbs"], 2), "load_gbs": round(iso["load_gbs"], 2),
                       "peak_d2h": round(peak["d2h"], 2), "peak_h2d": round(peak["h2d"], 2),
                       "peak_bidir": round(peak["bidir"], 2),
-                      "frac_store": round(store_gbs / peak["d2h"], 4),
-                      "frac_load": round(load_gbs / peak["h2d"], 4)},
+                      "frac_store": round(iso["store_gbs"] / peak["d2h"], 4),
+                      "frac_load": round(iso["load_gbs"] / peak["h2d"], 4),
+                      "duplex_step_gbs": round(steps["gbs"], 2),
+                      "frac_duplex_of_bidir": round(steps["gbs"] / peak["bidir"], 4)},
         "cpu_baseline": cpu,
     }
-    os.makedirs(os.path.dirname(args.detail), exist_ok=True)
-    with open(args.detail, "w") as f:
-        json.dump({"line": out, "detail": detail}, f, indent=1, default=float)
+    json.dump({"line": out, "steps": steps, "isolated": iso, "peak": peak}, open(args.detail, "w"),
+              indent=1, default=float)
     print(json.dumps(out), flush=True)
 
 

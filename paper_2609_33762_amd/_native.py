@@ -10,7 +10,8 @@ import ctypes as C
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libea.so")
+# EA_LIB_PATH selects another build of the same library (e.g. for A/B timing)
+LIB_PATH = os.environ.get("EA_LIB_PATH") or os.path.join(_PKG, "libea.so")
 
 EA_OK, EA_EINVAL, EA_ENOMEM, EA_ENOSPC, EA_EHIP, EA_ENOTSUP = 0, -1, -2, -3, -4, -5
 EA_ADMIT_CONDITIONED, EA_ADMIT_ALWAYS, EA_ADMIT_FIXED = 0, 1, 2

@@ -29,6 +29,10 @@ struct PieceCopy {
   int32_t layer_begin;
   int32_t layer_count;
   int32_t identity_slots;    // slot index of entry i is i (staging buffers)
+  // Workgroups are dispatched round-robin over the XCDs (workgroup b runs on
+  // XCD b % num_xcd); only workgroups on XCDs in xcd_mask do work.
+  int32_t num_xcd;
+  uint32_t xcd_mask;
 };
 
 struct InlineIdx {
@@ -39,9 +43,13 @@ struct InlineIdx {
 // Remember the HIP error behind an EA_EHIP return on this thread.
 void set_last_hip(int err);
 
-// Launch one piece-copy kernel.  grid_cap bounds the workgroups (0 = auto).
-hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir,
-                             int grid_cap, hipStream_t stream);
+// Which memory the slot-layout buffer of a piece copy lives in.
+enum Route : int { kRouteHostLink = 0, kRouteHbm = 1 };
+
+// Launch one piece-copy kernel with at most `workgroups` (> 0) working
+// workgroups, placed on the XCDs of a.xcd_mask.
+hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
+                             int64_t workgroups, hipStream_t stream);
 
 // SHA-256 chained keys.
 //  mid:  device [n_keys][8] words scratch
