@@ -1,0 +1,204 @@
+"""Workload drivers over the C ABI: the agent pool, dense scattered batches
+and the layer-pipelined prefix load.  Each driver only issues library calls
+(hash, lookup, admission, alloc, store, load, unpin) and records what it did,
+so that the tests can replay every call on the oracle and the benchmark can
+time them.  Page contents of the agent pool are a counter-based function of
+the block's key (`key_pattern`), so any loaded page can be checked against
+its key.
+"""
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import api
+from . import workloads as W
+
+
+# ------------------------------------------------------------ key pattern
+
+_M32 = 0xFFFFFFFF
+
+
+def key_pattern(torch, keys, words, device):
+    """int32 [len(keys), words] page contents for blocks with these keys:
+    word j of a block whose key starts with the little-endian uint32 s is
+    fmix32(s + 0x9E3779B1 * j mod 2^32) (MurmurHash3's finaliser)."""
+    seeds = torch.as_tensor(np.ascontiguousarray(keys[:, :4]).view(np.uint32).astype(np.int64)
+                            .reshape(-1, 1), device=device)
+    j = torch.arange(words, dtype=torch.int64, device=device).reshape(1, -1)
+    x = (seeds + j * 0x9E3779B1) & _M32
+    x = x ^ (x >> 16)
+    x = (x * 0x85EBCA6B) & _M32
+    x = x ^ (x >> 13)
+    x = (x * 0xC2B2AE35) & _M32
+    x = x ^ (x >> 16)
+    return (x - ((x >> 31) << 32)).to(torch.int32)  # two's complement view
+
+
+def write_pages(torch, kv3, pages, content):
+    """kv3: uint8 view [L, P, piece]; content int32 [n, L*piece/4]."""
+    L, _, piece = kv3.shape
+    c = content.view(torch.uint8).view(len(pages), L, piece).permute(1, 0, 2)
+    kv3[:, torch.as_tensor(pages, device=kv3.device, dtype=torch.int64)] = c
+
+
+def read_pages(torch, kv3, pages):
+    L, _, piece = kv3.shape
+    idx = torch.as_tensor(pages, device=kv3.device, dtype=torch.int64)
+    return kv3[:, idx].permute(1, 0, 2).reshape(len(pages), L * piece)
+
+
+# ------------------------------------------------------------ agent pool
+
+@dataclass
+class TurnRecord:
+    turn: int
+    agent: int
+    n_tokens: int
+    keys: np.ndarray
+    hit: int
+    hit_slots: np.ndarray
+    save: int
+    mask: np.ndarray
+    alloc_slots: np.ndarray
+    stored: int
+    loaded_ok: bool
+    load_pages: np.ndarray = field(default=None)
+    store_pages: np.ndarray = field(default=None)
+
+
+class AgentPool:
+    """Agents served round-robin; each turn is one request of one agent.
+
+    A prompt keeps the first floor(0.98 * len) tokens of the agent's previous
+    prompt, then fresh tokens up to len' = min(len + U[500, 3000], 65536); an
+    agent at 65,536 tokens starts a new task at 8,192.  A turn hashes only
+    the blocks after the last unchanged full block (from the cached parent
+    key), looks up the prompt's keys, loads the hit prefix into free GPU
+    pages, writes the remaining blocks' KV (a function of their keys) into
+    other free pages, decides admission, allocates slots, stores the admitted
+    blocks and releases the pins.  GPU pages are free again after each turn."""
+
+    def __init__(self, torch, cache, tier, kv, shape, policy, agents=W.POOL_AGENTS,
+                 seed=W.SEED_WORKLOAD, verify=True, stream=None):
+        self.torch, self.cache, self.tier, self.kv = torch, cache, tier, kv
+        self.sh, self.policy, self.verify = shape, policy, verify
+        self.kv3 = kv.view(shape.num_layers, shape.num_pages, shape.piece_bytes)
+        self.words = shape.num_layers * shape.piece_bytes // 4
+        self.b = shape.page_tokens
+        self.agents = agents
+        self.r = W.rng(seed)
+        self.tok_rng = [W.rng(seed * 1000 + a) for a in range(agents)]
+        self.prompts = [None] * agents
+        self.keys = [np.zeros((0, 32), np.uint8)] * agents
+        self.turn_no = 0
+        self.stream = stream
+        self.bytes_loaded = 0
+        self.bytes_stored = 0
+
+    def _next_prompt(self, a):
+        rng = self.tok_rng[a]
+        prev = self.prompts[a]
+        if prev is None or len(prev) >= W.POOL_MAX_TOKENS:
+            n = W.POOL_START_TOKENS
+            p = rng.integers(0, W.VOCAB, size=n, dtype=np.int64).astype(np.int32)
+            keep = 0
+        else:
+            n = min(len(prev) + int(rng.integers(W.POOL_GROWTH[0], W.POOL_GROWTH[1] + 1)),
+                    W.POOL_MAX_TOKENS)
+            keep = int(np.floor(W.POOL_KEEP * len(prev)))
+            fresh = rng.integers(0, W.VOCAB, size=n - keep, dtype=np.int64).astype(np.int32)
+            p = np.concatenate([prev[:keep], fresh])
+        return p, keep
+
+    def turn(self):
+        torch, tier, cache, b = self.torch, self.tier, self.cache, self.b
+        a = self.turn_no % self.agents
+        t = self.turn_no
+        prompt, keep = self._next_prompt(a)
+        n_full = len(prompt) // b
+        # incremental hash: blocks before the first changed token keep their keys
+        j0 = min(keep // b, len(self.keys[a]), n_full)
+        parent = self.keys[a][j0 - 1].reshape(1, 32) if j0 > 0 else None
+        tail = prompt[j0 * b:]
+        new_keys, _ = api.hash_blocks(tail, np.array([0, len(tail)]), b, parent)
+        keys = np.concatenate([self.keys[a][:j0], new_keys])[:n_full]
+        self.prompts[a], self.keys[a] = prompt, keys
+
+        h, hit_slots = tier.lookup(keys)
+        pages = W.distinct(self.r, self.sh.num_pages, n_full)
+        load_pages, fill_pages = pages[:h], pages[h:]
+        if h:
+            tier.load(cache, hit_slots, load_pages, stream=self.stream)
+            self.bytes_loaded += h * tier.slot_bytes
+        if n_full > h:  # compute (here: synthesise) the KV the tier did not have
+            for c0 in range(h, n_full, 512):
+                c1 = min(n_full, c0 + 512)
+                write_pages(torch, self.kv3, pages[c0:c1],
+                            key_pattern(torch, keys[c0:c1], self.words, self.kv.device))
+        save, mask = tier.admission(self.policy, len(prompt), h * b, a, t, keys)
+        _, slots = tier.alloc(keys, mask)
+        ok = slots >= 0
+        if ok.any():
+            tier.store(cache, pages[ok], slots[ok], stream=self.stream)
+            self.bytes_stored += int(ok.sum()) * tier.slot_bytes
+        loaded_ok = True
+        if self.verify and h:
+            torch.cuda.synchronize()
+            for c0 in range(0, h, 512):
+                c1 = min(h, c0 + 512)
+                want = key_pattern(torch, keys[c0:c1], self.words, self.kv.device)
+                got = read_pages(torch, self.kv3, load_pages[c0:c1]).view(torch.int32)
+                loaded_ok &= bool(torch.equal(got, want))
+        if ok.any():
+            tier.unpin(slots[ok])
+        if h:
+            tier.unpin(hit_slots)
+        self.turn_no += 1
+        return TurnRecord(t, a, len(prompt), keys, h, hit_slots, save, mask, slots,
+                          int(ok.sum()), loaded_ok, load_pages, pages[ok])
+
+
+# ------------------------------------------------- dense scattered batches
+
+def non_adjacent_pages(r, num_pages, k):
+    """k distinct page ids, no two adjacent."""
+    while True:
+        p = np.sort(r.choice(num_pages, size=k, replace=False))
+        if k < 2 or np.all(np.diff(p) > 1):
+            return r.permutation(p)
+
+
+class DenseScattered:
+    """Alternating store and load calls of 1-8 random non-adjacent pages; a
+    load reads slots that an earlier store wrote.  Stores allocate slots
+    through the tier under fresh random keys (the tier evicts by LRU once
+    full); loads pick random resident slots."""
+
+    def __init__(self, cache, tier, shape, seed=W.SEED_WORKLOAD, stream=None):
+        self.cache, self.tier, self.sh = cache, tier, shape
+        self.r = W.rng(seed)
+        self.stream = stream
+        self.calls = []
+
+    def call(self, i):
+        r, sh = self.r, self.sh
+        k = int(r.integers(1, 9))
+        if i % 2 == 0:
+            pages = non_adjacent_pages(r, sh.num_pages, k)
+            keys = r.integers(0, 256, size=(k, 32), dtype=np.uint8)
+            _, slots = self.tier.alloc(keys)
+            ok = slots >= 0
+            self.tier.store(self.cache, pages[ok], slots[ok], stream=self.stream)
+            self.tier.unpin(slots[ok])
+            rec = ("store", pages[ok], slots[ok])
+        else:
+            state = self.tier.export()["state"]
+            resident = np.nonzero(state == 2)[0]
+            k = min(k, len(resident))
+            slots = r.choice(resident, size=k, replace=False)
+            pages = non_adjacent_pages(r, sh.num_pages, k)
+            self.tier.load(self.cache, slots, pages, stream=self.stream)
+            rec = ("load", pages, slots)
+        self.calls.append(rec)
+        return rec

@@ -1,0 +1,251 @@
+"""GPU parity at the workloads' full sizes.
+
+* One Qwen3-30B-A3B turn (20,000-page cache, 16 GiB tier, 2,000 pages stored,
+  1,500 loaded), both transfer plans: round-trip identity on every page,
+  sampled pages and slots against the oracle one by one, sampled untouched
+  pages and slots.
+* Layer-pipelined fp8 prefix load (64k tokens = 4,096 pages, 48 layers,
+  per-page scales): a consumer stream snapshots each layer right after its
+  event; every snapshot and the end state match the source pages, sampled
+  entries match the oracle's per-layer load.
+* Dense scattered batches (4,096-page cache, 4,096-slot tier, 10,000 calls of
+  1-8 non-adjacent pages): the oracle replays every call on full host images
+  and the final cache and tier images must be equal byte for byte.
+* Agent pool (64 agents, 64 GiB tier, 6 turns each): every turn's lookup,
+  admission, allocation and the tier's full metadata are compared with the
+  oracle, and every loaded page is checked against its key's pattern.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_33762_amd import api, drivers, _native as N, workloads as W
+
+from gpu_common import need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def release(torch):
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def oshape_of(sh, num_pages=None):
+    return oracle.make_shape(num_pages or sh.num_pages, sh.num_layers, sh.page_tokens,
+                             sh.num_kv_heads, sh.head_dim, sh.elem_bytes, sh.has_scales)
+
+
+@pytest.mark.parametrize("plan", ["direct", "staged"])
+def test_qwen3_turn_full_size(plan):
+    torch = need_gpu()
+    sh = W.QWEN3
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    kv3 = kv.view(L, P, piece)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.QWEN3_TIER_BYTES)
+    tier.set_plan(N.EA_DIR_BOTH, N.EA_PLAN_DIRECT if plan == "direct" else N.EA_PLAN_STAGED)
+    r = W.rng(W.SEED_IDS)
+    n_l, n_s = W.QWEN3_LOAD_PAGES, W.QWEN3_STORE_PAGES
+    prefix_pages = W.distinct(r, P, n_l)
+    store_pages = W.distinct(r, P, n_s, exclude=prefix_pages)
+    dst = W.distinct(r, P, n_l, exclude=np.concatenate([prefix_pages, store_pages]))
+    host = tier.host_view()
+    # poison a sample of slots that nothing writes, and snapshot sampled pages
+    never = W.distinct(r, tier.capacity, 64, exclude=np.arange(n_l + n_s))
+    host[never] = 0xC3
+    keep_pages = W.distinct(r, P, 64, exclude=dst)
+    keep_before = drivers.read_pages(torch, kv3, keep_pages).cpu().numpy()
+
+    toks = W.tokens(W.SEED_TOKENS, n_l * sh.page_tokens)
+    pkeys, _ = api.hash_blocks(toks, np.array([0, len(toks)]), sh.page_tokens)
+    cnt, pslots = tier.alloc(pkeys)
+    assert cnt == n_l and list(pslots) == list(range(n_l))
+    tier.store(cache, prefix_pages, pslots)
+    tier.unpin(pslots)
+    rkeys = W.rng(7).integers(0, 256, size=(n_s, 32), dtype=np.uint8)
+    cnt, sslots = tier.alloc(rkeys)
+    assert cnt == n_s
+    s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
+    h, hslots = tier.lookup(pkeys)
+    assert h == n_l
+    tier.load(cache, hslots, dst, stream=s_load)
+    tier.store(cache, store_pages, sslots, stream=s_store)
+    torch.cuda.synchronize()
+    tier.unpin(sslots)
+    tier.unpin(hslots)
+
+    # round trip on every page: destination pages hold the prefix pages
+    assert torch.equal(kv3[:, torch.as_tensor(dst, device="cuda")],
+                       kv3[:, torch.as_tensor(prefix_pages, device="cuda")])
+    # sampled entries against the oracle, one by one
+    sample = W.distinct(r, n_s, 48)
+    o = oshape_of(sh, num_pages=len(sample))
+    mini = drivers.read_pages(torch, kv3, store_pages[sample]).cpu().numpy()
+    mini_cache = np.ascontiguousarray(mini.reshape(len(sample), L, piece).transpose(1, 0, 2))
+    want = np.zeros((len(sample), tier.slot_bytes), np.uint8)
+    oracle.store_blocks(o, mini_cache.reshape(-1), None, want, np.arange(len(sample)),
+                        np.arange(len(sample)))
+    assert np.array_equal(host[sslots[sample]], want)
+    lsample = W.distinct(r, n_l, 48)
+    lo = np.zeros((L, len(lsample), piece), np.uint8)
+    oracle.load_blocks(o, host[pslots[lsample]].copy(), lo.reshape(-1), None,
+                       np.arange(len(lsample)), np.arange(len(lsample)))
+    got = drivers.read_pages(torch, kv3, dst[lsample]).cpu().numpy()
+    assert np.array_equal(got, lo.transpose(1, 0, 2).reshape(len(lsample), -1))
+    # untouched pages and slots
+    assert np.array_equal(drivers.read_pages(torch, kv3, keep_pages).cpu().numpy(), keep_before)
+    assert (host[never] == 0xC3).all()
+    tier.close()
+    cache.close()
+    del kv, kv3
+    release(torch)
+
+
+def test_layered_fp8_prefix_full_size():
+    torch = need_gpu()
+    sh = W.LAYERED
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_random_bytes(kv, W.SEED_DATA)
+    sc = torch.empty(L * P * 8, dtype=torch.uint8, device="cuda")
+    W.fill_random_bytes(sc, W.SEED_DATA + 1)
+    kv3, sc3 = kv.view(L, P, piece), sc.view(L, P, 8)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes,
+                      scales=sc)
+    n = W.LAYERED_PREFIX_PAGES
+    slot_bytes = L * piece + 512
+    tier = api.Tier(cache, n * slot_bytes)
+    assert tier.capacity == n and tier.slot_bytes == slot_bytes
+    r = W.rng(W.SEED_IDS)
+    src = W.distinct(r, P, n)
+    dst = np.setdiff1d(np.arange(P), src)
+    r.shuffle(dst)
+    toks = W.tokens(W.SEED_TOKENS, n * sh.page_tokens)
+    keys, _ = api.hash_blocks(toks, np.array([0, len(toks)]), sh.page_tokens)
+    cnt, slots = tier.alloc(keys)
+    assert cnt == n
+    tier.store(cache, src, slots)
+    tier.unpin(slots)
+    d = torch.as_tensor(dst, device="cuda")
+    s_ = torch.as_tensor(src, device="cuda")
+    kv3[:, d] = 0xA5
+    sc3[:, d] = 0x5A
+    torch.cuda.synchronize()
+    h, hslots = tier.lookup(keys)
+    assert h == n
+    copy_s, cons_s = torch.cuda.Stream(), torch.cuda.Stream()
+    events = [torch.cuda.Event() for _ in range(L)]
+    tier.load_layered(cache, hslots, dst, copy_s, events)
+    snaps = []
+    with torch.cuda.stream(cons_s):
+        for l in range(L):
+            cons_s.wait_event(events[l])
+            snaps.append((kv3[l].index_select(0, d).clone(), sc3[l].index_select(0, d).clone()))
+    torch.cuda.synchronize()
+    tier.unpin(hslots)
+    for l in range(L):
+        assert torch.equal(snaps[l][0], kv3[l].index_select(0, s_)), l
+        assert torch.equal(snaps[l][1], sc3[l].index_select(0, s_)), l
+    assert torch.equal(kv3[:, d], kv3[:, s_]) and torch.equal(sc3[:, d], sc3[:, s_])
+    # sampled entries against the oracle's per-layer load
+    host = tier.host_view()
+    pick = W.distinct(r, n, 16)
+    o = oshape_of(sh, num_pages=len(pick))
+    ocache = np.zeros((L, len(pick), piece), np.uint8)
+    osc = np.zeros((L, len(pick), 8), np.uint8)
+    for l in range(L):
+        oracle.load_layer(o, host[hslots[pick]].copy(), ocache.reshape(-1), osc.reshape(-1),
+                          np.arange(len(pick)), np.arange(len(pick)), l)
+    pd = torch.as_tensor(dst[pick], device="cuda")
+    assert np.array_equal(kv3[:, pd].cpu().numpy(), ocache)
+    assert np.array_equal(sc3[:, pd].cpu().numpy(), osc)
+    tier.close()
+    cache.close()
+    del kv, sc, kv3, sc3
+    release(torch)
+
+
+def test_dense_scattered_calls_full_images():
+    torch = need_gpu()
+    sh = W.DENSE
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.DENSE_TIER_SLOTS * L * piece)
+    host = tier.host_view()
+    host[:] = 0
+    torch.cuda.synchronize()
+    o_cache = kv.cpu().numpy()
+    o_tier = np.zeros_like(host)
+    o = oshape_of(sh)
+    drv = drivers.DenseScattered(cache, tier, sh)
+    for i in range(W.DENSE_CALLS):
+        op, pages, slots = drv.call(i)
+        if op == "store":
+            oracle.store_blocks(o, o_cache, None, o_tier, pages, slots)
+        else:
+            oracle.load_blocks(o, o_tier, o_cache, None, slots, pages)
+    torch.cuda.synchronize()
+    assert tier.stats()["evictions_total"] > 0  # the tier filled and recycled slots
+    assert np.array_equal(host, o_tier)
+    assert np.array_equal(kv.cpu().numpy(), o_cache)
+    tier.close()
+    cache.close()
+    del kv
+    release(torch)
+
+
+def test_agent_pool_metadata_and_bytes():
+    torch = need_gpu()
+    sh = W.QWEN3
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.POOL_TIER_BYTES)
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    # kappa = 256 blocks: refills above 4,096 tokens are declined under pressure
+    kw = dict(kappa=256, block_tokens=sh.page_tokens, activity_window=W.POOL_AGENTS)
+    pol = api.make_policy(beta_rank=beta, **kw)
+    opol = oracle.make_policy(beta=beta, **kw)
+    ot = oracle.Tier(oshape_of(sh), W.POOL_TIER_BYTES)
+    assert ot.capacity == tier.capacity == 43690
+    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol)
+    declined = evicted = 0
+    for t in range(6 * W.POOL_AGENTS):
+        rec = pool.turn()
+        assert rec.loaded_ok, f"turn {t}: a loaded page differs from its key's pattern"
+        h, hs = ot.lookup(rec.keys)
+        assert h == rec.hit and np.array_equal(hs, rec.hit_slots), t
+        save, mask = ot.admission(opol, rec.n_tokens, rec.hit * sh.page_tokens, rec.agent, t,
+                                  rec.keys)
+        assert save == rec.save and np.array_equal(mask, rec.mask), t
+        _, slots = ot.alloc(rec.keys, mask)
+        assert np.array_equal(slots, rec.alloc_slots), t
+        ok = slots >= 0
+        ot.mark_stored(slots[ok])
+        if ok.any():
+            ot.unpin(slots[ok])
+        if h:
+            ot.unpin(hs)
+        declined += int(not save)
+        if t % 16 == 15 or t == 6 * W.POOL_AGENTS - 1:
+            a, b = tier.export(), ot.export()
+            for k in ("state", "pins", "keys", "lru"):
+                assert np.array_equal(a[k], b[k]), (t, k)
+        sa, sb = tier.stats(), ot.stats()
+        for k in ("registered", "resident", "evictions_total", "active_tasks", "last_pressure"):
+            assert sa[k] == sb[k], (t, k)
+        evicted = sa["evictions_total"]
+    # the run crosses the capacity transition: the tier evicts and declines refills
+    assert evicted > 0 and declined > 0
+    tier.close()
+    cache.close()
+    del kv
+    release(torch)
