@@ -276,6 +276,187 @@ def isolated(ctx):
     return out
 
 
+# ------------------------------------------------- the other workloads
+
+def _line(workload, value, unit, ms, steps, extra, higher=True):
+    return {"metric": "host-link GB/s for KV block store/load; HBM GB/s of paged gather/scatter",
+            "value": value, "unit": unit, "n_gpus": 1, "steps": steps, "warmup": 0,
+            "ms_per_step": ms, "higher_is_better": higher, "scaling": "weak",
+            "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+            "config": {"workload": workload}, **extra}
+
+
+def run_agent_pool(args):
+    """64 agents round-robin, 24 turns each (1,536 turns), 64 GiB tier."""
+    import torch
+    from paper_2609_33762_amd import api, drivers, workloads as W
+    torch.cuda.set_device(0)
+    sh = W.QWEN3
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.POOL_TIER_BYTES)
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    pol = api.make_policy(kappa=256, block_tokens=sh.page_tokens, beta_rank=beta,
+                          activity_window=W.POOL_AGENTS)
+    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, verify=False, time_fill=True)
+    turns = args.turns_per_agent * W.POOL_AGENTS
+    hits = declined = stored = 0
+    gamma = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(turns):
+        rec = pool.turn()
+        hits += rec.hit
+        declined += int(not rec.save)
+        stored += rec.stored
+        if t % W.POOL_AGENTS == W.POOL_AGENTS - 1:
+            st = tier.stats()
+            gamma.append(round(st["working_set"] / W.POOL_TIER_BYTES, 3))
+    torch.cuda.synchronize()
+    # the synthetic KV fill stands in for prefill compute: not part of the path
+    el = time.perf_counter() - t0 - pool.fill_seconds
+    st = tier.stats()
+    moved = pool.bytes_loaded + pool.bytes_stored
+    extra = {"pool": {"turns": turns, "fill_seconds_excluded": round(pool.fill_seconds, 3),
+                      "hit_blocks": hits, "stored_blocks": stored,
+                      "declined_requests": declined, "evictions": st["evictions_total"],
+                      "gamma_H_per_round": gamma, "bytes_loaded": pool.bytes_loaded,
+                      "bytes_stored": pool.bytes_stored}}
+    tier.close()
+    cache.close()
+    return _line("agent_pool: 64 agents x %d turns, contexts 8k->64k, 64 GiB tier"
+                 % args.turns_per_agent, round(moved / el / GB, 3), "GB/s",
+                 round(el / turns * 1e3, 3), turns, extra)
+
+
+def run_dense_scattered(args):
+    """10,000 alternating store/load calls of 1-8 non-adjacent 2 MiB pages."""
+    import torch
+    from paper_2609_33762_amd import api, drivers, workloads as W
+    torch.cuda.set_device(0)
+    sh = W.DENSE
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.DENSE_TIER_SLOTS * sh.num_layers * sh.piece_bytes)
+    page = tier.info["page_bytes"]
+    # per-call latency: enqueue to completion, one call at a time
+    drv = drivers.DenseScattered(cache, tier, sh)
+    lat, moved = [], 0
+    for i in range(W.DENSE_CALLS):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        _, pages, _ = drv.call(i)
+        torch.cuda.synchronize()
+        lat.append(time.perf_counter() - t0)
+        moved += len(pages) * page
+    lat_ms = np.array(lat) * 1e3
+    # throughput: the same calls issued back to back
+    drv2 = drivers.DenseScattered(cache, tier, sh, seed=W.SEED_WORKLOAD + 1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    moved2 = 0
+    for i in range(W.DENSE_CALLS):
+        _, pages, _ = drv2.call(i)
+        moved2 += len(pages) * page
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    extra = {"latency_ms": {"p50": round(float(np.percentile(lat_ms, 50)), 4),
+                            "p99": round(float(np.percentile(lat_ms, 99)), 4),
+                            "mean_bytes_per_call": moved / W.DENSE_CALLS,
+                            "serial_gbs": round(moved / lat_ms.sum() * 1e3 / GB, 3)},
+             "calls_per_s": round(W.DENSE_CALLS / el, 1)}
+    tier.close()
+    cache.close()
+    return _line("dense_scattered: 32 layers x 8 heads x d128 bf16, 10,000 calls of 1-8 pages",
+                 round(moved2 / el / GB, 3), "GB/s", round(el / W.DENSE_CALLS * 1e3, 4),
+                 W.DENSE_CALLS, extra)
+
+
+def run_layered(args):
+    """64k-token fp8 prefix (4,096 pages, 48 layers, per-page scales) loaded
+    one layer at a time, each layer signalled by an event."""
+    import torch
+    from paper_2609_33762_amd import api, workloads as W
+    torch.cuda.set_device(0)
+    sh = W.LAYERED
+    L, P = sh.num_layers, sh.num_pages
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_random_bytes(kv, W.SEED_DATA)
+    sc = torch.empty(L * P * 8, dtype=torch.uint8, device="cuda")
+    W.fill_random_bytes(sc, W.SEED_DATA + 1)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes,
+                      scales=sc)
+    n = W.LAYERED_PREFIX_PAGES
+    tier = api.Tier(cache, n * (L * sh.piece_bytes + 512))
+    r = W.rng(W.SEED_IDS)
+    src = W.distinct(r, P, n)
+    dst = np.setdiff1d(np.arange(P), src)
+    tier.store(cache, src, np.arange(n))
+    copy_s = torch.cuda.Stream()
+    res = []
+    for rep in range(args.steps + 1):
+        start = torch.cuda.Event(enable_timing=True)
+        events = [torch.cuda.Event(enable_timing=True) for _ in range(L)]
+        torch.cuda.synchronize()
+        start.record(copy_s)
+        tier.load_layered(cache, np.arange(n), dst, copy_s, events)
+        torch.cuda.synchronize()
+        if rep:
+            res.append([start.elapsed_time(e) for e in events])
+    res = np.array(res)
+    total_ms = float(np.median(res[:, -1]))
+    moved = n * tier.slot_bytes
+    extra = {"layered": {"time_to_first_layer_ms": round(float(np.median(res[:, 0])), 4),
+                         "per_layer_ms": round(float(np.median(np.diff(res, axis=1))), 4),
+                         "layer_done_ms": [round(float(x), 3) for x in np.median(res, axis=0)]}}
+    tier.close()
+    cache.close()
+    return _line("layered_fp8: 64k-token prefix, 48 layers x 4 heads x d128 fp8 + scales",
+                 round(moved / (total_ms * 1e-3) / GB, 3), "GB/s", round(total_ms, 3),
+                 args.steps, extra)
+
+
+def run_tiny(args):
+    """The tiny case: store 32 pages, load them into 32 other pages, hash
+    4 x 512 tokens.  Launch-bound by construction (512 KiB per op)."""
+    import torch
+    from paper_2609_33762_amd import api, workloads as W
+    torch.cuda.set_device(0)
+    sh = W.TINY
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, W.TINY_TIER_SLOTS * sh.num_layers * sh.piece_bytes)
+    r = W.rng(W.SEED_IDS)
+    src = W.distinct(r, sh.num_pages, 32)
+    dst = W.distinct(r, sh.num_pages, 32, exclude=src)
+    slots = W.distinct(r, tier.capacity, 32)
+    toks, offs = W.sequences(W.SEED_TOKENS, [512] * 4)
+    steps = max(args.steps, 50)
+    for _ in range(5):
+        api.hash_blocks(toks, offs, sh.page_tokens)
+        tier.store(cache, src, slots)
+        tier.load(cache, slots, dst)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        api.hash_blocks(toks, offs, sh.page_tokens)
+        tier.store(cache, src, slots)
+        tier.load(cache, slots, dst)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    moved = 2 * 32 * tier.info["page_bytes"] * steps
+    tier.close()
+    cache.close()
+    return _line("tiny: 2 layers x 2 heads x d64 bf16, 32 pages stored and loaded, 4 x 512 "
+                 "tokens hashed", round(moved / el / GB, 3), "GB/s", round(el / steps * 1e3, 4),
+                 steps, {})
+
+
 # ------------------------------------------------------------ profiles
 
 def _short(name):
@@ -380,6 +561,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--isolated-only", action="store_true")
     ap.add_argument("--summarize-profiles", metavar="DIR")
+    ap.add_argument("--workload", default="qwen3_turn",
+                    choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny"])
+    ap.add_argument("--turns-per-agent", type=int, default=24)
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
     args = ap.parse_args()
     if args.summarize_profiles:
@@ -390,6 +574,13 @@ def main():
               "no exchange between ranks, and only single-GPU runs are part of this build "
               "(use --gpus 1)", file=sys.stderr)
         sys.exit(2)
+    other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,
+             "layered_fp8": run_layered, "tiny": run_tiny}
+    if args.workload in other:
+        out = other[args.workload](args)
+        log(json.dumps(out))
+        print(json.dumps(out), flush=True)
+        return
 
     ctx = setup(args)
     N = ctx["N"]

@@ -6,6 +6,7 @@ time them.  Page contents of the agent pool are a counter-based function of
 the block's key (`key_pattern`), so any loaded page can be checked against
 its key.
 """
+import time
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -80,7 +81,11 @@ class AgentPool:
     blocks and releases the pins.  GPU pages are free again after each turn."""
 
     def __init__(self, torch, cache, tier, kv, shape, policy, agents=W.POOL_AGENTS,
-                 seed=W.SEED_WORKLOAD, verify=True, stream=None):
+                 seed=W.SEED_WORKLOAD, verify=True, stream=None, time_fill=False):
+        # time_fill: measure the synthetic KV fill (the stand-in for prefill
+        # compute) so that a benchmark can leave it out of the path's time
+        self.time_fill = time_fill
+        self.fill_seconds = 0.0
         self.torch, self.cache, self.tier, self.kv = torch, cache, tier, kv
         self.sh, self.policy, self.verify = shape, policy, verify
         self.kv3 = kv.view(shape.num_layers, shape.num_pages, shape.piece_bytes)
@@ -132,10 +137,16 @@ class AgentPool:
             tier.load(cache, hit_slots, load_pages, stream=self.stream)
             self.bytes_loaded += h * tier.slot_bytes
         if n_full > h:  # compute (here: synthesise) the KV the tier did not have
+            if self.time_fill:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
             for c0 in range(h, n_full, 512):
                 c1 = min(n_full, c0 + 512)
                 write_pages(torch, self.kv3, pages[c0:c1],
                             key_pattern(torch, keys[c0:c1], self.words, self.kv.device))
+            if self.time_fill:
+                torch.cuda.synchronize()
+                self.fill_seconds += time.perf_counter() - t0
         save, mask = tier.admission(self.policy, len(prompt), h * b, a, t, keys)
         _, slots = tier.alloc(keys, mask)
         ok = slots >= 0
