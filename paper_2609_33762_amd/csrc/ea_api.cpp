@@ -67,9 +67,15 @@ int env_int(const char *name, int dflt) {
   return v && *v ? std::atoi(v) : dflt;
 }
 
-// Workgroups for the HBM-bound kernels (gather/scatter): 4 per CU (16 wave64s)
-// measured best on MI355X.
-int64_t grid_hbm() { return std::max(1, env_int("EA_GRID_HBM", 1024)); }
+// Workgroups for the HBM-bound kernels, measured best on MI355X (256 CUs):
+// the gather (random reads, sequential writes) peaks with 2 workgroups per
+// CU, the scatter (sequential reads, random writes) with one per CU: more
+// random writes in flight lower its rate.  EA_GRID_HBM sets both.
+int64_t grid_hbm(int dir) {
+  const int both = env_int("EA_GRID_HBM", 0);
+  if (dir == ea::kToSlots) return std::max(1, env_int("EA_GRID_GATHER", both ? both : 512));
+  return std::max(1, env_int("EA_GRID_SCATTER", both ? both : 256));
+}
 
 // Host-link kernels: 8 workgroups (32 waves) per direction already reach the
 // pinned-copy peak one way.  With a store and a load in flight together,
@@ -256,7 +262,7 @@ struct ea_tier {
   std::vector<EvRec> evs;
   std::vector<int32_t> free_evs;
   int64_t bytes_stored = 0, bytes_loaded = 0, store_calls = 0, load_calls = 0;
-  int64_t grid_link = 8, grid_hbm = 1024;
+  int64_t grid_link = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
 };
@@ -426,7 +432,7 @@ int copy_staged(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
     a.slots = stage;
     if (dir == ea::kToSlots)
       EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0, c1 - c0, dir, ea::kRouteHbm,
-                            t->grid_hbm, s));
+                            t->grid_gather, s));
     for (int64_t j0 = c0; j0 < c1;) {
       int64_t j1 = j0 + 1;
       while (j1 < c1 && ss[j1] == ss[j1 - 1] + 1) ++j1;
@@ -441,7 +447,7 @@ int copy_staged(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
     }
     if (dir == ea::kToPages)
       EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0, c1 - c0, dir, ea::kRouteHbm,
-                            t->grid_hbm, s));
+                            t->grid_scatter, s));
   }
   EA_HIP(hipEventRecord(R.staging_ev, s));
   R.staging_used = true;
@@ -545,7 +551,11 @@ int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes, int numa_node,
   // two different XCDs for the two directions when the device has them
   t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", 0x1u, t->num_xcd);
   t->xcd_load = xcd_mask_from_env("EA_XCD_LOAD", t->num_xcd > 1 ? 0x2u : 0x1u, t->num_xcd);
-  t->grid_hbm = grid_hbm();
+  t->grid_gather = grid_hbm(ea::kToSlots);
+  t->grid_scatter = grid_hbm(ea::kToPages);
+  // a layered load is one short kernel per layer: 16 workgroups hide the
+  // start and drain of each (56 GB/s against 51 with 8 on MI355X)
+  t->grid_layered = std::max(1, env_int("EA_LINK_WG_LAYERED", 16));
   // Fine-grained (coherent) by default: kernels and DMA engines then see one
   // another's writes to the slots without any cache maintenance.
   unsigned flags = hipHostMallocMapped | hipHostMallocPortable;
@@ -775,7 +785,7 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
   }
   for (int32_t l = 0; l < c->d.num_layers; ++l) {
     a.layer_begin = l;
-    EA_HIP(ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_link,
+    EA_HIP(ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
                                  copy_stream));
     EA_HIP(hipEventRecord(layer_done[l], copy_stream));
   }
@@ -801,7 +811,7 @@ int ea_gather_blocks(ea_cache *c, const int32_t *block_ids, int32_t n, void *d_d
   ea::PieceCopy a = base_copy(c, c->slot);
   a.slots = static_cast<uint8_t *>(d_dst);
   return launch_entries(a, c->ring, nullptr, block_ids, n, ea::kToSlots, ea::kRouteHbm,
-                        grid_hbm(), stream);
+                        grid_hbm(ea::kToSlots), stream);
 }
 
 int ea_scatter_blocks(ea_cache *c, const void *d_src, const int32_t *dst_pages, int32_t n,
@@ -818,7 +828,7 @@ int ea_scatter_blocks(ea_cache *c, const void *d_src, const int32_t *dst_pages, 
   ea::PieceCopy a = base_copy(c, c->slot);
   a.slots = static_cast<uint8_t *>(const_cast<void *>(d_src));
   return launch_entries(a, c->ring, nullptr, dst_pages, n, ea::kToPages, ea::kRouteHbm,
-                        grid_hbm(), stream);
+                        grid_hbm(ea::kToPages), stream);
 }
 
 // --------------------------------------------------------------- peak probe
