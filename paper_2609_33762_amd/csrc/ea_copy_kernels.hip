@@ -34,20 +34,43 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ u32x4 load_nt(const u32x4 *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void store_nt(u32x4 *p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
-// Page and slot of entry i.  The entry index is wave-uniform and the index
-// arrays are read-only and unaliased for the whole kernel, so these compile
-// to scalar loads (from the kernel arguments or the uploaded index arrays).
-template <bool INLINE>
-__device__ __forceinline__ void entry(const PieceCopy &a, const int32_t *__restrict__ pages,
-                                      const int64_t *__restrict__ slot_idx,
-                                      const InlineIdx &inl, int64_t i, int64_t &page,
-                                      int64_t &slot) {
-  if constexpr (INLINE) {
-    page = inl.pages[i];
-    slot = inl.slots[i];
-  } else {
-    page = pages[i];
-    slot = a.identity_slots ? i : slot_idx[i];
+// Copy unit u: layer layer_begin + (u mod layer_count) of entry i, whose
+// page and slot the caller has made wave-uniform.
+template <int DIR, bool INLINE, int VEC>
+__device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t i, int64_t page,
+                                          int64_t slot, int lane) {
+  const int64_t nvec = a.piece_bytes >> 4;
+  const int64_t l = a.layer_begin + (u - i * a.layer_count);
+  uint8_t *cache_piece = a.cache + (l * a.num_pages + page) * a.piece_bytes;
+  uint8_t *slot_base = a.slots + slot * a.slot_bytes;
+  uint8_t *slot_piece = slot_base + l * a.piece_bytes;
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(DIR == kToSlots ? cache_piece : slot_piece);
+  u32x4 *dst = reinterpret_cast<u32x4 *>(DIR == kToSlots ? slot_piece : cache_piece);
+  for (int64_t base = 0; base < nvec; base += (int64_t)kWave * VEC) {
+    u32x4 r[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+      const int64_t v = base + k * kWave + lane;
+      if (v < nvec) r[k] = load_nt(src + v);
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+      const int64_t v = base + k * kWave + lane;
+      if (v < nvec) store_nt(dst + v, r[k]);
+    }
+  }
+  if (a.scales != nullptr) {
+    uint64_t *cs = reinterpret_cast<uint64_t *>(a.scales + (l * a.num_pages + page) * 8);
+    uint64_t *ss = reinterpret_cast<uint64_t *>(slot_base + a.page_bytes + l * 8);
+    if (lane == 0) {
+      if (DIR == kToSlots) *ss = *cs; else *cs = *ss;
+    }
+    if (DIR == kToSlots && l == 0) {
+      const int64_t pad_begin = a.page_bytes + 8 * (int64_t)a.num_layers;
+      const int64_t pad_words = (a.slot_bytes - pad_begin) >> 3;
+      uint64_t *pad = reinterpret_cast<uint64_t *>(slot_base + pad_begin);
+      for (int64_t w = lane; w < pad_words; w += kWave) pad[w] = 0;
+    }
   }
 }
 
@@ -56,9 +79,7 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
                                            const int64_t *__restrict__ slot_idx,
                                            const InlineIdx &inl) {
   const int64_t units = a.n * a.layer_count;
-  const int64_t nvec = a.piece_bytes >> 4;
   const int lane = threadIdx.x & (kWave - 1);
-  // rank of this workgroup among the working ones (those on xcd_mask)
   const int xcd = (int)(blockIdx.x % (unsigned)a.num_xcd);
   if (!((a.xcd_mask >> xcd) & 1u)) return;
   const int active = __popc(a.xcd_mask);
@@ -66,47 +87,38 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
                         __popc(a.xcd_mask & ((1u << xcd) - 1u));
   const int64_t groups = (int64_t)(gridDim.x / (unsigned)a.num_xcd) * active;
   const int64_t waves = groups * (kThreads / kWave);
-  // the unit a wave works on is the same for all of its lanes
   const int64_t first =
       group * (kThreads / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  for (int64_t u = first; u < units; u += waves) {
-    const int64_t i = u / a.layer_count;
-    const int64_t l = a.layer_begin + (u - i * a.layer_count);
-    int64_t page, slot;
-    entry<INLINE>(a, pages, slot_idx, inl, i, page, slot);
-    uint8_t *cache_piece = a.cache + (l * a.num_pages + page) * a.piece_bytes;
-    uint8_t *slot_base = a.slots + slot * a.slot_bytes;
-    uint8_t *slot_piece = slot_base + l * a.piece_bytes;
-    const u32x4 *src =
-        reinterpret_cast<const u32x4 *>(DIR == kToSlots ? cache_piece : slot_piece);
-    u32x4 *dst = reinterpret_cast<u32x4 *>(DIR == kToSlots ? slot_piece : cache_piece);
-    for (int64_t base = 0; base < nvec; base += (int64_t)kWave * VEC) {
-      u32x4 r[VEC];
-#pragma unroll
-      for (int k = 0; k < VEC; ++k) {
-        const int64_t v = base + k * kWave + lane;
-        if (v < nvec) r[k] = load_nt(src + v);
-      }
-#pragma unroll
-      for (int k = 0; k < VEC; ++k) {
-        const int64_t v = base + k * kWave + lane;
-        if (v < nvec) store_nt(dst + v, r[k]);
-      }
+  if constexpr (INLINE) {
+    // indices from the kernel arguments (scalar loads, u is wave-uniform)
+    for (int64_t u = first; u < units; u += waves) {
+      const int64_t i = u / a.layer_count;
+      copy_unit<DIR, INLINE, VEC>(a, u, i, inl.pages[i], inl.slots[i], lane);
     }
-    if (a.scales != nullptr) {
-      // 8 bytes (K scale, V scale) per (layer, page).  In a slot they sit in
-      // the trailer after the page data, 8 bytes per layer, followed by zero
-      // padding up to slot_bytes that a store writes with layer 0.
-      uint64_t *cs = reinterpret_cast<uint64_t *>(a.scales + (l * a.num_pages + page) * 8);
-      uint64_t *ss = reinterpret_cast<uint64_t *>(slot_base + a.page_bytes + l * 8);
-      if (lane == 0) {
-        if (DIR == kToSlots) *ss = *cs; else *cs = *ss;
+  } else {
+    // The index arrays live in pinned host memory that the kernel reads
+    // over the link.  Lane k fetches the page and slot of the wave's k-th
+    // next unit in one vector load per 64 units, and the loop broadcasts
+    // them with readlane, so a unit's copy never waits on an index fetch.
+    for (int64_t k0 = 0;; k0 += kWave) {
+      const int64_t u0 = first + k0 * waves;
+      if (u0 >= units) break;
+      const int64_t ul = u0 + (int64_t)lane * waves;
+      int32_t vpage = 0;
+      int64_t vslot = 0;
+      if (ul < units) {
+        const int64_t il = ul / a.layer_count;
+        vpage = pages[il];
+        vslot = a.identity_slots ? il : slot_idx[il];
       }
-      if (DIR == kToSlots && l == 0) {
-        const int64_t pad_begin = a.page_bytes + 8 * (int64_t)a.num_layers;
-        const int64_t pad_words = (a.slot_bytes - pad_begin) >> 3;
-        uint64_t *pad = reinterpret_cast<uint64_t *>(slot_base + pad_begin);
-        for (int64_t w = lane; w < pad_words; w += kWave) pad[w] = 0;
+      for (int k = 0; k < kWave; ++k) {
+        const int64_t u = u0 + (int64_t)k * waves;
+        if (u >= units) break;
+        const int64_t i = u / a.layer_count;
+        const int64_t page = __builtin_amdgcn_readlane(vpage, k);
+        const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)vslot, k);
+        const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)vslot >> 32), k);
+        copy_unit<DIR, INLINE, VEC>(a, u, i, page, (int64_t)(((uint64_t)hi << 32) | lo), lane);
       }
     }
   }
