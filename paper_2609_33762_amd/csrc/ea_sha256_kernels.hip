@@ -10,8 +10,10 @@
 //   sha256_chain:     one lane per sequence, runs the final compression of
 //                     each key in order, feeding key_{i-1} in as message
 //                     words 0..7 (the serial part: one compression per key).
-// Rotations compile to v_alignbit_b32, Ch/Maj to v_bfi_b32 and the adds to
-// v_add3_u32; everything stays in VGPRs (no LDS, no scratch).
+// A lone chain runs at the issue rate of one wave, so the instruction count
+// per compression is what matters: rotations are v_alignbit_b32, every
+// three-input XOR and Ch/Maj one v_bitop3_b32 (gfx950's three-input logic
+// op), sums v_add3_u32; everything stays in VGPRs (no LDS, no scratch).
 #include <hip/hip_runtime.h>
 
 #include "ea_internal.hpp"
@@ -41,6 +43,16 @@ __device__ __forceinline__ uint32_t rotr(uint32_t x, int n) {
   return __builtin_amdgcn_alignbit(x, x, n);
 }
 
+// v_bitop3_b32 truth tables over inputs (x, y, z) = (0xF0, 0xCC, 0xAA).
+constexpr uint32_t kXor3 = 0x96;  // x ^ y ^ z
+constexpr uint32_t kCh = 0xCA;    // x ? y : z
+constexpr uint32_t kMaj = 0xE8;   // majority
+
+template <uint32_t TABLE>
+__device__ __forceinline__ uint32_t bitop3(uint32_t x, uint32_t y, uint32_t z) {
+  return __builtin_amdgcn_bitop3_b32(x, y, z, TABLE);
+}
+
 // One compression: st <- st + rounds(st, w).  w is consumed (used as the
 // rolling 16-word message schedule).
 __device__ __forceinline__ void compress(uint32_t st[8], uint32_t w[16]) {
@@ -53,16 +65,16 @@ __device__ __forceinline__ void compress(uint32_t st[8], uint32_t w[16]) {
       wt = w[t];
     } else {
       const uint32_t w2 = w[(t - 2) & 15], w15 = w[(t - 15) & 15];
-      const uint32_t s1 = rotr(w2, 17) ^ rotr(w2, 19) ^ (w2 >> 10);
-      const uint32_t s0 = rotr(w15, 7) ^ rotr(w15, 18) ^ (w15 >> 3);
+      const uint32_t s1 = bitop3<kXor3>(rotr(w2, 17), rotr(w2, 19), w2 >> 10);
+      const uint32_t s0 = bitop3<kXor3>(rotr(w15, 7), rotr(w15, 18), w15 >> 3);
       wt = s1 + w[(t - 7) & 15] + s0 + w[t & 15];
       w[t & 15] = wt;
     }
-    const uint32_t S1 = rotr(e, 6) ^ rotr(e, 11) ^ rotr(e, 25);
-    const uint32_t ch = (e & f) ^ (~e & g);
+    const uint32_t S1 = bitop3<kXor3>(rotr(e, 6), rotr(e, 11), rotr(e, 25));
+    const uint32_t ch = bitop3<kCh>(e, f, g);
     const uint32_t t1 = h + S1 + ch + kRound[t] + wt;
-    const uint32_t S0 = rotr(a, 2) ^ rotr(a, 13) ^ rotr(a, 22);
-    const uint32_t mj = (a & b) ^ (a & c) ^ (b & c);
+    const uint32_t S0 = bitop3<kXor3>(rotr(a, 2), rotr(a, 13), rotr(a, 22));
+    const uint32_t mj = bitop3<kMaj>(a, b, c);
     const uint32_t t2 = S0 + mj;
     h = g; g = f; f = e; e = d + t1;
     d = c; c = b; b = a; a = t1 + t2;
