@@ -93,6 +93,7 @@ def lib():
             "eao_tier_unpin": (C.c_int, [P, P, I64]),
             "eao_tier_stats_get": (C.c_int, [P, P]),
             "eao_tier_export": (C.c_int, [P, P, P, P, P, P]),
+            "eao_lru_reference": (C.c_int, [P, I64, P, I64, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -294,3 +295,21 @@ class Tier:
         _check("eao_tier_export", lib().eao_tier_export(
             self._h, _ptr(state), _ptr(pins), _ptr(keys), _ptr(lru), C.byref(m)))
         return dict(state=state, pins=pins, keys=keys, lru=lru[:m.value].copy())
+
+
+# ------------------------------------------------- LRU reference model
+
+def lru_reference(refs, capacity, declined=None):
+    """Hits (uint8 [n]) of the reference model of the paper's appendix for
+    one tier capacity in chunks.  refs: uint8 [n, 32] chunk keys in
+    reference order; declined: optional bool/uint8 [n], misses to decline."""
+    refs = np.ascontiguousarray(refs, dtype=np.uint8).reshape(-1, 32)
+    n = len(refs)
+    dec = None if declined is None else np.ascontiguousarray(declined, dtype=np.uint8)
+    if dec is not None and len(dec) != n:
+        raise ValueError("declined must have one entry per reference")
+    hits = np.zeros(max(n, 1), np.uint8)
+    _check("eao_lru_reference", lib().eao_lru_reference(
+        _ptr(refs) if n else None, n, _ptr(dec) if n else None, int(capacity), _ptr(hits)))
+    return hits[:n]
+

@@ -8,7 +8,7 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["eao.c", "eao_tier.c"]
+SOURCES = ["eao.c", "eao_tier.c", "eao_stack.c"]
 LIB = os.path.join(HERE, "libeao.so")
 
 

@@ -239,6 +239,20 @@ int eao_tier_stats_get(const eao_tier *t, eao_tier_stats *s);
 int eao_tier_export(const eao_tier *t, uint8_t *state_out, int32_t *pins_out,
                     uint8_t *keys_out, int64_t *lru_out, int64_t *n_lru);
 
+
+/* ------------------------------------------------- LRU reference model */
+
+/* The appendix's LRU reference model (behind Equation (3), Lemma 1 and
+ * Proposition 1), simulated for one capacity.  refs holds n 32-byte chunk
+ * keys in reference order; declined (n bytes, NULL = full admission) marks
+ * references whose miss is declined.  The tier of `capacity` chunks starts
+ * empty.  hit_out[i] = 1 if reference i finds its chunk resident (and
+ * promotes it to the most-recent end), else 0 (an admitted miss inserts the
+ * chunk at the most-recent end, evicting the least-recent one if the tier
+ * is full; a declined miss changes nothing). */
+int eao_lru_reference(const uint8_t *refs, int64_t n, const uint8_t *declined,
+                      int64_t capacity, uint8_t *hit_out);
+
 #ifdef __cplusplus
 }
 #endif
