@@ -94,6 +94,7 @@ def lib():
             "eao_tier_stats_get": (C.c_int, [P, P]),
             "eao_tier_export": (C.c_int, [P, P, P, P, P, P]),
             "eao_lru_reference": (C.c_int, [P, I64, P, I64, P]),
+            "eao_lru_prefix_model": (C.c_int, [P, P, I64, P, I64, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -312,4 +313,21 @@ def lru_reference(refs, capacity, declined=None):
     _check("eao_lru_reference", lib().eao_lru_reference(
         _ptr(refs) if n else None, n, _ptr(dec) if n else None, int(capacity), _ptr(hits)))
     return hits[:n]
+
+
+def lru_prefix_model(refs, req_off, capacity, declined=None):
+    """Lookup hits per request (int64 [n_req]) under the host tier's own
+    order; declined: optional bool [n_req], requests whose writes are
+    skipped."""
+    refs = np.ascontiguousarray(refs, dtype=np.uint8).reshape(-1, 32)
+    offs = np.ascontiguousarray(req_off, dtype=np.int64)
+    n_req = len(offs) - 1
+    dec = None if declined is None else np.ascontiguousarray(declined, dtype=np.uint8)
+    if dec is not None and len(dec) != n_req:
+        raise ValueError("declined must have one entry per request")
+    h = np.zeros(max(n_req, 1), np.int64)
+    _check("eao_lru_prefix_model", lib().eao_lru_prefix_model(
+        _ptr(refs) if len(refs) else None, _ptr(offs), n_req,
+        _ptr(dec) if (dec is not None and n_req) else None, int(capacity), _ptr(h)))
+    return h[:n_req]
 

@@ -253,6 +253,17 @@ int eao_tier_export(const eao_tier *t, uint8_t *state_out, int32_t *pins_out,
 int eao_lru_reference(const uint8_t *refs, int64_t n, const uint8_t *declined,
                       int64_t capacity, uint8_t *hit_out);
 
+/* The host tier's own order, request by request (App. "Recency order of
+ * the host tier"; section 4, Eq. 6 and copy-time deduplication): request j
+ * (refs[req_off[j] .. req_off[j+1]-1], req_off[0] = 0) promotes its leading
+ * resident chunks (h_out[j] of them, the lookup's hits); unless declined[j]
+ * it then inserts, in order, each later chunk absent at that moment; an
+ * insertion into a full tier evicts the least-recent chunk the request has
+ * not itself promoted or inserted, and is skipped if there is none.
+ * declined may be NULL (every request admitted). */
+int eao_lru_prefix_model(const uint8_t *refs, const int64_t *req_off, int64_t n_req,
+                         const uint8_t *declined, int64_t capacity, int64_t *h_out);
+
 #ifdef __cplusplus
 }
 #endif

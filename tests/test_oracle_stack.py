@@ -164,3 +164,60 @@ def test_edge_cases():
     assert list(oracle.lru_reference(keys, 1, [1, 1, 1])) == [0, 0, 0]
     with pytest.raises(oracle.OracleError):
         oracle.lru_reference(keys, -1)
+
+
+# ------------------------------------------- the host tier's own order
+
+def tier_replay(keys, offs, K, save_flags):
+    """Replay a stream on the oracle's host tier (lookup, deduplicated
+    admission mask, allocation, store, unpin) and return the lookup hits
+    per request.  Misses of requests with save_flags[j] == 0 are declined."""
+    shape = oracle.make_shape(8, 1, 16, 1, 16, 2)  # 1 KiB slots
+    slot = oracle.sizes(shape)["slot"]
+    t = oracle.Tier(shape, K * slot)
+    assert t.capacity == K
+    pol = oracle.make_policy(kappa=1, block_tokens=16, beta=64, mode=oracle.ADMIT_ALWAYS)
+    hits = []
+    for j in range(len(offs) - 1):
+        k = keys[offs[j]:offs[j + 1]]
+        h, hs = t.lookup(k)
+        save, mask = t.admission(pol, 16 * len(k), 16 * h, j, j, k)
+        assert save == 1
+        mask = mask & np.uint8(save_flags[j])
+        _, slots = t.alloc(k, mask)
+        ok = slots >= 0
+        t.mark_stored(slots[ok])
+        t.unpin(slots[ok])
+        if h:
+            t.unpin(hs)
+        hits.append(h)
+    t.close()
+    return np.array(hits)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_prefix_model_is_the_tier_order(seed):
+    ids, offs = agent_like_ids(200 + seed, agents=6, turns=7, start=5, grow=(1, 5), keep=0.75)
+    keys = keys_from_ids(ids, seed=200 + seed)
+    r = np.random.default_rng(300 + seed)
+    save = (r.random(len(offs) - 1) < [1.0, 0.8, 0.5, 0.8, 0.3, 0.0][seed]).astype(np.uint8)
+    for K in (3, 12, 30, 55, 90, 400):
+        want = tier_replay(keys, offs, K, save)
+        got = oracle.lru_prefix_model(keys, offs, K, 1 - save)
+        assert np.array_equal(got, want), (seed, K)
+
+
+def test_prefix_model_edge_cases():
+    keys = keys_from_ids([0, 1, 2, 0, 1, 2, 0, 9])
+    offs = np.array([0, 3, 3, 6, 8])
+    # unbounded tier: every repeated leading chunk hits
+    assert list(oracle.lru_prefix_model(keys, offs, 100)) == [0, 0, 3, 1]
+    # nothing admitted: nothing ever hits
+    assert list(oracle.lru_prefix_model(keys, offs, 100, [1, 1, 1, 1])) == [0, 0, 0, 0]
+    assert list(oracle.lru_prefix_model(keys, offs, 0)) == [0, 0, 0, 0]
+    # K = 1: the request's own inserts are pinned, so only its first new chunk
+    # fits and later ones are not inserted
+    assert list(oracle.lru_prefix_model(keys, offs, 1)) == [0, 0, 1, 1]
+    assert len(oracle.lru_prefix_model(np.zeros((0, 32), np.uint8), [0], 4)) == 0
+    with pytest.raises(oracle.OracleError):
+        oracle.lru_prefix_model(keys, [0, 5, 3], 4)
