@@ -303,10 +303,12 @@ def run_agent_pool(args):
     turns = args.turns_per_agent * W.POOL_AGENTS
     hits = declined = stored = 0
     gamma = []
+    records = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(turns):
         rec = pool.turn()
+        records.append(rec)
         hits += rec.hit
         declined += int(not rec.save)
         stored += rec.stored
@@ -323,6 +325,11 @@ def run_agent_pool(args):
                       "declined_requests": declined, "evictions": st["evictions_total"],
                       "gamma_H_per_round": gamma, "bytes_loaded": pool.bytes_loaded,
                       "bytes_stored": pool.bytes_stored}}
+    extra["pool"]["reference_model"] = drivers.stack_report(
+        records, tier.capacity, tier.slot_bytes, [16 << 30, 32 << 30, 64 << 30, 128 << 30,
+                                                  256 << 30])
+    extra["pool"]["reference_model"].pop("hits_tier_order_per_request")
+    log(f"reference model: {extra['pool']['reference_model']}")
     tier.close()
     cache.close()
     return _line("agent_pool: 64 agents x %d turns, contexts 8k->64k, 64 GiB tier"

@@ -315,6 +315,64 @@ int ea_tier_get_plan(const ea_tier *tier, int direction, int *plan);
 int ea_peak_probe(ea_tier *tier, void *d_buf, int64_t bytes, int direction,
                   int reps, double *gbps);
 
+/* ------------------------------------------- reuse-distance capacity tool
+ *
+ * Host-only analysis of a chunk reference stream for sizing the host tier
+ * (section 3.2, Eq. 4, the stack-distance principle; App. "Prefix coverage
+ * from a reference stream").  No GPU work, no tier needed.  A stream lists
+ * 32-byte chunk keys in reference order; in the paper's reference model
+ * every request references the full chunks of its prompt, in order, at its
+ * first prefix lookup.
+ *
+ * ea_reuse_distances: prev_dist[i] = the number of distinct chunks other
+ * than refs[i] referenced strictly between the previous reference to the
+ * same chunk and reference i (the reuse distance D of Eq. 4), or -1 for a
+ * first reference; next_dist[i] = the same count from i to the next
+ * reference of the chunk, or -1 if there is none.  Either output may be
+ * NULL; n may be 0.  O(n log n) time, 40 n bytes of temporary memory.
+ *
+ * In an LRU tier of K chunks that admits every miss (App. "Reference
+ * model"), reference i hits exactly when 0 <= prev_dist[i] < K, for every K
+ * at once (Lemma 1 with nothing declined).
+ *
+ * ea_prefix_coverage: requests j = 0..n_req-1 own the references
+ * req_off[j] .. req_off[j+1]-1 (req_off[0] >= 0, non-decreasing, n_req+1
+ * entries).  For each capacity caps[c] >= 0 (in chunks),
+ * coverage[j*n_caps + c] = the number of leading references of request j
+ * that hit in such a tier: its consecutive-prefix host coverage H_j in
+ * chunks.  prev_dist comes from ea_reuse_distances over the same stream. */
+int ea_reuse_distances(const uint8_t *refs, int64_t n, int64_t *prev_dist,
+                       int64_t *next_dist);
+int ea_prefix_coverage(const int64_t *prev_dist, const int64_t *req_off,
+                       int64_t n_req, const int64_t *caps, int64_t n_caps,
+                       int64_t *coverage);
+
+/* The same reference model for one capacity with some misses declined
+ * (App. "Reference model"; the setting of Proposition 1): reference i hits
+ * if refs[i] is resident and then becomes most recent; a miss with
+ * declined[i] != 0 changes nothing; any other miss inserts refs[i] as most
+ * recent, first evicting the least-recent chunk when `capacity` chunks are
+ * resident.  declined may be NULL (full admission).  hits[i] = 1 for a hit,
+ * else 0.  O(n) expected time, O(capacity) memory. */
+int ea_lru_simulate(const uint8_t *refs, int64_t n, const uint8_t *declined,
+                    int64_t capacity, uint8_t *hits);
+
+/* The host tier's own recency order (App. "Recency order of the host
+ * tier": a lookup hit moves only the matched prefix to the most-recent
+ * end), request by request, for one capacity: request j (refs
+ * req_off[j] .. req_off[j+1]-1, req_off[0] = 0) promotes its leading
+ * resident chunks, hit_blocks[j] of them; unless declined[j] != 0 it then
+ * inserts every later chunk that is absent at that moment, in order
+ * (copy-time deduplication, section 4); an insertion into a full tier
+ * evicts the least-recent chunk that the request has not promoted or
+ * inserted itself (those stay pinned until it ends) and is skipped when
+ * there is none.  This is the order ea_tier_lookup / ea_admission_fill /
+ * ea_tier_alloc / ea_tier_unpin maintain when every request releases its
+ * pins before the next one.  declined may be NULL. */
+int ea_lru_simulate_prefix(const uint8_t *refs, const int64_t *req_off,
+                           int64_t n_req, const uint8_t *declined,
+                           int64_t capacity, int64_t *hit_blocks);
+
 #ifdef __cplusplus
 }
 #endif

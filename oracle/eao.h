@@ -242,7 +242,7 @@ int eao_tier_export(const eao_tier *t, uint8_t *state_out, int32_t *pins_out,
 
 /* ------------------------------------------------- LRU reference model */
 
-/* The appendix's LRU reference model (behind Equation (3), Lemma 1 and
+/* The appendix's LRU reference model (behind Equation (4), Lemma 1 and
  * Proposition 1), simulated for one capacity.  refs holds n 32-byte chunk
  * keys in reference order; declined (n bytes, NULL = full admission) marks
  * references whose miss is declined.  The tier of `capacity` chunks starts

@@ -84,6 +84,10 @@ SIGNATURES = {
     "ea_tier_set_plan": (_INT, [_P, _INT, _INT]),
     "ea_tier_get_plan": (_INT, [_P, _INT, _P]),
     "ea_peak_probe": (_INT, [_P, _P, _I64, _INT, _INT, _P]),
+    "ea_reuse_distances": (_INT, [_P, _I64, _P, _P]),
+    "ea_prefix_coverage": (_INT, [_P, _P, _I64, _P, _I64, _P]),
+    "ea_lru_simulate": (_INT, [_P, _I64, _P, _I64, _P]),
+    "ea_lru_simulate_prefix": (_INT, [_P, _P, _I64, _P, _I64, _P]),
 }
 
 _lib = None

@@ -245,3 +245,66 @@ def hash_blocks_device(d_tokens, seq_offsets, block_tokens, d_keys_out, d_parent
         None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),
         _ptr(koffs), _stream(stream)))
     return koffs
+
+
+# ------------------------------------------- reuse-distance capacity tool
+
+def reuse_distances(refs):
+    """(prev_dist, next_dist), int64 [n] each, of a chunk reference stream
+    (uint8 [n, 32] keys in reference order); -1 marks a first or last
+    reference.  Host-only."""
+    refs = _u8(refs).reshape(-1, 32)
+    n = len(refs)
+    prev = np.zeros(max(n, 1), np.int64)
+    nxt = np.zeros(max(n, 1), np.int64)
+    N.check("ea_reuse_distances", N.load().ea_reuse_distances(
+        _ptr(refs) if n else None, n, _ptr(prev), _ptr(nxt)))
+    return prev[:n], nxt[:n]
+
+
+def prefix_coverage(prev_dist, req_off, caps):
+    """int64 [n_requests, n_caps]: leading hits of each request in an LRU
+    tier of caps[c] chunks that admits every miss.  Host-only."""
+    prev, offs, caps = _i64(prev_dist), _i64(req_off), _i64(caps)
+    n_req, n_caps = len(offs) - 1, len(caps)
+    if n_req < 0:
+        raise ValueError("req_off needs at least one entry")
+    if offs[-1] > len(prev):
+        raise ValueError("req_off runs past the distance array")
+    out = np.zeros((max(n_req, 1), max(n_caps, 1)), np.int64)
+    N.check("ea_prefix_coverage", N.load().ea_prefix_coverage(
+        _ptr(prev) if len(prev) else None, _ptr(offs), n_req,
+        _ptr(caps) if n_caps else None, n_caps, _ptr(out)))
+    return out[:n_req, :n_caps]
+
+
+def lru_simulate(refs, capacity, declined=None):
+    """uint8 [n] hits of the reference model in an LRU tier of `capacity`
+    chunks, misses at `declined` references left out.  Host-only."""
+    refs = _u8(refs).reshape(-1, 32)
+    n = len(refs)
+    dec = None if declined is None else _u8(declined)
+    if dec is not None and len(dec) != n:
+        raise ValueError("declined must have one entry per reference")
+    hits = np.zeros(max(n, 1), np.uint8)
+    N.check("ea_lru_simulate", N.load().ea_lru_simulate(
+        _ptr(refs) if n else None, n, _ptr(dec) if (dec is not None and n) else None,
+        int(capacity), _ptr(hits)))
+    return hits[:n]
+
+
+def lru_simulate_prefix(refs, req_off, capacity, declined=None):
+    """int64 [n_requests] lookup hits under the host tier's own order;
+    declined: optional bool [n_requests].  Host-only."""
+    refs = _u8(refs).reshape(-1, 32)
+    offs = _i64(req_off)
+    n_req = len(offs) - 1
+    dec = None if declined is None else _u8(declined)
+    if dec is not None and len(dec) != n_req:
+        raise ValueError("declined must have one entry per request")
+    out = np.zeros(max(n_req, 1), np.int64)
+    N.check("ea_lru_simulate_prefix", N.load().ea_lru_simulate_prefix(
+        _ptr(refs) if len(refs) else None, _ptr(offs), n_req,
+        _ptr(dec) if (dec is not None and n_req) else None, int(capacity), _ptr(out)))
+    return out[:n_req]
+

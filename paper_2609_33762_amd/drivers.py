@@ -213,3 +213,70 @@ class DenseScattered:
             rec = ("load", pages, slots)
         self.calls.append(rec)
         return rec
+
+
+# --------------------------------------------- reference-model capacity report
+
+def stack_report(records, capacity_slots, slot_bytes, curve_bytes=()):
+    """Predict the agent pool's host hits with the reuse-distance tool and
+    compare them with what the tier measured.
+
+    The reference stream lists, request by request, every full block of the
+    prompt in order (the paper's reference model).  Reported, in blocks:
+      hits_measured           leading hits the tier returned (sum of h)
+      hits_model_full         leading hits of an LRU tier of K_H slots that
+                              admits every miss (one-pass reuse distances)
+      hits_model_run_declines the same tier with the misses of the requests
+                              the run declined left out (Proposition 1's
+                              setting)
+      hits_model_tier_order   the tier's own order (a lookup promotes only
+                              the matched prefix) with the run's declines:
+                              this reproduces hits_measured
+      declined_new_blocks     new blocks (after the measured hit prefix) of
+                              declined requests, and the share of them whose
+                              next reuse distance is >= K_H or that are
+                              never referenced again (the proposition's
+                              condition)
+    and, for each tier size in curve_bytes, the coverage of an LRU tier that
+    admits every miss in both orders."""
+    lens = np.array([len(r.keys) for r in records], np.int64)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    refs = np.concatenate([r.keys for r in records]) if len(records) else np.zeros((0, 32), np.uint8)
+    req_declined = np.array([not r.save for r in records], bool)
+    declined = np.repeat(req_declined, lens).astype(np.uint8)
+    t0 = time.perf_counter()
+    prev, nxt = api.reuse_distances(refs)
+    caps = [capacity_slots] + [int(c // slot_bytes) for c in curve_bytes]
+    cov = api.prefix_coverage(prev, offs, caps)
+    tool_s = time.perf_counter() - t0
+    sim = api.lru_simulate(refs, capacity_slots, declined).astype(bool)
+    lead = 0
+    for j in range(len(records)):
+        h = sim[offs[j]:offs[j + 1]]
+        lead += int(np.argmin(h)) if not h.all() else len(h)
+    tier_order = api.lru_simulate_prefix(refs, offs, capacity_slots, req_declined)
+    curve_tier = [api.lru_simulate_prefix(refs, offs, int(c // slot_bytes)).sum()
+                  for c in curve_bytes]
+    new_mask = np.zeros(len(refs), bool)
+    for j, r in enumerate(records):
+        if not r.save:
+            new_mask[offs[j] + r.hit:offs[j + 1]] = True
+    nd = nxt[new_mask]
+    far = int(np.sum((nd < 0) | (nd >= capacity_slots)))
+    return {
+        "references": int(len(refs)), "capacity_slots": int(capacity_slots),
+        "hits_measured": int(sum(r.hit for r in records)),
+        "hits_model_full": int(cov[:, 0].sum()),
+        "hits_model_run_declines": lead,
+        "hits_model_tier_order": int(tier_order.sum()),
+        "hits_tier_order_per_request": tier_order,
+        "declined_new_blocks": int(new_mask.sum()),
+        "declined_meeting_condition": round(far / max(1, int(new_mask.sum())), 4),
+        "coverage_curve_full_admission": {
+            str(int(b) >> 30) + "GiB": round(float(cov[:, 1 + i].sum()) / max(1, int(lens.sum())), 4)
+            for i, b in enumerate(curve_bytes)},
+        "coverage_curve_tier_order": {
+            str(int(b) >> 30) + "GiB": round(float(curve_tier[i]) / max(1, int(lens.sum())), 4)
+            for i, b in enumerate(curve_bytes)},
+        "tool_seconds": round(tool_s, 3),
+    }

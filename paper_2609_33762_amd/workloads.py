@@ -120,3 +120,35 @@ def fill_random_bytes(t_bytes, seed, chunk=1 << 30):
 def host_bytes(seed, n):
     """Uniform random bytes on the host (small CPU-side cases)."""
     return rng(seed).integers(0, 256, size=n, dtype=np.uint8)
+
+
+def chunk_stream(seed, agents, turns, start_chunks, max_chunks, growth_chunks, keep):
+    """A synthetic chunk reference stream with the agent pool's shape, in
+    chunk units and without tokens: agents are served round-robin; a request
+    keeps the first floor(keep * len) chunk keys of the agent's previous
+    request and continues with fresh random keys up to
+    min(len + U[growth_chunks], max_chunks) chunks; an agent at max_chunks
+    starts a new task of start_chunks fresh chunks.  Returns (keys uint8
+    [n, 32], req_off int64 [agents * turns + 1])."""
+    r = rng(seed)
+    ctx = [r.integers(0, 256, size=(start_chunks, 32), dtype=np.uint8) for _ in range(agents)]
+    first = [True] * agents
+    out, offs = [], [0]
+    for _ in range(turns):
+        for a in range(agents):
+            c = ctx[a]
+            if first[a]:
+                first[a] = False
+            elif len(c) >= max_chunks:
+                c = r.integers(0, 256, size=(start_chunks, 32), dtype=np.uint8)
+            else:
+                n = min(len(c) + int(r.integers(growth_chunks[0], growth_chunks[1] + 1)),
+                        max_chunks)
+                k = int(np.floor(keep * len(c)))
+                c = np.concatenate([c[:k], r.integers(0, 256, size=(n - k, 32), dtype=np.uint8)])
+            ctx[a] = c
+            out.append(c)
+            offs.append(offs[-1] + len(c))
+    keys = np.concatenate(out) if out else np.zeros((0, 32), np.uint8)
+    return keys, np.asarray(offs, np.int64)
+

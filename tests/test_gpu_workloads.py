@@ -218,8 +218,10 @@ def test_agent_pool_metadata_and_bytes():
     assert ot.capacity == tier.capacity == 43690
     pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol)
     declined = evicted = 0
+    records = []
     for t in range(6 * W.POOL_AGENTS):
         rec = pool.turn()
+        records.append(rec)
         assert rec.loaded_ok, f"turn {t}: a loaded page differs from its key's pattern"
         h, hs = ot.lookup(rec.keys)
         assert h == rec.hit and np.array_equal(hs, rec.hit_slots), t
@@ -245,6 +247,21 @@ def test_agent_pool_metadata_and_bytes():
         evicted = sa["evictions_total"]
     # the run crosses the capacity transition: the tier evicts and declines refills
     assert evicted > 0 and declined > 0
+    # the capacity tool on the run's own reference stream, against the oracle's
+    # reference model at the tier's K_H, with and without the run's declines
+    refs = np.concatenate([r.keys for r in records])
+    lens = [len(r.keys) for r in records]
+    dec = np.repeat([not r.save for r in records], lens).astype(np.uint8)
+    prev, _ = api.reuse_distances(refs)
+    full = oracle.lru_reference(refs, tier.capacity).astype(bool)
+    assert np.array_equal((prev >= 0) & (prev < tier.capacity), full)
+    assert np.array_equal(api.lru_simulate(refs, tier.capacity, dec),
+                          oracle.lru_reference(refs, tier.capacity, dec))
+    rep = drivers.stack_report(records, tier.capacity, tier.slot_bytes, [64 << 30])
+    assert rep["hits_measured"] == sum(r.hit for r in records)
+    # the tier's own order with the run's declines predicts every lookup
+    assert np.array_equal(rep["hits_tier_order_per_request"], [r.hit for r in records])
+    assert rep["references"] == len(refs) and rep["declined_new_blocks"] > 0
     tier.close()
     cache.close()
     del kv

@@ -1,9 +1,9 @@
 """Pins of the oracle's LRU reference model (App. "Reference model",
-Lemma 1, Proposition 1; section 3.2, Eq. 3 and Eq. 5).
+Lemma 1, Proposition 1; section 3.2, Eq. 4 and Eq. 5).
 
 The oracle simulates the tier one reference at a time.  These tests check it
 against facts fixed independently of that simulation: reuse distances
-counted by brute force over the stream (Eq. 3 / Lemma 1), the proposition's
+counted by brute force over the stream (Eq. 4 / Lemma 1), the proposition's
 containment of hits, the closed form of a backlogged round-robin pool,
 Mattson's inclusion property, and the unbounded tier.
 """
