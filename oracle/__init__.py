@@ -33,7 +33,7 @@ class Shape(C.Structure):
     _fields_ = [("num_pages", C.c_int32), ("num_layers", C.c_int32),
                 ("page_tokens", C.c_int32), ("num_kv_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("elem_bytes", C.c_int32),
-                ("has_scales", C.c_int32)]
+                ("has_scales", C.c_int32), ("chunk_pages", C.c_int32)]
 
 
 class Policy(C.Structure):
@@ -78,6 +78,7 @@ def lib():
             "eao_tier_chunks": (I64, [I64, I64, I64]),
             "eao_piece_bytes": (I64, [P]), "eao_page_bytes": (I64, [P]),
             "eao_trailer_bytes": (I64, [P]), "eao_slot_bytes": (I64, [P]),
+            "eao_payload_bytes": (I64, [P]),
             "eao_cache_bytes": (I64, [P]), "eao_scale_bytes": (I64, [P]),
             "eao_hash_blocks": (C.c_int, [P, P, I32, I32, P, P, P]),
             "eao_store_blocks": (C.c_int, [P, P, P, P, I64, P, P, U8, I32]),
@@ -144,15 +145,16 @@ def tier_chunks(capacity_bytes, block_tokens, beta):
 
 
 def make_shape(num_pages, num_layers, page_tokens, num_kv_heads, head_dim,
-               elem_bytes, has_scales=False):
+               elem_bytes, has_scales=False, chunk_pages=1):
     return Shape(num_pages, num_layers, page_tokens, num_kv_heads, head_dim,
-                 elem_bytes, int(bool(has_scales)))
+                 elem_bytes, int(bool(has_scales)), chunk_pages)
 
 
 def sizes(shape):
     L = lib()
     p = C.byref(shape)
     return dict(piece=L.eao_piece_bytes(p), page=L.eao_page_bytes(p),
+                payload=L.eao_payload_bytes(p),
                 trailer=L.eao_trailer_bytes(p), slot=L.eao_slot_bytes(p),
                 cache=L.eao_cache_bytes(p), scales=L.eao_scale_bytes(p))
 
@@ -179,33 +181,42 @@ def hash_blocks(tokens, seq_offsets, block_tokens, parents=None):
 
 # ------------------------------------------------------------------- copies
 
+def _chunked(shape, pages, slots):
+    if len(pages) != len(slots) * shape.chunk_pages:
+        raise ValueError("need chunk_pages page ids per slot")
+
+
 def store_blocks(shape, cache, scales, tier, block_ids, host_slots, mask=None):
+    """block_ids: chunk_pages ids per entry of host_slots."""
     num_slots = tier.shape[0]
     block_ids = np.ascontiguousarray(block_ids, dtype=np.int32)
     host_slots = np.ascontiguousarray(host_slots, dtype=np.int64)
+    _chunked(shape, block_ids, host_slots)
     if mask is not None:
         mask = np.ascontiguousarray(mask, dtype=np.uint8)
     rc = lib().eao_store_blocks(C.byref(shape), _ptr(cache), _ptr(scales),
                                 _ptr(tier), num_slots, _ptr(block_ids),
-                                _ptr(host_slots), _ptr(mask), len(block_ids))
+                                _ptr(host_slots), _ptr(mask), len(host_slots))
     _check("eao_store_blocks", rc)
 
 
 def load_blocks(shape, tier, cache, scales, host_slots, dst_pages):
     host_slots = np.ascontiguousarray(host_slots, dtype=np.int64)
     dst_pages = np.ascontiguousarray(dst_pages, dtype=np.int32)
+    _chunked(shape, dst_pages, host_slots)
     rc = lib().eao_load_blocks(C.byref(shape), _ptr(tier), tier.shape[0],
                                _ptr(cache), _ptr(scales), _ptr(host_slots),
-                               _ptr(dst_pages), len(dst_pages))
+                               _ptr(dst_pages), len(host_slots))
     _check("eao_load_blocks", rc)
 
 
 def load_layer(shape, tier, cache, scales, host_slots, dst_pages, layer):
     host_slots = np.ascontiguousarray(host_slots, dtype=np.int64)
     dst_pages = np.ascontiguousarray(dst_pages, dtype=np.int32)
+    _chunked(shape, dst_pages, host_slots)
     rc = lib().eao_load_layer(C.byref(shape), _ptr(tier), tier.shape[0],
                               _ptr(cache), _ptr(scales), _ptr(host_slots),
-                              _ptr(dst_pages), len(dst_pages), layer)
+                              _ptr(dst_pages), len(host_slots), layer)
     _check("eao_load_layer", rc)
 
 

@@ -148,13 +148,16 @@ int64_t eao_piece_bytes(const eao_shape *sh) {
 int64_t eao_page_bytes(const eao_shape *sh) {
   return (int64_t)sh->num_layers * eao_piece_bytes(sh);
 }
+int64_t eao_payload_bytes(const eao_shape *sh) {
+  return (int64_t)sh->chunk_pages * eao_page_bytes(sh);
+}
 int64_t eao_trailer_bytes(const eao_shape *sh) {
   if (!sh->has_scales) return 0;
-  int64_t raw = (int64_t)sh->num_layers * 2 * 4;
+  int64_t raw = (int64_t)sh->num_layers * sh->chunk_pages * 2 * 4;
   return (raw + 255) / 256 * 256;
 }
 int64_t eao_slot_bytes(const eao_shape *sh) {
-  return eao_page_bytes(sh) + eao_trailer_bytes(sh);
+  return eao_payload_bytes(sh) + eao_trailer_bytes(sh);
 }
 int64_t eao_cache_bytes(const eao_shape *sh) {
   return (int64_t)sh->num_layers * sh->num_pages * eao_piece_bytes(sh);
@@ -169,6 +172,7 @@ static int shape_ok(const eao_shape *sh) {
       sh->num_kv_heads < 1 || sh->head_dim < 1 || sh->elem_bytes < 1)
     return 0;
   if (sh->has_scales != 0 && sh->has_scales != 1) return 0;
+  if (sh->chunk_pages < 1) return 0;
   return 1;
 }
 
@@ -232,10 +236,13 @@ int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
   /* validate everything before writing anything */
   uint8_t *seen = (uint8_t *)calloc((size_t)(num_slots > 0 ? num_slots : 1), 1);
   if (!seen) return EAO_ENOMEM;
+  const int64_t C = sh->chunk_pages;
   for (int32_t i = 0; i < n; ++i) {
     if (mask && !mask[i]) continue;
-    if (block_ids[i] < 0 || block_ids[i] >= sh->num_pages ||
-        host_slots[i] < 0 || host_slots[i] >= num_slots || seen[host_slots[i]]) {
+    int bad = host_slots[i] < 0 || host_slots[i] >= num_slots || seen[host_slots[i]];
+    for (int64_t c = 0; c < C && !bad; ++c)
+      bad = block_ids[i * C + c] < 0 || block_ids[i * C + c] >= sh->num_pages;
+    if (bad) {
       free(seen);
       return EAO_EINVAL;
     }
@@ -246,19 +253,21 @@ int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
   const int64_t piece = eao_piece_bytes(sh);
   const int64_t slot_bytes = eao_slot_bytes(sh);
   const int64_t P = sh->num_pages;
+  const int64_t L = sh->num_layers;
   for (int32_t i = 0; i < n; ++i) {
     if (mask && !mask[i]) continue;
     uint8_t *slot = tier + host_slots[i] * slot_bytes;
-    for (int32_t l = 0; l < sh->num_layers; ++l)
-      memcpy(slot + l * piece, cache + ((int64_t)l * P + block_ids[i]) * piece,
-             (size_t)piece);
+    for (int64_t l = 0; l < L; ++l)
+      for (int64_t c = 0; c < C; ++c)  /* chunk position c of layer l */
+        memcpy(slot + (l * C + c) * piece,
+               cache + (l * P + block_ids[i * C + c]) * piece, (size_t)piece);
     if (sh->has_scales) {
-      /* trailer: 8 bytes of scales per layer, then zero padding */
-      uint8_t *trailer = slot + eao_page_bytes(sh);
-      for (int32_t l = 0; l < sh->num_layers; ++l)
-        memcpy(trailer + 8 * l, scales + ((int64_t)l * P + block_ids[i]) * 8, 8);
-      memset(trailer + 8 * (int64_t)sh->num_layers, 0,
-             (size_t)(eao_trailer_bytes(sh) - 8 * (int64_t)sh->num_layers));
+      /* trailer: 8 bytes of scales per (layer, chunk position), then zeros */
+      uint8_t *trailer = slot + eao_payload_bytes(sh);
+      for (int64_t l = 0; l < L; ++l)
+        for (int64_t c = 0; c < C; ++c)
+          memcpy(trailer + 8 * (l * C + c), scales + (l * P + block_ids[i * C + c]) * 8, 8);
+      memset(trailer + 8 * L * C, 0, (size_t)(eao_trailer_bytes(sh) - 8 * L * C));
     }
   }
   return EAO_OK;
@@ -274,13 +283,18 @@ static int load_validate(const eao_shape *sh, const uint8_t *tier,
   if (!cache || !tier || !host_slots || !dst_pages) return EAO_EINVAL;
   uint8_t *seen = (uint8_t *)calloc((size_t)sh->num_pages, 1);
   if (!seen) return EAO_ENOMEM;
+  const int64_t C = sh->chunk_pages;
   for (int32_t i = 0; i < n; ++i) {
-    if (host_slots[i] < 0 || host_slots[i] >= num_slots || dst_pages[i] < 0 ||
-        dst_pages[i] >= sh->num_pages || seen[dst_pages[i]]) {
+    int bad = host_slots[i] < 0 || host_slots[i] >= num_slots;
+    for (int64_t c = 0; c < C && !bad; ++c) {
+      const int32_t d = dst_pages[i * C + c];
+      bad = d < 0 || d >= sh->num_pages || seen[d];
+      if (!bad) seen[d] = 1;
+    }
+    if (bad) {
       free(seen);
       return EAO_EINVAL;
     }
-    seen[dst_pages[i]] = 1;
   }
   free(seen);
   return EAO_OK;
@@ -293,13 +307,17 @@ static void load_one_layer(const eao_shape *sh, const uint8_t *tier,
   const int64_t piece = eao_piece_bytes(sh);
   const int64_t slot_bytes = eao_slot_bytes(sh);
   const int64_t P = sh->num_pages;
+  const int64_t C = sh->chunk_pages;
   for (int32_t i = 0; i < n; ++i) {
     const uint8_t *slot = tier + host_slots[i] * slot_bytes;
-    memcpy(cache + ((int64_t)l * P + dst_pages[i]) * piece, slot + l * piece,
-           (size_t)piece);
-    if (sh->has_scales)
-      memcpy(scales + ((int64_t)l * P + dst_pages[i]) * 8,
-             slot + eao_page_bytes(sh) + 8 * l, 8);
+    for (int64_t c = 0; c < C; ++c) {
+      const int64_t d = dst_pages[i * C + c];
+      memcpy(cache + ((int64_t)l * P + d) * piece, slot + ((int64_t)l * C + c) * piece,
+             (size_t)piece);
+      if (sh->has_scales)
+        memcpy(scales + ((int64_t)l * P + d) * 8,
+               slot + eao_payload_bytes(sh) + 8 * ((int64_t)l * C + c), 8);
+    }
   }
 }
 

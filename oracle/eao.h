@@ -16,11 +16,12 @@
  *   cache  : [L][P][2][T][H][D] elements of elem_bytes  (one (layer, page)
  *            "piece" of 2*T*H*D*elem_bytes bytes is contiguous)
  *   scales : optional [L][P][2] float32 (K scale, V scale), copied as bytes
- *   tier   : [S][slot_bytes]; a slot holds one page of every layer,
- *            [L][2][T][H][D] bytes, followed (when scales exist) by an
- *            [L][2] float32 trailer padded with zeros to a multiple of 256
- *            bytes (a store writes the padding too, so a stored slot is a
- *            complete image).
+ *   tier   : [S][slot_bytes]; a slot holds one chunk of C = chunk_pages
+ *            pages (C = 1: one page) of every layer, [L][C][2][T][H][D]
+ *            bytes (so one layer of a chunk is contiguous), followed (when
+ *            scales exist) by an [L][C][2] float32 trailer padded with
+ *            zeros to a multiple of 256 bytes (a store writes the padding
+ *            too, so a stored slot is a complete image).
  *
  * Status codes mirror the product library: 0 ok, negative on error, and on
  * error nothing is written.
@@ -82,12 +83,15 @@ typedef struct {
   int32_t head_dim;     /* D                                                 */
   int32_t elem_bytes;   /* s: bytes per element (2 for bf16, 1 for fp8)      */
   int32_t has_scales;   /* 1 when a [L][P][2] float32 scale plane exists     */
+  int32_t chunk_pages;  /* C: pages per host slot, one key each (>= 1; the
+                           paper's 1,024-token host chunk is 64 pages of 16) */
 } eao_shape;
 
 int64_t eao_piece_bytes(const eao_shape *sh);  /* 2*T*H*D*s                 */
 int64_t eao_page_bytes(const eao_shape *sh);   /* L * piece                 */
-int64_t eao_trailer_bytes(const eao_shape *sh);/* L*2*4 rounded up to 256, or 0 */
-int64_t eao_slot_bytes(const eao_shape *sh);   /* page + trailer            */
+int64_t eao_payload_bytes(const eao_shape *sh);/* C * L * piece: slot data  */
+int64_t eao_trailer_bytes(const eao_shape *sh);/* L*C*2*4 rounded up to 256, or 0 */
+int64_t eao_slot_bytes(const eao_shape *sh);   /* payload + trailer         */
 int64_t eao_cache_bytes(const eao_shape *sh);  /* L * P * piece             */
 int64_t eao_scale_bytes(const eao_shape *sh);  /* L * P * 8, or 0           */
 
@@ -112,18 +116,19 @@ int eao_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
 /* ------------------------------------------------------------------ copies */
 
 /* Store (host write, "KV copied from GPU to host", section 2): for every i
- * with mask[i] != 0 (mask NULL = all), slot host_slots[i] receives page
- * block_ids[i] of every layer (K and V) and, with scales, the page's
- * [L][2] scales plus zero padding as the slot trailer.  Nothing else
- * changes.  Admitted slots
- * must be distinct; ids and slots must be in range. */
+ * with mask[i] != 0 (mask NULL = all), slot host_slots[i] receives pages
+ * block_ids[i*C .. i*C+C-1] of every layer (K and V), page i*C+c at chunk
+ * position c, and, with scales, their scales plus zero padding as the slot
+ * trailer.  Nothing else changes.  Admitted slots must be distinct; ids
+ * and slots must be in range.  n counts slots (block_ids has n*C entries). */
 int eao_store_blocks(const eao_shape *sh, const uint8_t *cache,
                      const uint8_t *scales, uint8_t *tier, int64_t num_slots,
                      const int32_t *block_ids, const int64_t *host_slots,
                      const uint8_t *mask, int32_t n);
 
-/* Load (host restore, section 3.1): page dst_pages[i] of every layer
- * receives slot host_slots[i] (and its scale trailer).  Destination pages
+/* Load (host restore, section 3.1): pages dst_pages[i*C .. i*C+C-1] of
+ * every layer receive the chunk in slot host_slots[i], chunk position c
+ * into page dst_pages[i*C+c] (with its scales).  The n*C destination pages
  * must be distinct. */
 int eao_load_blocks(const eao_shape *sh, const uint8_t *tier,
                     int64_t num_slots, uint8_t *cache, uint8_t *scales,

@@ -152,3 +152,86 @@ def test_duplicate_sources_allowed():
     oracle.load_blocks(sh, tier, cache, sc, np.array([5, 5]), np.array([0, 1], np.int32))
     c = cache.reshape(sh.num_layers, sh.num_pages, -1)
     assert np.array_equal(c[:, 0], c[:, 1])
+
+
+# ------------------------------------------------- chunked host slots (C > 1)
+
+def _setup_chunked(seed, C, P=48, L=3, scales=False, S=6):
+    sh = oracle.make_shape(P, L, 4, 2, 8, 2, scales, chunk_pages=C)
+    sz = oracle.sizes(sh)
+    rng = np.random.default_rng(seed)
+    cache = rng.integers(0, 256, size=sz["cache"], dtype=np.uint8)
+    sc = rng.integers(0, 256, size=sz["scales"], dtype=np.uint8) if scales else None
+    tier = rng.integers(0, 256, size=(S, sz["slot"]), dtype=np.uint8)
+    return sh, sz, rng, cache, sc, tier
+
+
+def test_chunked_sizes():
+    sh = oracle.make_shape(48, 3, 4, 2, 8, 2, True, chunk_pages=5)
+    sz = oracle.sizes(sh)
+    assert sz["piece"] == 2 * 4 * 2 * 8 * 2 and sz["page"] == 3 * sz["piece"]
+    assert sz["payload"] == 5 * sz["page"]
+    assert sz["trailer"] == 256  # 3 layers x 5 pages x 8 B = 120, padded
+    assert sz["slot"] == sz["payload"] + 256
+    # the paper's host chunk: 1,024 tokens = 64 pages of 16, 24 KiB/token/rank
+    tp8 = oracle.sizes(oracle.make_shape(64, 48, 16, 1, 128, 2, chunk_pages=64))
+    assert tp8["slot"] == 24 << 20
+    # with fp32 scales: 48 layers x 64 pages x 8 B = 24,576 B, already a
+    # multiple of 256
+    fp8 = oracle.sizes(oracle.make_shape(64, 48, 16, 1, 128, 1, True, chunk_pages=64))
+    assert fp8["trailer"] == 24576 and fp8["slot"] == (12 << 20) + 24576
+
+
+@pytest.mark.parametrize("C,scales", [(2, False), (5, True), (8, True)])
+def test_chunked_store_and_load_match_numpy_layout(C, scales):
+    # slot layout [L][C][piece], trailer [L][C][2] float32 then zeros
+    sh, sz, rng, cache, sc, tier = _setup_chunked(10 + C, C, scales=scales)
+    L, P, piece = sh.num_layers, sh.num_pages, sz["piece"]
+    n = 4
+    ids = rng.choice(P, n * C, replace=True).astype(np.int32)  # repeats allowed
+    slots = rng.choice(tier.shape[0], n, replace=False).astype(np.int64)
+    want = tier.copy()
+    c3 = cache.reshape(L, P, piece)
+    for i in range(n):
+        pages = ids[i * C:(i + 1) * C]
+        want[slots[i], :sz["payload"]] = c3[:, pages, :].reshape(-1)  # [L][C][piece]
+        if scales:
+            s3 = sc.reshape(L, P, 8)
+            want[slots[i], sz["payload"]:sz["payload"] + 8 * L * C] = s3[:, pages, :].reshape(-1)
+            want[slots[i], sz["payload"] + 8 * L * C:] = 0
+    oracle.store_blocks(sh, cache, sc, tier, ids, slots)
+    assert np.array_equal(tier, want)
+    # load the chunks back into distinct pages: chunk position c -> dst[i*C+c]
+    dst = rng.choice(P, n * C, replace=False).astype(np.int32)
+    before = cache.copy()
+    before_sc = None if sc is None else sc.copy()
+    oracle.load_blocks(sh, tier, cache, sc, slots, dst)
+    got, was = cache.reshape(L, P, piece), before.reshape(L, P, piece)
+    assert np.array_equal(got[:, dst], was[:, ids])
+    rest = np.setdiff1d(np.arange(P), dst)
+    assert np.array_equal(got[:, rest], was[:, rest])
+    if scales:
+        assert np.array_equal(sc.reshape(L, P, 8)[:, dst], before_sc.reshape(L, P, 8)[:, ids])
+    # per-layer loads compose to the same image
+    cache2 = before.copy()
+    sc2 = None if sc is None else before_sc.copy()
+    for layer in range(L):
+        oracle.load_layer(sh, tier, cache2, sc2, slots, dst, layer)
+    assert np.array_equal(cache2, cache)
+    if scales:
+        assert np.array_equal(sc2, sc)
+
+
+def test_chunked_errors_write_nothing():
+    sh, sz, rng, cache, sc, tier = _setup_chunked(30, 4)
+    t0, c0 = tier.copy(), cache.copy()
+    with pytest.raises(ValueError):  # not chunk_pages ids per slot
+        oracle.store_blocks(sh, cache, sc, tier, np.arange(7, dtype=np.int32), [0, 1])
+    with pytest.raises(oracle.OracleError):  # a page id out of range in the last chunk
+        oracle.store_blocks(sh, cache, sc, tier, np.array([0, 1, 2, 3, 4, 5, 6, 48]), [0, 1])
+    with pytest.raises(oracle.OracleError):  # duplicate destination across chunks
+        oracle.load_blocks(sh, tier, cache, sc, [0, 1], np.array([0, 1, 2, 3, 4, 5, 6, 3]))
+    assert np.array_equal(tier, t0) and np.array_equal(cache, c0)
+    bad = oracle.make_shape(48, 3, 4, 2, 8, 2, chunk_pages=0)
+    with pytest.raises(oracle.OracleError):
+        oracle.store_blocks(bad, cache, None, tier, np.zeros(0, np.int32), np.zeros(0, np.int64))
