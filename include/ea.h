@@ -29,10 +29,12 @@
  *    (layer, page) form one contiguous "piece" of 2*T*H*D*elem_bytes bytes.
  *    The optional scale plane is a caller-owned float32 array [L][P][2]
  *    (K scale, V scale of each layer and page), moved as opaque bytes.
- *  - Host slot layout (library-owned pinned memory): slot s holds one page of
- *    every layer, [L][2][T][H][D], followed when scales exist by an [L][2]
+ *  - Host slot layout (library-owned pinned memory): slot s holds one chunk
+ *    of C = chunk_pages pages (C = 1 unless the tier was created with
+ *    ea_tier_create_chunked) of every layer, [L][C][2][T][H][D], so one layer
+ *    of a chunk is contiguous, followed when scales exist by an [L][C][2]
  *    float32 trailer padded to a multiple of 256 bytes.  The tier holds
- *    K_H = floor(capacity_bytes / slot_bytes) slots.
+ *    K_H = floor(capacity_bytes / slot_bytes) slots; each has one key.
  *  - A tier is internally locked; one tier may be used from several threads.
  *    Calls are bound to the device that was current when the cache or tier
  *    was created.
@@ -91,11 +93,12 @@ typedef struct {
   int64_t capacity_slots; /* K_H                                              */
   int64_t slot_bytes;
   int64_t piece_bytes;
-  int64_t page_bytes;     /* data bytes of a slot (trailer excluded)          */
+  int64_t page_bytes;     /* data bytes of a slot (trailer excluded): C*L*piece */
   int64_t trailer_bytes;
   int64_t capacity_bytes; /* C_H as given at creation                         */
   void *host_base;        /* host address of slot 0 (pinned, mapped)          */
   void *device_base;      /* the same memory as seen by kernels               */
+  int64_t chunk_pages;    /* C: pages per slot                                */
 } ea_tier_info;
 
 /* Create the host tier: K_H = floor(capacity_bytes / slot_bytes) slots of
@@ -107,6 +110,15 @@ typedef struct {
  * EA_EINVAL if K_H < 1, EA_ENOMEM if the pinned allocation fails. */
 int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes,
                    int numa_node, ea_tier **out);
+
+/* The same with host chunks of chunk_pages (C >= 1) pages: one key, one LRU
+ * entry and one slot per chunk (the paper's host chunk of 1,024 tokens is
+ * C = 64 pages of 16 tokens, 24 MiB per rank at TP8: Table "Serving
+ * configuration").  Keys then come from ea_hash_blocks with block_tokens =
+ * C * page_tokens, and stores and loads take C page ids per slot. */
+int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages,
+                           int64_t capacity_bytes, int numa_node,
+                           ea_tier **out);
 
 /* Waits for every transfer the library issued on this tier, then frees it. */
 int ea_tier_destroy(ea_tier *tier);
@@ -258,19 +270,26 @@ int ea_tier_export(const ea_tier *tier, uint8_t *state_out, int32_t *pins_out,
 
 /* ---------------------------------------------------------------- copies */
 
-/* Store ("KV copied from GPU to host", section 2): for every i with
- * admit_mask[i] != 0 (NULL = all), host slot host_slots[i] receives page
- * block_ids[i] of every layer (K and V) and, with scales, the page's [L][2]
- * scales as its trailer.  Admitted slots must be distinct and in [0, K_H);
- * ids in [0, P).  Slots allocated by ea_tier_alloc become resident.  The
- * cache must have the tier's shape. */
+/* Store ("KV copied from GPU to host", section 2): for every i < n with
+ * admit_mask[i] != 0 (NULL = all), host slot host_slots[i] receives pages
+ * block_ids[i*C .. i*C+C-1] of every layer (K and V), page i*C+c at chunk
+ * position c, and, with scales, their scales as its trailer (then zeros).
+ * block_ids has n*C entries (C = the tier's chunk_pages), host_slots and
+ * admit_mask n.  Admitted slots must be distinct and in [0, K_H); ids in
+ * [0, P) (they may repeat).  Slots allocated by ea_tier_alloc become
+ * resident.  The cache must have the tier's shape.  Absent chunks of one
+ * request usually get consecutive slots (lowest free first), so a store
+ * writes long contiguous runs of host memory (App. "Runtime Admission
+ * Details": deduplication passes runs of absent chunks to the store). */
 int ea_store_blocks(ea_cache *cache, ea_tier *tier, const int32_t *block_ids,
                     const int64_t *host_slots, const uint8_t *admit_mask,
                     int32_t n, hipStream_t stream);
 
-/* Load (host restore, the T_load of Eq. 2): page dst_pages[i] of every layer
- * receives host slot host_slots[i] (and its scales).  Destination pages must
- * be distinct; sources may repeat. */
+/* Load (host restore, the T_load of Eq. 2): pages dst_pages[i*C .. i*C+C-1]
+ * of every layer receive the chunk in host slot host_slots[i] (chunk
+ * position c into page dst_pages[i*C+c], with its scales).  host_slots has
+ * n entries, dst_pages n*C.  Destination pages must be distinct; sources may
+ * repeat. */
 int ea_load_blocks(ea_tier *tier, ea_cache *cache, const int64_t *host_slots,
                    const int32_t *dst_pages, int32_t n, hipStream_t stream);
 
@@ -284,11 +303,12 @@ int ea_load_blocks_layered(ea_tier *tier, ea_cache *cache,
                            int32_t n, hipStream_t copy_stream,
                            hipEvent_t *layer_done);
 
-/* Paged gather / scatter between the cache and a DEVICE buffer in slot
- * layout (the HBM half of a staged transfer, also usable on its own):
+/* Paged gather / scatter between the cache and a DEVICE buffer in the slot
+ * layout of one page per slot (the HBM half of a staged transfer, also
+ * usable on its own):
  * gather writes page block_ids[i] (with scales) to d_dst + i*slot_bytes;
  * scatter writes d_src + i*slot_bytes into page dst_pages[i] (destinations
- * distinct).  slot_bytes is the tier's (ea_tier_info) for the same shape. */
+ * distinct).  slot_bytes is that of a tier of the same shape with C = 1. */
 int ea_gather_blocks(ea_cache *cache, const int32_t *block_ids, int32_t n,
                      void *d_dst, hipStream_t stream);
 int ea_scatter_blocks(ea_cache *cache, const void *d_src,

@@ -31,7 +31,8 @@ class TierInfo(C.Structure):
     _fields_ = [("capacity_slots", C.c_int64), ("slot_bytes", C.c_int64),
                 ("piece_bytes", C.c_int64), ("page_bytes", C.c_int64),
                 ("trailer_bytes", C.c_int64), ("capacity_bytes", C.c_int64),
-                ("host_base", C.c_void_p), ("device_base", C.c_void_p)]
+                ("host_base", C.c_void_p), ("device_base", C.c_void_p),
+                ("chunk_pages", C.c_int64)]
 
 
 class Policy(C.Structure):
@@ -66,6 +67,7 @@ SIGNATURES = {
     "ea_cache_create": (_INT, [_P, _P]),
     "ea_cache_destroy": (_INT, [_P]),
     "ea_tier_create": (_INT, [_P, _I64, _INT, _P]),
+    "ea_tier_create_chunked": (_INT, [_P, _I32, _I64, _INT, _P]),
     "ea_tier_destroy": (_INT, [_P]),
     "ea_tier_get_info": (_INT, [_P, _P]),
     "ea_hash_blocks": (_INT, [_P, _P, _I32, _I32, _P, _P, _P, _P]),

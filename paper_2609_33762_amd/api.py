@@ -99,18 +99,20 @@ def make_policy(kappa, block_tokens, beta_rank, theta_ppm=950000, activity_windo
 
 
 class Tier:
-    """Library-owned pinned host tier shaped like `cache`."""
+    """Library-owned pinned host tier shaped like `cache`, one key per slot of
+    chunk_pages pages."""
 
-    def __init__(self, cache, capacity_bytes, numa_node=-1):
+    def __init__(self, cache, capacity_bytes, numa_node=-1, chunk_pages=1):
         lib = N.load()
         self._h = C.c_void_p()
-        N.check("ea_tier_create", lib.ea_tier_create(cache.handle, capacity_bytes, numa_node,
-                                                     C.byref(self._h)))
+        N.check("ea_tier_create_chunked", lib.ea_tier_create_chunked(
+            cache.handle, chunk_pages, capacity_bytes, numa_node, C.byref(self._h)))
         info = N.TierInfo()
         N.check("ea_tier_get_info", lib.ea_tier_get_info(self._h, C.byref(info)))
         self.info = {f: getattr(info, f) for f, _ in N.TierInfo._fields_}
         self.capacity = info.capacity_slots
         self.slot_bytes = info.slot_bytes
+        self.chunk_pages = info.chunk_pages
 
     def close(self):
         if self._h:
@@ -189,27 +191,35 @@ class Tier:
         return p.value
 
     # -------------------------------------------------------------- copies
+    def _pages_per_slot(self, pages, slots):
+        if len(pages) != len(slots) * self.chunk_pages:
+            raise ValueError("need chunk_pages page ids per slot")
+
     def store(self, cache, block_ids, host_slots, mask=None, stream=None):
+        """block_ids: chunk_pages page ids per entry of host_slots."""
         ids, slots = _i32(block_ids), _i64(host_slots)
+        self._pages_per_slot(ids, slots)
         mask = None if mask is None else _u8(mask)
         N.check("ea_store_blocks", N.load().ea_store_blocks(
-            cache.handle, self._h, _ptr(ids), _ptr(slots), _ptr(mask), len(ids),
+            cache.handle, self._h, _ptr(ids), _ptr(slots), _ptr(mask), len(slots),
             _stream(stream)))
 
     def load(self, cache, host_slots, dst_pages, stream=None):
         slots, dst = _i64(host_slots), _i32(dst_pages)
+        self._pages_per_slot(dst, slots)
         N.check("ea_load_blocks", N.load().ea_load_blocks(
-            self._h, cache.handle, _ptr(slots), _ptr(dst), len(dst), _stream(stream)))
+            self._h, cache.handle, _ptr(slots), _ptr(dst), len(slots), _stream(stream)))
 
     def load_layered(self, cache, host_slots, dst_pages, copy_stream, layer_events):
         """layer_events: torch.cuda.Event objects, one per layer."""
         slots, dst = _i64(host_slots), _i32(dst_pages)
+        self._pages_per_slot(dst, slots)
         for e in layer_events:
             if not e.cuda_event:  # torch creates the HIP event at its first record
                 e.record(copy_stream)
         evs = (C.c_void_p * len(layer_events))(*[e.cuda_event for e in layer_events])
         N.check("ea_load_blocks_layered", N.load().ea_load_blocks_layered(
-            self._h, cache.handle, _ptr(slots), _ptr(dst), len(dst),
+            self._h, cache.handle, _ptr(slots), _ptr(dst), len(slots),
             _stream(copy_stream), evs))
 
     def peak_probe(self, dev_buf, nbytes, direction, reps=10):

@@ -251,7 +251,8 @@ struct ea_tier {
   int device = 0;
   int32_t num_layers = 0;
   int32_t has_scales = 0;
-  int64_t piece = 0, page = 0, trailer = 0, slot = 0;
+  int32_t chunk = 1;  // pages per slot
+  int64_t piece = 0, page = 0, payload = 0, trailer = 0, slot = 0;
   int64_t K = 0, capacity_bytes = 0;
   uint8_t *host = nullptr;
   uint8_t *dev = nullptr;
@@ -356,14 +357,17 @@ bool same_shape(const ea_tier *t, const ea_cache *c) {
          (c->d.scale_base != nullptr) == (t->has_scales != 0);
 }
 
-ea::PieceCopy base_copy(const ea_cache *c, int64_t slot_bytes) {
+// A piece copy between the cache and buffers of slots that hold `chunk`
+// pages each (chunk 1 for the cache-level gather/scatter).
+ea::PieceCopy base_copy(const ea_cache *c, int64_t slot_bytes, int32_t chunk) {
   ea::PieceCopy a{};
   a.cache = static_cast<uint8_t *>(c->d.base);
   a.scales = static_cast<uint8_t *>(c->d.scale_base);
   a.num_pages = c->d.num_pages;
   a.piece_bytes = c->piece;
   a.slot_bytes = slot_bytes;
-  a.page_bytes = c->page;
+  a.payload_bytes = c->page * chunk;
+  a.chunk = chunk;
   a.num_layers = c->d.num_layers;
   a.layer_begin = 0;
   a.layer_count = c->d.num_layers;
@@ -372,8 +376,9 @@ ea::PieceCopy base_copy(const ea_cache *c, int64_t slot_bytes) {
   return a;
 }
 
-// Launch a piece copy for n (slot, page) entries: small batches carry their
-// indices in the kernel arguments, larger ones go through the index ring.
+// Launch a piece copy for n (slot, page) entries, one per page (slots null:
+// entry i goes to slot i / a.chunk): small batches carry their indices in
+// the kernel arguments, larger ones go through the index ring.
 int launch_entries(ea::PieceCopy a, IndexRing &ring, const int64_t *slots,
                    const int32_t *pages, int64_t n, int dir, int route, int64_t grid,
                    hipStream_t s) {
@@ -382,7 +387,7 @@ int launch_entries(ea::PieceCopy a, IndexRing &ring, const int64_t *slots,
     ea::InlineIdx inl;
     for (int64_t i = 0; i < n; ++i) {
       inl.pages[i] = pages[i];
-      inl.slots[i] = slots ? slots[i] : i;
+      inl.slots[i] = slots ? slots[i] : i / a.chunk;
     }
     EA_HIP(ea::launch_piece_copy(a, &inl, dir, route, grid, s));
     return EA_OK;
@@ -395,9 +400,10 @@ int launch_entries(ea::PieceCopy a, IndexRing &ring, const int64_t *slots,
 }
 
 // Direct plan: one kernel between the cache and the mapped pinned slots.
+// n entries, one per page; slots[i] is the slot of page entry i.
 int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pages,
                 int64_t n, int dir, hipStream_t s) {
-  ea::PieceCopy a = base_copy(c, t->slot);
+  ea::PieceCopy a = base_copy(c, t->slot, t->chunk);
   a.slots = t->dev;
   a.xcd_mask = dir == ea::kToSlots ? t->xcd_store : t->xcd_load;
   const int res_dir = dir == ea::kToSlots ? EA_DIR_STORE : EA_DIR_LOAD;
@@ -406,7 +412,8 @@ int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
 }
 
 // Staged plan: HBM staging + DMA copies of runs of consecutive slots.
-// Entries are processed in slot order so that consecutive slots coalesce.
+// n slots (slots[i] holds pages[i*C .. i*C+C-1]); slots are processed in
+// increasing order so that consecutive slots coalesce into one DMA.
 int copy_staged(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pages,
                 int64_t n, int dir, hipStream_t s) {
   const int res_dir = dir == ea::kToSlots ? EA_DIR_STORE : EA_DIR_LOAD;
@@ -414,25 +421,26 @@ int copy_staged(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
   DirRes &R = t->res[res_dir];
   if (R.staging_used && R.staging_stream != s) EA_HIP(hipStreamWaitEvent(s, R.staging_ev, 0));
 
+  const int64_t C = t->chunk;
   std::vector<int64_t> order((size_t)n);
   for (int64_t i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(),
                    [&](int64_t x, int64_t y) { return slots[x] < slots[y]; });
   std::vector<int64_t> ss((size_t)n);
-  std::vector<int32_t> pp((size_t)n);
+  std::vector<int32_t> pp((size_t)(n * C));
   for (int64_t i = 0; i < n; ++i) {
     ss[i] = slots[order[i]];
-    pp[i] = pages[order[i]];
+    std::memcpy(&pp[i * C], pages + order[i] * C, (size_t)C * sizeof(int32_t));
   }
   const int64_t per = R.per_half;
-  for (int64_t c0 = 0, chunk = 0; c0 < n; c0 += per, ++chunk) {
+  for (int64_t c0 = 0, half = 0; c0 < n; c0 += per, ++half) {
     const int64_t c1 = std::min(n, c0 + per);
-    uint8_t *stage = R.staging + (chunk & 1) * per * t->slot;
-    ea::PieceCopy a = base_copy(c, t->slot);
+    uint8_t *stage = R.staging + (half & 1) * per * t->slot;
+    ea::PieceCopy a = base_copy(c, t->slot, t->chunk);
     a.slots = stage;
     if (dir == ea::kToSlots)
-      EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0, c1 - c0, dir, ea::kRouteHbm,
-                            t->grid_gather, s));
+      EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0 * C, (c1 - c0) * C, dir,
+                            ea::kRouteHbm, t->grid_gather, s));
     for (int64_t j0 = c0; j0 < c1;) {
       int64_t j1 = j0 + 1;
       while (j1 < c1 && ss[j1] == ss[j1 - 1] + 1) ++j1;
@@ -446,8 +454,8 @@ int copy_staged(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
       j0 = j1;
     }
     if (dir == ea::kToPages)
-      EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0, c1 - c0, dir, ea::kRouteHbm,
-                            t->grid_scatter, s));
+      EA_TRY(launch_entries(a, R.ring, nullptr, pp.data() + c0 * C, (c1 - c0) * C, dir,
+                            ea::kRouteHbm, t->grid_scatter, s));
   }
   EA_HIP(hipEventRecord(R.staging_ev, s));
   R.staging_used = true;
@@ -467,18 +475,29 @@ int validate_cache_desc(const ea_cache_desc *d) {
   return EA_OK;
 }
 
+// n slots, n * C destination pages (all distinct).
 int validate_load(ea_tier *t, ea_cache *c, const int64_t *host_slots,
                   const int32_t *dst_pages, int32_t n) {
   if (!c || !t || n < 0) return EA_EINVAL;
   if (!same_shape(t, c)) return EA_EINVAL;
   if (n == 0) return EA_OK;
   if (!host_slots || !dst_pages) return EA_EINVAL;
-  for (int32_t i = 0; i < n; ++i) {
-    if (dst_pages[i] < 0 || dst_pages[i] >= c->d.num_pages) return EA_EINVAL;
+  if ((int64_t)n * t->chunk > INT32_MAX) return EA_EINVAL;
+  const int64_t m = (int64_t)n * t->chunk;
+  for (int32_t i = 0; i < n; ++i)
     if (host_slots[i] < 0 || host_slots[i] >= t->K) return EA_EINVAL;
-  }
-  if (!all_distinct(dst_pages, n)) return EA_EINVAL;
+  for (int64_t i = 0; i < m; ++i)
+    if (dst_pages[i] < 0 || dst_pages[i] >= c->d.num_pages) return EA_EINVAL;
+  if (!all_distinct(dst_pages, m)) return EA_EINVAL;
   return EA_OK;
+}
+
+// The slot of every page entry: slot i repeated C times.
+std::vector<int64_t> per_page_slots(const int64_t *slots, int64_t n, int64_t C) {
+  std::vector<int64_t> v((size_t)(n * C));
+  for (int64_t i = 0; i < n; ++i)
+    for (int64_t c = 0; c < C; ++c) v[(size_t)(i * C + c)] = slots[i];
+  return v;
 }
 
 }  // namespace
@@ -530,8 +549,17 @@ int ea_cache_destroy(ea_cache *cache) {
 
 int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes, int numa_node,
                    ea_tier **out) {
-  if (!shape || !out || capacity_bytes <= 0) return EA_EINVAL;
-  const int64_t K = capacity_bytes / shape->slot;
+  return ea_tier_create_chunked(shape, 1, capacity_bytes, numa_node, out);
+}
+
+int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t capacity_bytes,
+                           int numa_node, ea_tier **out) {
+  if (!shape || !out || capacity_bytes <= 0 || chunk_pages < 1) return EA_EINVAL;
+  const int64_t payload = shape->page * chunk_pages;
+  const int64_t trailer =
+      shape->d.scale_base ? ((int64_t)shape->d.num_layers * chunk_pages * 8 + 255) / 256 * 256 : 0;
+  const int64_t slot_bytes = payload + trailer;
+  const int64_t K = capacity_bytes / slot_bytes;
   if (K < 1) return EA_EINVAL;
   DeviceScope ds(shape->device);
   EA_TRY(ds.status());
@@ -540,10 +568,12 @@ int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes, int numa_node,
   t->device = shape->device;
   t->num_layers = shape->d.num_layers;
   t->has_scales = shape->d.scale_base != nullptr;
+  t->chunk = chunk_pages;
   t->piece = shape->piece;
   t->page = shape->page;
-  t->trailer = shape->trailer;
-  t->slot = shape->slot;
+  t->payload = payload;
+  t->trailer = trailer;
+  t->slot = slot_bytes;
   t->K = K;
   t->capacity_bytes = capacity_bytes;
   t->grid_link = grid_link();
@@ -617,11 +647,12 @@ int ea_tier_get_info(const ea_tier *t, ea_tier_info *info) {
   info->capacity_slots = t->K;
   info->slot_bytes = t->slot;
   info->piece_bytes = t->piece;
-  info->page_bytes = t->page;
+  info->page_bytes = t->payload;
   info->trailer_bytes = t->trailer;
   info->capacity_bytes = t->capacity_bytes;
   info->host_base = t->host;
   info->device_base = t->dev;
+  info->chunk_pages = t->chunk;
   return EA_OK;
 }
 
@@ -700,16 +731,21 @@ int ea_store_blocks(ea_cache *c, ea_tier *t, const int32_t *block_ids,
   if (!same_shape(t, c)) return EA_EINVAL;
   if (n == 0) return EA_OK;
   if (!block_ids || !host_slots) return EA_EINVAL;
+  const int64_t C = t->chunk;
+  if ((int64_t)n * C > INT32_MAX) return EA_EINVAL;
   std::vector<int64_t> slots;
   std::vector<int32_t> pages;
   slots.reserve((size_t)n);
-  pages.reserve((size_t)n);
+  pages.reserve((size_t)(n * C));
   for (int32_t i = 0; i < n; ++i) {
     if (admit_mask && !admit_mask[i]) continue;
-    if (block_ids[i] < 0 || block_ids[i] >= c->d.num_pages) return EA_EINVAL;
     if (host_slots[i] < 0 || host_slots[i] >= t->K) return EA_EINVAL;
+    for (int64_t k = 0; k < C; ++k) {
+      const int32_t p = block_ids[i * C + k];
+      if (p < 0 || p >= c->d.num_pages) return EA_EINVAL;
+      pages.push_back(p);
+    }
     slots.push_back(host_slots[i]);
-    pages.push_back(block_ids[i]);
   }
   const int64_t m = (int64_t)slots.size();
   if (!all_distinct(slots.data(), m)) return EA_EINVAL;
@@ -718,10 +754,12 @@ int ea_store_blocks(ea_cache *c, ea_tier *t, const int32_t *block_ids,
   EA_TRY(ds.status());
   std::lock_guard<std::mutex> lk(t->mu);
   EA_TRY(wait_slot_hazards(t, slots.data(), m, stream));
-  if (resolve_plan(t, EA_DIR_STORE) == EA_PLAN_STAGED)
+  if (resolve_plan(t, EA_DIR_STORE) == EA_PLAN_STAGED) {
     EA_TRY(copy_staged(t, c, slots.data(), pages.data(), m, ea::kToSlots, stream));
-  else
-    EA_TRY(copy_direct(t, c, slots.data(), pages.data(), m, ea::kToSlots, stream));
+  } else {
+    const std::vector<int64_t> each = per_page_slots(slots.data(), m, C);
+    EA_TRY(copy_direct(t, c, each.data(), pages.data(), m * C, ea::kToSlots, stream));
+  }
   EA_TRY(note_slot_transfer(t, slots.data(), m, stream));
   for (int64_t i = 0; i < m; ++i) t->meta->mark_stored(slots[i]);
   t->bytes_stored += m * t->slot;
@@ -737,10 +775,13 @@ int ea_load_blocks(ea_tier *t, ea_cache *c, const int64_t *host_slots,
   EA_TRY(ds.status());
   std::lock_guard<std::mutex> lk(t->mu);
   EA_TRY(wait_slot_hazards(t, host_slots, n, stream));
-  if (resolve_plan(t, EA_DIR_LOAD) == EA_PLAN_STAGED)
+  if (resolve_plan(t, EA_DIR_LOAD) == EA_PLAN_STAGED) {
     EA_TRY(copy_staged(t, c, host_slots, dst_pages, n, ea::kToPages, stream));
-  else
-    EA_TRY(copy_direct(t, c, host_slots, dst_pages, n, ea::kToPages, stream));
+  } else {
+    const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
+    EA_TRY(copy_direct(t, c, each.data(), dst_pages, (int64_t)n * t->chunk, ea::kToPages,
+                       stream));
+  }
   EA_TRY(note_slot_transfer(t, host_slots, n, stream));
   t->bytes_loaded += (int64_t)n * t->slot;
   t->load_calls += 1;
@@ -765,23 +806,25 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
   EA_TRY(wait_slot_hazards(t, host_slots, n, copy_stream));
   // the pieces of one layer are strided inside the slots, so every layer is
   // its own direct kernel over all n slots
-  ea::PieceCopy a = base_copy(c, t->slot);
+  const int64_t m = (int64_t)n * t->chunk;  // page entries
+  const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
+  ea::PieceCopy a = base_copy(c, t->slot, t->chunk);
   a.slots = t->dev;
   a.xcd_mask = t->xcd_load;
-  a.n = n;
+  a.n = m;
   a.layer_count = 1;
   ea::InlineIdx inl;
   const ea::InlineIdx *pin = nullptr;
   IndexRing &ring = t->res[EA_DIR_LOAD].ring;
   int region = -1;
-  if (n <= ea::kInlineMax) {
-    for (int32_t i = 0; i < n; ++i) {
+  if (m <= ea::kInlineMax) {
+    for (int64_t i = 0; i < m; ++i) {
       inl.pages[i] = dst_pages[i];
-      inl.slots[i] = host_slots[i];
+      inl.slots[i] = each[(size_t)i];
     }
     pin = &inl;
   } else {
-    EA_TRY(ring.upload(host_slots, dst_pages, n, &a.slot_idx, &a.pages, &region));
+    EA_TRY(ring.upload(each.data(), dst_pages, m, &a.slot_idx, &a.pages, &region));
   }
   for (int32_t l = 0; l < c->d.num_layers; ++l) {
     a.layer_begin = l;
@@ -808,7 +851,7 @@ int ea_gather_blocks(ea_cache *c, const int32_t *block_ids, int32_t n, void *d_d
   DeviceScope ds(c->device);
   EA_TRY(ds.status());
   std::lock_guard<std::mutex> lk(c->mu);
-  ea::PieceCopy a = base_copy(c, c->slot);
+  ea::PieceCopy a = base_copy(c, c->slot, 1);
   a.slots = static_cast<uint8_t *>(d_dst);
   return launch_entries(a, c->ring, nullptr, block_ids, n, ea::kToSlots, ea::kRouteHbm,
                         grid_hbm(ea::kToSlots), stream);
@@ -825,7 +868,7 @@ int ea_scatter_blocks(ea_cache *c, const void *d_src, const int32_t *dst_pages, 
   DeviceScope ds(c->device);
   EA_TRY(ds.status());
   std::lock_guard<std::mutex> lk(c->mu);
-  ea::PieceCopy a = base_copy(c, c->slot);
+  ea::PieceCopy a = base_copy(c, c->slot, 1);
   a.slots = static_cast<uint8_t *>(const_cast<void *>(d_src));
   return launch_entries(a, c->ring, nullptr, dst_pages, n, ea::kToPages, ea::kRouteHbm,
                         grid_hbm(ea::kToPages), stream);

@@ -35,15 +35,18 @@ __device__ __forceinline__ u32x4 load_nt(const u32x4 *p) { return __builtin_nont
 __device__ __forceinline__ void store_nt(u32x4 *p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
 // Copy unit u: layer layer_begin + (u mod layer_count) of entry i, whose
-// page and slot the caller has made wave-uniform.
+// page and slot the caller has made wave-uniform.  The entry's piece sits at
+// chunk position c = i mod C of layer l inside the slot.
 template <int DIR, bool INLINE, int VEC>
 __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t i, int64_t page,
                                           int64_t slot, int lane) {
   const int64_t nvec = a.piece_bytes >> 4;
   const int64_t l = a.layer_begin + (u - i * a.layer_count);
+  const int64_t c = a.chunk == 1 ? 0 : (int64_t)((uint32_t)i % (uint32_t)a.chunk);
+  const int64_t at = l * a.chunk + c;  // piece index inside the slot
   uint8_t *cache_piece = a.cache + (l * a.num_pages + page) * a.piece_bytes;
   uint8_t *slot_base = a.slots + slot * a.slot_bytes;
-  uint8_t *slot_piece = slot_base + l * a.piece_bytes;
+  uint8_t *slot_piece = slot_base + at * a.piece_bytes;
   const u32x4 *src = reinterpret_cast<const u32x4 *>(DIR == kToSlots ? cache_piece : slot_piece);
   u32x4 *dst = reinterpret_cast<u32x4 *>(DIR == kToSlots ? slot_piece : cache_piece);
   for (int64_t base = 0; base < nvec; base += (int64_t)kWave * VEC) {
@@ -61,12 +64,12 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t
   }
   if (a.scales != nullptr) {
     uint64_t *cs = reinterpret_cast<uint64_t *>(a.scales + (l * a.num_pages + page) * 8);
-    uint64_t *ss = reinterpret_cast<uint64_t *>(slot_base + a.page_bytes + l * 8);
+    uint64_t *ss = reinterpret_cast<uint64_t *>(slot_base + a.payload_bytes + at * 8);
     if (lane == 0) {
       if (DIR == kToSlots) *ss = *cs; else *cs = *ss;
     }
-    if (DIR == kToSlots && l == 0) {
-      const int64_t pad_begin = a.page_bytes + 8 * (int64_t)a.num_layers;
+    if (DIR == kToSlots && at == 0) {  // once per slot
+      const int64_t pad_begin = a.payload_bytes + 8 * (int64_t)a.num_layers * a.chunk;
       const int64_t pad_words = (a.slot_bytes - pad_begin) >> 3;
       uint64_t *pad = reinterpret_cast<uint64_t *>(slot_base + pad_begin);
       for (int64_t w = lane; w < pad_words; w += kWave) pad[w] = 0;
@@ -109,7 +112,7 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
       if (ul < units) {
         const int64_t il = ul / a.layer_count;
         vpage = pages[il];
-        vslot = a.identity_slots ? il : slot_idx[il];
+        vslot = a.identity_slots ? (int64_t)((uint32_t)il / (uint32_t)a.chunk) : slot_idx[il];
       }
       for (int k = 0; k < kWave; ++k) {
         const int64_t u = u0 + (int64_t)k * waves;
@@ -171,6 +174,8 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
   if (a.num_xcd < 1 || a.num_xcd > 32 || a.xcd_mask == 0 ||
       (a.num_xcd < 32 && (a.xcd_mask >> a.num_xcd) != 0))
     return hipErrorInvalidValue;
+  // entry indices and chunk positions are computed in 32 bits
+  if (a.chunk < 1 || a.n > INT32_MAX) return hipErrorInvalidValue;
   const int64_t waves_per_group = kThreads / kWave;
   const int64_t needed = (units + waves_per_group - 1) / waves_per_group;
   const int64_t work = needed < workgroups ? needed : workgroups;

@@ -14,21 +14,26 @@ enum CopyDir : int { kToSlots = 0, kToPages = 1 };
 // device index array (the small-batch latency path).
 constexpr int kInlineMax = 32;
 
+// A slot holds a chunk of `chunk` (C) pages laid out [L][C][piece], then the
+// [L][C][8]-byte scale trailer.  Entry i is one page: it goes to chunk
+// position i % C of its slot.
 struct PieceCopy {
   uint8_t *cache;            // [L][P][piece] bytes
   uint8_t *scales;           // [L][P][8] bytes or nullptr
   uint8_t *slots;            // slot-layout buffer (host mapping or HBM staging)
   const int32_t *pages;      // device [n] or nullptr when inline
-  const int64_t *slot_idx;   // device [n] or nullptr when inline / identity
-  int64_t n;                 // entries
+  const int64_t *slot_idx;   // device [n] (slot of each entry) or nullptr when
+                             // inline / identity
+  int64_t n;                 // entries (pages)
   int64_t num_pages;         // P
   int64_t piece_bytes;       // multiple of 16
   int64_t slot_bytes;
-  int64_t page_bytes;        // offset of the scale trailer inside a slot
-  int32_t num_layers;        // L (the trailer holds 8 bytes per layer)
+  int64_t payload_bytes;     // C * L * piece: offset of the scale trailer
+  int32_t num_layers;        // L
+  int32_t chunk;             // C >= 1
   int32_t layer_begin;
   int32_t layer_count;
-  int32_t identity_slots;    // slot index of entry i is i (staging buffers)
+  int32_t identity_slots;    // slot of entry i is i / C (staging buffers)
   // Workgroups are dispatched round-robin over the XCDs (workgroup b runs on
   // XCD b % num_xcd); only workgroups on XCDs in xcd_mask do work.
   int32_t num_xcd;

@@ -49,6 +49,10 @@ QWEN3 = Shape("qwen3_30b_a3b_turn", 48, 4, 128, 2, 16, 20000)
 QWEN3_TIER_BYTES = 16 << 30
 QWEN3_STORE_PAGES = 2000
 QWEN3_LOAD_PAGES = 1500
+# The same model's KV on one rank of TP8 (1 KV head: 24 KiB per token) with
+# the paper's host chunk of 1,024 tokens = 64 pages (24 MiB per slot).
+QWEN3_TP8 = Shape("qwen3_30b_a3b_tp8_shard", 48, 1, 128, 2, 16, 20000)
+CHUNK_PAGES = 64
 # Agent pool: same KV shape, 64 agents, 64 GiB tier.
 POOL_TIER_BYTES = 64 << 30
 POOL_AGENTS = 64

@@ -19,11 +19,11 @@ class Pair:
     """A GPU cache + pinned tier and the oracle's view of the same shape."""
 
     def __init__(self, num_pages, num_layers, page_tokens, heads, head_dim, elem_bytes,
-                 slots, scales=False, seed=0, fp8=False):
+                 slots, scales=False, seed=0, fp8=False, chunk_pages=1):
         torch = need_gpu()
         self.torch = torch
         self.oshape = oracle.make_shape(num_pages, num_layers, page_tokens, heads, head_dim,
-                                        elem_bytes, scales)
+                                        elem_bytes, scales, chunk_pages)
         self.sizes = oracle.sizes(self.oshape)
         self.kv = torch.empty(self.sizes["cache"], dtype=torch.uint8, device="cuda")
         if fp8 or elem_bytes == 1:
@@ -36,7 +36,7 @@ class Pair:
             W.fill_random_bytes(self.sc, seed + 1000)
         self.cache = api.Cache(self.kv, num_pages, num_layers, page_tokens, heads, head_dim,
                                elem_bytes, scales=self.sc)
-        self.tier = api.Tier(self.cache, slots * self.sizes["slot"])
+        self.tier = api.Tier(self.cache, slots * self.sizes["slot"], chunk_pages=chunk_pages)
         assert self.tier.capacity == slots
         assert self.tier.slot_bytes == self.sizes["slot"]
         # poison the host tier so that untouched slots are recognisable
