@@ -559,6 +559,136 @@ def summarize_profiles(d):
     print(open(TRAFFIC_SUMMARY).read())
 
 
+def _quiet_cache(torch, api, sh, num_pages=None):
+    """A cache of shape sh (contents irrelevant for timing: left unfilled)."""
+    P = num_pages or sh.num_pages
+    kv = torch.empty(sh.num_layers * P * sh.piece_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, P, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                      sh.elem_bytes)
+    return kv, cache
+
+
+def run_load_cost(args):
+    """Restore cost of Eq. 2, T_load(n) = n beta / B_eff + tau_load, fitted
+    from load sweeps on the Qwen3 turn shape (96 KiB/token), the dense shape
+    (128 KiB/token), one TP8 rank of Qwen3 (24 KiB/token) with 16-token slots
+    and with 1,024-token chunks.  Each point is the median of repeated loads
+    of n random resident slots into random free pages, timed on the device
+    (HIP events) and end to end (call to completion on the host clock)."""
+    import torch
+    from paper_2609_33762_amd import api, drivers, workloads as W
+    torch.cuda.set_device(0)
+    cur = torch.cuda.current_stream()
+    setups = [
+        ("qwen3_96KiB_per_token", W.QWEN3, 1, [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 1500]),
+        ("dense_128KiB_per_token", W.DENSE, 1, [1, 2, 3, 4, 5, 6, 7, 8, 16, 64, 256, 1024]),
+        ("qwen3_tp8_24KiB_per_token", W.QWEN3_TP8, 1,
+         [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 1500]),
+        ("qwen3_tp8_1024_token_chunks", W.QWEN3_TP8, W.CHUNK_PAGES, [1, 2, 4, 8, 16, 23]),
+    ]
+    r = W.rng(W.SEED_IDS)
+    res = {}
+    for name, sh, C, sizes in setups:
+        kv, cache = _quiet_cache(torch, api, sh)
+        beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+        top = max(sizes)
+        tier = api.Tier(cache, top * C * sh.num_layers * sh.piece_bytes + 4096, chunk_pages=C)
+        assert tier.capacity >= top
+        src = W.distinct(r, sh.num_pages, top * C)
+        tier.store(cache, src, np.arange(top), stream=cur)
+        torch.cuda.synchronize()
+        pts = []
+        for n in sizes:
+            reps = 40 if n * C <= 64 else (10 if n * C <= 512 else 5)
+            dev_ms, wall_ms = [], []
+            for _ in range(reps):
+                slots = W.distinct(r, top, n)
+                dst = W.distinct(r, sh.num_pages, n * C)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                e0.record(cur)
+                tier.load(cache, slots, dst, stream=cur)
+                e1.record(cur)
+                e1.synchronize()
+                wall_ms.append((time.perf_counter() - t0) * 1e3)
+                dev_ms.append(e0.elapsed_time(e1))
+            pts.append([n * C * sh.page_tokens, n * tier.slot_bytes, float(np.median(dev_ms)),
+                        float(np.median(wall_ms))])
+        tier.close()
+        cache.close()
+        del kv
+        torch.cuda.empty_cache()
+        tok = np.array([p[0] for p in pts], np.float64)
+        nb = tok * beta
+        fits = {}
+        for k, col in (("device", 2), ("end_to_end", 3)):
+            B, tau, resid = drivers.fit_load_cost(nb, np.array([p[col] for p in pts]) * 1e-3)
+            fits[k] = {"B_eff_gbs": round(float(B) / GB, 2), "tau_load_us": round(float(tau) * 1e6, 1),
+                       "us_per_token_large_n": round(float(beta / B) * 1e6, 4),
+                       "max_rel_residual": round(resid, 3)}
+        res[name] = {"beta_bytes_per_token": beta, "chunk_pages": C, "fit": fits,
+                     "points_tokens_bytes_devms_wallms": [[int(a), int(b), round(c, 4), round(d, 4)]
+                                                         for a, b, c, d in pts]}
+        log(f"{name}: {fits}")
+    head = res["qwen3_96KiB_per_token"]["fit"]["device"]
+    return _line("load_cost: load sweeps, T_load(n) = n beta / B_eff + tau_load fitted at "
+                 "96/128/24 KiB per token and 1,024-token chunks", head["B_eff_gbs"], "GB/s",
+                 None, sum(len(x[3]) for x in setups), {"load_cost": res})
+
+
+def run_tp8_shard(args):
+    """One Qwen3 turn on a TP8 rank's share (1 KV head, 24 KiB/token):
+    a 2,000-page refill stored and a 1,500-page prefix loaded, alone and
+    together on two streams, with 16-token slots and with 1,024-token chunks
+    (31 and 23 chunks of 24 MiB)."""
+    import torch
+    from paper_2609_33762_amd import api, workloads as W
+    torch.cuda.set_device(0)
+    sh = W.QWEN3_TP8
+    r = W.rng(W.SEED_IDS)
+    kv, cache = _quiet_cache(torch, api, sh)
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    out = {}
+    for C, n_s, n_l in ((1, 2000, 1500), (W.CHUNK_PAGES, 31, 23)):
+        tier = api.Tier(cache, W.QWEN3_TIER_BYTES, chunk_pages=C)
+        prefix = W.distinct(r, sh.num_pages, n_l * C)
+        refill = W.distinct(r, sh.num_pages, n_s * C, exclude=prefix)
+        dst = W.distinct(r, sh.num_pages, n_l * C, exclude=np.concatenate([prefix, refill]))
+        pslots = np.arange(n_l)
+        sslots = np.arange(n_l, n_l + n_s)
+        tier.store(cache, prefix, pslots)
+        torch.cuda.synchronize()
+        cur = torch.cuda.current_stream()
+        st_ms = event_ms(torch, lambda: tier.store(cache, refill, sslots, stream=cur), cur, 5)
+        ld_ms = event_ms(torch, lambda: tier.load(cache, pslots, dst, stream=cur), cur, 5)
+        s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
+        both = []
+        for _ in range(5):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            tier.load(cache, pslots, dst, stream=s_load)
+            tier.store(cache, refill, sslots, stream=s_store)
+            torch.cuda.synchronize()
+            both.append(time.perf_counter() - t0)
+        sb, lb = n_s * tier.slot_bytes, n_l * tier.slot_bytes
+        key = "page_slots" if C == 1 else "chunk_slots_1024_tokens"
+        out[key] = {"slot_bytes": tier.slot_bytes, "store_slots": n_s, "load_slots": n_l,
+                    "store_gbs": round(sb / (st_ms * 1e-3) / GB, 2),
+                    "load_gbs": round(lb / (ld_ms * 1e-3) / GB, 2),
+                    "duplex_gbs": round((sb + lb) / float(np.median(both)) / GB, 2),
+                    "load_us_per_token": round(ld_ms * 1e3 / (n_l * C * sh.page_tokens), 4)}
+        log(f"tp8 shard, {key}: {out[key]}")
+        tier.close()
+    cache.close()
+    del kv
+    torch.cuda.empty_cache()
+    return _line("tp8_shard: Qwen3 turn on one TP8 rank (24 KiB/token), 16-token slots and "
+                 "1,024-token chunks", out["page_slots"]["duplex_gbs"], "GB/s", None, 5,
+                 {"tp8_shard": out, "beta_bytes_per_token": beta})
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -569,7 +699,8 @@ def main():
     ap.add_argument("--isolated-only", action="store_true")
     ap.add_argument("--summarize-profiles", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
-                    choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny"])
+                    choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
+                             "load_cost", "tp8_shard"])
     ap.add_argument("--turns-per-agent", type=int, default=24)
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
     args = ap.parse_args()
@@ -582,7 +713,8 @@ def main():
               "(use --gpus 1)", file=sys.stderr)
         sys.exit(2)
     other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,
-             "layered_fp8": run_layered, "tiny": run_tiny}
+             "layered_fp8": run_layered, "tiny": run_tiny, "load_cost": run_load_cost,
+             "tp8_shard": run_tp8_shard}
     if args.workload in other:
         out = other[args.workload](args)
         log(json.dumps(out))

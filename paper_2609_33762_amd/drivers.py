@@ -280,3 +280,16 @@ def stack_report(records, capacity_slots, slot_bytes, curve_bytes=()):
             for i, b in enumerate(curve_bytes)},
         "tool_seconds": round(tool_s, 3),
     }
+
+
+# ------------------------------------------------------ restore cost (Eq. 2)
+
+def fit_load_cost(nbytes, seconds):
+    """Least-squares fit of T_load = bytes / B_eff + tau_load (Eq. 2 with
+    n * beta_rank bytes).  Returns (B_eff in bytes/s, tau_load in s, largest
+    relative residual)."""
+    x = np.asarray(nbytes, np.float64)
+    y = np.asarray(seconds, np.float64)
+    a, tau = np.polyfit(x, y, 1)
+    resid = np.abs(a * x + tau - y) / y
+    return 1.0 / a, tau, float(resid.max())
