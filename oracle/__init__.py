@@ -49,6 +49,11 @@ class Request(C.Structure):
                 ("decided", C.c_int32), ("_pad", C.c_int32)]
 
 
+class TierReport(C.Structure):
+    _fields_ = [("time", C.c_int64), ("registered", C.c_int64),
+                ("capacity_slots", C.c_int64), ("evictions", C.c_int64)]
+
+
 class TierStats(C.Structure):
     _fields_ = [("capacity_slots", C.c_int64), ("registered", C.c_int64),
                 ("resident", C.c_int64), ("pinned", C.c_int64),
@@ -89,6 +94,8 @@ def lib():
             "eao_tier_capacity": (I64, [P]),
             "eao_tier_lookup": (C.c_int, [P, P, I64, P, P]),
             "eao_admission_fill": (C.c_int, [P, P, P, P, I64, P, P]),
+            "eao_admission_fill_report": (C.c_int, [P, P, P, P, I64, P, I64, P, P]),
+            "eao_tier_publish": (C.c_int, [P, I64, I64, P]),
             "eao_tier_alloc": (C.c_int, [P, P, P, I64, P, P]),
             "eao_tier_mark_stored": (C.c_int, [P, P, P, I64]),
             "eao_tier_unpin": (C.c_int, [P, P, I64]),
@@ -267,6 +274,27 @@ class Tier:
         _check("eao_admission_fill", lib().eao_admission_fill(
             self._h, C.byref(policy), C.byref(req), _ptr(keys) if n else None, n,
             _ptr(mask), C.byref(save)))
+        return save.value, mask[:n].copy()
+
+    def publish(self, now, window):
+        """Telemetry report at time `now` (advances the tier's clock)."""
+        rep = TierReport()
+        _check("eao_tier_publish", lib().eao_tier_publish(self._h, now, window, C.byref(rep)))
+        return rep
+
+    def admission_report(self, policy, n_tokens, h_tokens, task_id, now, keys, report,
+                         max_age, decided=-1):
+        """Admission with the telemetry factor from `report` (a TierReport or
+        None) when it is fresh."""
+        keys = np.ascontiguousarray(keys, dtype=np.uint8).reshape(-1, 32)
+        n = keys.shape[0]
+        req = Request(n_tokens, h_tokens, task_id, now, decided, 0)
+        mask = np.zeros(max(n, 1), np.uint8)
+        save = C.c_int32()
+        _check("eao_admission_fill_report", lib().eao_admission_fill_report(
+            self._h, C.byref(policy), C.byref(req),
+            None if report is None else C.byref(report), max_age,
+            _ptr(keys) if n else None, n, _ptr(mask), C.byref(save)))
         return save.value, mask[:n].copy()
 
     def alloc(self, keys, mask=None):

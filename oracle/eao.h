@@ -218,6 +218,31 @@ int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
                        const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
                        int32_t *save_out);
 
+/* Telemetry a worker publishes (App. "Runtime Admission Details": every
+ * second, the chunks registered in the tier, its capacity K_H and the
+ * evictions made to allocate in the last window). */
+typedef struct {
+  int64_t time;            /* clock value the report was taken at           */
+  int64_t registered;      /* pending + resident chunks                     */
+  int64_t capacity_slots;  /* K_H                                           */
+  int64_t evictions;       /* e_t: evictions stamped in (time - window, time] */
+} eao_tier_report;
+
+/* Take the report at time `now` (not below the tier's clock) and advance
+ * the tier's clock to it: evictions are stamped with the tier's clock, the
+ * latest time it has been told by a decision or a report. */
+int eao_tier_publish(eao_tier *t, int64_t now, int64_t window, eao_tier_report *out);
+
+/* eao_admission_fill with the "full and evicting" factor taken from the
+ * scheduler's copy of a published report: used when policy->telemetry is 1,
+ * report is not NULL and 0 <= r->now - report->time <= max_age (a fresh
+ * report); otherwise the working-set estimate alone decides (Eq. 10 and the
+ * text after it).  max_age >= 0. */
+int eao_admission_fill_report(eao_tier *t, const eao_policy *p, const eao_request *r,
+                              const eao_tier_report *report, int64_t max_age,
+                              const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                              int32_t *save_out);
+
 /* Allocate a slot for every i with mask[i] != 0 whose key is not already
  * registered: the lowest-numbered free slot, else the least-recent resident
  * unpinned slot (an eviction).  New slots are PENDING, registered under the

@@ -180,10 +180,15 @@ static int log_append(eao_tier *t, int64_t task, int64_t n, int64_t now) {
   return EAO_OK;
 }
 
-int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
-                       const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
-                       int32_t *save_out) {
+/* Where the "tier full and evicting" factor comes from. */
+enum { TELEMETRY_POLICY = 0, TELEMETRY_REPORT = 1 };
+
+static int admission(eao_tier *t, const eao_policy *p, const eao_request *r,
+                     int source, const eao_tier_report *rep, int64_t max_age,
+                     const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                     int32_t *save_out) {
   if (!t || !p || !r || !save_out || n_keys < 0) return EAO_EINVAL;
+  if (source == TELEMETRY_REPORT && max_age < 0) return EAO_EINVAL;
   if (n_keys > 0 && (!keys || !mask_out)) return EAO_EINVAL;
   if (p->block_tokens < 1 || p->kappa < 0 || p->beta_rank < 0 ||
       p->activity_window < 0 || p->length_window < 1 || p->theta_ppm < 0 ||
@@ -235,7 +240,18 @@ int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
     int over = lhs > rhs;
 
     int pressure;
-    if (p->telemetry) {
+    if (source == TELEMETRY_REPORT) {
+      /* the scheduler's copy of the last published report, if fresh */
+      int fresh = p->telemetry && rep != NULL && rep->time <= r->now &&
+                  r->now - rep->time <= max_age;
+      if (fresh) {
+        int full = (unsigned __int128)rep->registered * 1000000u >=
+                   (unsigned __int128)p->theta_ppm * (unsigned __int128)rep->capacity_slots;
+        pressure = over && full && rep->evictions > 0;
+      } else {
+        pressure = over;  /* no fresh report: the estimate alone decides */
+      }
+    } else if (p->telemetry) {
       /* tier full and evicting: o_t >= theta and e_t > 0 (Eq. 10) */
       int full = (unsigned __int128)t->registered * 1000000u >=
                  (unsigned __int128)p->theta_ppm * (unsigned __int128)t->K;
@@ -261,6 +277,37 @@ int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
   for (int64_t i = 0; i < n_keys; ++i)
     mask_out[i] = (uint8_t)(save && map_find(t, keys + 32 * i) < 0);
   *save_out = save;
+  return EAO_OK;
+}
+
+int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
+                       const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                       int32_t *save_out) {
+  return admission(t, p, r, TELEMETRY_POLICY, NULL, 0, keys, n_keys, mask_out, save_out);
+}
+
+int eao_admission_fill_report(eao_tier *t, const eao_policy *p, const eao_request *r,
+                              const eao_tier_report *report, int64_t max_age,
+                              const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                              int32_t *save_out) {
+  return admission(t, p, r, TELEMETRY_REPORT, report, max_age, keys, n_keys, mask_out,
+                   save_out);
+}
+
+int eao_tier_publish(eao_tier *t, int64_t now, int64_t window, eao_tier_report *out) {
+  if (!t || !out || window < 0) return EAO_EINVAL;
+  if (t->have_clock && now < t->clock) return EAO_EINVAL;
+  t->clock = now;  /* later evictions are stamped no earlier than this */
+  t->have_clock = 1;
+  int64_t e = 0;
+  for (int64_t i = t->evictions_total - 1; i >= 0; --i) {
+    if (!(t->evict_stamp[i] > now - window)) break;
+    ++e;
+  }
+  out->time = now;
+  out->registered = t->registered;
+  out->capacity_slots = t->K;
+  out->evictions = e;
   return EAO_OK;
 }
 
