@@ -220,6 +220,95 @@ int ea_admission_fill(ea_tier *tier, const ea_policy *policy,
                       const ea_request *request, const uint8_t *keys,
                       int64_t n_keys, uint8_t *mask_out, int32_t *save_out);
 
+/* ------------------------------------------------- published telemetry
+ *
+ * The paper splits the rule between the worker that owns the tier and the
+ * scheduler that decides (App. "Runtime Admission Details"): the worker
+ * publishes a report every second, the scheduler reads the latest one every
+ * half second and uses it only while it is fresh (at most 5 s old); without
+ * a fresh report the working-set estimate alone decides. */
+typedef struct {
+  int64_t time;            /* clock value the report was taken at             */
+  int64_t registered;      /* pending + resident chunks                       */
+  int64_t capacity_slots;  /* K_H                                             */
+  int64_t evictions;       /* e_t: evictions made to allocate with a stamp in
+                              (time - window, time]                           */
+} ea_tier_report;
+
+/* Take the tier's report at time `now` (caller clock, not below the tier's
+ * clock) over `window`, and advance the tier's clock to `now` (evictions are
+ * stamped with the tier's clock: the latest time a decision or a report gave
+ * it).  EA_EINVAL if now is earlier than the clock or window < 0. */
+int ea_tier_publish(ea_tier *tier, int64_t now, int64_t window,
+                    ea_tier_report *out);
+
+/* ea_admission_fill with the "full and evicting" factor taken from the
+ * scheduler's copy of a report (Eq. 10): used when policy->telemetry is 1,
+ * report is not NULL and 0 <= request->now - report->time <= max_age;
+ * otherwise the working-set estimate alone decides.  report may be NULL;
+ * max_age >= 0.  Everything else is as in ea_admission_fill. */
+int ea_admission_fill_report(ea_tier *tier, const ea_policy *policy,
+                             const ea_request *request,
+                             const ea_tier_report *report, int64_t max_age,
+                             const uint8_t *keys, int64_t n_keys,
+                             uint8_t *mask_out, int32_t *save_out);
+
+/* -------------------------------------------------- wall-clock controller
+ *
+ * The same split as a runtime: a controller attached to a tier publishes
+ * its report every report_interval, refreshes the scheduler's copy every
+ * read_interval (the copy is the latest report published at or before that
+ * read), and decides requests on a microsecond clock with A_t and e_t over
+ * `window` (App. "Runtime Admission Details", Table "Write-admission
+ * parameters": 1 s, 0.5 s, 5 s, 60 s).  Ticks fall at k * interval after
+ * creation (k >= 1); a publish and a read at the same time publish first.
+ * With manual_clock = 0 a background thread publishes on the steady clock,
+ * decisions take the steady clock, and the tier stamps its evictions with
+ * it: decide through the controller only.  With manual_clock = 1 no thread
+ * runs and ea_controller_advance moves the clock (creation is time 0), which
+ * makes every decision reproducible. */
+typedef struct {
+  int64_t report_interval; /* microseconds, > 0 (paper: 1,000,000)           */
+  int64_t read_interval;   /* microseconds, > 0 (paper: 500,000)             */
+  int64_t max_report_age;  /* microseconds, >= 0 (paper: 5,000,000)          */
+  int64_t window;          /* microseconds, >= 0, A_t and e_t (paper: 60 s)  */
+  int32_t manual_clock;    /* 0: steady clock and a publisher thread          */
+  int32_t _pad;
+} ea_controller_config;
+
+typedef struct ea_controller ea_controller;
+
+typedef struct {
+  int64_t now;                 /* the controller's clock                      */
+  int64_t reports_published;
+  ea_tier_report published;    /* the last report published                   */
+  ea_tier_report seen;         /* the scheduler's copy (valid if have_seen)   */
+  int32_t have_seen;
+  int32_t fresh;               /* the copy is fresh at `now`                  */
+  int64_t decisions;           /* first lookups decided                       */
+  int64_t skips;               /* of those, writes declined                   */
+  int64_t fresh_decisions;     /* of those, decided with a fresh report       */
+} ea_controller_status;
+
+/* policy is copied, with its activity_window replaced by config->window.
+ * The tier must outlive the controller. */
+int ea_controller_create(ea_tier *tier, const ea_policy *policy,
+                         const ea_controller_config *config,
+                         ea_controller **out);
+/* Stops and joins the publisher thread, then frees the controller. */
+int ea_controller_destroy(ea_controller *ctl);
+/* Manual clock only: run every publish and read due up to `now` (not below
+ * the controller's clock), then set the clock to `now`. */
+int ea_controller_advance(ea_controller *ctl, int64_t now);
+/* The write rule at a request's first prefix lookup (decided = -1), or a
+ * later lookup of the same request keeping its choice (0 or 1), at the
+ * controller's clock, with the scheduler's copy of the report; fills the
+ * deduplicated mask like ea_admission_fill_report. */
+int ea_controller_decide(ea_controller *ctl, int64_t n_tokens, int64_t h_tokens,
+                         int64_t task_id, int32_t decided, const uint8_t *keys,
+                         int64_t n_keys, uint8_t *mask_out, int32_t *save_out);
+int ea_controller_get_status(ea_controller *ctl, ea_controller_status *out);
+
 /* Allocate host slots for the keys with mask[i] != 0 (mask NULL = all) that
  * are not already registered: the lowest-numbered free slot, else the
  * least-recent resident slot that no lookup, allocation or transfer pins (an

@@ -59,6 +59,25 @@ class TierStats(C.Structure):
                 ("store_calls", C.c_int64), ("load_calls", C.c_int64)]
 
 
+class TierReport(C.Structure):
+    _fields_ = [("time", C.c_int64), ("registered", C.c_int64),
+                ("capacity_slots", C.c_int64), ("evictions", C.c_int64)]
+
+
+class ControllerConfig(C.Structure):
+    _fields_ = [("report_interval", C.c_int64), ("read_interval", C.c_int64),
+                ("max_report_age", C.c_int64), ("window", C.c_int64),
+                ("manual_clock", C.c_int32), ("_pad", C.c_int32)]
+
+
+class ControllerStatus(C.Structure):
+    _fields_ = [("now", C.c_int64), ("reports_published", C.c_int64),
+                ("published", TierReport), ("seen", TierReport),
+                ("have_seen", C.c_int32), ("fresh", C.c_int32),
+                ("decisions", C.c_int64), ("skips", C.c_int64),
+                ("fresh_decisions", C.c_int64)]
+
+
 _P, _I32, _I64, _INT = C.c_void_p, C.c_int32, C.c_int64, C.c_int
 
 SIGNATURES = {
@@ -74,6 +93,13 @@ SIGNATURES = {
     "ea_hash_blocks_device": (_INT, [_P, _P, _I32, _I32, _P, _P, _P, _P]),
     "ea_tier_lookup": (_INT, [_P, _P, _I64, _P, _P]),
     "ea_admission_fill": (_INT, [_P, _P, _P, _P, _I64, _P, _P]),
+    "ea_admission_fill_report": (_INT, [_P, _P, _P, _P, _I64, _P, _I64, _P, _P]),
+    "ea_tier_publish": (_INT, [_P, _I64, _I64, _P]),
+    "ea_controller_create": (_INT, [_P, _P, _P, _P]),
+    "ea_controller_destroy": (_INT, [_P]),
+    "ea_controller_advance": (_INT, [_P, _I64]),
+    "ea_controller_decide": (_INT, [_P, _I64, _I64, _I64, _I32, _P, _I64, _P, _P]),
+    "ea_controller_get_status": (_INT, [_P, _P]),
     "ea_tier_alloc": (_INT, [_P, _P, _P, _I64, _P, _P]),
     "ea_tier_unpin": (_INT, [_P, _P, _I64]),
     "ea_tier_stats_get": (_INT, [_P, _P]),

@@ -152,6 +152,27 @@ class Tier:
             _ptr(mask), C.byref(save)))
         return save.value, mask[:n].copy()
 
+    def publish(self, now, window):
+        """The tier's telemetry report at time `now` (N.TierReport)."""
+        rep = N.TierReport()
+        N.check("ea_tier_publish", N.load().ea_tier_publish(self._h, now, window, C.byref(rep)))
+        return rep
+
+    def admission_report(self, policy, n_tokens, h_tokens, task_id, now, keys, report,
+                         max_age, decided=-1):
+        """Admission with the telemetry factor from `report` (N.TierReport or
+        None) when it is fresh."""
+        keys = _u8(keys).reshape(-1, 32)
+        n = keys.shape[0]
+        req = N.Request(n_tokens, h_tokens, task_id, now, decided, 0)
+        mask = np.zeros(max(n, 1), np.uint8)
+        save = C.c_int32()
+        N.check("ea_admission_fill_report", N.load().ea_admission_fill_report(
+            self._h, C.byref(policy), C.byref(req),
+            None if report is None else C.byref(report), max_age,
+            _ptr(keys) if n else None, n, _ptr(mask), C.byref(save)))
+        return save.value, mask[:n].copy()
+
     def alloc(self, keys, mask=None):
         keys = _u8(keys).reshape(-1, 32)
         n = keys.shape[0]
@@ -317,4 +338,54 @@ def lru_simulate_prefix(refs, req_off, capacity, declined=None):
         _ptr(refs) if len(refs) else None, _ptr(offs), n_req,
         _ptr(dec) if (dec is not None and n_req) else None, int(capacity), _ptr(out)))
     return out[:n_req]
+
+
+# ------------------------------------------------- wall-clock controller
+
+class Controller:
+    """Write-admission controller on a tier: reports every report_interval,
+    scheduler reads every read_interval, fresh for max_report_age, windows
+    of `window` (all microseconds; the paper's 1 s, 0.5 s, 5 s and 60 s by
+    default).  manual_clock=True: no thread, advance() moves the clock."""
+
+    def __init__(self, tier, policy, report_interval=1_000_000, read_interval=500_000,
+                 max_report_age=5_000_000, window=60_000_000, manual_clock=False):
+        self._h = C.c_void_p()
+        cfg = N.ControllerConfig(report_interval, read_interval, max_report_age, window,
+                                 int(bool(manual_clock)), 0)
+        N.check("ea_controller_create", N.load().ea_controller_create(
+            tier._h, C.byref(policy), C.byref(cfg), C.byref(self._h)))
+
+    def close(self):
+        if self._h:
+            N.load().ea_controller_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def advance(self, now):
+        N.check("ea_controller_advance", N.load().ea_controller_advance(self._h, now))
+
+    def decide(self, n_tokens, h_tokens, task_id, keys, decided=-1):
+        keys = _u8(keys).reshape(-1, 32)
+        n = keys.shape[0]
+        mask = np.zeros(max(n, 1), np.uint8)
+        save = C.c_int32()
+        N.check("ea_controller_decide", N.load().ea_controller_decide(
+            self._h, n_tokens, h_tokens, task_id, decided, _ptr(keys) if n else None, n,
+            _ptr(mask), C.byref(save)))
+        return save.value, mask[:n].copy()
+
+    def status(self):
+        st = N.ControllerStatus()
+        N.check("ea_controller_get_status", N.load().ea_controller_get_status(
+            self._h, C.byref(st)))
+        rep = lambda r: {f: getattr(r, f) for f, _ in N.TierReport._fields_}  # noqa: E731
+        out = {f: getattr(st, f) for f, _ in N.ControllerStatus._fields_}
+        out["published"], out["seen"] = rep(st.published), rep(st.seen)
+        return out
 

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libea.so")
 SOURCES = ["ea_copy_kernels.hip", "ea_sha256_kernels.hip", "ea_tier_meta.cpp",
-           "ea_api.cpp", "ea_hash.cpp", "ea_stack.cpp"]
+           "ea_api.cpp", "ea_hash.cpp", "ea_stack.cpp", "ea_controller.cpp"]
 ARCH = "gfx950"
 
 

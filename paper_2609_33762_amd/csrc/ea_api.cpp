@@ -642,6 +642,15 @@ int ea_tier_destroy(ea_tier *t) {
   return EA_OK;
 }
 
+}  // extern "C"
+
+void ea::tier_use_steady_clock(ea_tier *t, bool on) {
+  std::lock_guard<std::mutex> lk(t->mu);
+  t->meta->use_steady_clock(on);
+}
+
+extern "C" {
+
 int ea_tier_get_info(const ea_tier *t, ea_tier_info *info) {
   if (!t || !info) return EA_EINVAL;
   info->capacity_slots = t->K;
@@ -671,6 +680,22 @@ int ea_admission_fill(ea_tier *t, const ea_policy *p, const ea_request *r,
   if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
   std::lock_guard<std::mutex> lk(t->mu);
   return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out);
+}
+
+int ea_admission_fill_report(ea_tier *t, const ea_policy *p, const ea_request *r,
+                             const ea_tier_report *report, int64_t max_age,
+                             const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
+                             int32_t *save_out) {
+  if (!t || !p || !r || !save_out || n_keys < 0 || max_age < 0) return EA_EINVAL;
+  if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
+  std::lock_guard<std::mutex> lk(t->mu);
+  return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out, true, report, max_age);
+}
+
+int ea_tier_publish(ea_tier *t, int64_t now, int64_t window, ea_tier_report *out) {
+  if (!t || !out) return EA_EINVAL;
+  std::lock_guard<std::mutex> lk(t->mu);
+  return t->meta->publish(now, window, out);
 }
 
 int ea_tier_alloc(ea_tier *t, const uint8_t *keys, const uint8_t *mask, int64_t n,

@@ -48,6 +48,14 @@ struct InlineIdx {
 // Remember the HIP error behind an EA_EHIP return on this thread.
 void set_last_hip(int err);
 
+}  // namespace ea
+struct ea_tier;
+namespace ea {
+
+// Make the tier read the steady clock itself for decisions, reports and
+// eviction stamps (a tier driven by a wall-clock controller).
+void tier_use_steady_clock(ea_tier *t, bool on);
+
 // Which memory the slot-layout buffer of a piece copy lives in.
 enum Route : int { kRouteHostLink = 0, kRouteHbm = 1 };
 

@@ -7,6 +7,7 @@
 // that a pending lookup, an allocation or a transfer pins.
 #include "ea_tier_meta.hpp"
 
+#include <algorithm>
 #include <unordered_set>
 
 namespace ea {
@@ -75,7 +76,9 @@ int TierMeta::lookup(const uint8_t *keys, int64_t n, int64_t *hit,
 
 int TierMeta::admission(const ea_policy &p, const ea_request &r,
                         const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
-                        int32_t *save_out) {
+                        int32_t *save_out, bool use_report, const ea_tier_report *rep,
+                        int64_t max_age) {
+  if (use_report && max_age < 0) return EA_EINVAL;
   if (p.block_tokens < 1 || p.kappa < 0 || p.beta_rank < 0 ||
       p.activity_window < 0 || p.length_window < 1 || p.theta_ppm < 0 ||
       p.mode < EA_ADMIT_CONDITIONED || p.mode > EA_ADMIT_FIXED ||
@@ -84,7 +87,11 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
   if (r.n_tokens < 0 || r.h_tokens < 0 || r.h_tokens > r.n_tokens) return EA_EINVAL;
   if (n_keys != r.n_tokens / p.block_tokens) return EA_EINVAL;
   if (r.decided < -1 || r.decided > 1) return EA_EINVAL;
-  if (r.decided == -1 && have_clock_ && r.now < clock_) return EA_EINVAL;
+  // on the steady clock the tier reads the time itself, under its lock, so
+  // decisions, reports and evictions stay in order whatever the threads do
+  const int64_t now =
+      steady_ ? std::max(have_clock_ ? clock_ : INT64_MIN, steady_now_us()) : r.now;
+  if (r.decided == -1 && have_clock_ && now < clock_) return EA_EINVAL;
 
   // new full chunks the request needs (section 4)
   const int64_t u = r.n_tokens / p.block_tokens - r.h_tokens / p.block_tokens;
@@ -92,10 +99,10 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
   if (r.decided >= 0) {
     save = r.decided;  // a later lookup of the request keeps the first choice
   } else {
-    log_.push_back(Lookup{r.now, r.task_id, r.n_tokens});
-    clock_ = r.now;
+    log_.push_back(Lookup{now, r.task_id, r.n_tokens});
+    clock_ = now;
     have_clock_ = true;
-    const int64_t horizon = r.now - p.activity_window;
+    const int64_t horizon = now - p.activity_window;
 
     // A_t: distinct tasks whose first lookup falls inside the window
     std::unordered_set<int64_t> tasks;
@@ -118,7 +125,18 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
     const bool over = lhs > rhs;
 
     bool pressure;
-    if (p.telemetry) {
+    if (use_report) {
+      // the scheduler's copy of the worker's last report, when fresh
+      const bool fresh = p.telemetry && rep != nullptr && rep->time <= now &&
+                         now - rep->time <= max_age;
+      if (fresh) {
+        const bool full = (u128)rep->registered * 1000000u >=
+                          (u128)p.theta_ppm * (u128)rep->capacity_slots;
+        pressure = over && full && rep->evictions > 0;
+      } else {
+        pressure = over;
+      }
+    } else if (p.telemetry) {
       // tier full and evicting: o_t >= theta and e_t > 0 (Eq. 10)
       const bool full = (u128)registered_ * 1000000u >= (u128)p.theta_ppm * (u128)K_;
       const bool evicting = !evict_stamps_.empty() && evict_stamps_.back() > horizon;
@@ -145,8 +163,28 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
   return EA_OK;
 }
 
+int TierMeta::publish(int64_t now, int64_t window, ea_tier_report *out) {
+  if (window < 0) return EA_EINVAL;
+  if (steady_) now = std::max(have_clock_ ? clock_ : INT64_MIN, steady_now_us());
+  if (have_clock_ && now < clock_) return EA_EINVAL;
+  clock_ = now;
+  have_clock_ = true;
+  int64_t e = 0;
+  for (auto it = evict_stamps_.rbegin(); it != evict_stamps_.rend() && *it > now - window; ++it)
+    ++e;
+  out->time = now;
+  out->registered = registered_;
+  out->capacity_slots = K_;
+  out->evictions = e;
+  return EA_OK;
+}
+
 int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
                     int64_t *slots_out, int64_t *allocated) {
+  if (steady_) {
+    clock_ = std::max(clock_, steady_now_us());
+    have_clock_ = true;
+  }
   int64_t count = 0;
   bool exhausted = false;
   for (int64_t i = 0; i < n; ++i) {

@@ -5,6 +5,7 @@
 
 #include <stdint.h>
 
+#include <chrono>
 #include <cstring>
 #include <functional>
 #include <queue>
@@ -14,6 +15,13 @@
 #include "ea.h"
 
 namespace ea {
+
+// Microseconds on the steady clock: the time base of a wall-clock controller.
+inline int64_t steady_now_us() {
+  return std::chrono::duration_cast<std::chrono::microseconds>(
+             std::chrono::steady_clock::now().time_since_epoch())
+      .count();
+}
 
 struct Key {
   uint64_t w[4];
@@ -39,8 +47,18 @@ class TierMeta {
   int64_t capacity() const { return K_; }
 
   int lookup(const uint8_t *keys, int64_t n, int64_t *hit, int64_t *slots_out);
+  // The write rule; with use_report the "full and evicting" factor comes
+  // from `rep` when it is fresh (0 <= r.now - rep->time <= max_age), else
+  // the working-set estimate alone decides.
   int admission(const ea_policy &p, const ea_request &r, const uint8_t *keys,
-                int64_t n_keys, uint8_t *mask_out, int32_t *save_out);
+                int64_t n_keys, uint8_t *mask_out, int32_t *save_out,
+                bool use_report = false, const ea_tier_report *rep = nullptr,
+                int64_t max_age = 0);
+  // Telemetry at time now (not below the clock); advances the clock.
+  int publish(int64_t now, int64_t window, ea_tier_report *out);
+  // Stamp evictions with the steady clock in microseconds (a tier driven by
+  // a wall-clock controller) instead of the last time the tier was told.
+  void use_steady_clock(bool on) { steady_ = on; }
   int alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
             int64_t *slots_out, int64_t *allocated);
   // A store was issued to `slot`: an allocated slot becomes resident.
@@ -77,6 +95,7 @@ class TierMeta {
   std::vector<Lookup> log_;
   int64_t clock_ = 0;
   bool have_clock_ = false;
+  bool steady_ = false;
   int64_t last_window_ = 0, last_active_ = 0;
   double last_mean_ = 0.0, last_ws_ = 0.0;
   int32_t last_pressure_ = 0, last_save_ = 0;
