@@ -54,15 +54,19 @@ def kernel_source_hash():
 
 
 def event_ms(torch, fn, stream, reps):
-    """Average duration of fn() bracketed by HIP events on `stream`."""
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    for i in range(reps):
-        starts[i].record(stream)
-        fn()
-        ends[i].record(stream)
+    """Average duration of one fn() call: `reps` back-to-back calls between
+    one pair of HIP events on `stream`, after one untimed call (events
+    between the calls would add their own cost to every launch)."""
+    fn()
     torch.cuda.synchronize()
-    return float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
 
 
 def cpu_baseline(W, n_s, n_l, prefix_tokens, refill_tokens):
@@ -689,6 +693,51 @@ def run_tp8_shard(args):
                  {"tp8_shard": out, "beta_bytes_per_token": beta})
 
 
+# Lane-instructions per key of this build's hash kernels with 16-token
+# blocks, counted in their gfx950 assembly: one compression of the token
+# block (sha256_midstates) and one chained compression (sha256_chain, two
+# lanes per sequence: 1,249 instructions per lane pair).
+HASH_INSTR_PER_KEY = 1409 + 2 * 1249
+# Integer VALU peak of MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a
+# wave64 instruction occupies a SIMD for 4 cycles; the 157.3 TFLOP/s fp32
+# figure counts packed two-wide FMAs, which integer ops do not have).
+VALU_INT_PEAK = 256 * 4 * 16 * 2.4e9
+
+
+def run_hash(args):
+    """Chained keys (16-token blocks) on the device, tokens already in HBM:
+    the turn's two sequences (24k + 32k tokens), one 64k-token sequence, 64
+    such sequences, and 16,384 sequences of 1,024 tokens; every run checked
+    against the host entry point's keys."""
+    import torch
+    from paper_2609_33762_amd import api, workloads as W
+    torch.cuda.set_device(0)
+    cur = torch.cuda.current_stream()
+    out = {}
+    for name, lengths in (("turn_24k_32k", [24000, 32000]), ("one_64k", [65536]),
+                          ("pool_64x64k", [65536] * 64), ("batch_16384x1k", [1024] * 16384)):
+        toks, offs = W.sequences(W.SEED_TOKENS, lengths)
+        d_tok = torch.as_tensor(toks, device="cuda")
+        nk = int(sum(n // 16 for n in lengths))
+        d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
+        ms = event_ms(torch, lambda: api.hash_blocks_device(d_tok, offs, 16, d_keys, stream=cur),
+                      cur, 5)
+        host, _ = api.hash_blocks(toks, offs, 16)
+        assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32))
+        out[name] = {"ms": round(ms, 4), "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
+                     "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1)}
+        log(f"hash {name}: {out[name]}")
+    b = out["batch_16384x1k"]
+    achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
+    roof = {"bound": "alu", "kernel": "sha256_midstates + sha256_chain (16,384 x 1,024 tokens)",
+            "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
+            "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
+            "traffic": None}
+    return _line("hash: chained SHA-256 keys of 16-token blocks, tokens in HBM",
+                 round(b["tokens_per_s"] / 1e9, 3), "G tokens/s", b["ms"], 5,
+                 {"hash": out, "roofline": roof})
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -700,7 +749,7 @@ def main():
     ap.add_argument("--summarize-profiles", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
-                             "load_cost", "tp8_shard"])
+                             "load_cost", "tp8_shard", "hash"])
     ap.add_argument("--turns-per-agent", type=int, default=24)
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
     args = ap.parse_args()
@@ -714,7 +763,7 @@ def main():
         sys.exit(2)
     other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,
              "layered_fp8": run_layered, "tiny": run_tiny, "load_cost": run_load_cost,
-             "tp8_shard": run_tp8_shard}
+             "tp8_shard": run_tp8_shard, "hash": run_hash}
     if args.workload in other:
         out = other[args.workload](args)
         log(json.dumps(out))
