@@ -303,7 +303,10 @@ def run_agent_pool(args):
     beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
     pol = api.make_policy(kappa=256, block_tokens=sh.page_tokens, beta_rank=beta,
                           activity_window=W.POOL_AGENTS)
-    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, verify=False, time_fill=True)
+    # loads and stores on their own streams: a turn's store overlaps the next
+    # turn's load on the host link
+    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, verify=False, time_fill=True,
+                             load_stream=torch.cuda.Stream(), store_stream=torch.cuda.Stream())
     turns = args.turns_per_agent * W.POOL_AGENTS
     hits = declined = stored = 0
     gamma = []

@@ -78,10 +78,19 @@ class AgentPool:
     key), looks up the prompt's keys, loads the hit prefix into free GPU
     pages, writes the remaining blocks' KV (a function of their keys) into
     other free pages, decides admission, allocates slots, stores the admitted
-    blocks and releases the pins.  GPU pages are free again after each turn."""
+    blocks and releases the pins.  GPU pages are free again after each turn.
+
+    With load_stream and store_stream, loads and stores run on their own
+    streams and a turn does not wait for the previous turn's store: the
+    host link carries that store and the next turn's load at once.  The
+    library orders transfers that touch the same slot.  GPU pages are the
+    caller's: a turn draws its pages apart from the pages of every load and
+    store that may still run (an event recorded after each tells), and a
+    load starts after the fills issued before it."""
 
     def __init__(self, torch, cache, tier, kv, shape, policy, agents=W.POOL_AGENTS,
-                 seed=W.SEED_WORKLOAD, verify=True, stream=None, time_fill=False):
+                 seed=W.SEED_WORKLOAD, verify=True, stream=None, time_fill=False,
+                 load_stream=None, store_stream=None):
         # time_fill: measure the synthetic KV fill (the stand-in for prefill
         # compute) so that a benchmark can leave it out of the path's time
         self.time_fill = time_fill
@@ -98,8 +107,30 @@ class AgentPool:
         self.keys = [np.zeros((0, 32), np.uint8)] * agents
         self.turn_no = 0
         self.stream = stream
+        self.load_stream = load_stream if load_stream is not None else stream
+        self.store_stream = store_stream if store_stream is not None else stream
+        self.overlap = load_stream is not None or store_stream is not None
+        self.pending = []  # (event, pages) of loads and stores that may still run
         self.bytes_loaded = 0
         self.bytes_stored = 0
+
+    def _note(self, stream, pages):
+        if self.overlap:
+            ev = self.torch.cuda.Event()
+            ev.record(stream)
+            self.pending.append((ev, np.asarray(pages, np.int64)))
+
+    def _busy_pages(self):
+        """Pages that a load or store issued earlier may still touch; drains
+        them first if they would leave fewer than half the pages free."""
+        self.pending = [(e, p) for e, p in self.pending if not e.query()]
+        if sum(len(p) for _, p in self.pending) > self.sh.num_pages // 2:
+            for e, _ in self.pending:
+                e.synchronize()
+            self.pending = []
+        if not self.pending:
+            return np.zeros(0, np.int64)
+        return np.concatenate([p for _, p in self.pending])
 
     def _next_prompt(self, a):
         rng = self.tok_rng[a]
@@ -131,13 +162,20 @@ class AgentPool:
         self.prompts[a], self.keys[a] = prompt, keys
 
         h, hit_slots = tier.lookup(keys)
-        pages = W.distinct(self.r, self.sh.num_pages, n_full)
+        if self.overlap:
+            pages = W.distinct(self.r, self.sh.num_pages, n_full, exclude=self._busy_pages())
+        else:
+            pages = W.distinct(self.r, self.sh.num_pages, n_full)
         load_pages, fill_pages = pages[:h], pages[h:]
         if h:
-            tier.load(cache, hit_slots, load_pages, stream=self.stream)
+            if self.overlap and self.load_stream is not None:
+                self.load_stream.wait_stream(torch.cuda.current_stream())
+            tier.load(cache, hit_slots, load_pages, stream=self.load_stream)
             self.bytes_loaded += h * tier.slot_bytes
+            self._note(self.load_stream, load_pages)
         if n_full > h:  # compute (here: synthesise) the KV the tier did not have
             if self.time_fill:
+                # nothing of the path runs while the excluded fill is timed
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
             for c0 in range(h, n_full, 512):
@@ -151,8 +189,12 @@ class AgentPool:
         _, slots = tier.alloc(keys, mask)
         ok = slots >= 0
         if ok.any():
-            tier.store(cache, pages[ok], slots[ok], stream=self.stream)
+            if self.overlap and self.store_stream is not None:
+                # the store reads the pages the fill just wrote
+                self.store_stream.wait_stream(torch.cuda.current_stream())
+            tier.store(cache, pages[ok], slots[ok], stream=self.store_stream)
             self.bytes_stored += int(ok.sum()) * tier.slot_bytes
+            self._note(self.store_stream, pages[ok])
         loaded_ok = True
         if self.verify and h:
             torch.cuda.synchronize()

@@ -266,3 +266,50 @@ def test_agent_pool_metadata_and_bytes():
     cache.close()
     del kv
     release(torch)
+
+
+def test_agent_pool_overlapped_streams():
+    # loads and stores on two streams, a turn not waiting for the previous
+    # store: metadata still equals the oracle's every turn, and every loaded
+    # page still carries its key's pattern
+    torch = need_gpu()
+    sh = W.QWEN3
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, 16 << 30)  # 10,922 slots: the tier evicts early
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    kw = dict(kappa=256, block_tokens=sh.page_tokens, activity_window=16)
+    pol = api.make_policy(beta_rank=beta, **kw)
+    opol = oracle.make_policy(beta=beta, **kw)
+    ot = oracle.Tier(oshape_of(sh), 16 << 30)
+    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, agents=16,
+                             load_stream=torch.cuda.Stream(), store_stream=torch.cuda.Stream())
+    hits = 0
+    for t in range(4 * 16):
+        rec = pool.turn()
+        assert rec.loaded_ok, f"turn {t}: a loaded page differs from its key's pattern"
+        h, hs = ot.lookup(rec.keys)
+        assert h == rec.hit and np.array_equal(hs, rec.hit_slots), t
+        save, mask = ot.admission(opol, rec.n_tokens, rec.hit * sh.page_tokens, rec.agent, t,
+                                  rec.keys)
+        assert save == rec.save and np.array_equal(mask, rec.mask), t
+        _, slots = ot.alloc(rec.keys, mask)
+        assert np.array_equal(slots, rec.alloc_slots), t
+        ok = slots >= 0
+        ot.mark_stored(slots[ok])
+        if ok.any():
+            ot.unpin(slots[ok])
+        if h:
+            ot.unpin(hs)
+        hits += h
+    torch.cuda.synchronize()
+    a, b = tier.export(), ot.export()
+    for k in ("state", "pins", "keys", "lru"):
+        assert np.array_equal(a[k], b[k]), k
+    assert hits > 0 and tier.stats()["evictions_total"] > 0
+    tier.close()
+    cache.close()
+    del kv
+    release(torch)
+
