@@ -699,8 +699,8 @@ def run_tp8_shard(args):
 # Lane-instructions per key of this build's hash kernels with 16-token
 # blocks, counted in their gfx950 assembly: one compression of the token
 # block (sha256_midstates) and one chained compression (sha256_chain, two
-# lanes per sequence: 1,249 instructions per lane pair).
-HASH_INSTR_PER_KEY = 1409 + 2 * 1249
+# lanes per sequence: 1,163 instructions per lane pair).
+HASH_INSTR_PER_KEY = 1409 + 2 * 1163
 # Integer VALU peak of MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a
 # wave64 instruction occupies a SIMD for 4 cycles; the 157.3 TFLOP/s fp32
 # figure counts packed two-wide FMAs, which integer ops do not have).

@@ -14,9 +14,9 @@
 // compression set its speed: rotations are v_alignbit_b32, every
 // three-input XOR and Ch/Maj one v_bitop3_b32 (gfx950's three-input logic
 // op), sums v_add3_u32; everything stays in VGPRs (no LDS, no scratch).
-// Splitting the working state over two lanes (below) brings a chained
-// compression to 1,249 instructions from 1,374 in one lane, and gives twice
-// as many waves for a given number of sequences.
+// Splitting the working state and the message schedule over two lanes
+// (below) brings a chained compression to 1,163 instructions from 1,374 in
+// one lane, and gives twice as many waves for a given number of sequences.
 #include <hip/hip_runtime.h>
 
 #include "ea_internal.hpp"
@@ -127,7 +127,9 @@ __global__ __launch_bounds__(256) void sha256_midstates(
 // the a-side, Sigma1(e) and Ch(e, f, g) on the e-side (Maj(a, b, c) equals
 // Ch(a ^ c, b, c), so one bitop3 serves both); T1 crosses from the e-lane to
 // the a-lane and d from the a-lane to the e-lane through DPP lane moves.
-// Both lanes run the message schedule (only the e-lane's T1 uses it).
+// The message schedule is split the same way: one step computes W_2j on
+// the e-lane and W_2j+1 on the a-lane, each lane taking the two terms that
+// live on the other lane through a lane swap.
 constexpr int kPermFromE = 0xF5;  // quad_perm [1,1,3,3]: read lane 2q+1
 constexpr int kPermFromA = 0xA0;  // quad_perm [0,0,2,2]: read lane 2q
 constexpr int kPermSwap = 0xB1;   // quad_perm [1,0,3,2]: read the other lane
@@ -146,7 +148,7 @@ __global__ __launch_bounds__(64) void sha256_chain(
   const bool e_side = lane & 1;
   const int32_t s = blockIdx.x * 32 + (lane >> 1);
   if (s >= n_seqs) return;  // both lanes of a pair leave together
-  const uint32_t r1 = e_side ? 6 : 2, r2 = e_side ? 11 : 13, r3 = e_side ? 25 : 22;
+  const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
   const uint32_t m = e_side ? 0u : 0xffffffffu;
   uint32_t prev[8];
   if (parents != nullptr) {
@@ -162,28 +164,43 @@ __global__ __launch_bounds__(64) void sha256_chain(
   const int64_t k0 = key_off[s], k1 = key_off[s + 1];
   const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
   uint4 nx = k0 < k1 ? mh[2 * k0 + (e_side ? 1 : 0)] : make_uint4(0, 0, 0, 0);
+  // message words in pairs: x[j] holds W_2j on the e-lane, W_2j+1 on the
+  // a-lane; x[0..3] come from the previous key, x[4..7] are the padding
+  const uint32_t pad8 = e_side ? 0x80000000u : 0u;   // (W8, W9)
+  const uint32_t pad14 = e_side ? 0u : len_bits;      // (W14, W15)
+  uint32_t x[8];
+  {
+    // the parent key: e-lane (W_2j), a-lane (W_2j+1)
+    x[0] = e_side ? prev[0] : prev[1];
+    x[1] = e_side ? prev[2] : prev[3];
+    x[2] = e_side ? prev[4] : prev[5];
+    x[3] = e_side ? prev[6] : prev[7];
+  }
   for (int64_t k = k0; k < k1; ++k) {
     const uint4 h0 = nx;  // this lane's half of the midstate
     if (k + 1 < k1) nx = mh[2 * (k + 1) + (e_side ? 1 : 0)];
     uint32_t s0 = h0.x, s1 = h0.y, s2 = h0.z, s3 = h0.w;
-    uint32_t w[16] = {prev[0], prev[1], prev[2], prev[3], prev[4], prev[5],
-                      prev[6], prev[7], 0x80000000u, 0u, 0u, 0u, 0u, 0u, 0u,
-                      len_bits};
+    uint32_t X[32];
+    X[0] = x[0]; X[1] = x[1]; X[2] = x[2]; X[3] = x[3];
+    X[4] = pad8; X[5] = 0u; X[6] = 0u; X[7] = pad14;
 #pragma unroll
     for (int t = 0; t < 64; ++t) {
-      uint32_t wt;
-      if (t < 16) {
-        wt = w[t];
-      } else {
-        const uint32_t w2 = w[(t - 2) & 15], w15 = w[(t - 15) & 15];
-        const uint32_t g1 = bitop3<kXor3>(rotr(w2, 17), rotr(w2, 19), w2 >> 10);
-        const uint32_t g0 = bitop3<kXor3>(rotr(w15, 7), rotr(w15, 18), w15 >> 3);
-        wt = g1 + w[(t - 7) & 15] + g0 + w[t & 15];
-        w[t & 15] = wt;
+      const int j = t >> 1;
+      if ((t & 1) == 0 && j >= 8) {
+        // W_2j (e-lane) and W_2j+1 (a-lane) at once: the partner's terms
+        // come through a lane swap of a register each lane fills for it
+        const uint32_t r1 = e_side ? X[j - 3] : X[j - 4];
+        const uint32_t r2 = e_side ? X[j - 7] : X[j - 8];
+        const uint32_t x1 = X[j - 1];
+        const uint32_t g1 = bitop3<kXor3>(rotr(x1, 17), rotr(x1, 19), x1 >> 10);
+        const uint32_t g0 = bitop3<kXor3>(rotr(r2, 7), rotr(r2, 18), r2 >> 3);
+        X[j] = (g1 + dpp_from<kPermSwap>(g0)) + (X[j - 8] + dpp_from<kPermSwap>(r1));
       }
-      const uint32_t S = bitop3<kXor3>(__builtin_amdgcn_alignbit(s0, s0, r1),
-                                       __builtin_amdgcn_alignbit(s0, s0, r2),
-                                       __builtin_amdgcn_alignbit(s0, s0, r3));
+      // W_t on the e-lane: its own word for even t, the a-lane's for odd t
+      const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[j]) : X[j];
+      const uint32_t S = bitop3<kXor3>(__builtin_amdgcn_alignbit(s0, s0, r1c),
+                                       __builtin_amdgcn_alignbit(s0, s0, r2c),
+                                       __builtin_amdgcn_alignbit(s0, s0, r3c));
       const uint32_t F = bitop3<kCh>(bitop3<kXorAnd>(s0, s2, m), s1, s2);
       const uint32_t U = S + F;                       // a-lane: T2
       const uint32_t T1 = U + s3 + (kRound[t] + wt);  // e-lane: T1
@@ -197,13 +214,15 @@ __global__ __launch_bounds__(64) void sha256_chain(
     uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k + (e_side ? 16 : 0));
     *out = make_uint4(__builtin_bswap32(o0), __builtin_bswap32(o1), __builtin_bswap32(o2),
                       __builtin_bswap32(o3));
-    // the key is the next message's words 0..7: own half and the other lane's
-    const uint32_t p0 = dpp_from<kPermSwap>(o0), p1 = dpp_from<kPermSwap>(o1);
-    const uint32_t p2 = dpp_from<kPermSwap>(o2), p3 = dpp_from<kPermSwap>(o3);
-    prev[0] = e_side ? p0 : o0; prev[1] = e_side ? p1 : o1;
-    prev[2] = e_side ? p2 : o2; prev[3] = e_side ? p3 : o3;
-    prev[4] = e_side ? o0 : p0; prev[5] = e_side ? o1 : p1;
-    prev[6] = e_side ? o2 : p2; prev[7] = e_side ? o3 : p3;
+    // the key is the next message's words 0..7 (H0..H3 on the a-lane, H4..H7
+    // on the e-lane): x[0] = (H0, H1), x[1] = (H2, H3), x[2] = (H4, H5),
+    // x[3] = (H6, H7) as (e-lane, a-lane)
+    const uint32_t a0 = dpp_from<kPermFromA>(o0), a2 = dpp_from<kPermFromA>(o2);
+    const uint32_t e1 = dpp_from<kPermFromE>(o1), e3 = dpp_from<kPermFromE>(o3);
+    x[0] = e_side ? a0 : o1;
+    x[1] = e_side ? a2 : o3;
+    x[2] = e_side ? o0 : e1;
+    x[3] = e_side ? o2 : e3;
   }
 }
 
