@@ -73,3 +73,18 @@ def test_incremental_hash_from_cached_parent():
     tail, _ = api.hash_blocks(toks[16 * k:], np.array([0, 4096 - 16 * k]), 16,
                               parents=full[k - 1].reshape(1, 32))
     assert np.array_equal(tail, full[k:])
+
+
+@pytest.mark.parametrize("b", [16, 48])
+def test_full_int32_range_tokens(b):
+    # token values are hashed as the bytes of their two's-complement value:
+    # negative ids and both extremes included
+    need_gpu()
+    r = W.rng(77 + b)
+    lengths = [5 * b + 7, 0, 3 * b, 11 * b + 1]
+    toks = r.integers(-2**31, 2**31, size=sum(lengths), dtype=np.int64).astype(np.int32)
+    toks[:4] = [-2**31, 2**31 - 1, -1, 0]
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    keys, koffs = api.hash_blocks(toks, offs, b)
+    okeys, okoffs = oracle.hash_blocks(toks, offs, b)
+    assert np.array_equal(koffs, okoffs) and np.array_equal(keys, okeys)
