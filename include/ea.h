@@ -120,7 +120,8 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages,
                            int64_t capacity_bytes, int numa_node,
                            ea_tier **out);
 
-/* Waits for every transfer the library issued on this tier, then frees it. */
+/* Waits for every transfer the library issued on this tier, then frees it.
+ * EA_EINVAL (and nothing freed) while an ea_controller is attached to it. */
 int ea_tier_destroy(ea_tier *tier);
 
 int ea_tier_get_info(const ea_tier *tier, ea_tier_info *info);
@@ -291,7 +292,8 @@ typedef struct {
 } ea_controller_status;
 
 /* policy is copied, with its activity_window replaced by config->window.
- * The tier must outlive the controller. */
+ * The tier must outlive the controller: ea_tier_destroy refuses a tier with
+ * controllers attached. */
 int ea_controller_create(ea_tier *tier, const ea_policy *policy,
                          const ea_controller_config *config,
                          ea_controller **out);

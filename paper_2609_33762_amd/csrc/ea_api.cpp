@@ -266,6 +266,7 @@ struct ea_tier {
   int64_t grid_link = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
+  int32_t controllers = 0;  // attached admission controllers (guarded by mu)
 };
 
 namespace {
@@ -622,6 +623,10 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
 int ea_tier_destroy(ea_tier *t) {
   if (!t) return EA_EINVAL;
   {
+    std::lock_guard<std::mutex> lk(t->mu);
+    if (t->controllers > 0) return EA_EINVAL;  // a controller still uses it
+  }
+  {
     DeviceScope ds(t->device);
     std::lock_guard<std::mutex> lk(t->mu);
     for (auto &ev : t->evs) {
@@ -647,6 +652,11 @@ int ea_tier_destroy(ea_tier *t) {
 void ea::tier_use_steady_clock(ea_tier *t, bool on) {
   std::lock_guard<std::mutex> lk(t->mu);
   t->meta->use_steady_clock(on);
+}
+
+void ea::tier_attach_controller(ea_tier *t, int delta) {
+  std::lock_guard<std::mutex> lk(t->mu);
+  t->controllers += delta;
 }
 
 extern "C" {

@@ -134,6 +134,7 @@ int ea_controller_create(ea_tier *tier, const ea_policy *policy,
       return EA_ENOMEM;
     }
   }
+  ea::tier_attach_controller(tier, +1);
   *out = c;
   return EA_OK;
 }
@@ -147,6 +148,7 @@ int ea_controller_destroy(ea_controller *c) {
   c->cv.notify_all();
   if (c->publisher.joinable()) c->publisher.join();
   if (!c->cfg.manual_clock) ea::tier_use_steady_clock(c->tier, false);
+  ea::tier_attach_controller(c->tier, -1);
   delete c;
   return EA_OK;
 }

@@ -55,6 +55,9 @@ namespace ea {
 // Make the tier read the steady clock itself for decisions, reports and
 // eviction stamps (a tier driven by a wall-clock controller).
 void tier_use_steady_clock(ea_tier *t, bool on);
+// Count a controller attached to (+1) or detached from (-1) the tier; a tier
+// with controllers attached refuses ea_tier_destroy.
+void tier_attach_controller(ea_tier *t, int delta);
 
 // Which memory the slot-layout buffer of a piece copy lives in.
 enum Route : int { kRouteHostLink = 0, kRouteHbm = 1 };

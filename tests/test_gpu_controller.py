@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 import oracle
-from paper_2609_33762_amd import api, workloads as W
+from paper_2609_33762_amd import _native as N, api, workloads as W
 
 from gpu_common import need_gpu
 
@@ -180,6 +180,8 @@ def test_steady_clock_without_a_report_uses_the_estimate_alone():
     st = ctl.status()
     assert st["reports_published"] == 0 and not st["have_seen"]
     assert st["fresh_decisions"] == 0 and st["skips"] == 6
+    # the tier refuses to go while the controller is attached
+    assert N.load().ea_tier_destroy(tier._h) == N.EA_EINVAL
     t0 = time.perf_counter()
     ctl.close()  # the publisher waits on a 60 s tick: closing must not wait for it
     assert time.perf_counter() - t0 < 1.0
