@@ -287,8 +287,8 @@ int ensure_staging(ea_tier *t, int dir) {
   if (R.staging) return EA_OK;
   const int64_t half = ((int64_t)env_int("EA_STAGING_MB", 512) << 20) / 2;
   const int64_t per_half = std::max<int64_t>(1, half / t->slot);
+  if (!R.staging_ev) EA_HIP(hipEventCreateWithFlags(&R.staging_ev, hipEventDisableTiming));
   EA_HIP(hipMalloc((void **)&R.staging, (size_t)(2 * per_half * t->slot)));
-  EA_HIP(hipEventCreateWithFlags(&R.staging_ev, hipEventDisableTiming));
   R.per_half = per_half;
   return EA_OK;
 }
@@ -555,69 +555,73 @@ int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes, int numa_node,
 
 int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t capacity_bytes,
                            int numa_node, ea_tier **out) {
-  if (!shape || !out || capacity_bytes <= 0 || chunk_pages < 1) return EA_EINVAL;
-  const int64_t payload = shape->page * chunk_pages;
-  const int64_t trailer =
-      shape->d.scale_base ? ((int64_t)shape->d.num_layers * chunk_pages * 8 + 255) / 256 * 256 : 0;
-  const int64_t slot_bytes = payload + trailer;
-  const int64_t K = capacity_bytes / slot_bytes;
-  if (K < 1) return EA_EINVAL;
-  DeviceScope ds(shape->device);
-  EA_TRY(ds.status());
-  std::unique_ptr<ea_tier> t(new (std::nothrow) ea_tier);
-  if (!t) return EA_ENOMEM;
-  t->device = shape->device;
-  t->num_layers = shape->d.num_layers;
-  t->has_scales = shape->d.scale_base != nullptr;
-  t->chunk = chunk_pages;
-  t->piece = shape->piece;
-  t->page = shape->page;
-  t->payload = payload;
-  t->trailer = trailer;
-  t->slot = slot_bytes;
-  t->K = K;
-  t->capacity_bytes = capacity_bytes;
-  t->grid_link = grid_link();
-  t->num_xcd = shape->num_xcd;
-  // two different XCDs for the two directions when the device has them
-  t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", 0x1u, t->num_xcd);
-  t->xcd_load = xcd_mask_from_env("EA_XCD_LOAD", t->num_xcd > 1 ? 0x2u : 0x1u, t->num_xcd);
-  t->grid_gather = grid_hbm(ea::kToSlots);
-  t->grid_scatter = grid_hbm(ea::kToPages);
-  // a layered load is one short kernel per layer: 16 workgroups hide the
-  // start and drain of each (56 GB/s against 51 with 8 on MI355X)
-  t->grid_layered = std::max(1, env_int("EA_LINK_WG_LAYERED", 16));
-  // Fine-grained (coherent) by default: kernels and DMA engines then see one
-  // another's writes to the slots without any cache maintenance.
-  unsigned flags = hipHostMallocMapped | hipHostMallocPortable;
-  flags |= env_int("EA_HOST_COHERENT", 1) ? hipHostMallocCoherent : hipHostMallocNonCoherent;
-  bool numa_set = false;
-  if (numa_node >= 0 && numa_node < 64) {
-    // prefer the requested node for the pinned pages (MPOL_PREFERRED = 1)
-    unsigned long mask = 1ul << numa_node;
-    numa_set = syscall(SYS_set_mempolicy, 1, &mask, 64) == 0;
-    if (numa_set) flags |= hipHostMallocNumaUser;
-  }
-  hipError_t e = hipHostMalloc((void **)&t->host, (size_t)(K * t->slot), flags);
-  if (numa_set) (void)syscall(SYS_set_mempolicy, 0, nullptr, 0);
-  if (e != hipSuccess) {
-    g_last_hip = (int)e;
+  try {
+    if (!shape || !out || capacity_bytes <= 0 || chunk_pages < 1) return EA_EINVAL;
+    const int64_t payload = shape->page * chunk_pages;
+    const int64_t trailer =
+        shape->d.scale_base ? ((int64_t)shape->d.num_layers * chunk_pages * 8 + 255) / 256 * 256 : 0;
+    const int64_t slot_bytes = payload + trailer;
+    const int64_t K = capacity_bytes / slot_bytes;
+    if (K < 1) return EA_EINVAL;
+    DeviceScope ds(shape->device);
+    EA_TRY(ds.status());
+    std::unique_ptr<ea_tier> t(new (std::nothrow) ea_tier);
+    if (!t) return EA_ENOMEM;
+    t->device = shape->device;
+    t->num_layers = shape->d.num_layers;
+    t->has_scales = shape->d.scale_base != nullptr;
+    t->chunk = chunk_pages;
+    t->piece = shape->piece;
+    t->page = shape->page;
+    t->payload = payload;
+    t->trailer = trailer;
+    t->slot = slot_bytes;
+    t->K = K;
+    t->capacity_bytes = capacity_bytes;
+    t->grid_link = grid_link();
+    t->num_xcd = shape->num_xcd;
+    // two different XCDs for the two directions when the device has them
+    t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", 0x1u, t->num_xcd);
+    t->xcd_load = xcd_mask_from_env("EA_XCD_LOAD", t->num_xcd > 1 ? 0x2u : 0x1u, t->num_xcd);
+    t->grid_gather = grid_hbm(ea::kToSlots);
+    t->grid_scatter = grid_hbm(ea::kToPages);
+    // a layered load is one short kernel per layer: 16 workgroups hide the
+    // start and drain of each (56 GB/s against 51 with 8 on MI355X)
+    t->grid_layered = std::max(1, env_int("EA_LINK_WG_LAYERED", 16));
+    // Fine-grained (coherent) by default: kernels and DMA engines then see one
+    // another's writes to the slots without any cache maintenance.
+    unsigned flags = hipHostMallocMapped | hipHostMallocPortable;
+    flags |= env_int("EA_HOST_COHERENT", 1) ? hipHostMallocCoherent : hipHostMallocNonCoherent;
+    bool numa_set = false;
+    if (numa_node >= 0 && numa_node < 64) {
+      // prefer the requested node for the pinned pages (MPOL_PREFERRED = 1)
+      unsigned long mask = 1ul << numa_node;
+      numa_set = syscall(SYS_set_mempolicy, 1, &mask, 64) == 0;
+      if (numa_set) flags |= hipHostMallocNumaUser;
+    }
+    hipError_t e = hipHostMalloc((void **)&t->host, (size_t)(K * t->slot), flags);
+    if (numa_set) (void)syscall(SYS_set_mempolicy, 0, nullptr, 0);
+    if (e != hipSuccess) {
+      g_last_hip = (int)e;
+      return EA_ENOMEM;
+    }
+    e = hipHostGetDevicePointer((void **)&t->dev, t->host, 0);
+    if (e != hipSuccess) {
+      (void)hipHostFree(t->host);
+      g_last_hip = (int)e;
+      return EA_EHIP;
+    }
+    t->meta.reset(new (std::nothrow) ea::TierMeta(K, capacity_bytes));
+    if (!t->meta) {
+      (void)hipHostFree(t->host);
+      return EA_ENOMEM;
+    }
+    t->slot_ev.assign((size_t)K, -1);
+    *out = t.release();
+    return EA_OK;
+  } catch (const std::bad_alloc &) {
     return EA_ENOMEM;
   }
-  e = hipHostGetDevicePointer((void **)&t->dev, t->host, 0);
-  if (e != hipSuccess) {
-    (void)hipHostFree(t->host);
-    g_last_hip = (int)e;
-    return EA_EHIP;
-  }
-  t->meta.reset(new (std::nothrow) ea::TierMeta(K, capacity_bytes));
-  if (!t->meta) {
-    (void)hipHostFree(t->host);
-    return EA_ENOMEM;
-  }
-  t->slot_ev.assign((size_t)K, -1);
-  *out = t.release();
-  return EA_OK;
 }
 
 int ea_tier_destroy(ea_tier *t) {
@@ -677,51 +681,75 @@ int ea_tier_get_info(const ea_tier *t, ea_tier_info *info) {
 
 int ea_tier_lookup(ea_tier *t, const uint8_t *keys, int64_t n, int64_t *hit_blocks,
                    int64_t *slots_out) {
-  if (!t || n < 0 || !hit_blocks) return EA_EINVAL;
-  if (n > 0 && (!keys || !slots_out)) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->lookup(keys, n, hit_blocks, slots_out);
+  try {
+    if (!t || n < 0 || !hit_blocks) return EA_EINVAL;
+    if (n > 0 && (!keys || !slots_out)) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->lookup(keys, n, hit_blocks, slots_out);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_admission_fill(ea_tier *t, const ea_policy *p, const ea_request *r,
                       const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
                       int32_t *save_out) {
-  if (!t || !p || !r || !save_out || n_keys < 0) return EA_EINVAL;
-  if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out);
+  try {
+    if (!t || !p || !r || !save_out || n_keys < 0) return EA_EINVAL;
+    if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_admission_fill_report(ea_tier *t, const ea_policy *p, const ea_request *r,
                              const ea_tier_report *report, int64_t max_age,
                              const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
                              int32_t *save_out) {
-  if (!t || !p || !r || !save_out || n_keys < 0 || max_age < 0) return EA_EINVAL;
-  if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out, true, report, max_age);
+  try {
+    if (!t || !p || !r || !save_out || n_keys < 0 || max_age < 0) return EA_EINVAL;
+    if (n_keys > 0 && (!keys || !mask_out)) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->admission(*p, *r, keys, n_keys, mask_out, save_out, true, report, max_age);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_tier_publish(ea_tier *t, int64_t now, int64_t window, ea_tier_report *out) {
-  if (!t || !out) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->publish(now, window, out);
+  try {
+    if (!t || !out) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->publish(now, window, out);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_tier_alloc(ea_tier *t, const uint8_t *keys, const uint8_t *mask, int64_t n,
                   int64_t *slots_out, int64_t *allocated) {
-  if (!t || n < 0 || !allocated) return EA_EINVAL;
-  if (n > 0 && (!keys || !slots_out)) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->alloc(keys, mask, n, slots_out, allocated);
+  try {
+    if (!t || n < 0 || !allocated) return EA_EINVAL;
+    if (n > 0 && (!keys || !slots_out)) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->alloc(keys, mask, n, slots_out, allocated);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_tier_unpin(ea_tier *t, const int64_t *slots, int64_t n) {
-  if (!t || n < 0) return EA_EINVAL;
-  if (n == 0) return EA_OK;
-  if (!slots) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(t->mu);
-  return t->meta->unpin(slots, n);
+  try {
+    if (!t || n < 0) return EA_EINVAL;
+    if (n == 0) return EA_OK;
+    if (!slots) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(t->mu);
+    return t->meta->unpin(slots, n);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_tier_stats_get(const ea_tier *t, ea_tier_stats *s) {
@@ -762,151 +790,171 @@ int ea_tier_get_plan(const ea_tier *t, int direction, int *plan) {
 int ea_store_blocks(ea_cache *c, ea_tier *t, const int32_t *block_ids,
                     const int64_t *host_slots, const uint8_t *admit_mask, int32_t n,
                     hipStream_t stream) {
-  if (!c || !t || n < 0) return EA_EINVAL;
-  if (!same_shape(t, c)) return EA_EINVAL;
-  if (n == 0) return EA_OK;
-  if (!block_ids || !host_slots) return EA_EINVAL;
-  const int64_t C = t->chunk;
-  if ((int64_t)n * C > INT32_MAX) return EA_EINVAL;
-  std::vector<int64_t> slots;
-  std::vector<int32_t> pages;
-  slots.reserve((size_t)n);
-  pages.reserve((size_t)(n * C));
-  for (int32_t i = 0; i < n; ++i) {
-    if (admit_mask && !admit_mask[i]) continue;
-    if (host_slots[i] < 0 || host_slots[i] >= t->K) return EA_EINVAL;
-    for (int64_t k = 0; k < C; ++k) {
-      const int32_t p = block_ids[i * C + k];
-      if (p < 0 || p >= c->d.num_pages) return EA_EINVAL;
-      pages.push_back(p);
+  try {
+    if (!c || !t || n < 0) return EA_EINVAL;
+    if (!same_shape(t, c)) return EA_EINVAL;
+    if (n == 0) return EA_OK;
+    if (!block_ids || !host_slots) return EA_EINVAL;
+    const int64_t C = t->chunk;
+    if ((int64_t)n * C > INT32_MAX) return EA_EINVAL;
+    std::vector<int64_t> slots;
+    std::vector<int32_t> pages;
+    slots.reserve((size_t)n);
+    pages.reserve((size_t)(n * C));
+    for (int32_t i = 0; i < n; ++i) {
+      if (admit_mask && !admit_mask[i]) continue;
+      if (host_slots[i] < 0 || host_slots[i] >= t->K) return EA_EINVAL;
+      for (int64_t k = 0; k < C; ++k) {
+        const int32_t p = block_ids[i * C + k];
+        if (p < 0 || p >= c->d.num_pages) return EA_EINVAL;
+        pages.push_back(p);
+      }
+      slots.push_back(host_slots[i]);
     }
-    slots.push_back(host_slots[i]);
+    const int64_t m = (int64_t)slots.size();
+    if (!all_distinct(slots.data(), m)) return EA_EINVAL;
+    if (m == 0) return EA_OK;
+    DeviceScope ds(t->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(t->mu);
+    EA_TRY(wait_slot_hazards(t, slots.data(), m, stream));
+    if (resolve_plan(t, EA_DIR_STORE) == EA_PLAN_STAGED) {
+      EA_TRY(copy_staged(t, c, slots.data(), pages.data(), m, ea::kToSlots, stream));
+    } else {
+      const std::vector<int64_t> each = per_page_slots(slots.data(), m, C);
+      EA_TRY(copy_direct(t, c, each.data(), pages.data(), m * C, ea::kToSlots, stream));
+    }
+    EA_TRY(note_slot_transfer(t, slots.data(), m, stream));
+    for (int64_t i = 0; i < m; ++i) t->meta->mark_stored(slots[i]);
+    t->bytes_stored += m * t->slot;
+    t->store_calls += 1;
+    return EA_OK;
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
   }
-  const int64_t m = (int64_t)slots.size();
-  if (!all_distinct(slots.data(), m)) return EA_EINVAL;
-  if (m == 0) return EA_OK;
-  DeviceScope ds(t->device);
-  EA_TRY(ds.status());
-  std::lock_guard<std::mutex> lk(t->mu);
-  EA_TRY(wait_slot_hazards(t, slots.data(), m, stream));
-  if (resolve_plan(t, EA_DIR_STORE) == EA_PLAN_STAGED) {
-    EA_TRY(copy_staged(t, c, slots.data(), pages.data(), m, ea::kToSlots, stream));
-  } else {
-    const std::vector<int64_t> each = per_page_slots(slots.data(), m, C);
-    EA_TRY(copy_direct(t, c, each.data(), pages.data(), m * C, ea::kToSlots, stream));
-  }
-  EA_TRY(note_slot_transfer(t, slots.data(), m, stream));
-  for (int64_t i = 0; i < m; ++i) t->meta->mark_stored(slots[i]);
-  t->bytes_stored += m * t->slot;
-  t->store_calls += 1;
-  return EA_OK;
 }
 
 int ea_load_blocks(ea_tier *t, ea_cache *c, const int64_t *host_slots,
                    const int32_t *dst_pages, int32_t n, hipStream_t stream) {
-  EA_TRY(validate_load(t, c, host_slots, dst_pages, n));
-  if (n == 0) return EA_OK;
-  DeviceScope ds(t->device);
-  EA_TRY(ds.status());
-  std::lock_guard<std::mutex> lk(t->mu);
-  EA_TRY(wait_slot_hazards(t, host_slots, n, stream));
-  if (resolve_plan(t, EA_DIR_LOAD) == EA_PLAN_STAGED) {
-    EA_TRY(copy_staged(t, c, host_slots, dst_pages, n, ea::kToPages, stream));
-  } else {
-    const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
-    EA_TRY(copy_direct(t, c, each.data(), dst_pages, (int64_t)n * t->chunk, ea::kToPages,
-                       stream));
+  try {
+    EA_TRY(validate_load(t, c, host_slots, dst_pages, n));
+    if (n == 0) return EA_OK;
+    DeviceScope ds(t->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(t->mu);
+    EA_TRY(wait_slot_hazards(t, host_slots, n, stream));
+    if (resolve_plan(t, EA_DIR_LOAD) == EA_PLAN_STAGED) {
+      EA_TRY(copy_staged(t, c, host_slots, dst_pages, n, ea::kToPages, stream));
+    } else {
+      const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
+      EA_TRY(copy_direct(t, c, each.data(), dst_pages, (int64_t)n * t->chunk, ea::kToPages,
+                         stream));
+    }
+    EA_TRY(note_slot_transfer(t, host_slots, n, stream));
+    t->bytes_loaded += (int64_t)n * t->slot;
+    t->load_calls += 1;
+    return EA_OK;
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
   }
-  EA_TRY(note_slot_transfer(t, host_slots, n, stream));
-  t->bytes_loaded += (int64_t)n * t->slot;
-  t->load_calls += 1;
-  return EA_OK;
 }
 
 int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
                            const int32_t *dst_pages, int32_t n, hipStream_t copy_stream,
                            hipEvent_t *layer_done) {
-  if (!layer_done) return EA_EINVAL;
-  EA_TRY(validate_load(t, c, host_slots, dst_pages, n));
-  for (int32_t l = 0; l < c->d.num_layers; ++l)
-    if (!layer_done[l]) return EA_EINVAL;
-  DeviceScope ds(t->device);
-  EA_TRY(ds.status());
-  std::lock_guard<std::mutex> lk(t->mu);
-  if (n == 0) {
+  try {
+    if (!layer_done) return EA_EINVAL;
+    EA_TRY(validate_load(t, c, host_slots, dst_pages, n));
     for (int32_t l = 0; l < c->d.num_layers; ++l)
-      EA_HIP(hipEventRecord(layer_done[l], copy_stream));
-    return EA_OK;
-  }
-  EA_TRY(wait_slot_hazards(t, host_slots, n, copy_stream));
-  // the pieces of one layer are strided inside the slots, so every layer is
-  // its own direct kernel over all n slots
-  const int64_t m = (int64_t)n * t->chunk;  // page entries
-  const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
-  ea::PieceCopy a = base_copy(c, t->slot, t->chunk);
-  a.slots = t->dev;
-  a.xcd_mask = t->xcd_load;
-  a.n = m;
-  a.layer_count = 1;
-  ea::InlineIdx inl;
-  const ea::InlineIdx *pin = nullptr;
-  IndexRing &ring = t->res[EA_DIR_LOAD].ring;
-  int region = -1;
-  if (m <= ea::kInlineMax) {
-    for (int64_t i = 0; i < m; ++i) {
-      inl.pages[i] = dst_pages[i];
-      inl.slots[i] = each[(size_t)i];
+      if (!layer_done[l]) return EA_EINVAL;
+    DeviceScope ds(t->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(t->mu);
+    if (n == 0) {
+      for (int32_t l = 0; l < c->d.num_layers; ++l)
+        EA_HIP(hipEventRecord(layer_done[l], copy_stream));
+      return EA_OK;
     }
-    pin = &inl;
-  } else {
-    EA_TRY(ring.upload(each.data(), dst_pages, m, &a.slot_idx, &a.pages, &region));
+    EA_TRY(wait_slot_hazards(t, host_slots, n, copy_stream));
+    // the pieces of one layer are strided inside the slots, so every layer is
+    // its own direct kernel over all n slots
+    const int64_t m = (int64_t)n * t->chunk;  // page entries
+    const std::vector<int64_t> each = per_page_slots(host_slots, n, t->chunk);
+    ea::PieceCopy a = base_copy(c, t->slot, t->chunk);
+    a.slots = t->dev;
+    a.xcd_mask = t->xcd_load;
+    a.n = m;
+    a.layer_count = 1;
+    ea::InlineIdx inl;
+    const ea::InlineIdx *pin = nullptr;
+    IndexRing &ring = t->res[EA_DIR_LOAD].ring;
+    int region = -1;
+    if (m <= ea::kInlineMax) {
+      for (int64_t i = 0; i < m; ++i) {
+        inl.pages[i] = dst_pages[i];
+        inl.slots[i] = each[(size_t)i];
+      }
+      pin = &inl;
+    } else {
+      EA_TRY(ring.upload(each.data(), dst_pages, m, &a.slot_idx, &a.pages, &region));
+    }
+    for (int32_t l = 0; l < c->d.num_layers; ++l) {
+      a.layer_begin = l;
+      EA_HIP(ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
+                                   copy_stream));
+      EA_HIP(hipEventRecord(layer_done[l], copy_stream));
+    }
+    if (region >= 0) EA_TRY(ring.release(region, copy_stream));
+    EA_TRY(note_slot_transfer(t, host_slots, n, copy_stream));
+    t->bytes_loaded += (int64_t)n * t->slot;
+    t->load_calls += 1;
+    return EA_OK;
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
   }
-  for (int32_t l = 0; l < c->d.num_layers; ++l) {
-    a.layer_begin = l;
-    EA_HIP(ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
-                                 copy_stream));
-    EA_HIP(hipEventRecord(layer_done[l], copy_stream));
-  }
-  if (region >= 0) EA_TRY(ring.release(region, copy_stream));
-  EA_TRY(note_slot_transfer(t, host_slots, n, copy_stream));
-  t->bytes_loaded += (int64_t)n * t->slot;
-  t->load_calls += 1;
-  return EA_OK;
 }
 
 // ------------------------------------------------- gather / scatter (HBM)
 
 int ea_gather_blocks(ea_cache *c, const int32_t *block_ids, int32_t n, void *d_dst,
                      hipStream_t stream) {
-  if (!c || n < 0) return EA_EINVAL;
-  if (n == 0) return EA_OK;
-  if (!block_ids || !d_dst || !aligned(d_dst, 16)) return EA_EINVAL;
-  for (int32_t i = 0; i < n; ++i)
-    if (block_ids[i] < 0 || block_ids[i] >= c->d.num_pages) return EA_EINVAL;
-  DeviceScope ds(c->device);
-  EA_TRY(ds.status());
-  std::lock_guard<std::mutex> lk(c->mu);
-  ea::PieceCopy a = base_copy(c, c->slot, 1);
-  a.slots = static_cast<uint8_t *>(d_dst);
-  return launch_entries(a, c->ring, nullptr, block_ids, n, ea::kToSlots, ea::kRouteHbm,
-                        grid_hbm(ea::kToSlots), stream);
+  try {
+    if (!c || n < 0) return EA_EINVAL;
+    if (n == 0) return EA_OK;
+    if (!block_ids || !d_dst || !aligned(d_dst, 16)) return EA_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+      if (block_ids[i] < 0 || block_ids[i] >= c->d.num_pages) return EA_EINVAL;
+    DeviceScope ds(c->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(c->mu);
+    ea::PieceCopy a = base_copy(c, c->slot, 1);
+    a.slots = static_cast<uint8_t *>(d_dst);
+    return launch_entries(a, c->ring, nullptr, block_ids, n, ea::kToSlots, ea::kRouteHbm,
+                          grid_hbm(ea::kToSlots), stream);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 int ea_scatter_blocks(ea_cache *c, const void *d_src, const int32_t *dst_pages, int32_t n,
                       hipStream_t stream) {
-  if (!c || n < 0) return EA_EINVAL;
-  if (n == 0) return EA_OK;
-  if (!dst_pages || !d_src || !aligned(d_src, 16)) return EA_EINVAL;
-  for (int32_t i = 0; i < n; ++i)
-    if (dst_pages[i] < 0 || dst_pages[i] >= c->d.num_pages) return EA_EINVAL;
-  if (!all_distinct(dst_pages, n)) return EA_EINVAL;
-  DeviceScope ds(c->device);
-  EA_TRY(ds.status());
-  std::lock_guard<std::mutex> lk(c->mu);
-  ea::PieceCopy a = base_copy(c, c->slot, 1);
-  a.slots = static_cast<uint8_t *>(const_cast<void *>(d_src));
-  return launch_entries(a, c->ring, nullptr, dst_pages, n, ea::kToPages, ea::kRouteHbm,
-                        grid_hbm(ea::kToPages), stream);
+  try {
+    if (!c || n < 0) return EA_EINVAL;
+    if (n == 0) return EA_OK;
+    if (!dst_pages || !d_src || !aligned(d_src, 16)) return EA_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+      if (dst_pages[i] < 0 || dst_pages[i] >= c->d.num_pages) return EA_EINVAL;
+    if (!all_distinct(dst_pages, n)) return EA_EINVAL;
+    DeviceScope ds(c->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(c->mu);
+    ea::PieceCopy a = base_copy(c, c->slot, 1);
+    a.slots = static_cast<uint8_t *>(const_cast<void *>(d_src));
+    return launch_entries(a, c->ring, nullptr, dst_pages, n, ea::kToPages, ea::kRouteHbm,
+                          grid_hbm(ea::kToPages), stream);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
 }
 
 // --------------------------------------------------------------- peak probe

@@ -154,45 +154,53 @@ int ea_controller_destroy(ea_controller *c) {
 }
 
 int ea_controller_advance(ea_controller *c, int64_t now) {
-  if (!c || !c->cfg.manual_clock) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(c->mu);
-  if (now < c->now) return EA_EINVAL;
-  while (true) {
-    const int64_t t = std::min(c->next_publish, c->next_read);
-    if (t > now) break;
-    if (c->next_publish <= c->next_read) {  // a publish first at equal times
-      const int rc = publish_at(c, c->next_publish);
-      if (rc != EA_OK) return rc;
-      c->next_publish += c->cfg.report_interval;
-    } else {
-      read_at(c, c->next_read);
-      c->next_read += c->cfg.read_interval;
+  try {
+    if (!c || !c->cfg.manual_clock) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (now < c->now) return EA_EINVAL;
+    while (true) {
+      const int64_t t = std::min(c->next_publish, c->next_read);
+      if (t > now) break;
+      if (c->next_publish <= c->next_read) {  // a publish first at equal times
+        const int rc = publish_at(c, c->next_publish);
+        if (rc != EA_OK) return rc;
+        c->next_publish += c->cfg.report_interval;
+      } else {
+        read_at(c, c->next_read);
+        c->next_read += c->cfg.read_interval;
+      }
     }
+    c->now = now;
+    return EA_OK;
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
   }
-  c->now = now;
-  return EA_OK;
 }
 
 int ea_controller_decide(ea_controller *c, int64_t n_tokens, int64_t h_tokens,
                          int64_t task_id, int32_t decided, const uint8_t *keys,
                          int64_t n_keys, uint8_t *mask_out, int32_t *save_out) {
-  if (!c || !save_out) return EA_EINVAL;
-  std::lock_guard<std::mutex> lk(c->mu);
-  if (!c->cfg.manual_clock) {
-    c->now = std::max(c->now, ea::steady_now_us());
-    reads_due(c, c->now);
+  try {
+    if (!c || !save_out) return EA_EINVAL;
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (!c->cfg.manual_clock) {
+      c->now = std::max(c->now, ea::steady_now_us());
+      reads_due(c, c->now);
+    }
+    ea_request r{n_tokens, h_tokens, task_id, c->now, decided, 0};
+    const int rc = ea_admission_fill_report(c->tier, &c->policy, &r,
+                                            c->have_seen ? &c->seen : nullptr,
+                                            c->cfg.max_report_age, keys, n_keys, mask_out,
+                                            save_out);
+    if (rc == EA_OK && decided == -1) {
+      c->decisions += 1;
+      c->skips += *save_out ? 0 : 1;
+      c->fresh_decisions += (c->policy.telemetry && fresh_at(c, c->now)) ? 1 : 0;
+    }
+    return rc;
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
   }
-  ea_request r{n_tokens, h_tokens, task_id, c->now, decided, 0};
-  const int rc = ea_admission_fill_report(c->tier, &c->policy, &r,
-                                          c->have_seen ? &c->seen : nullptr,
-                                          c->cfg.max_report_age, keys, n_keys, mask_out,
-                                          save_out);
-  if (rc == EA_OK && decided == -1) {
-    c->decisions += 1;
-    c->skips += *save_out ? 0 : 1;
-    c->fresh_decisions += (c->policy.telemetry && fresh_at(c, c->now)) ? 1 : 0;
-  }
-  return rc;
 }
 
 int ea_controller_get_status(ea_controller *c, ea_controller_status *s) {
