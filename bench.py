@@ -53,11 +53,12 @@ def kernel_source_hash():
     return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
 
 
-def event_ms(torch, fn, stream, reps):
+def event_ms(torch, fn, stream, reps, warm=1):
     """Average duration of one fn() call: `reps` back-to-back calls between
-    one pair of HIP events on `stream`, after one untimed call (events
+    one pair of HIP events on `stream`, after `warm` untimed calls (events
     between the calls would add their own cost to every launch)."""
-    fn()
+    for _ in range(warm):
+        fn()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
@@ -85,23 +86,42 @@ def cpu_baseline(W, n_s, n_l, prefix_tokens, refill_tokens):
     offs = np.array([0, len(prefix_tokens), len(toks)], np.int64)
     prev = os.sched_getaffinity(0)
     os.sched_setaffinity(0, {sorted(prev)[0]})
-    reps, times = 3, []
+    reps, times = 5, {"hash": [], "store": [], "load": []}
     try:
         for _ in range(reps):
             t0 = time.perf_counter()
             oracle.hash_blocks(toks, offs, sh.page_tokens)
+            t1 = time.perf_counter()
             oracle.store_blocks(oshape, cache, None, tier, np.arange(n_s, dtype=np.int32),
                                 np.arange(n_l, P, dtype=np.int64))
+            t2 = time.perf_counter()
             oracle.load_blocks(oshape, tier, cache, None, np.arange(n_l, 2 * n_l, dtype=np.int64),
                                np.arange(n_s, n_s + n_l, dtype=np.int32))
-            times.append(time.perf_counter() - t0)
+            t3 = time.perf_counter()
+            times["hash"].append(t1 - t0)
+            times["store"].append(t2 - t1)
+            times["load"].append(t3 - t2)
     finally:
         os.sched_setaffinity(0, prev)
-    t = float(np.median(times))
+    med = {k: float(np.median(v)) for k, v in times.items()}
+    t = sum(med.values())
     moved = (n_s + n_l) * sz["page"]
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(moved / t / GB, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "hash_tokens_per_s": round(len(toks) / med["hash"], 1),
+            "store_gbs": round(n_s * sz["page"] / med["store"] / GB, 3),
+            "load_gbs": round(n_l * sz["page"] / med["load"] / GB, 3),
+            "nproc": os.cpu_count(), "cpu_model": model,
             "sample": f"one full step (hash {len(toks)} tokens, store {n_s} pages, load {n_l} "
-                      f"pages of {sz['page']} B) on a {P}-page host cache, median of {reps}",
+                      f"pages of {sz['page']} B) on a {P}-page host cache; the sum of each "
+                      f"phase's median over {reps} runs",
             "ms_per_step": round(t * 1e3, 1)}
 
 
@@ -710,29 +730,33 @@ VALU_INT_PEAK = 256 * 4 * 16 * 2.4e9
 def run_hash(args):
     """Chained keys (16-token blocks) on the device, tokens already in HBM:
     the turn's two sequences (24k + 32k tokens), one 64k-token sequence, 64
-    such sequences, and 16,384 sequences of 1,024 tokens; every run checked
-    against the host entry point's keys."""
+    such sequences, 16,384 sequences of 1,024 tokens (the chain kernel then
+    has 512 waves for the 1,024 SIMDs) and 65,536 of 256 tokens (2,048 waves:
+    every SIMD has work); every run checked against the host entry point's
+    keys.  The roofline is taken on the last."""
     import torch
     from paper_2609_33762_amd import api, workloads as W
     torch.cuda.set_device(0)
     cur = torch.cuda.current_stream()
     out = {}
     for name, lengths in (("turn_24k_32k", [24000, 32000]), ("one_64k", [65536]),
-                          ("pool_64x64k", [65536] * 64), ("batch_16384x1k", [1024] * 16384)):
+                          ("pool_64x64k", [65536] * 64), ("batch_16384x1k", [1024] * 16384),
+                          ("batch_65536x256", [256] * 65536)):
         toks, offs = W.sequences(W.SEED_TOKENS, lengths)
         d_tok = torch.as_tensor(toks, device="cuda")
         nk = int(sum(n // 16 for n in lengths))
         d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
+        # two untimed calls: asynchronous calls alternate between two buffer sets
         ms = event_ms(torch, lambda: api.hash_blocks_device(d_tok, offs, 16, d_keys, stream=cur),
-                      cur, 5)
+                      cur, 5, warm=2)
         host, _ = api.hash_blocks(toks, offs, 16)
         assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32))
         out[name] = {"ms": round(ms, 4), "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
                      "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1)}
         log(f"hash {name}: {out[name]}")
-    b = out["batch_16384x1k"]
+    b = out["batch_65536x256"]
     achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
-    roof = {"bound": "alu", "kernel": "sha256_midstates + sha256_chain (16,384 x 1,024 tokens)",
+    roof = {"bound": "alu", "kernel": "sha256_midstates + sha256_chain (65,536 x 256 tokens)",
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
             "traffic": None}

@@ -20,6 +20,17 @@ namespace {
     }                              \
   } while (0)
 
+// Offsets and midstates of one asynchronous (device) call.  Two of them
+// alternate, so the host prepares the next call while the GPU runs one.
+struct DevSlot {
+  uint8_t *h_meta = nullptr, *d_meta = nullptr;
+  int64_t cap_meta = 0;
+  uint32_t *d_mid = nullptr;
+  int64_t cap_mid = 0;  // keys
+  hipEvent_t done = nullptr;
+  bool used = false;
+};
+
 // Grow-only device/pinned buffers for hashing on the current device.
 struct HashWs {
   int device = -1;
@@ -34,6 +45,8 @@ struct HashWs {
   uint8_t *d_meta = nullptr;
   uint8_t *d_keys = nullptr;
   uint32_t *d_mid = nullptr; int64_t cap_mid = 0;   // keys
+  DevSlot slots[2];                                 // ea_hash_blocks_device
+  int next = 0;
 };
 
 HashWs g_ws;
@@ -67,6 +80,13 @@ int prepare(HashWs &w) {
     if (w.d_keys) (void)hipFree(w.d_keys);
     if (w.d_mid) (void)hipFree(w.d_mid);
     if (w.done) (void)hipEventDestroy(w.done);
+    for (DevSlot &d : w.slots) {
+      if (d.used) (void)hipEventSynchronize(d.done);
+      if (d.h_meta) (void)hipHostFree(d.h_meta);
+      if (d.d_meta) (void)hipFree(d.d_meta);
+      if (d.d_mid) (void)hipFree(d.d_mid);
+      if (d.done) (void)hipEventDestroy(d.done);
+    }
     w = HashWs();
     w.device = dev;
   }
@@ -89,14 +109,14 @@ int validate(const int64_t *seq_offsets, int32_t n_seqs, int32_t block_tokens,
   return EA_OK;
 }
 
-int ensure_mid(HashWs &w, int64_t keys) {
-  if (keys <= w.cap_mid) return EA_OK;
-  if (w.d_mid) (void)hipFree(w.d_mid);
-  w.d_mid = nullptr;
-  w.cap_mid = 0;
+int ensure_mid(uint32_t **mid, int64_t *cap, int64_t keys) {
+  if (keys <= *cap) return EA_OK;
+  if (*mid) (void)hipFree(*mid);
+  *mid = nullptr;
+  *cap = 0;
   const int64_t c = std::max<int64_t>(keys, 4096);
-  HS_HIP(hipMalloc((void **)&w.d_mid, (size_t)c * 32));
-  w.cap_mid = c;
+  HS_HIP(hipMalloc((void **)mid, (size_t)c * 32));
+  *cap = c;
   return EA_OK;
 }
 
@@ -125,7 +145,7 @@ extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
   if ((rc = grow_pair(&w.h_tok, &w.d_tok, &w.cap_tok, tok_bytes)) != EA_OK) return rc;
   if ((rc = grow_pair(&w.h_meta, &w.d_meta, &w.cap_meta, meta_bytes)) != EA_OK) return rc;
   if ((rc = grow_pair(&w.h_keys, &w.d_keys, &w.cap_keys, total * 32)) != EA_OK) return rc;
-  if ((rc = ensure_mid(w, total)) != EA_OK) return rc;
+  if ((rc = ensure_mid(&w.d_mid, &w.cap_mid, total)) != EA_OK) return rc;
 
   int64_t *koff = reinterpret_cast<int64_t *>(w.h_meta);
   int64_t *toff = koff + n_seqs + 1;
@@ -175,21 +195,27 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq
 
   std::lock_guard<std::mutex> lk(g_ws_mu);
   HashWs &w = g_ws;
-  if ((rc = prepare(w)) != EA_OK) return rc;
+  int dev;
+  HS_HIP(hipGetDevice(&dev));
+  if (w.device != dev && (rc = prepare(w)) != EA_OK) return rc;
+  DevSlot &d = w.slots[w.next];
+  w.next ^= 1;
+  if (d.used) HS_HIP(hipEventSynchronize(d.done));  // the call two back is done
+  if (!d.done) HS_HIP(hipEventCreateWithFlags(&d.done, hipEventDisableTiming));
   const int64_t meta_bytes = (2 * (int64_t)n_seqs + 1) * 8;
-  if ((rc = grow_pair(&w.h_meta, &w.d_meta, &w.cap_meta, meta_bytes)) != EA_OK) return rc;
-  if ((rc = ensure_mid(w, total)) != EA_OK) return rc;
-  int64_t *koff = reinterpret_cast<int64_t *>(w.h_meta);
+  if ((rc = grow_pair(&d.h_meta, &d.d_meta, &d.cap_meta, meta_bytes)) != EA_OK) return rc;
+  if ((rc = ensure_mid(&d.d_mid, &d.cap_mid, total)) != EA_OK) return rc;
+  int64_t *koff = reinterpret_cast<int64_t *>(d.h_meta);
   int64_t *toff = koff + n_seqs + 1;
   for (int32_t s = 0; s <= n_seqs; ++s) koff[s] = key_offsets_out[s];
   for (int32_t s = 0; s < n_seqs; ++s) toff[s] = seq_offsets[s];
-  HS_HIP(hipMemcpyAsync(w.d_meta, w.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
-  const int64_t *d_koff = reinterpret_cast<const int64_t *>(w.d_meta);
+  HS_HIP(hipMemcpyAsync(d.d_meta, d.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
+  const int64_t *d_koff = reinterpret_cast<const int64_t *>(d.d_meta);
   HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_koff + n_seqs + 1, n_seqs, total,
-                                     block_tokens, w.d_mid, stream));
-  HS_HIP(ea::launch_sha256_chain(w.d_mid, d_koff, n_seqs, block_tokens, d_parents,
+                                     block_tokens, d.d_mid, stream));
+  HS_HIP(ea::launch_sha256_chain(d.d_mid, d_koff, n_seqs, block_tokens, d_parents,
                                  d_keys_out, stream));
-  HS_HIP(hipEventRecord(w.done, stream));
-  w.used = true;
+  HS_HIP(hipEventRecord(d.done, stream));
+  d.used = true;
   return EA_OK;
 }

@@ -88,3 +88,22 @@ def test_full_int32_range_tokens(b):
     keys, koffs = api.hash_blocks(toks, offs, b)
     okeys, okoffs = oracle.hash_blocks(toks, offs, b)
     assert np.array_equal(koffs, okoffs) and np.array_equal(keys, okeys)
+
+
+def test_device_calls_back_to_back():
+    # asynchronous calls reuse their offset and midstate buffers in turn:
+    # four calls in flight on one stream, different inputs, all correct
+    torch = need_gpu()
+    cases = [[100, 0, 513, 1024], [4096], [16] * 300, [2000, 31, 777]]
+    outs, want = [], []
+    for c, lengths in enumerate(cases):
+        toks, offs = W.sequences(40 + c, lengths)
+        okeys, _ = oracle.hash_blocks(toks, offs, 16)
+        d_tok = torch.as_tensor(toks, device="cuda")
+        out = torch.zeros((len(okeys), 32), dtype=torch.uint8, device="cuda")
+        api.hash_blocks_device(d_tok, offs, 16, out)
+        outs.append((d_tok, out))
+        want.append(okeys)
+    torch.cuda.synchronize()
+    for (_, out), okeys in zip(outs, want):
+        assert np.array_equal(out.cpu().numpy(), okeys)
