@@ -96,6 +96,29 @@ def test_argument_errors_need_no_gpu(lib):
     assert list(koffs) == [0, 0]
 
 
+def test_newer_entry_points_reject_bad_arguments_without_a_gpu(lib):
+    out = C.c_void_p()
+    assert lib.ea_tier_create_chunked(None, 64, 1 << 30, -1, C.byref(out)) == N.EA_EINVAL
+    rep = N.TierReport()
+    assert lib.ea_tier_publish(None, 0, 10, C.byref(rep)) == N.EA_EINVAL
+    pol = N.Policy(950000, 8, 16, 1024, 60, 256, 0, 1, 0)
+    req = N.Request(16, 0, 0, 0, -1, 0)
+    save = C.c_int32()
+    assert lib.ea_admission_fill_report(None, C.byref(pol), C.byref(req), None, 5, None, 0,
+                                        None, C.byref(save)) == N.EA_EINVAL
+    cfg = N.ControllerConfig(1_000_000, 500_000, 5_000_000, 60_000_000, 0, 0)
+    assert lib.ea_controller_create(None, C.byref(pol), C.byref(cfg),
+                                    C.byref(out)) == N.EA_EINVAL
+    assert lib.ea_controller_destroy(None) == N.EA_EINVAL
+    assert lib.ea_controller_advance(None, 5) == N.EA_EINVAL
+    assert lib.ea_controller_decide(None, 16, 0, 0, -1, None, 1, None,
+                                    C.byref(save)) == N.EA_EINVAL
+    st = N.ControllerStatus()
+    assert lib.ea_controller_get_status(None, C.byref(st)) == N.EA_EINVAL
+    assert lib.ea_lru_simulate(None, -1, None, 4, None) == N.EA_EINVAL
+    assert lib.ea_lru_simulate_prefix(None, None, 1, None, 4, None) == N.EA_EINVAL
+
+
 def test_kernel_source_sha_constants_match_the_oracles_derivation():
     # the GPU kernels carry the FIPS 180-4 table typed in; the oracle derives
     # it from primes: they must agree
