@@ -82,8 +82,13 @@ int64_t grid_hbm(int dir) {
 // more waves lower the sum (posted writes and read requests queue behind one
 // another), and keeping the two directions on different XCDs raised the
 // duplex sum from 63 to 83-88 GB/s in measurements on MI355X.  The store runs
-// on XCD 0 and the load on XCD 1 by default.
-int64_t grid_link() { return std::max(1, env_int("EA_LINK_WG", 8)); }
+// on XCD 0 and the load on XCD 1 by default.  EA_LINK_WG sets both
+// directions, EA_LINK_WG_STORE / EA_LINK_WG_LOAD one each (the share of the
+// link each direction gets while both run follows its wave count).
+int64_t grid_link(int dir) {
+  const int both = std::max(1, env_int("EA_LINK_WG", 8));
+  return std::max(1, env_int(dir == ea::kToSlots ? "EA_LINK_WG_STORE" : "EA_LINK_WG_LOAD", both));
+}
 
 // XCDs of the device (workgroups are dispatched round-robin over them).
 int device_xcds(int dev) {
@@ -263,7 +268,7 @@ struct ea_tier {
   std::vector<EvRec> evs;
   std::vector<int32_t> free_evs;
   int64_t bytes_stored = 0, bytes_loaded = 0, store_calls = 0, load_calls = 0;
-  int64_t grid_link = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
+  int64_t grid_store = 8, grid_load = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
   int32_t controllers = 0;  // attached admission controllers (guarded by mu)
@@ -409,7 +414,7 @@ int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
   a.xcd_mask = dir == ea::kToSlots ? t->xcd_store : t->xcd_load;
   const int res_dir = dir == ea::kToSlots ? EA_DIR_STORE : EA_DIR_LOAD;
   return launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir, ea::kRouteHostLink,
-                        t->grid_link, s);
+                        dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
 }
 
 // Staged plan: HBM staging + DMA copies of runs of consecutive slots.
@@ -578,7 +583,8 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
     t->slot = slot_bytes;
     t->K = K;
     t->capacity_bytes = capacity_bytes;
-    t->grid_link = grid_link();
+    t->grid_store = grid_link(ea::kToSlots);
+    t->grid_load = grid_link(ea::kToPages);
     t->num_xcd = shape->num_xcd;
     // two different XCDs for the two directions when the device has them
     t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", 0x1u, t->num_xcd);
