@@ -86,9 +86,12 @@ def cpu_baseline(W, n_s, n_l, prefix_tokens, refill_tokens):
     offs = np.array([0, len(prefix_tokens), len(toks)], np.int64)
     prev = os.sched_getaffinity(0)
     os.sched_setaffinity(0, {sorted(prev)[0]})
-    reps, times = 5, {"hash": [], "store": [], "load": []}
+    # a bounded sample: repeat the step until 10 s of CPU work (5 to 100 runs)
+    times = {"hash": [], "store": [], "load": []}
+    start = time.perf_counter()
     try:
-        for _ in range(reps):
+        while len(times["hash"]) < 5 or (time.perf_counter() - start < 10.0
+                                          and len(times["hash"]) < 100):
             t0 = time.perf_counter()
             oracle.hash_blocks(toks, offs, sh.page_tokens)
             t1 = time.perf_counter()
@@ -103,6 +106,7 @@ def cpu_baseline(W, n_s, n_l, prefix_tokens, refill_tokens):
             times["load"].append(t3 - t2)
     finally:
         os.sched_setaffinity(0, prev)
+    reps = len(times["hash"])
     med = {k: float(np.median(v)) for k, v in times.items()}
     t = sum(med.values())
     moved = (n_s + n_l) * sz["page"]
