@@ -278,7 +278,9 @@ def stack_report(records, capacity_slots, slot_bytes, curve_bytes=()):
                               declined requests, and the share of them whose
                               next reuse distance is >= K_H or that are
                               never referenced again (the proposition's
-                              condition)
+                              condition), the share never referenced again,
+                              and the median next reuse distance over K_H of
+                              those that are
     and, for each tier size in curve_bytes, the coverage of an LRU tier that
     admits every miss in both orders."""
     lens = np.array([len(r.keys) for r in records], np.int64)
@@ -305,6 +307,7 @@ def stack_report(records, capacity_slots, slot_bytes, curve_bytes=()):
             new_mask[offs[j] + r.hit:offs[j + 1]] = True
     nd = nxt[new_mask]
     far = int(np.sum((nd < 0) | (nd >= capacity_slots)))
+    again = nd[nd >= 0]
     return {
         "references": int(len(refs)), "capacity_slots": int(capacity_slots),
         "hits_measured": int(sum(r.hit for r in records)),
@@ -314,6 +317,9 @@ def stack_report(records, capacity_slots, slot_bytes, curve_bytes=()):
         "hits_tier_order_per_request": tier_order,
         "declined_new_blocks": int(new_mask.sum()),
         "declined_meeting_condition": round(far / max(1, int(new_mask.sum())), 4),
+        "declined_never_again": round(int(np.sum(nd < 0)) / max(1, len(nd)), 4),
+        "declined_median_next_distance_over_KH":
+            round(float(np.median(again)) / capacity_slots, 3) if len(again) else None,
         "coverage_curve_full_admission": {
             str(int(b) >> 30) + "GiB": round(float(cov[:, 1 + i].sum()) / max(1, int(lens.sum())), 4)
             for i, b in enumerate(curve_bytes)},
