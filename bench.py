@@ -368,6 +368,58 @@ def run_agent_pool(args):
                  round(el / turns * 1e3, 3), turns, extra)
 
 
+def run_agent_pool_chunked(args):
+    """The agent pool at the paper's deployment parameters on one TP8 rank:
+    24 KiB per token, 1,024-token host chunks (64 pages, 24 MiB), 16 agents,
+    kappa = 8 chunks, host tiers of 5, 10 and 40 GiB (213, 426 and 1,706
+    chunks), 24 turns per agent; loads and stores on two streams."""
+    import torch
+    from paper_2609_33762_amd import api, drivers, workloads as W
+    torch.cuda.set_device(0)
+    sh, C = W.QWEN3_TP8, W.CHUNK_PAGES
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    agents = 16
+    turns = args.turns_per_agent * agents
+    runs, total_moved, total_s = {}, 0, 0.0
+    for gib in (5, 10, 40):
+        tier = api.Tier(cache, gib << 30, chunk_pages=C)
+        pol = api.make_policy(kappa=8, block_tokens=C * sh.page_tokens, beta_rank=beta,
+                              activity_window=agents)
+        pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, agents=agents, verify=False,
+                                 time_fill=True, load_stream=torch.cuda.Stream(),
+                                 store_stream=torch.cuda.Stream())
+        records = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(turns):
+            records.append(pool.turn())
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0 - pool.fill_seconds
+        st = tier.stats()
+        moved = pool.bytes_loaded + pool.bytes_stored
+        total_moved += moved
+        total_s += el
+        rep = drivers.stack_report(records, tier.capacity, tier.slot_bytes)
+        rep.pop("hits_tier_order_per_request")
+        runs[f"{gib}GiB"] = {
+            "K_H": tier.capacity, "gbs": round(moved / el / GB, 2),
+            "ms_per_turn": round(el / turns * 1e3, 3),
+            "hit_chunks": int(sum(r.hit for r in records)),
+            "prompt_chunks": int(sum(len(r.keys) for r in records)),
+            "stored_chunks": int(sum(r.stored for r in records)),
+            "declined_requests": int(sum(not r.save for r in records)),
+            "evictions": st["evictions_total"], "reference_model": rep}
+        log(f"chunked pool {gib} GiB: {runs[f'{gib}GiB']}")
+        tier.close()
+    cache.close()
+    return _line("agent_pool_chunked: one TP8 rank, 1,024-token chunks, 16 agents x %d turns, "
+                 "5/10/40 GiB tiers" % args.turns_per_agent, round(total_moved / total_s / GB, 3),
+                 "GB/s", round(total_s / (3 * turns) * 1e3, 3), 3 * turns, {"pool_chunked": runs})
+
+
 def run_dense_scattered(args):
     """10,000 alternating store/load calls of 1-8 non-adjacent 2 MiB pages."""
     import torch
@@ -780,7 +832,7 @@ def main():
     ap.add_argument("--summarize-profiles", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
-                             "load_cost", "tp8_shard", "hash"])
+                             "load_cost", "tp8_shard", "hash", "agent_pool_chunked"])
     ap.add_argument("--turns-per-agent", type=int, default=24)
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
     args = ap.parse_args()
@@ -794,7 +846,8 @@ def main():
         sys.exit(2)
     other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,
              "layered_fp8": run_layered, "tiny": run_tiny, "load_cost": run_load_cost,
-             "tp8_shard": run_tp8_shard, "hash": run_hash}
+             "tp8_shard": run_tp8_shard, "hash": run_hash,
+             "agent_pool_chunked": run_agent_pool_chunked}
     if args.workload in other:
         out = other[args.workload](args)
         log(json.dumps(out))

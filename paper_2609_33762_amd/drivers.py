@@ -20,12 +20,14 @@ from . import workloads as W
 _M32 = 0xFFFFFFFF
 
 
-def key_pattern(torch, keys, words, device):
-    """int32 [len(keys), words] page contents for blocks with these keys:
-    word j of a block whose key starts with the little-endian uint32 s is
-    fmix32(s + 0x9E3779B1 * j mod 2^32) (MurmurHash3's finaliser)."""
-    seeds = torch.as_tensor(np.ascontiguousarray(keys[:, :4]).view(np.uint32).astype(np.int64)
-                            .reshape(-1, 1), device=device)
+def key_pattern(torch, keys, words, device, chunk_pages=1):
+    """int32 [len(keys) * chunk_pages, words] page contents for blocks with
+    these keys: word j of page c of a block whose key starts with the
+    little-endian uint32 s is fmix32(s + 0x632BE5AB * c + 0x9E3779B1 * j mod
+    2^32) (MurmurHash3's finaliser)."""
+    s0 = np.ascontiguousarray(keys[:, :4]).view(np.uint32).astype(np.int64).reshape(-1, 1)
+    c = np.arange(chunk_pages, dtype=np.int64).reshape(1, -1)
+    seeds = torch.as_tensor(((s0 + c * 0x632BE5AB) & _M32).reshape(-1, 1), device=device)
     j = torch.arange(words, dtype=torch.int64, device=device).reshape(1, -1)
     x = (seeds + j * 0x9E3779B1) & _M32
     x = x ^ (x >> 16)
@@ -71,6 +73,8 @@ class TurnRecord:
 class AgentPool:
     """Agents served round-robin; each turn is one request of one agent.
 
+    A block is one host slot: C = tier.chunk_pages pages of T tokens (one
+    key per b = C * T tokens).
     A prompt keeps the first floor(0.98 * len) tokens of the agent's previous
     prompt, then fresh tokens up to len' = min(len + U[500, 3000], 65536); an
     agent at 65,536 tokens starts a new task at 8,192.  A turn hashes only
@@ -99,7 +103,8 @@ class AgentPool:
         self.sh, self.policy, self.verify = shape, policy, verify
         self.kv3 = kv.view(shape.num_layers, shape.num_pages, shape.piece_bytes)
         self.words = shape.num_layers * shape.piece_bytes // 4
-        self.b = shape.page_tokens
+        self.C = tier.chunk_pages  # pages per host slot (one key per C pages)
+        self.b = shape.page_tokens * self.C
         self.agents = agents
         self.r = W.rng(seed)
         self.tok_rng = [W.rng(seed * 1000 + a) for a in range(agents)]
@@ -148,11 +153,11 @@ class AgentPool:
         return p, keep
 
     def turn(self):
-        torch, tier, cache, b = self.torch, self.tier, self.cache, self.b
+        torch, tier, cache, b, C = self.torch, self.tier, self.cache, self.b, self.C
         a = self.turn_no % self.agents
         t = self.turn_no
         prompt, keep = self._next_prompt(a)
-        n_full = len(prompt) // b
+        n_full = len(prompt) // b  # full blocks (chunks of C pages)
         # incremental hash: blocks before the first changed token keep their keys
         j0 = min(keep // b, len(self.keys[a]), n_full)
         parent = self.keys[a][j0 - 1].reshape(1, 32) if j0 > 0 else None
@@ -163,10 +168,10 @@ class AgentPool:
 
         h, hit_slots = tier.lookup(keys)
         if self.overlap:
-            pages = W.distinct(self.r, self.sh.num_pages, n_full, exclude=self._busy_pages())
+            pages = W.distinct(self.r, self.sh.num_pages, n_full * C, exclude=self._busy_pages())
         else:
-            pages = W.distinct(self.r, self.sh.num_pages, n_full)
-        load_pages, fill_pages = pages[:h], pages[h:]
+            pages = W.distinct(self.r, self.sh.num_pages, n_full * C)
+        load_pages = pages[:h * C]
         if h:
             if self.overlap and self.load_stream is not None:
                 self.load_stream.wait_stream(torch.cuda.current_stream())
@@ -178,30 +183,33 @@ class AgentPool:
                 # nothing of the path runs while the excluded fill is timed
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
-            for c0 in range(h, n_full, 512):
-                c1 = min(n_full, c0 + 512)
-                write_pages(torch, self.kv3, pages[c0:c1],
-                            key_pattern(torch, keys[c0:c1], self.words, self.kv.device))
+            step = max(1, 512 // C)
+            for c0 in range(h, n_full, step):
+                c1 = min(n_full, c0 + step)
+                write_pages(torch, self.kv3, pages[c0 * C:c1 * C],
+                            key_pattern(torch, keys[c0:c1], self.words, self.kv.device, C))
             if self.time_fill:
                 torch.cuda.synchronize()
                 self.fill_seconds += time.perf_counter() - t0
         save, mask = tier.admission(self.policy, len(prompt), h * b, a, t, keys)
         _, slots = tier.alloc(keys, mask)
         ok = slots >= 0
+        store_pages = pages.reshape(n_full, C)[ok].reshape(-1)
         if ok.any():
             if self.overlap and self.store_stream is not None:
                 # the store reads the pages the fill just wrote
                 self.store_stream.wait_stream(torch.cuda.current_stream())
-            tier.store(cache, pages[ok], slots[ok], stream=self.store_stream)
+            tier.store(cache, store_pages, slots[ok], stream=self.store_stream)
             self.bytes_stored += int(ok.sum()) * tier.slot_bytes
-            self._note(self.store_stream, pages[ok])
+            self._note(self.store_stream, store_pages)
         loaded_ok = True
         if self.verify and h:
             torch.cuda.synchronize()
-            for c0 in range(0, h, 512):
-                c1 = min(h, c0 + 512)
-                want = key_pattern(torch, keys[c0:c1], self.words, self.kv.device)
-                got = read_pages(torch, self.kv3, load_pages[c0:c1]).view(torch.int32)
+            step = max(1, 512 // C)
+            for c0 in range(0, h, step):
+                c1 = min(h, c0 + step)
+                want = key_pattern(torch, keys[c0:c1], self.words, self.kv.device, C)
+                got = read_pages(torch, self.kv3, load_pages[c0 * C:c1 * C]).view(torch.int32)
                 loaded_ok &= bool(torch.equal(got, want))
         if ok.any():
             tier.unpin(slots[ok])
@@ -209,7 +217,7 @@ class AgentPool:
             tier.unpin(hit_slots)
         self.turn_no += 1
         return TurnRecord(t, a, len(prompt), keys, h, hit_slots, save, mask, slots,
-                          int(ok.sum()), loaded_ok, load_pages, pages[ok])
+                          int(ok.sum()), loaded_ok, load_pages, store_pages)
 
 
 # ------------------------------------------------- dense scattered batches

@@ -313,3 +313,52 @@ def test_agent_pool_overlapped_streams():
     del kv
     release(torch)
 
+
+
+def test_agent_pool_in_1024_token_chunks():
+    # the paper's deployment parameters on one TP8 rank: 24 KiB per token,
+    # 1,024-token host chunks (64 pages, 24 MiB), a 5 GiB tier (213 chunks),
+    # 16 agents, kappa = 8 chunks; metadata equals the oracle's every turn
+    torch = need_gpu()
+    sh, C = W.QWEN3_TP8, W.CHUNK_PAGES
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    cache = api.Cache(kv, sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                      sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, 5 << 30, chunk_pages=C)
+    assert tier.capacity == 213
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    kw = dict(kappa=8, block_tokens=C * sh.page_tokens, activity_window=16)
+    pol = api.make_policy(beta_rank=beta, **kw)
+    opol = oracle.make_policy(beta=beta, **kw)
+    oshape = oracle.make_shape(sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                               sh.head_dim, sh.elem_bytes, chunk_pages=C)
+    ot = oracle.Tier(oshape, 5 << 30)
+    pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, agents=16)
+    hits = declined = 0
+    for t in range(4 * 16):
+        rec = pool.turn()
+        assert rec.loaded_ok, f"turn {t}: a loaded page differs from its chunk key's pattern"
+        assert len(rec.keys) == rec.n_tokens // (C * sh.page_tokens)
+        h, hs = ot.lookup(rec.keys)
+        assert h == rec.hit and np.array_equal(hs, rec.hit_slots), t
+        save, mask = ot.admission(opol, rec.n_tokens, rec.hit * C * sh.page_tokens, rec.agent,
+                                  t, rec.keys)
+        assert save == rec.save and np.array_equal(mask, rec.mask), t
+        _, slots = ot.alloc(rec.keys, mask)
+        assert np.array_equal(slots, rec.alloc_slots), t
+        ok = slots >= 0
+        ot.mark_stored(slots[ok])
+        if ok.any():
+            ot.unpin(slots[ok])
+        if h:
+            ot.unpin(hs)
+        hits += h
+        declined += int(not save)
+    a, b = tier.export(), ot.export()
+    for k in ("state", "pins", "keys", "lru"):
+        assert np.array_equal(a[k], b[k]), k
+    assert hits > 0 and tier.stats()["evictions_total"] > 0
+    tier.close()
+    cache.close()
+    del kv
+    release(torch)
