@@ -372,7 +372,9 @@ def run_agent_pool_chunked(args):
     """The agent pool at the paper's deployment parameters on one TP8 rank:
     24 KiB per token, 1,024-token host chunks (64 pages, 24 MiB), 16 agents,
     kappa = 8 chunks, host tiers of 5, 10 and 40 GiB (213, 426 and 1,706
-    chunks), 24 turns per agent; loads and stores on two streams."""
+    chunks), 24 turns per agent; loads and stores on two streams.  Each tier
+    runs under the three admission modes of section 4: offload without
+    admission (p = 0), fixed admission (p = 1) and the conditioned rule."""
     import torch
     from paper_2609_33762_amd import api, drivers, workloads as W
     torch.cuda.set_device(0)
@@ -383,11 +385,14 @@ def run_agent_pool_chunked(args):
     beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
     agents = 16
     turns = args.turns_per_agent * agents
+    from paper_2609_33762_amd import _native as N
+    modes = {"offload": N.EA_ADMIT_ALWAYS, "fixed": N.EA_ADMIT_FIXED,
+             "conditioned": N.EA_ADMIT_CONDITIONED}
     runs, total_moved, total_s = {}, 0, 0.0
-    for gib in (5, 10, 40):
+    for gib, (mname, mode) in [(g, m) for g in (5, 10, 40) for m in modes.items()]:
         tier = api.Tier(cache, gib << 30, chunk_pages=C)
         pol = api.make_policy(kappa=8, block_tokens=C * sh.page_tokens, beta_rank=beta,
-                              activity_window=agents)
+                              activity_window=agents, mode=mode)
         pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, agents=agents, verify=False,
                                  time_fill=True, load_stream=torch.cuda.Stream(),
                                  store_stream=torch.cuda.Stream())
@@ -404,7 +409,7 @@ def run_agent_pool_chunked(args):
         total_s += el
         rep = drivers.stack_report(records, tier.capacity, tier.slot_bytes)
         rep.pop("hits_tier_order_per_request")
-        runs[f"{gib}GiB"] = {
+        runs[f"{gib}GiB_{mname}"] = {
             "K_H": tier.capacity, "gbs": round(moved / el / GB, 2),
             "ms_per_turn": round(el / turns * 1e3, 3),
             "hit_chunks": int(sum(r.hit for r in records)),
@@ -412,12 +417,17 @@ def run_agent_pool_chunked(args):
             "stored_chunks": int(sum(r.stored for r in records)),
             "declined_requests": int(sum(not r.save for r in records)),
             "evictions": st["evictions_total"], "reference_model": rep}
-        log(f"chunked pool {gib} GiB: {runs[f'{gib}GiB']}")
+        r = runs[f"{gib}GiB_{mname}"]
+        log(f"chunked pool {gib} GiB {mname}: hit {r['hit_chunks']} of {r['prompt_chunks']}, "
+            f"stored {r['stored_chunks']}, declined {r['declined_requests']}, evictions "
+            f"{r['evictions']}, {r['gbs']} GB/s, declined meeting Prop. 1 "
+            f"{rep['declined_meeting_condition']}, tier-order model {rep['hits_model_tier_order']}")
         tier.close()
     cache.close()
     return _line("agent_pool_chunked: one TP8 rank, 1,024-token chunks, 16 agents x %d turns, "
-                 "5/10/40 GiB tiers" % args.turns_per_agent, round(total_moved / total_s / GB, 3),
-                 "GB/s", round(total_s / (3 * turns) * 1e3, 3), 3 * turns, {"pool_chunked": runs})
+                 "5/10/40 GiB tiers x 3 admission modes" % args.turns_per_agent,
+                 round(total_moved / total_s / GB, 3), "GB/s",
+                 round(total_s / (9 * turns) * 1e3, 3), 9 * turns, {"pool_chunked": runs})
 
 
 def run_dense_scattered(args):
