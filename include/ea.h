@@ -421,8 +421,9 @@ int ea_tier_get_plan(const ea_tier *tier, int direction, int *plan);
  * tier's pinned memory, best of `reps`, in GB/s (1e9 bytes/s).  direction:
  * EA_DIR_STORE (device to host), EA_DIR_LOAD (host to device) or EA_DIR_BOTH
  * (both at once on two streams; total bytes over the slower one).  Overwrites
- * the first bytes (2*bytes for BOTH) of the tier's slots: use it on a tier
- * that holds nothing yet. */
+ * the first bytes (2*bytes for BOTH) of the tier's slots, so it returns
+ * EA_EINVAL, moving nothing, while any slot in that range is allocated or
+ * holds a stored chunk: use it on a tier that holds nothing yet. */
 int ea_peak_probe(ea_tier *tier, void *d_buf, int64_t bytes, int direction,
                   int reps, double *gbps);
 

@@ -974,6 +974,8 @@ int ea_peak_probe(ea_tier *t, void *d_buf, int64_t bytes, int direction, int rep
   DeviceScope ds(t->device);
   EA_TRY(ds.status());
   std::lock_guard<std::mutex> lk(t->mu);
+  // the probe overwrites the first slots: refuse while any of them is in use
+  if (!t->meta->slots_free(0, (need + t->slot - 1) / t->slot)) return EA_EINVAL;
   for (auto &ev : t->evs) EA_HIP(hipEventSynchronize(ev.ev));
   hipStream_t s[2] = {nullptr, nullptr};
   hipEvent_t e0[2] = {nullptr, nullptr}, e1[2] = {nullptr, nullptr};

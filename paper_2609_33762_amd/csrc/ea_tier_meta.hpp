@@ -67,6 +67,13 @@ class TierMeta {
   void stats(ea_tier_stats *s) const;
   void export_state(uint8_t *state, int32_t *pins, uint8_t *keys, int64_t *lru,
                     int64_t *n_lru) const;
+  // True when slots [first, first + count) hold nothing (no allocation, no
+  // stored chunk).
+  bool slots_free(int64_t first, int64_t count) const {
+    for (int64_t s = first; s < first + count && s < K_; ++s)
+      if (state_[s] != EA_SLOT_FREE) return false;
+    return true;
+  }
 
  private:
   bool registered(const Key &k) const { return map_.find(k) != map_.end(); }

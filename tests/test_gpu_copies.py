@@ -120,6 +120,30 @@ def test_errors_move_nothing():
     p.close()
 
 
+def test_peak_probe_refuses_a_tier_in_use():
+    # the probe overwrites the first slots; with one of them allocated it
+    # must move nothing
+    torch = need_gpu()
+    p = tiny_pair(seed=4)
+    slot = p.sizes["slot"]
+    buf = torch.empty(4 * slot, dtype=torch.uint8, device="cuda")
+    assert p.tier.peak_probe(buf, 2 * slot, N.EA_DIR_BOTH, 1) > 0  # empty tier: fine
+    key = np.arange(32, dtype=np.uint8)[None, :]
+    cnt, slots = p.tier.alloc(key)
+    assert cnt == 1 and slots[0] == 0
+    p.tier.store(p.cache, [7], slots)
+    torch.cuda.synchronize()
+    before = p.tier.host_view().copy()
+    for direction in (N.EA_DIR_STORE, N.EA_DIR_LOAD, N.EA_DIR_BOTH):
+        with pytest.raises(N.EAError) as e:
+            p.tier.peak_probe(buf, slot, direction, 1)
+        assert e.value.code == N.EA_EINVAL
+    torch.cuda.synchronize()
+    assert np.array_equal(p.tier.host_view(), before)
+    p.tier.unpin(slots)
+    p.close()
+
+
 def test_load_on_another_stream_waits_for_the_store():
     torch = need_gpu()
     p = tiny_pair(seed=9, slots=256)
