@@ -234,21 +234,28 @@ def run_steps(ctx, args):
     for k in range(args.warmup):
         step(k, False)
     torch.cuda.synchronize()
-    stored = 0
+    stored = []
     t0 = time.perf_counter()
     for k in range(args.warmup, total):
-        stored += step(k, True)
+        stored.append(step(k, True))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    store_ms = [a.elapsed_time(c) for a, c in zip(ev["s0"], ev["s1"])]
+    load_ms = [a.elapsed_time(c) for a, c in zip(ev["l0"], ev["l1"])]
+    page = ctx["page"]
     res = {"ms": elapsed / args.steps * 1e3,
-           "gbs": (stored + args.steps * n_load) * ctx["page"] / elapsed / GB,
-           "store_ms": float(np.mean([a.elapsed_time(c) for a, c in zip(ev["s0"], ev["s1"])])),
-           "load_ms": float(np.mean([a.elapsed_time(c) for a, c in zip(ev["l0"], ev["l1"])])),
-           "tier": tier.stats()}
+           "gbs": (sum(stored) + args.steps * n_load) * page / elapsed / GB,
+           "store_ms": float(np.mean(store_ms)), "load_ms": float(np.mean(load_ms)),
+           # each timed store is one kernel launch of `stored` pages, each load
+           # one launch of n_load pages; HIP events on the launching stream
+           "store_gbs_in_step": sum(stored) * page / (sum(store_ms) * 1e-3) / GB,
+           "load_gbs_in_step": args.steps * n_load * page / (sum(load_ms) * 1e-3) / GB,
+           "stored_pages": stored, "tier": tier.stats()}
     ctx["last_store_pages"], ctx["last_load_dst"], ctx["last_refill"] = (
         store_pages[-1], load_dst[-1], refills[-1])
     log(f"step {res['ms']:.2f} ms, {res['gbs']:.1f} GB/s over the link; in-step store "
-        f"{res['store_ms']:.2f} ms, load {res['load_ms']:.2f} ms; evictions "
+        f"{res['store_ms']:.2f} ms ({res['store_gbs_in_step']:.1f} GB/s), load "
+        f"{res['load_ms']:.2f} ms ({res['load_gbs_in_step']:.1f} GB/s); evictions "
         f"{res['tier']['evictions_total']}")
     return res
 
@@ -570,53 +577,80 @@ def _short(name):
 
 
 def summarize_profiles(d):
-    """Write the committed rocprofv3 summaries from the CSVs of the three
-    --isolated-only runs under directory d."""
+    """Write the committed rocprofv3 summaries from the CSVs of three runs of
+    the default bench command under directory d: a kernel trace and two
+    counter passes.  Store and load are read from the launches of the timed
+    steps (their place in launch order is in the run's detail file), gather
+    and scatter from their isolated series."""
     cmd_trace = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_trace "
-                 "-o trace -- python3 bench.py --isolated-only --detail "
-                 "gpurun_out/bench_detail_trace.json")
+                 "-o trace -- python3 bench.py --detail gpurun_out/bench_detail_trace.json")
     cmd_pmc = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{l} -o {l} -- python3 "
-               "bench.py --isolated-only --detail gpurun_out/bench_detail_{l}.json")
-    detail = json.load(open(os.path.join(d, "bench_detail_trace.json")))["isolated"]
+               "bench.py --no-cpu-baseline --detail gpurun_out/bench_detail_{l}.json")
+
+    def pick(k, vals, plan):
+        """The launches of kernel k that belong to the timed steps (store,
+        load) or to the isolated series (gather, scatter)."""
+        if k in plan:
+            p = plan[k]
+            want = p["before"] + p["timed"] + p["after"]
+            if len(vals) != want:
+                raise SystemExit(f"{k}: {len(vals)} launches in the profile, the run made {want}")
+            return vals[p["before"]:p["before"] + p["timed"]]
+        return vals[-N_ISO[k]:]
+
+    det = json.load(open(os.path.join(d, "bench_detail_trace.json")))
+    plan, steps, iso = det["dispatches"], det["steps"], det["isolated"]
     rows = list(csv.DictReader(open(os.path.join(d, "prof_trace", "trace_kernel_trace.csv"))))
     disp = {}
     for x in rows:
-        s = _short(x["Kernel_Name"])
-        if s:
-            disp.setdefault(s, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e6)
-    # the isolated phase: the last N_ISO launches of each copy kernel
+        k = _short(x["Kernel_Name"])
+        if k:
+            disp.setdefault(k, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e6)
+    stats = {}
+    for x in csv.DictReader(open(os.path.join(d, "prof_trace", "trace_kernel_stats.csv"))):
+        k = _short(x["Name"])
+        if k:
+            stats[k] = (int(x["Calls"]), float(x["AverageNs"]) / 1e6)
     n_store, n_load, page, slot = 2000, 1500, 1572864, 1572864
     alg = {"store": n_store * page, "load": n_load * page,
            "gather": 2 * n_store * slot, "scatter": 2 * n_store * slot}
+    ev = {"store": steps["store_ms"], "load": steps["load_ms"], "gather": iso["gather_ms"],
+          "scatter": iso["scatter_ms"]}
     lines = ["# Kernel durations: piece copies, Qwen3-30B-A3B turn (2,000 stored / 1,500 loaded "
              "pages of 1.5 MiB)", "",
              "Command (from the repository root on the MI355X):", "", f"    {cmd_trace}",
              "    python3 bench.py --summarize-profiles gpurun_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
-             "| kernel | launches | rocprof avg ms | HIP-event avg ms (same run) | algorithmic "
-             "GB/s (rocprof) |", "|---|---|---|---|---|"]
-    ev_key = {"store": "store_ms", "load": "load_ms", "gather": "gather_ms", "scatter": "scatter_ms"}
+             "Store and load: the launches of the timed steps, where the two run together on "
+             "two streams (launch order from the run's detail file).  Gather and scatter: their "
+             "isolated series.  The HIP-event column is the same run's own timing of the same "
+             "launches (events on the launching stream).", "",
+             "| kernel | launches used | rocprof avg ms | HIP-event avg ms (same run) | "
+             "algorithmic GB/s (rocprof) | all launches: count, --stats avg ms |",
+             "|---|---|---|---|---|---|"]
     for k in ("store", "load", "gather", "scatter"):
-        ds = disp.get(k, [])[-N_ISO[k]:]
-        avg = float(np.mean(ds)) if ds else float("nan")
-        lines.append(f"| {k} | {len(ds)} | {avg:.4f} | {detail[ev_key[k]]:.4f} | "
-                     f"{alg[k] / (avg * 1e-3) / GB:.1f} |")
+        ds = pick(k, disp.get(k, []), plan)
+        avg = float(np.mean(ds))
+        c, a = stats.get(k, (0, float("nan")))
+        lines.append(f"| {k} | {len(ds)} | {avg:.4f} | {ev[k]:.4f} | "
+                     f"{alg[k] / (avg * 1e-3) / GB:.1f} | {c}, {a:.4f} |")
     for k in ("sha256_midstates", "sha256_chain"):
-        ds = disp.get(k, [])
-        if ds:
-            lines.append(f"| {k} | {len(ds)} | {np.mean(ds):.4f} | - | - |")
+        if k in stats:
+            c, a = stats[k]
+            lines.append(f"| {k} | {c} | {a:.4f} | - | - | {c}, {a:.4f} |")
     open(TRACE_SUMMARY, "w").write("\n".join(lines) + "\n")
 
     counters = {}
     for label, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        pplan = json.load(open(os.path.join(d, f"bench_detail_{label}.json")))["dispatches"]
         rows = list(csv.DictReader(open(os.path.join(d, f"prof_{label}",
                                                      f"{label}_counter_collection.csv"))))
         per = {}
         for x in rows:
-            s = _short(x["Kernel_Name"])
-            if s and x["Counter_Name"] == ctr:
-                per.setdefault(s, []).append(float(x["Counter_Value"]))
-        counters[ctr] = per
+            k = _short(x["Kernel_Name"])
+            if k and x["Counter_Name"] == ctr:
+                per.setdefault(k, []).append(float(x["Counter_Value"]))
+        counters[ctr] = {k: (pick(k, v, pplan) if k in alg else v) for k, v in per.items()}
     # calibration: the last rocclr copy is the plain 1 GiB device copy
     cal_f = counters["FETCH_SIZE"]["rocclr_copyBuffer"][-1]
     cal_w = counters["WRITE_SIZE"]["rocclr_copyBuffer"][-1]
@@ -632,12 +666,13 @@ def summarize_profiles(d):
              f"Calibration: a plain 1 GiB device copy (rocclr copyBuffer) reads FETCH_SIZE "
              f"{cal_f:.0f} KiB and WRITE_SIZE {cal_w:.0f} KiB for 1,048,576 KiB each way, so "
              f"FETCH_SIZE is scaled by {f_fac:.3f} and WRITE_SIZE by {w_fac:.3f}.  Reads and "
-             "writes of the mapped pinned host slots count in the same counters.", "",
-             "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes | algorithmic bytes | "
+             "writes of the mapped pinned host slots count in the same counters.  Store and load "
+             "are the launches of the timed steps, gather and scatter their isolated series.",
+             "", "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes | algorithmic bytes | "
              "ratio |", "|---|---|---|---|---|---|"]
     for k in ("store", "load", "gather", "scatter"):
-        fv = counters["FETCH_SIZE"].get(k, [])[-N_ISO[k]:]
-        wv = counters["WRITE_SIZE"].get(k, [])[-N_ISO[k]:]
+        fv = counters["FETCH_SIZE"].get(k, [])
+        wv = counters["WRITE_SIZE"].get(k, [])
         if not fv or not wv:
             continue
         fk, wk = float(np.mean(fv)), float(np.mean(wv))
@@ -891,14 +926,17 @@ def main():
 
     peak = ctx["peak"]
     traffic = committed_traffic() or {}
-    # the dominant kernel of the step is the store (2,000 pages over the link)
+    # the dominant kernel of the step is the store (2,000 pages over the
+    # link), timed in the step itself: it shares the link with the load
     roofline = {
         "bound": "host-link", "kernel": f"copy_host_link<store> ({plans['store']} plan, "
-                                        f"2,000 pages)",
-        "achieved": round(iso["store_gbs"], 2), "peak": round(peak["d2h"], 2),
+                                        f"2,000 pages, alongside the 1,500-page load)",
+        "achieved": round(steps["store_gbs_in_step"], 2), "peak": round(peak["d2h"], 2),
         "peak_kind": "measured pinned hipMemcpyAsync device-to-host, 1 GiB, best of 10",
-        "unit": "GB/s", "frac": round(iso["store_gbs"] / peak["d2h"], 4),
+        "unit": "GB/s", "frac": round(steps["store_gbs_in_step"] / peak["d2h"], 4),
         "traffic": traffic.get("store"),
+        "timing": f"HIP events on the store's stream around each of the {args.steps} timed "
+                  f"launches",
     }
     roofline_hbm = {
         "bound": "hbm", "kernel": "copy_hbm<gather> (paged gather of 2,000 pages to HBM)",
@@ -919,6 +957,8 @@ def main():
                    "load_pages": ctx["n_load"], "plans": plans},
         "roofline": roofline, "roofline_hbm": roofline_hbm,
         "host_link": {"store_gbs": round(iso["store_gbs"], 2), "load_gbs": round(iso["load_gbs"], 2),
+                      "store_gbs_in_step": round(steps["store_gbs_in_step"], 2),
+                      "load_gbs_in_step": round(steps["load_gbs_in_step"], 2),
                       "peak_d2h": round(peak["d2h"], 2), "peak_h2d": round(peak["h2d"], 2),
                       "peak_bidir": round(peak["bidir"], 2),
                       "frac_store": round(iso["store_gbs"] / peak["d2h"], 4),
@@ -927,7 +967,16 @@ def main():
                       "frac_duplex_of_bidir": round(steps["gbs"] / peak["bidir"], 4)},
         "cpu_baseline": cpu,
     }
-    json.dump({"line": out, "steps": steps, "isolated": iso, "peak": peak}, open(args.detail, "w"),
+    # launch order of each copy kernel in this run, for the profile summary:
+    # the setup's prefix store, the warmup and timed steps, then the
+    # isolated series (one untimed call before each)
+    dispatches = {
+        "store": {"before": 1 + args.warmup, "timed": args.steps,
+                  "after": 1 + 3 + 1 + N_ISO["store"]},
+        "load": {"before": args.warmup, "timed": args.steps, "after": 1 + 3 + 1 + N_ISO["load"]},
+    }
+    json.dump({"line": out, "steps": steps, "isolated": iso, "peak": peak,
+               "dispatches": dispatches, "argv": sys.argv[1:]}, open(args.detail, "w"),
               indent=1, default=float)
     print(json.dumps(out), flush=True)
 

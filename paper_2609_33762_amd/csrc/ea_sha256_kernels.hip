@@ -164,6 +164,13 @@ __global__ __launch_bounds__(64) void sha256_chain(
   const int64_t k0 = key_off[s], k1 = key_off[s + 1];
   const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
   uint4 nx = k0 < k1 ? mh[2 * k0 + (e_side ? 1 : 0)] : make_uint4(0, 0, 0, 0);
+  // Take the first midstate before the loop.  Memory operations complete in
+  // issue order as far as the wait counter is concerned, so a load still
+  // pending at the loop head would make every key wait for the previous
+  // key's store to be acknowledged; with none pending there, a key waits
+  // only for the prefetch of its midstate, issued a whole compression
+  // earlier and ahead of that store.
+  asm volatile("" ::"v"(nx.x), "v"(nx.y), "v"(nx.z), "v"(nx.w));
   // message words in pairs: x[j] holds W_2j on the e-lane, W_2j+1 on the
   // a-lane; x[0..3] come from the previous key, x[4..7] are the padding
   const uint32_t pad8 = e_side ? 0x80000000u : 0u;   // (W8, W9)
