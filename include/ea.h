@@ -189,6 +189,12 @@ typedef struct {
   int64_t activity_window; /* window of A_t and e_t in caller clock units; an
                               event at time t counts when t > now - window    */
   int32_t length_window;   /* N_t = mean n of the last this-many first lookups*/
+                           /* Memory stays bounded: once the tier holds more
+                              than 65,536 lookups (or eviction stamps) it
+                              keeps only those that the largest activity,
+                              report and length windows given so far can
+                              still reach; a window larger than all earlier
+                              ones then sees no events older than they did.   */
   int32_t mode;            /* EA_ADMIT_*                                      */
   int32_t telemetry;       /* 1: the tier's own state is a fresh report;
                               0: no report, the estimate alone decides        */

@@ -47,6 +47,18 @@ int64_t TierMeta::take_free_slot() {
   return -1;
 }
 
+void TierMeta::trim() {
+  constexpr size_t kTrimAt = size_t(1) << 16;  // history kept whole up to this size
+  if (!have_clock_) return;
+  const __int128 old = (__int128)clock_ - keep_time_;
+  if (log_.size() > kTrimAt)
+    while ((int64_t)log_.size() > keep_count_ && (__int128)log_.front().time <= old)
+      log_.pop_front();
+  if (evict_stamps_.size() > kTrimAt)
+    while (!evict_stamps_.empty() && (__int128)evict_stamps_.front() <= old)
+      evict_stamps_.pop_front();
+}
+
 void TierMeta::release_slot(int64_t s) {
   map_.erase(keys_[s]);
   lru_remove(s);
@@ -102,6 +114,8 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
     log_.push_back(Lookup{now, r.task_id, r.n_tokens});
     clock_ = now;
     have_clock_ = true;
+    keep_time_ = std::max(keep_time_, p.activity_window);
+    keep_count_ = std::max<int64_t>(keep_count_, p.length_window);
     const int64_t horizon = now - p.activity_window;
 
     // A_t: distinct tasks whose first lookup falls inside the window
@@ -155,6 +169,7 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
     last_ws_ = (double)(active - 1) * last_mean_ * (double)p.beta_rank;
     last_pressure_ = pressure ? 1 : 0;
     last_save_ = save;
+    trim();
   }
   // copy-time deduplication: chunks the tier already holds are not copied
   for (int64_t i = 0; i < n_keys; ++i)
@@ -169,6 +184,7 @@ int TierMeta::publish(int64_t now, int64_t window, ea_tier_report *out) {
   if (have_clock_ && now < clock_) return EA_EINVAL;
   clock_ = now;
   have_clock_ = true;
+  keep_time_ = std::max(keep_time_, window);
   int64_t e = 0;
   for (auto it = evict_stamps_.rbegin(); it != evict_stamps_.rend() && *it > now - window; ++it)
     ++e;
@@ -176,6 +192,7 @@ int TierMeta::publish(int64_t now, int64_t window, ea_tier_report *out) {
   out->registered = registered_;
   out->capacity_slots = K_;
   out->evictions = e;
+  trim();
   return EA_OK;
 }
 
@@ -202,6 +219,7 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
         continue;
       }
       evict_stamps_.push_back(clock_);
+      evictions_total_ += 1;
       map_.erase(keys_[v]);
       lru_remove(v);
       state_[v] = EA_SLOT_FREE;
@@ -219,6 +237,7 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
     ++count;
   }
   *allocated = count;
+  trim();
   return EA_OK;
 }
 
@@ -251,7 +270,7 @@ void TierMeta::stats(ea_tier_stats *s) const {
   int64_t pinned = 0;
   for (int32_t p : pins_) pinned += p > 0;
   s->pinned = pinned;
-  s->evictions_total = (int64_t)evict_stamps_.size();
+  s->evictions_total = evictions_total_;
   int64_t in_window = 0;
   for (auto it = evict_stamps_.rbegin();
        it != evict_stamps_.rend() && *it > clock_ - last_window_; ++it)

@@ -7,6 +7,7 @@
 
 #include <chrono>
 #include <cstring>
+#include <deque>
 #include <functional>
 #include <queue>
 #include <unordered_map>
@@ -94,12 +95,22 @@ class TierMeta {
   // slots below fresh_, so the lowest free slot is returned_.top() or fresh_
   int64_t fresh_ = 0;
   std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> returned_;
+  // Bound the lookup log and the eviction stamps: once either holds more
+  // than 65,536 entries, drop those no window used so far can reach again.
+  // The clock only moves forward, so an entry at or before
+  // clock - keep_time_ is outside every such time window, and only the last
+  // keep_count_ lookups enter a mean.
+  void trim();
+
   int64_t registered_ = 0, resident_ = 0;
-  std::vector<int64_t> evict_stamps_;
+  std::deque<int64_t> evict_stamps_;
+  int64_t evictions_total_ = 0;
   struct Lookup {
     int64_t time, task, n;
   };
-  std::vector<Lookup> log_;
+  std::deque<Lookup> log_;
+  int64_t keep_time_ = 0;   // largest activity or report window used
+  int64_t keep_count_ = 1;  // largest length window used
   int64_t clock_ = 0;
   bool have_clock_ = false;
   bool steady_ = false;

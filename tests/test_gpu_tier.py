@@ -85,3 +85,63 @@ def test_all_pinned_tier_reports_unallocated_blocks():
     with pytest.raises(N.EAError):
         p.tier.unpin([0, 0])
     p.close()
+
+
+def test_long_stream_with_bounded_history_matches_the_oracle():
+    # More first lookups and more evictions than the tier keeps whole
+    # (65,536): the library then drops history no window can reach again,
+    # the oracle keeps all of it; every decision, report and statistic must
+    # still agree.
+    K = 8
+    p = Pair(64, 1, 16, 1, 32, 2, K, seed=7)  # 2 KiB slots
+    beta = 2 * 32 * 2
+    ot = oracle.Tier(p.oshape, K * p.sizes["slot"])
+    kw = dict(kappa=1, block_tokens=16, activity_window=12, length_window=16,
+              mode=N.EA_ADMIT_CONDITIONED, telemetry=1)
+    pol_p = api.make_policy(beta_rank=beta, **kw)
+    pol_o = oracle.make_policy(beta=beta, **kw)
+    r = W.rng(77)
+    n_req = 80_000
+    nblocks = np.where(r.random(n_req) < 0.05, 3, 1)
+    repeat = r.random(n_req) < 0.1
+    pages = r.integers(0, 64, size=n_req)
+    serial = 0
+    recent = []
+    for t in range(n_req):
+        nb = int(nblocks[t])
+        if repeat[t] and recent:
+            keys = recent[-1 - t % len(recent)]  # one of the last requests again
+            nb = keys.shape[0]
+        else:
+            keys = np.zeros((nb, 32), np.uint8)
+            for j in range(nb):
+                serial += 1
+                keys[j, :8] = np.frombuffer(serial.to_bytes(8, "little"), np.uint8)
+        recent.append(keys)
+        recent = recent[-4:]
+        h, hs = p.tier.lookup(keys)
+        oh, ohs = ot.lookup(keys)
+        assert h == oh and np.array_equal(hs, ohs), t
+        save, mask = p.tier.admission(pol_p, 16 * nb, 16 * h, t % 40, t, keys)
+        osave, omask = ot.admission(pol_o, 16 * nb, 16 * h, t % 40, t, keys)
+        assert save == osave and np.array_equal(mask, omask), t
+        cnt, slots = p.tier.alloc(keys, mask)
+        ocnt, oslots = ot.alloc(keys, mask)
+        assert cnt == ocnt and np.array_equal(slots, oslots), t
+        got = slots >= 0
+        if got.any():
+            p.tier.store(p.cache, np.full(int(got.sum()), pages[t]), slots[got])
+            ot.mark_stored(slots[got])
+            p.tier.unpin(slots[got])
+            ot.unpin(slots[got])
+        if h:
+            p.tier.unpin(hs)
+            ot.unpin(ohs)
+        if t % 997 == 0 or t == n_req - 1:
+            rp, ro = p.tier.publish(t, 12), ot.publish(t, 12)
+            assert (rp.registered, rp.capacity_slots, rp.evictions) == \
+                (ro.registered, ro.capacity_slots, ro.evictions), t
+            compare(p.tier, ot, f"request {t}")
+    st = p.tier.stats()
+    assert st["evictions_total"] > 65_536
+    p.close()
