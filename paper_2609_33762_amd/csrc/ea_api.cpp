@@ -272,6 +272,7 @@ struct ea_tier {
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
   int32_t controllers = 0;  // attached admission controllers (guarded by mu)
+  int32_t steady_users = 0; // attached steady-clock controllers (guarded by mu)
 };
 
 namespace {
@@ -661,7 +662,10 @@ int ea_tier_destroy(ea_tier *t) {
 
 void ea::tier_use_steady_clock(ea_tier *t, bool on) {
   std::lock_guard<std::mutex> lk(t->mu);
-  t->meta->use_steady_clock(on);
+  // one count per steady-clock controller: the tier keeps the steady clock
+  // until the last of them detaches
+  t->steady_users += on ? 1 : -1;
+  t->meta->use_steady_clock(t->steady_users > 0);
 }
 
 void ea::tier_attach_controller(ea_tier *t, int delta) {

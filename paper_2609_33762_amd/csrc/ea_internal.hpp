@@ -52,8 +52,9 @@ void set_last_hip(int err);
 struct ea_tier;
 namespace ea {
 
-// Make the tier read the steady clock itself for decisions, reports and
-// eviction stamps (a tier driven by a wall-clock controller).
+// A wall-clock controller attaches (on) to or detaches (off) from the tier;
+// while at least one is attached the tier reads the steady clock itself for
+// decisions, reports and eviction stamps.
 void tier_use_steady_clock(ea_tier *t, bool on);
 // Count a controller attached to (+1) or detached from (-1) the tier; a tier
 // with controllers attached refuses ea_tier_destroy.

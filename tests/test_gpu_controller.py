@@ -187,3 +187,27 @@ def test_steady_clock_without_a_report_uses_the_estimate_alone():
     assert time.perf_counter() - t0 < 1.0
     tier.close()
     cache.close()
+
+
+def test_tier_keeps_the_steady_clock_until_the_last_controller_detaches():
+    # two wall-clock controllers on one tier: closing one leaves the other's
+    # steady clock in place (an allocation then stamps the tier with the
+    # steady clock); closing both returns the tier to the caller's clock
+    torch = need_gpu()
+    kv, cache, tier, slot = make_tier(torch, 8)
+    pol = api.make_policy(kappa=2, block_tokens=B, beta_rank=slot // B)
+    cfg = dict(report_interval=60_000_000, read_interval=30_000_000,
+               max_report_age=5_000_000, window=2_000_000)
+    a = api.Controller(tier, pol, **cfg)
+    b = api.Controller(tier, pol, **cfg)
+    a.close()
+    before = time.monotonic_ns() // 1000  # the steady clock, in microseconds
+    tier.alloc(key_of(1)[None, :])
+    assert tier.stats()["clock"] >= before
+    b.close()
+    clock = tier.stats()["clock"]
+    time.sleep(0.01)
+    tier.alloc(key_of(2)[None, :])
+    assert tier.stats()["clock"] == clock
+    tier.close()
+    cache.close()
