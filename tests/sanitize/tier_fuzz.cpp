@@ -6,13 +6,15 @@
 // admission of section 4, Eq. 6 and Eq. 10; ea_stack.cpp: the reuse-distance
 // capacity tool of section 3.2, Eq. 4) together with the oracle, drives both
 // with the same seeded random request streams, and stops at the first
-// difference.  No GPU is involved: the tier metadata needs no device memory.
+// difference.  The oracle's own hashing and copies run on random ragged
+// inputs too.  No GPU is involved: the tier metadata needs no device memory.
 //
 // Usage: tier_fuzz <seed> <requests>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 #include <random>
 #include <vector>
 
@@ -297,6 +299,77 @@ void fuzz_stack(uint64_t seed) {
   }
 }
 
+// The oracle's hashing and copies on random ragged inputs (memory safety
+// under the sanitizers, buffers sized exactly), with two invariants: keys
+// appear only for full blocks, and a store followed by a load into other
+// pages reproduces the source pages and scales byte for byte.
+void fuzz_oracle_bytes(uint64_t seed) {
+  Rng r(seed ^ 0xb17e5ull);
+  // hashing
+  const int32_t n_seqs = (int32_t)uniform(r, 0, 6);
+  const int32_t b = (int32_t)uniform(r, 1, 40);
+  std::vector<int64_t> off(1, 0);
+  for (int32_t q = 0; q < n_seqs; ++q) off.push_back(off.back() + uniform(r, 0, 130));
+  std::vector<int32_t> tok((size_t)off.back());
+  for (auto &x : tok) x = (int32_t)r();
+  int64_t total = 0;
+  for (int32_t q = 0; q < n_seqs; ++q) total += (off[q + 1] - off[q]) / b;
+  std::vector<uint8_t> parents(32 * (size_t)n_seqs), keys(32 * (size_t)total);
+  for (auto &x : parents) x = (uint8_t)r();
+  std::vector<int64_t> koff((size_t)n_seqs + 1);
+  CHECK(eao_hash_blocks(tok.empty() ? nullptr : tok.data(), off.data(), n_seqs, b,
+                        coin(r, 0.5) && n_seqs ? parents.data() : nullptr,
+                        keys.empty() ? nullptr : keys.data(), koff.data()) == 0,
+        "hash rc", -1);
+  for (int32_t q = 0; q < n_seqs; ++q)
+    CHECK(koff[q + 1] - koff[q] == (off[q + 1] - off[q]) / b, "key offsets", -1);
+
+  // store then load
+  eao_shape sh;
+  sh.num_pages = (int32_t)uniform(r, 4, 40);
+  sh.num_layers = (int32_t)uniform(r, 1, 3);
+  const int32_t ts[4] = {1, 2, 4, 16};
+  sh.page_tokens = ts[uniform(r, 0, 3)];
+  sh.num_kv_heads = (int32_t)uniform(r, 1, 2);
+  sh.head_dim = coin(r, 0.5) ? 8 : 16;
+  sh.elem_bytes = coin(r, 0.5) ? 1 : 2;
+  sh.has_scales = coin(r, 0.5) ? 1 : 0;
+  sh.chunk_pages = (int32_t)uniform(r, 1, 3);
+  const int64_t C = sh.chunk_pages, L = sh.num_layers, P = sh.num_pages;
+  const int64_t piece = eao_piece_bytes(&sh);
+  const int64_t S = uniform(r, 1, 6);
+  std::vector<uint8_t> cache((size_t)eao_cache_bytes(&sh)), tier((size_t)(S * eao_slot_bytes(&sh)));
+  std::vector<uint8_t> scales((size_t)eao_scale_bytes(&sh));
+  for (auto &x : cache) x = (uint8_t)r();
+  for (auto &x : scales) x = (uint8_t)r();
+  const int64_t n = std::min<int64_t>(S, P / (2 * C));
+  if (n < 1) return;
+  std::vector<int64_t> slots(S);
+  for (int64_t i = 0; i < S; ++i) slots[i] = i;
+  std::shuffle(slots.begin(), slots.end(), r);
+  slots.resize(n);
+  std::vector<int32_t> pages(P);
+  for (int64_t i = 0; i < P; ++i) pages[i] = (int32_t)i;
+  std::shuffle(pages.begin(), pages.end(), r);
+  std::vector<int32_t> src(pages.begin(), pages.begin() + n * C);
+  std::vector<int32_t> dst(pages.begin() + n * C, pages.begin() + 2 * n * C);
+  uint8_t *sc = sh.has_scales ? scales.data() : nullptr;
+  CHECK(eao_store_blocks(&sh, cache.data(), sc, tier.data(), S, src.data(), slots.data(),
+                         nullptr, (int32_t)n) == 0, "store rc", -1);
+  CHECK(eao_load_blocks(&sh, tier.data(), S, cache.data(), sc, slots.data(), dst.data(),
+                        (int32_t)n) == 0, "load rc", -1);
+  for (int64_t l = 0; l < L; ++l)
+    for (int64_t i = 0; i < n * C; ++i) {
+      CHECK(std::memcmp(&cache[(size_t)((l * P + dst[i]) * piece)],
+                        &cache[(size_t)((l * P + src[i]) * piece)], (size_t)piece) == 0,
+            "round trip", i);
+      if (sc)
+        CHECK(std::memcmp(&scales[(size_t)((l * P + dst[i]) * 8)],
+                          &scales[(size_t)((l * P + src[i]) * 8)], 8) == 0,
+              "round trip scales", i);
+    }
+}
+
 }  // namespace
 
 int main(int argc, char **argv) {
@@ -308,6 +381,7 @@ int main(int argc, char **argv) {
   const int64_t requests = std::strtoll(argv[2], nullptr, 10);
   fuzz_tier(seed, requests);
   fuzz_stack(seed);
+  fuzz_oracle_bytes(seed);
   std::printf("ok seed %llu requests %lld\n", (unsigned long long)seed, (long long)requests);
   return 0;
 }

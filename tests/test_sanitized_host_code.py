@@ -9,8 +9,10 @@ published report, refused calls, allocation with eviction and exhaustion,
 stores, pins held across requests, over-unpins, reports.  Every result and the
 full metadata image must agree.  One long stream (80,000 requests) takes the
 tier past the point where it starts dropping history no window can reach.
-Planted mistakes in a scratch copy of the tier (trimming one clock unit too
-much, a hit not promoted) are caught by these seeds.
+The oracle's hashing and copies also run on random ragged inputs (keys only
+for full blocks; store then load reproduces pages and scales).  Planted
+mistakes in a scratch copy of the tier (trimming one clock unit too much, a
+hit not promoted) are caught by these seeds.
 """
 import os
 import shutil
