@@ -16,7 +16,7 @@ Store and load run on two streams so the host link carries both directions.
 Every step hashes and stores a fresh refill (new tokens), so the tier fills
 and starts evicting after five steps, as a serving run would.
 
-Prints one JSON line; details go to stderr and gpurun_out/bench_detail.json.
+Prints one JSON line; details go to stderr and bench_out/bench_detail.json.
 
 Other modes:
   --isolated-only          set-up plus the isolated kernel measurements only
@@ -582,10 +582,10 @@ def summarize_profiles(d):
     counter passes.  Store and load are read from the launches of the timed
     steps (their place in launch order is in the run's detail file), gather
     and scatter from their isolated series."""
-    cmd_trace = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_trace "
-                 "-o trace -- python3 bench.py --detail gpurun_out/bench_detail_trace.json")
-    cmd_pmc = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{l} -o {l} -- python3 "
-               "bench.py --no-cpu-baseline --detail gpurun_out/bench_detail_{l}.json")
+    cmd_trace = ("rocprofv3 --kernel-trace --stats --output-format csv -d bench_out/prof_trace "
+                 "-o trace -- python3 bench.py --detail bench_out/bench_detail_trace.json")
+    cmd_pmc = ("rocprofv3 --pmc {c} --output-format csv -d bench_out/prof_{l} -o {l} -- python3 "
+               "bench.py --no-cpu-baseline --detail bench_out/bench_detail_{l}.json")
 
     def pick(k, vals, plan):
         """The launches of kernel k that belong to the timed steps (store,
@@ -619,7 +619,7 @@ def summarize_profiles(d):
     lines = ["# Kernel durations: piece copies, Qwen3-30B-A3B turn (2,000 stored / 1,500 loaded "
              "pages of 1.5 MiB)", "",
              "Command (from the repository root on the MI355X):", "", f"    {cmd_trace}",
-             "    python3 bench.py --summarize-profiles gpurun_out", "",
+             "    python3 bench.py --summarize-profiles bench_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
              "Store and load: the launches of the timed steps, where the two run together on "
              "two streams (launch order from the run's detail file).  Gather and scatter: their "
@@ -661,7 +661,7 @@ def summarize_profiles(d):
              "Commands (from the repository root on the MI355X):", "",
              "    " + cmd_pmc.format(c="FETCH_SIZE", l="fetch"),
              "    " + cmd_pmc.format(c="WRITE_SIZE", l="write"),
-             "    python3 bench.py --summarize-profiles gpurun_out", "",
+             "    python3 bench.py --summarize-profiles bench_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
              f"Calibration: a plain 1 GiB device copy (rocclr copyBuffer) reads FETCH_SIZE "
              f"{cal_f:.0f} KiB and WRITE_SIZE {cal_w:.0f} KiB for 1,048,576 KiB each way, so "
@@ -879,7 +879,7 @@ def main():
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
                              "load_cost", "tp8_shard", "hash", "agent_pool_chunked"])
     ap.add_argument("--turns-per-agent", type=int, default=24)
-    ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"))
+    ap.add_argument("--detail", default=os.path.join(ROOT, "bench_out", "bench_detail.json"))
     args = ap.parse_args()
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles)
