@@ -183,6 +183,9 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
   // each run of num_xcd consecutive workgroups holds `active` working ones
   const int64_t grid = (work + active - 1) / active * a.num_xcd;
   static const InlineIdx kEmpty{};
+  // report this launch's status only: drop any error an earlier runtime call
+  // left recorded on this thread (hipGetLastError returns and clears it)
+  (void)hipGetLastError();
   if (inl != nullptr) {
     if (dir == kToSlots) launch_dir<kToSlots, true>(a, *inl, route, grid, stream);
     else launch_dir<kToPages, true>(a, *inl, route, grid, stream);

@@ -242,6 +242,7 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens,
                                    uint32_t *d_mid, hipStream_t stream) {
   if (n_keys <= 0) return hipSuccess;
   const int64_t blocks = (n_keys + 255) / 256;
+  (void)hipGetLastError();  // report this launch's status only
   hipLaunchKernelGGL(sha256_midstates, dim3((unsigned)blocks), dim3(256), 0, stream,
                      d_tokens, d_key_offsets, d_tok_offsets, n_seqs, n_keys,
                      block_tokens, d_mid);
@@ -256,6 +257,7 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid,
   // message = 4b token bytes + 32 key bytes
   const uint32_t len_bits = (uint32_t)(8u * (4u * (uint32_t)block_tokens + 32u));
   const int blocks = (n_seqs + 31) / 32;
+  (void)hipGetLastError();  // report this launch's status only
   hipLaunchKernelGGL(sha256_chain, dim3(blocks), dim3(64), 0, stream, d_mid,
                      d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
   return hipGetLastError();

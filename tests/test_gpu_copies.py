@@ -213,3 +213,24 @@ def test_gather_scatter_through_device_buffer(n):
     oracle.load_blocks(p.oshape, want, p.o_cache, p.o_sc, np.arange(n), dst)
     p.assert_equal("scatter")
     p.close()
+
+
+def test_failed_tier_allocation_leaves_the_library_usable():
+    # an absurd capacity (2^62 bytes, beyond any address space) fails with
+    # EA_ENOMEM before anything is pinned; later launches still report their
+    # own status and move the right bytes
+    p = tiny_pair(seed=5)
+    from paper_2609_33762_amd import api
+    with pytest.raises(N.EAError) as e:
+        api.Tier(p.cache, 1 << 62)
+    assert e.value.code == N.EA_ENOMEM
+    r = W.rng(5)
+    src = W.distinct(r, W.TINY.num_pages, 40)
+    dst = W.distinct(r, W.TINY.num_pages, 40, exclude=src)
+    slots = W.distinct(r, p.tier.capacity, 40)
+    p.tier.store(p.cache, src, slots)
+    p.tier.load(p.cache, slots, dst)
+    p.o_store(src, slots)
+    p.o_load(slots, dst)
+    p.assert_equal("after a failed tier allocation")
+    p.close()
