@@ -4,6 +4,8 @@
   1,500 loaded), both transfer plans: round-trip identity on every page,
   sampled pages and slots against the oracle one by one, sampled untouched
   pages and slots.
+* The HBM gather and scatter of 2,000 pages in one launch each, as measured:
+  round trip on every page, sampled slots against the oracle.
 * Layer-pipelined fp8 prefix load (64k tokens = 4,096 pages, 48 layers,
   per-page scales): a consumer stream snapshots each layer right after its
   event; every snapshot and the end state match the source pages, sampled
@@ -104,6 +106,47 @@ def test_qwen3_turn_full_size(plan):
     tier.close()
     cache.close()
     del kv, kv3
+    release(torch)
+
+
+def test_hbm_gather_and_scatter_full_size():
+    # The measured HBM launches: one gather of 2,000 random pages of the
+    # 20,000-page Qwen3 cache into a slot-layout device buffer, one scatter of
+    # that buffer into 2,000 other pages (the default grids).  Every gathered
+    # slot is the oracle's store of its page (sampled one by one) and every
+    # scattered page equals its source page.
+    torch = need_gpu()
+    sh = W.QWEN3
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA + 3)
+    kv3 = kv.view(L, P, piece)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes)
+    r = W.rng(W.SEED_IDS + 3)
+    n = W.QWEN3_STORE_PAGES
+    src = W.distinct(r, P, n)
+    dst = W.distinct(r, P, n, exclude=src)
+    keep = W.distinct(r, P, 64, exclude=dst)
+    keep_before = drivers.read_pages(torch, kv3, keep).cpu().numpy()
+    slot = L * piece
+    staging = torch.empty(n * slot, dtype=torch.uint8, device="cuda")
+    cache.gather(src, staging)
+    cache.scatter(staging, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(kv3[:, torch.as_tensor(dst, device="cuda")],
+                       kv3[:, torch.as_tensor(src, device="cuda")])
+    sample = W.distinct(r, n, 48)
+    o = oshape_of(sh, num_pages=len(sample))
+    mini = drivers.read_pages(torch, kv3, src[sample]).cpu().numpy()
+    mini_cache = np.ascontiguousarray(mini.reshape(len(sample), L, piece).transpose(1, 0, 2))
+    want = np.zeros((len(sample), slot), np.uint8)
+    oracle.store_blocks(o, mini_cache.reshape(-1), None, want, np.arange(len(sample)),
+                        np.arange(len(sample)))
+    got = staging.view(n, slot)[torch.as_tensor(sample, device="cuda")].cpu().numpy()
+    assert np.array_equal(got, want)
+    assert np.array_equal(drivers.read_pages(torch, kv3, keep).cpu().numpy(), keep_before)
+    cache.close()
+    del kv, kv3, staging
     release(torch)
 
 
