@@ -835,7 +835,8 @@ VALU_INT_PEAK = 256 * 4 * 16 * 2.4e9
 
 def run_hash(args):
     """Chained keys (16-token blocks) on the device, tokens already in HBM:
-    the turn's 56k-token prompt (one 3,500-key chain), one 64k-token sequence, 64
+    the turn's 56k-token prompt (one 3,500-key chain, and in 1,024-token
+    chunks: 55 keys of 64 token blocks each), one 64k-token sequence, 64
     such sequences, 16,384 sequences of 1,024 tokens (the chain kernel then
     has 512 waves for the 1,024 SIMDs) and 65,536 of 256 tokens (2,048 waves:
     every SIMD has work); every run checked against the host entry point's
@@ -845,17 +846,19 @@ def run_hash(args):
     torch.cuda.set_device(0)
     cur = torch.cuda.current_stream()
     out = {}
-    for name, lengths in (("turn_56k_prompt", [56000]), ("one_64k", [65536]),
-                          ("pool_64x64k", [65536] * 64), ("batch_16384x1k", [1024] * 16384),
-                          ("batch_65536x256", [256] * 65536)):
+    for name, lengths, b in (("turn_56k_prompt", [56000], 16),
+                             ("turn_56k_prompt_1024_token_chunks", [56000], 1024),
+                             ("one_64k", [65536], 16), ("pool_64x64k", [65536] * 64, 16),
+                             ("batch_16384x1k", [1024] * 16384, 16),
+                             ("batch_65536x256", [256] * 65536, 16)):
         toks, offs = W.sequences(W.SEED_TOKENS, lengths)
         d_tok = torch.as_tensor(toks, device="cuda")
-        nk = int(sum(n // 16 for n in lengths))
+        nk = int(sum(n // b for n in lengths))
         d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
         # two untimed calls: asynchronous calls alternate between two buffer sets
-        ms = event_ms(torch, lambda: api.hash_blocks_device(d_tok, offs, 16, d_keys, stream=cur),
+        ms = event_ms(torch, lambda: api.hash_blocks_device(d_tok, offs, b, d_keys, stream=cur),
                       cur, 5, warm=2)
-        host, _ = api.hash_blocks(toks, offs, 16)
+        host, _ = api.hash_blocks(toks, offs, b)
         assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32))
         out[name] = {"ms": round(ms, 4), "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
                      "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1)}
