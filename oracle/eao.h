@@ -25,6 +25,18 @@
  *
  * Status codes mirror the product library: 0 ok, negative on error, and on
  * error nothing is written.
+ *
+ * What pins each part (tests/test_oracle_*.py, tests/test_stack_tool.py):
+ * SHA-256 by the FIPS 180-4 example values and by hashlib on every block's
+ * serialised message; the key chain by the invariants of section 3.2 (equal
+ * prefixes, rekeying after an edit, partial tails, continuation from a
+ * parent); copies by round trips, untouched bytes, fp8 NaN patterns and numpy
+ * restatements of the layout; the tier by a brute-force model, Lemma 1 and
+ * Proposition 1 on random streams, the Eq. 6 truth table with its endpoints
+ * and the paper's closed forms (footprints, working sets, K_H); the
+ * reference models by brute-force distinct counts and the round-robin closed
+ * form.  Parity unpinned: byte compatibility of the keys with LMCache or
+ * vLLM, which this definition does not claim.
  */
 #ifndef EAO_H
 #define EAO_H
