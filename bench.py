@@ -822,7 +822,7 @@ def run_tp8_shard(args):
                  {"tp8_shard": out, "beta_bytes_per_token": beta})
 
 
-# Lane-instructions per key of this build's hash kernels with 16-token
+# Lane-instructions per key of the library's hash kernels with 16-token
 # blocks, counted in their gfx950 assembly: one compression of the token
 # block (sha256_midstates) and one chained compression (sha256_chain, two
 # lanes per sequence: 1,163 instructions per lane pair).
@@ -894,7 +894,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
-              "no exchange between ranks, and only single-GPU runs are part of this build "
+              "no exchange between ranks, so a rank's throughput is measured alone "
               "(use --gpus 1)", file=sys.stderr)
         sys.exit(2)
     other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,

@@ -57,7 +57,7 @@ enum {
   EA_ENOSPC = -3,  /* reserved: no tier call fails for lack of space; a full
                       tier reports unallocated blocks instead                */
   EA_EHIP = -4,    /* a HIP call failed; see ea_last_hip_error()            */
-  EA_ENOTSUP = -5  /* valid request this build does not implement           */
+  EA_ENOTSUP = -5  /* valid request the library does not implement        */
 };
 
 const char *ea_strerror(int code);
