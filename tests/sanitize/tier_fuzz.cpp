@@ -86,7 +86,7 @@ void compare_state(ea::TierMeta &m, eao_tier *o, int64_t K, int64_t at) {
 void fuzz_tier(uint64_t seed, int64_t requests) {
   Rng r(seed);
   const int64_t slot_bytes = 2048;  // the oracle shape below: 2*16*1*32*2
-  const int64_t K = requests > 20000 ? uniform(r, 4, 12) : uniform(r, 3, 40);
+  const int64_t K = requests > 20000 ? uniform(r, 4, 12) : uniform(r, 1, 40);
   const int64_t cap = K * slot_bytes + uniform(r, 0, slot_bytes - 1);
   eao_shape sh{64, 1, 16, 1, 32, 2, 0, 1};
   CHECK(eao_slot_bytes(&sh) == slot_bytes, "oracle slot size", -1);

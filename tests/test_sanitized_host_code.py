@@ -60,7 +60,7 @@ def run(exe, seed, requests):
     assert "ERROR: AddressSanitizer" not in r.stderr and "runtime error" not in r.stderr, r.stderr
 
 
-@pytest.mark.parametrize("seed", range(1, 17))
+@pytest.mark.parametrize("seed", range(1, 25))
 def test_random_streams_match_the_oracle_under_sanitizers(fuzz_binary, seed):
     run(fuzz_binary, seed, 3000)
 
