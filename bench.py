@@ -42,6 +42,7 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_33762_amd", "csrc", "ea_copy_kernels.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_hbm_bytes.md")
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_kernel_trace.md")
+PLANS_SUMMARY = os.path.join(ROOT, "profiles", "transfer_plans_qwen3_turn.md")
 N_ISO = {"store": 5, "load": 5, "gather": 20, "scatter": 20}
 
 
@@ -770,6 +771,119 @@ def run_load_cost(args):
                  None, sum(len(x[3]) for x in setups), {"load_cost": res})
 
 
+def run_plans(args):
+    """The turn's store (2,000 pages) and load (1,500 pages) alone under one
+    transfer plan (--plan direct or staged), first to consecutive slots and
+    then to random ones.  Direct: one kernel between the cache and the mapped
+    pinned slots.  Staged: a paged gather or scatter through an HBM staging
+    buffer plus hipMemcpyAsync of each run of consecutive slots.  Each
+    operation is one untimed call and three timed ones between HIP events.
+    The cache is left unfilled (contents do not change the timing), so the
+    only copy kernels in the process are the plan's own: a rocprofv3 run of
+    this command attributes its kernels and byte counters to the plan."""
+    import torch
+    from paper_2609_33762_amd import api, _native as N, workloads as W
+    torch.cuda.set_device(0)
+    plan_name = "staged" if args.plan == "staged" else "direct"
+    plan = N.EA_PLAN_STAGED if plan_name == "staged" else N.EA_PLAN_DIRECT
+    sh = W.QWEN3
+    kv, cache = _quiet_cache(torch, api, sh)
+    r = W.rng(W.SEED_IDS)
+    n_s, n_l = W.QWEN3_STORE_PAGES, W.QWEN3_LOAD_PAGES
+    tier = api.Tier(cache, W.QWEN3_TIER_BYTES)
+    tier.set_plan(N.EA_DIR_BOTH, plan)
+    src = W.distinct(r, sh.num_pages, n_s)
+    dst = W.distinct(r, sh.num_pages, n_l, exclude=src)
+    page = tier.info["page_bytes"]
+    cur = torch.cuda.current_stream()
+    out, reps, link = {}, 3, 0
+    for slots_name, slots in (("consecutive", np.arange(n_s, dtype=np.int64)),
+                              ("random", W.distinct(r, tier.capacity, n_s))):
+        st = event_ms(torch, lambda: tier.store(cache, src, slots, stream=cur), cur, reps)
+        ld = event_ms(torch, lambda: tier.load(cache, slots[:n_l], dst, stream=cur), cur, reps)
+        out[slots_name] = {"store_ms": round(st, 4), "store_gbs": round(n_s * page / st / 1e6, 2),
+                           "load_ms": round(ld, 4), "load_gbs": round(n_l * page / ld / 1e6, 2)}
+        link += (1 + reps) * (n_s + n_l) * page
+        log(f"plan {plan_name}, {slots_name} slots: {out[slots_name]}")
+    torch.cuda.synchronize()
+    tier.close()
+    cache.close()
+    del kv
+    torch.cuda.empty_cache()
+    return _line(f"plans: the Qwen3 turn's store and load alone, {plan_name} plan, consecutive and "
+                 "random slots", out["random"]["store_gbs"], "GB/s", None, reps,
+                 {"plan": plan_name, "plans": out, "link_bytes_all_calls": link})
+
+
+def summarize_plans(d):
+    """profiles/transfer_plans_qwen3_turn.md from three rocprofv3 runs (kernel
+    trace, FETCH_SIZE, WRITE_SIZE) of each plan's `--workload plans` command,
+    under d/plans_<plan>/, beside the runs' own JSON lines."""
+    import re
+    m = re.search(r"FETCH_SIZE is scaled by ([0-9.]+) and WRITE_SIZE by ([0-9]+\.[0-9]+)",
+                  open(TRAFFIC_SUMMARY).read())
+    cal_f, cal_w = float(m.group(1)), float(m.group(2))
+    lines = ["# Transfer plans: direct kernels against HBM staging plus hipMemcpyAsync, "
+             "Qwen3-30B-A3B turn", "",
+             "Commands (from the repository root on the MI355X), for P in direct and staged:", "",
+             "    rocprofv3 --kernel-trace --memory-copy-trace --stats --output-format csv "
+             "-d bench_out/plans_P/trace -o trace -- python3 bench.py --workload plans --plan P",
+             "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d bench_out/plans_P/fetch -o fetch "
+             "-- python3 bench.py --workload plans --plan P",
+             "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d bench_out/plans_P/write -o write "
+             "-- python3 bench.py --workload plans --plan P",
+             "    python3 bench.py --summarize-plans bench_out", "",
+             f"kernel_source_sha256: {kernel_source_hash()}", "",
+             "Each process runs one plan: the turn's 2,000-page store and 1,500-page load alone, "
+             "to consecutive slots and then to random ones, one untimed and three timed calls "
+             "each.  Every copy kernel in a process belongs to its plan.  Byte counters are "
+             f"scaled as in the piece-copy summary (FETCH_SIZE x{cal_f:.3f}, WRITE_SIZE "
+             f"x{cal_w:.3f}) and include the host-memory side.", ""]
+    for plan in ("direct", "staged"):
+        base = os.path.join(d, f"plans_{plan}")
+        res = json.load(open(os.path.join(base, "line.json")))
+        lines += [f"## {plan}", "", "| slots | store GB/s (HIP events) | load GB/s (HIP events) |",
+                  "|---|---|---|"]
+        for k, v in res["plans"].items():
+            lines.append(f"| {k} | {v['store_gbs']} | {v['load_gbs']} |")
+        lines += ["", "| kernel | calls | total ms | avg ms |", "|---|---|---|---|"]
+        for x in csv.DictReader(open(os.path.join(base, "trace", "trace_kernel_stats.csv"))):
+            name = x["Name"]
+            if "copy_host_link" in name or "copy_hbm" in name or "__amd_rocclr" in name:
+                short = name.replace("void ", "").replace("ea::(anonymous namespace)::", "")
+                short = short.split("(")[0]
+                lines.append(f"| `{short}` | {x['Calls']} | {int(x['TotalDurationNs']) / 1e6:.2f} | "
+                             f"{float(x['AverageNs']) / 1e6:.4f} |")
+        mc = os.path.join(base, "trace", "trace_memory_copy_trace.csv")
+        copies = list(csv.DictReader(open(mc))) if os.path.exists(mc) else []
+        if copies:
+            dur = sum(int(x["End_Timestamp"]) - int(x["Start_Timestamp"]) for x in copies) / 1e6
+            lines += ["", f"Copies the runtime ran on its copy engines (not kernels, so absent "
+                      f"from the kernel table and the byte counters): {len(copies)} copies, "
+                      f"{dur:.2f} ms in total."]
+        elif plan == "staged":
+            lines += ["", "No copy ran on the copy engines: every hipMemcpyAsync was a blit "
+                      "kernel."]
+        tot = {}
+        for label, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+            s = 0.0
+            for x in csv.DictReader(open(os.path.join(base, label, f"{label}_counter_collection.csv"))):
+                n = x["Kernel_Name"]
+                if x["Counter_Name"] == ctr and ("copy_host_link" in n or "copy_hbm" in n or
+                                                  "__amd_rocclr" in n):
+                    s += float(x["Counter_Value"])
+            tot[ctr] = s
+        traffic = (tot["FETCH_SIZE"] * cal_f + tot["WRITE_SIZE"] * cal_w) * 1024
+        link = res["link_bytes_all_calls"]
+        lines += ["", f"Memory traffic of the plan's kernels over all calls: {traffic / 1e9:.2f} GB "
+                  f"for {link / 1e9:.2f} GB across the host link, {traffic / link:.2f} bytes per "
+                  "link byte (each byte read once and written once is 2.00"
+                  + (", and copies on the copy engines add traffic the counters do not see"
+                     if copies else "") + ").", ""]
+    open(PLANS_SUMMARY, "w").write("\n".join(lines) + "\n")
+    print(open(PLANS_SUMMARY).read())
+
+
 def run_tp8_shard(args):
     """One Qwen3 turn on a TP8 rank's share (1 KV head, 24 KiB/token):
     a 2,000-page refill stored and a 1,500-page prefix loaded, alone and
@@ -883,14 +997,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--isolated-only", action="store_true")
     ap.add_argument("--summarize-profiles", metavar="DIR")
+    ap.add_argument("--summarize-plans", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
-                             "load_cost", "tp8_shard", "hash", "agent_pool_chunked"])
+                             "load_cost", "tp8_shard", "hash", "agent_pool_chunked", "plans"])
     ap.add_argument("--turns-per-agent", type=int, default=24)
     ap.add_argument("--detail", default=os.path.join(ROOT, "bench_out", "bench_detail.json"))
     args = ap.parse_args()
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles)
+        return
+    if args.summarize_plans:
+        summarize_plans(args.summarize_plans)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
@@ -900,7 +1018,7 @@ def main():
     other = {"agent_pool": run_agent_pool, "dense_scattered": run_dense_scattered,
              "layered_fp8": run_layered, "tiny": run_tiny, "load_cost": run_load_cost,
              "tp8_shard": run_tp8_shard, "hash": run_hash,
-             "agent_pool_chunked": run_agent_pool_chunked}
+             "agent_pool_chunked": run_agent_pool_chunked, "plans": run_plans}
     if args.workload in other:
         out = other[args.workload](args)
         log(json.dumps(out))
