@@ -2,13 +2,14 @@
 
 Workload (48 layers, 4 KV heads, head_dim 128, bf16 = 96 KiB per token,
 16-token pages of 1.5 MiB, 20,000-page GPU cache = 29.3 GiB, 16 GiB pinned
-host tier = 10,922 slots).  One step is one pass of the whole path for one
-turn:
-  hash     chained keys of the turn's 24k-token cached prefix and of its new
-           32k-token refill (one call, two sequences);
-  lookup   consecutive-prefix lookup of the prefix keys (1,500 hits);
+host tier = 10,922 slots).  The turn's prompt is a cached 24k-token prefix
+followed by a fresh 32k-token refill.  One step is one pass of the whole path
+for one turn:
+  hash     chained keys of the whole 56k-token prompt (one chain: the
+           refill's keys depend on the prefix);
+  lookup   consecutive-prefix lookup (1,500 hits, up to the refill);
   load     the 1,500 prefix pages from the host tier into free GPU pages;
-  admit    write admission and deduplication of the refill's 2,000 keys;
+  admit    write admission for the request and deduplication of its keys;
   alloc    2,000 host slots (lowest free, LRU eviction once the tier is full);
   store    the 2,000 refill pages from HBM into the host tier;
   unpin    release the lookup and allocation pins.
@@ -19,10 +20,13 @@ and starts evicting after five steps, as a serving run would.
 Prints one JSON line; details go to stderr and bench_out/bench_detail.json.
 
 Other modes:
+  --workload W             the other workloads (agent pool, dense scattered
+                           calls, layered fp8 load, tiny, hash, restore-cost
+                           fit, TP8 shard, chunked pool, transfer plans)
   --isolated-only          set-up plus the isolated kernel measurements only
-                           (what the rocprofv3 runs profile)
-  --summarize-profiles D   turn rocprofv3 CSVs under D into the summaries in
-                           profiles/
+  --summarize-profiles D   turn the rocprofv3 CSVs of the default command
+                           under D into the summaries in profiles/
+  --summarize-plans D      the same for the two transfer plans
 """
 import argparse
 import csv
