@@ -23,7 +23,13 @@
  *  - Copies are asynchronous on the caller's HIP stream and ordered with the
  *    caller's other work on that stream.  A store or load that touches a host
  *    slot that an earlier call on another stream still transfers waits for
- *    that transfer on the device (no host blocking).
+ *    that transfer on the device (no host blocking).  A store and a load
+ *    share the host link in both directions at once only when their streams
+ *    run on different hardware queues: the HIP runtime places each stream on
+ *    one of GPU_MAX_HW_QUEUES queues, and two streams on one queue run one
+ *    after the other.  Create the copy streams after the process has first
+ *    used the default stream, and keep the streams in use within the
+ *    hardware queues.
  *  - GPU cache layout (caller-owned device memory): element array
  *    [L][P][2][T][H][D] of elem_bytes each, so the K and V data of one
  *    (layer, page) form one contiguous "piece" of 2*T*H*D*elem_bytes bytes.
