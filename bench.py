@@ -58,6 +58,23 @@ def kernel_source_hash():
     return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
 
 
+_STREAMS = []
+
+
+def copy_streams(torch):
+    """The process's two copy streams (stores, loads), created once and after
+    the process has first used the default stream.  The runtime places each
+    stream on one of a few hardware queues; streams created before the
+    default stream's first use lose part of their overlap once it is used,
+    and streams created beyond the hardware queues share them (measured: the
+    turn's duplex falls from 87 to 68-77 and 56 GB/s)."""
+    if not _STREAMS:
+        torch.zeros(1, device="cuda")  # a kernel on the default stream
+        torch.cuda.synchronize()
+        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+    return _STREAMS[0], _STREAMS[1]
+
+
 def event_ms(torch, fn, stream, reps, warm=1):
     """Average duration of one fn() call: `reps` back-to-back calls between
     one pair of HIP events on `stream`, after `warm` untimed calls (events
@@ -210,7 +227,7 @@ def run_steps(ctx, args):
     # the prefix), computed at the request's first lookup
     seqs = [np.concatenate([ctx["prefix"], refills[k]]) for k in range(total)]
     offs = np.array([0, (n_load + n_store) * b], np.int64)
-    s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
+    s_store, s_load = copy_streams(torch)
     ev = {k: [] for k in ("s0", "s1", "l0", "l1")}
 
     def step(k, timed):
@@ -346,8 +363,9 @@ def run_agent_pool(args):
                           activity_window=W.POOL_AGENTS)
     # loads and stores on their own streams: a turn's store overlaps the next
     # turn's load on the host link
+    s_store, s_load = copy_streams(torch)
     pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, verify=False, time_fill=True,
-                             load_stream=torch.cuda.Stream(), store_stream=torch.cuda.Stream())
+                             load_stream=s_load, store_stream=s_store)
     turns = args.turns_per_agent * W.POOL_AGENTS
     hits = declined = stored = 0
     gamma = []
@@ -410,9 +428,9 @@ def run_agent_pool_chunked(args):
         tier = api.Tier(cache, gib << 30, chunk_pages=C)
         pol = api.make_policy(kappa=8, block_tokens=C * sh.page_tokens, beta_rank=beta,
                               activity_window=agents, mode=mode)
+        s_store, s_load = copy_streams(torch)
         pool = drivers.AgentPool(torch, cache, tier, kv, sh, pol, agents=agents, verify=False,
-                                 time_fill=True, load_stream=torch.cuda.Stream(),
-                                 store_stream=torch.cuda.Stream())
+                                 time_fill=True, load_stream=s_load, store_stream=s_store)
         records = []
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -512,7 +530,7 @@ def run_layered(args):
     src = W.distinct(r, P, n)
     dst = np.setdiff1d(np.arange(P), src)
     tier.store(cache, src, np.arange(n))
-    copy_s = torch.cuda.Stream()
+    _, copy_s = copy_streams(torch)
     res = []
     for rep in range(args.steps + 1):
         start = torch.cuda.Event(enable_timing=True)
@@ -914,7 +932,7 @@ def run_tp8_shard(args):
         cur = torch.cuda.current_stream()
         st_ms = event_ms(torch, lambda: tier.store(cache, refill, sslots, stream=cur), cur, 5)
         ld_ms = event_ms(torch, lambda: tier.load(cache, pslots, dst, stream=cur), cur, 5)
-        s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
+        s_store, s_load = copy_streams(torch)
         both = []
         for _ in range(5):
             torch.cuda.synchronize()
