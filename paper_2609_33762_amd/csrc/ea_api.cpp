@@ -81,30 +81,45 @@ int64_t grid_hbm(int dir) {
 // pinned-copy peak one way.  With a store and a load in flight together,
 // more waves lower the sum (posted writes and read requests queue behind one
 // another), and keeping the two directions on different XCDs raised the
-// duplex sum from 63 to 83-88 GB/s in measurements on MI355X.  The store runs
-// on XCD 0 and the load on XCD 1 by default.  EA_LINK_WG sets both
-// directions, EA_LINK_WG_STORE / EA_LINK_WG_LOAD one each (the share of the
-// link each direction gets while both run follows its wave count).
+// duplex sum from 63 to 87 GB/s in measurements on MI355X; spreading each
+// direction's 8 workgroups over two XCDs (four on each) raised it to 89 and
+// the store alone from 55.3 to 56.0 GB/s, while four XCDs (two on each)
+// lowered both.  The store runs on XCDs 0 and 2 and the load on 1 and 3 by
+// default (EA_XCD_STORE / EA_XCD_LOAD override the masks).  EA_LINK_WG sets
+// both directions' workgroups, EA_LINK_WG_STORE / EA_LINK_WG_LOAD one each.
 int64_t grid_link(int dir) {
   const int both = std::max(1, env_int("EA_LINK_WG", 8));
   return std::max(1, env_int(dir == ea::kToSlots ? "EA_LINK_WG_STORE" : "EA_LINK_WG_LOAD", both));
 }
 
-// XCDs of the device (workgroups are dispatched round-robin over them).
-int device_xcds(int dev) {
+// XCDs of the device (workgroups are dispatched round-robin over them) and
+// whether kernels may place work by the XCD the hardware reports: a probe
+// at the device's first use checks that dispatches go round-robin over the
+// reported XCDs.  EA_XCD_PLACEMENT=index keeps the index-based placement.
+struct XcdInfo {
+  int num = 0;
+  bool hw = false;
+};
+
+XcdInfo device_xcds(int dev) {
   static std::mutex mu;
-  static int known[64] = {0};
+  static XcdInfo known[64];
   std::lock_guard<std::mutex> lk(mu);
-  if (dev < 0 || dev >= 64) return 1;
-  if (known[dev] == 0) {
+  if (dev < 0 || dev >= 64) return XcdInfo{1, false};
+  if (known[dev].num == 0) {
     int v = 0, cus = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess) v = 1;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       cus = 0;
     // a value that cannot be right (or a runtime without the attribute)
     // falls back to one XCD: no placement, every workgroup works
-    if (v < 1 || v > 32 || cus <= 0 || cus % v != 0) v = 1;
-    known[dev] = v;
+    if (v < 1 || v > 16 || cus <= 0 || cus % v != 0) v = 1;
+    bool hw = false;
+    const char *pl = std::getenv("EA_XCD_PLACEMENT");
+    if (v > 1 && !(pl && std::strcmp(pl, "index") == 0)) {
+      if (ea::probe_xcd_round_robin(v, &hw) != hipSuccess) hw = false;
+    }
+    known[dev] = XcdInfo{v, hw};
   }
   return known[dev];
 }
@@ -225,6 +240,7 @@ struct ea_cache {
   int device;
   int64_t piece, page, trailer, slot;
   int32_t num_xcd;
+  int32_t hw_xcd;
   std::mutex mu;  // guards the gather/scatter index ring
   IndexRing ring;
 };
@@ -380,6 +396,7 @@ ea::PieceCopy base_copy(const ea_cache *c, int64_t slot_bytes, int32_t chunk) {
   a.layer_count = c->d.num_layers;
   a.num_xcd = c->num_xcd;
   a.xcd_mask = all_xcds(c->num_xcd);
+  a.hw_xcd = c->hw_xcd;
   return a;
 }
 
@@ -534,7 +551,9 @@ int ea_cache_create(const ea_cache_desc *desc, ea_cache **out) {
   if (!c) return EA_ENOMEM;
   c->d = *desc;
   c->device = dev;
-  c->num_xcd = device_xcds(dev);
+  const XcdInfo xi = device_xcds(dev);
+  c->num_xcd = xi.num;
+  c->hw_xcd = xi.hw ? 1 : 0;
   c->piece = 2LL * desc->page_tokens * desc->num_kv_heads * desc->head_dim * desc->elem_bytes;
   c->page = c->piece * desc->num_layers;
   c->trailer = desc->scale_base ? ((int64_t)desc->num_layers * 8 + 255) / 256 * 256 : 0;
@@ -587,9 +606,11 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
     t->grid_store = grid_link(ea::kToSlots);
     t->grid_load = grid_link(ea::kToPages);
     t->num_xcd = shape->num_xcd;
-    // two different XCDs for the two directions when the device has them
-    t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", 0x1u, t->num_xcd);
-    t->xcd_load = xcd_mask_from_env("EA_XCD_LOAD", t->num_xcd > 1 ? 0x2u : 0x1u, t->num_xcd);
+    // the two directions on different XCDs: two each (store 0 and 2, load 1
+    // and 3) when the device has at least four, one each when it has two
+    const int nx = t->num_xcd;
+    t->xcd_store = xcd_mask_from_env("EA_XCD_STORE", nx >= 4 ? 0x5u : 0x1u, nx);
+    t->xcd_load = xcd_mask_from_env("EA_XCD_LOAD", nx >= 4 ? 0xAu : (nx > 1 ? 0x2u : 0x1u), nx);
     t->grid_gather = grid_hbm(ea::kToSlots);
     t->grid_scatter = grid_hbm(ea::kToPages);
     // a layered load is one short kernel per layer: 16 workgroups hide the

@@ -31,6 +31,15 @@ constexpr int kWave = 64;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// s_getreg operand for HW_REG_XCC_ID (hardware register 20), bits [3:0]:
+// the XCD the wave runs on.
+constexpr int kXccIdReg = (3 << 11) | (0 << 6) | 20;
+
+__device__ __forceinline__ int this_xcd(const PieceCopy &a) {
+  if (a.hw_xcd) return (int)((__builtin_amdgcn_s_getreg(kXccIdReg) & 0xFu) % (unsigned)a.num_xcd);
+  return (int)(blockIdx.x % (unsigned)a.num_xcd);
+}
+
 __device__ __forceinline__ u32x4 load_nt(const u32x4 *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void store_nt(u32x4 *p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
@@ -83,7 +92,7 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
                                            const InlineIdx &inl) {
   const int64_t units = a.n * a.layer_count;
   const int lane = threadIdx.x & (kWave - 1);
-  const int xcd = (int)(blockIdx.x % (unsigned)a.num_xcd);
+  const int xcd = this_xcd(a);
   if (!((a.xcd_mask >> xcd) & 1u)) return;
   const int active = __popc(a.xcd_mask);
   const int64_t group = (int64_t)(blockIdx.x / (unsigned)a.num_xcd) * active +
@@ -143,6 +152,11 @@ __global__ __launch_bounds__(kThreads) void copy_hbm(PieceCopy a, const int32_t 
   piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, inl);
 }
 
+// One workgroup of one wave per entry: out[b] = the XCD of workgroup b.
+__global__ __launch_bounds__(64) void xcd_probe(int32_t *__restrict__ out) {
+  if (threadIdx.x == 0) out[blockIdx.x] = (int32_t)(__builtin_amdgcn_s_getreg(kXccIdReg) & 0xFu);
+}
+
 template <int DIR, bool INLINE, int VEC>
 void launch_route(const PieceCopy &a, const InlineIdx &inl, int route, dim3 g, hipStream_t stream) {
   if (route == kRouteHostLink)
@@ -166,6 +180,44 @@ void launch_dir(const PieceCopy &a, const InlineIdx &inl, int route, int64_t gri
 }
 
 }  // namespace
+
+hipError_t probe_xcd_round_robin(int num_xcd, bool *ok) {
+  *ok = false;
+  if (num_xcd < 1 || num_xcd > 16) return hipSuccess;
+  const int most = 8 * num_xcd;
+  // a private stream: the probe stays off the legacy default stream
+  hipStream_t s = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  if (e != hipSuccess) return e;
+  int32_t *d = nullptr;
+  if ((e = hipMalloc((void **)&d, (size_t)most * sizeof(int32_t))) != hipSuccess) {
+    (void)hipStreamDestroy(s);
+    return e;
+  }
+  int32_t h[128];
+  bool good = true;
+  // several dispatch sizes, each twice: the offset may change between
+  // dispatches, the round-robin order within one must not
+  for (int rep = 0; rep < 2 && good && e == hipSuccess; ++rep) {
+    for (int grid : {num_xcd, 3 * num_xcd, 8 * num_xcd}) {
+      (void)hipGetLastError();
+      hipLaunchKernelGGL(xcd_probe, dim3((unsigned)grid), dim3(64), 0, s, d);
+      if ((e = hipGetLastError()) != hipSuccess) break;
+      if ((e = hipMemcpyAsync(h, d, (size_t)grid * sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
+          hipSuccess)
+        break;
+      if ((e = hipStreamSynchronize(s)) != hipSuccess) break;
+      for (int b = 0; b < grid && good; ++b)
+        good = h[b] >= 0 && h[b] % num_xcd == (h[0] % num_xcd + b) % num_xcd;
+      if (!good) break;
+    }
+  }
+  (void)hipStreamSynchronize(s);
+  (void)hipFree(d);
+  (void)hipStreamDestroy(s);
+  if (e == hipSuccess) *ok = good;
+  return e;
+}
 
 hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
                              int64_t workgroups, hipStream_t stream) {

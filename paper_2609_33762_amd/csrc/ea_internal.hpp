@@ -34,10 +34,15 @@ struct PieceCopy {
   int32_t layer_begin;
   int32_t layer_count;
   int32_t identity_slots;    // slot of entry i is i / C (staging buffers)
-  // Workgroups are dispatched round-robin over the XCDs (workgroup b runs on
-  // XCD b % num_xcd); only workgroups on XCDs in xcd_mask do work.
+  // Only workgroups on XCDs in xcd_mask do work.  Workgroups of a dispatch
+  // go round-robin over the XCDs starting at an offset the hardware chooses
+  // (workgroup b runs on XCD (b + offset) % num_xcd), so the workgroup's
+  // rank on its XCD is b / num_xcd.  hw_xcd = 1: the XCD is read from the
+  // hardware (HW_REG_XCC_ID); 0: it is taken as b % num_xcd, which places
+  // the work by luck of the offset but covers every unit all the same.
   int32_t num_xcd;
   uint32_t xcd_mask;
+  int32_t hw_xcd;
 };
 
 struct InlineIdx {
@@ -62,6 +67,12 @@ void tier_attach_controller(ea_tier *t, int delta);
 
 // Which memory the slot-layout buffer of a piece copy lives in.
 enum Route : int { kRouteHostLink = 0, kRouteHbm = 1 };
+
+// Check, with a probe kernel on the current device, that the workgroups of
+// a dispatch go round-robin over num_xcd XCDs as the hardware reports them
+// (the property the hardware-placed piece copies rely on).  *ok = false
+// when any probe dispatch breaks it.
+hipError_t probe_xcd_round_robin(int num_xcd, bool *ok);
 
 // Launch one piece-copy kernel with at most `workgroups` (> 0) working
 // workgroups, placed on the XCDs of a.xcd_mask.
