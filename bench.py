@@ -858,7 +858,8 @@ def summarize_plans(d):
              f"kernel_source_sha256: {kernel_source_hash()}", "",
              "Each process runs one plan: the turn's 2,000-page store and 1,500-page load alone, "
              "to consecutive slots and then to random ones, one untimed and three timed calls "
-             "each.  Every copy kernel in a process belongs to its plan.  Byte counters are "
+             "each.  Every copy kernel in a process belongs to its plan, apart from the few "
+             "bytes the library's one-time XCD probe copies back.  Byte counters are "
              f"scaled as in the piece-copy summary (FETCH_SIZE x{cal_f:.3f}, WRITE_SIZE "
              f"x{cal_w:.3f}) and include the host-memory side.", ""]
     for plan in ("direct", "staged"):
