@@ -234,3 +234,27 @@ def test_failed_tier_allocation_leaves_the_library_usable():
     p.o_load(slots, dst)
     p.assert_equal("after a failed tier allocation")
     p.close()
+
+
+@pytest.mark.parametrize("masks", [(0x1, 0x2), (0x80, 0x40), (0x3, 0xC), (0xFF, 0xFF),
+                                   (0x11, 0x22), (0x7F, 0x1)])
+def test_any_xcd_masks_copy_every_piece(masks):
+    # Work goes only to workgroups on the XCDs of the store and load masks;
+    # whatever the masks, every piece is copied exactly once.
+    os.environ["EA_XCD_STORE"], os.environ["EA_XCD_LOAD"] = hex(masks[0]), hex(masks[1])
+    try:
+        p = tiny_pair(seed=40 + masks[0], slots=256)
+    finally:
+        os.environ.pop("EA_XCD_STORE")
+        os.environ.pop("EA_XCD_LOAD")
+    r = W.rng(masks[0] * 7 + masks[1])
+    for n in (5, 120):  # kernel arguments, then the index ring
+        src = W.distinct(r, W.TINY.num_pages, n)
+        dst = W.distinct(r, W.TINY.num_pages, n, exclude=src)
+        slots = W.distinct(r, p.tier.capacity, n)
+        p.tier.store(p.cache, src, slots)
+        p.tier.load(p.cache, slots, dst)
+        p.o_store(src, slots)
+        p.o_load(slots, dst)
+        p.assert_equal(f"masks {masks} n={n}")
+    p.close()
