@@ -162,7 +162,11 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  * seq_offsets (HOST int64[n_seqs+1]), d_parents (device uint8[n_seqs][32] or
  * NULL), d_keys_out (device uint8[...][32]) and key_offsets_out (HOST
  * int64[n_seqs+1], filled before return).  Asynchronous: the keys are valid
- * once the work enqueued on `stream` completes. */
+ * once the work enqueued on `stream` completes.
+ *
+ * Both entry points run the chained compression two lanes per sequence, or
+ * one lane per sequence when there are more than 32 sequences per SIMD of
+ * the device (the keys are the same); EA_HASH_LANES=1 or 2 forces a form. */
 int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,
                           int32_t n_seqs, int32_t block_tokens,
                           const uint8_t *d_parents, uint8_t *d_keys_out,

@@ -270,7 +270,7 @@ def hash_blocks_device(d_tokens, seq_offsets, block_tokens, d_keys_out, d_parent
     """Asynchronous variant on device tensors; returns key_offsets."""
     offs = _i64(seq_offsets)
     n_seqs = len(offs) - 1
-    koffs = np.zeros(n_seqs + 1, np.int64)
+    koffs = np.empty(n_seqs + 1, np.int64)
     N.check("ea_hash_blocks_device", N.load().ea_hash_blocks_device(
         d_tokens.data_ptr(), _ptr(offs), n_seqs, block_tokens,
         None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),

@@ -94,16 +94,33 @@ int prepare(HashWs &w) {
   return EA_OK;
 }
 
+// floor(len / b), the full blocks of a sequence: a shift when b is a power
+// of two (16-token pages, 1,024-token chunks), else a division.
+struct BlockCount {
+  int64_t b;
+  int shift = -1;
+  explicit BlockCount(int64_t block) : b(block) {
+    if ((b & (b - 1)) == 0) shift = __builtin_ctzll((unsigned long long)b);
+  }
+  int64_t operator()(int64_t len) const { return shift >= 0 ? len >> shift : len / b; }
+};
+
+// Checks the arguments and fills key_offsets_out (running sums of full
+// blocks) in one pass over the sequences.
 int validate(const int64_t *seq_offsets, int32_t n_seqs, int32_t block_tokens,
              int64_t *key_offsets_out, int64_t *total_keys) {
   if (n_seqs < 0 || !key_offsets_out) return EA_EINVAL;
   if (n_seqs > 0 && !seq_offsets) return EA_EINVAL;
   if (block_tokens < 1 || block_tokens > (1 << 20)) return EA_EINVAL;
   if (block_tokens % 16 != 0) return EA_ENOTSUP;
+  const BlockCount blocks(block_tokens);
   int64_t k = 0;
+  key_offsets_out[0] = 0;
   for (int32_t s = 0; s < n_seqs; ++s) {
-    if (seq_offsets[s] < 0 || seq_offsets[s + 1] < seq_offsets[s]) return EA_EINVAL;
-    k += (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
+    const int64_t a = seq_offsets[s], e = seq_offsets[s + 1];
+    if (a < 0 || e < a) return EA_EINVAL;
+    k += blocks(e - a);
+    key_offsets_out[s + 1] = k;
   }
   *total_keys = k;
   return EA_OK;
@@ -130,10 +147,6 @@ extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
   int rc = validate(seq_offsets, n_seqs, block_tokens, key_offsets_out, &total);
   if (rc != EA_OK) return rc;
   if (total > 0 && (!tokens || !keys_out)) return EA_EINVAL;
-  key_offsets_out[0] = 0;
-  for (int32_t s = 0; s < n_seqs; ++s)
-    key_offsets_out[s + 1] =
-        key_offsets_out[s] + (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
   if (total == 0) return EA_OK;
 
   std::lock_guard<std::mutex> lk(g_ws_mu);
@@ -187,10 +200,6 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq
   if (rc != EA_OK) return rc;
   if (total > 0 && (!d_tokens || !d_keys_out)) return EA_EINVAL;
   if (d_keys_out && ((uintptr_t)d_keys_out & 15) != 0) return EA_EINVAL;
-  key_offsets_out[0] = 0;
-  for (int32_t s = 0; s < n_seqs; ++s)
-    key_offsets_out[s + 1] =
-        key_offsets_out[s] + (seq_offsets[s + 1] - seq_offsets[s]) / block_tokens;
   if (total == 0) return EA_OK;
 
   std::lock_guard<std::mutex> lk(g_ws_mu);
@@ -207,8 +216,8 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq
   if ((rc = ensure_mid(&d.d_mid, &d.cap_mid, total)) != EA_OK) return rc;
   int64_t *koff = reinterpret_cast<int64_t *>(d.h_meta);
   int64_t *toff = koff + n_seqs + 1;
-  for (int32_t s = 0; s <= n_seqs; ++s) koff[s] = key_offsets_out[s];
-  for (int32_t s = 0; s < n_seqs; ++s) toff[s] = seq_offsets[s];
+  std::memcpy(koff, key_offsets_out, (size_t)(n_seqs + 1) * 8);
+  std::memcpy(toff, seq_offsets, (size_t)n_seqs * 8);
   HS_HIP(hipMemcpyAsync(d.d_meta, d.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
   const int64_t *d_koff = reinterpret_cast<const int64_t *>(d.d_meta);
   HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_koff + n_seqs + 1, n_seqs, total,

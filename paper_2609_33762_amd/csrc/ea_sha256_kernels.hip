@@ -9,15 +9,26 @@
 //                     from the initial hash value (fully parallel);
 //   sha256_chain:     two lanes per sequence, run the final compression of
 //                     each key in order, feeding key_{i-1} in as message
-//                     words 0..7 (the serial part: one compression per key).
+//                     words 0..7 (the serial part: one compression per key);
+//   sha256_chain_lane: the same with one lane per sequence, for batches of
+//                     sequences large enough to give every SIMD more than
+//                     one wave of the two-lane form.
 // A lone chain runs at the issue rate of one wave, so the instructions per
 // compression set its speed: rotations are v_alignbit_b32, every
 // three-input XOR and Ch/Maj one v_bitop3_b32 (gfx950's three-input logic
 // op), sums v_add3_u32; everything stays in VGPRs (no LDS, no scratch).
 // Splitting the working state and the message schedule over two lanes
-// (below) brings a chained compression to 1,163 instructions from 1,374 in
+// (below) brings a chained compression to 1,162 instructions from 1,378 in
 // one lane, and gives twice as many waves for a given number of sequences.
+// The split costs lane-instructions (2 x 1,162 per key against 1,378), so
+// once the two-lane form would stack waves on a SIMD the one-lane form
+// finishes first: 65,536 sequences of 16 keys take 47 us in one lane
+// against 66 us in two, while 32,768 of 32 keys (one two-lane wave per
+// SIMD) take 83 us against 72 us.
 #include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdlib>
 
 #include "ea_internal.hpp"
 
@@ -97,6 +108,22 @@ __device__ __forceinline__ int32_t owner(const int64_t *key_off, int32_t n_seqs,
   return lo;
 }
 
+// The parent key of sequence s as eight big-endian words (zero without
+// parents: the chain starts from the all-zero root).
+__device__ __forceinline__ void parent_words(const uint8_t *parents, int32_t s,
+                                             uint32_t prev[8]) {
+  if (parents != nullptr) {
+    const uint8_t *p = parents + 32 * (int64_t)s;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      prev[j] = ((uint32_t)p[4 * j] << 24) | ((uint32_t)p[4 * j + 1] << 16) |
+                ((uint32_t)p[4 * j + 2] << 8) | (uint32_t)p[4 * j + 3];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) prev[j] = 0;
+  }
+}
+
 __global__ __launch_bounds__(256) void sha256_midstates(
     const int32_t *__restrict__ tokens, const int64_t *__restrict__ key_off,
     const int64_t *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys,
@@ -151,16 +178,7 @@ __global__ __launch_bounds__(64) void sha256_chain(
   const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
   const uint32_t m = e_side ? 0u : 0xffffffffu;
   uint32_t prev[8];
-  if (parents != nullptr) {
-    const uint8_t *p = parents + 32 * (int64_t)s;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      prev[j] = ((uint32_t)p[4 * j] << 24) | ((uint32_t)p[4 * j + 1] << 16) |
-                ((uint32_t)p[4 * j + 2] << 8) | (uint32_t)p[4 * j + 3];
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) prev[j] = 0;
-  }
+  parent_words(parents, s, prev);
   const int64_t k0 = key_off[s], k1 = key_off[s + 1];
   const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
   uint4 nx = k0 < k1 ? mh[2 * k0 + (e_side ? 1 : 0)] : make_uint4(0, 0, 0, 0);
@@ -233,6 +251,70 @@ __global__ __launch_bounds__(64) void sha256_chain(
   }
 }
 
+// One lane per sequence: the working state and the message schedule of a
+// chained compression all in one lane.  Message words 8..15 are the fixed
+// padding of a 32-byte parent (the 0x80 byte, zeros, the bit length).
+__global__ __launch_bounds__(256) void sha256_chain_lane(
+    const uint32_t *__restrict__ mid, const int64_t *__restrict__ key_off,
+    int32_t n_seqs, uint32_t len_bits, const uint8_t *__restrict__ parents,
+    uint8_t *__restrict__ keys) {
+  const int32_t s = blockIdx.x * 256 + threadIdx.x;
+  if (s >= n_seqs) return;
+  uint32_t prev[8];
+  parent_words(parents, s, prev);
+  const int64_t k0 = key_off[s], k1 = key_off[s + 1];
+  const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
+  uint4 n0 = make_uint4(0, 0, 0, 0), n1 = n0;
+  if (k0 < k1) {
+    n0 = mh[2 * k0];
+    n1 = mh[2 * k0 + 1];
+  }
+  // first midstate taken before the loop, as in the two-lane form
+  asm volatile("" ::"v"(n0.x), "v"(n0.y), "v"(n0.z), "v"(n0.w), "v"(n1.x), "v"(n1.y),
+               "v"(n1.z), "v"(n1.w));
+  for (int64_t k = k0; k < k1; ++k) {
+    uint32_t st[8] = {n0.x, n0.y, n0.z, n0.w, n1.x, n1.y, n1.z, n1.w};
+    if (k + 1 < k1) {
+      n0 = mh[2 * (k + 1)];
+      n1 = mh[2 * (k + 1) + 1];
+    }
+    uint32_t w[16];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = prev[j];
+    w[8] = 0x80000000u;
+#pragma unroll
+    for (int j = 9; j < 15; ++j) w[j] = 0u;
+    w[15] = len_bits;
+    compress(st, w);
+    uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k);
+    out[0] = make_uint4(__builtin_bswap32(st[0]), __builtin_bswap32(st[1]),
+                        __builtin_bswap32(st[2]), __builtin_bswap32(st[3]));
+    out[1] = make_uint4(__builtin_bswap32(st[4]), __builtin_bswap32(st[5]),
+                        __builtin_bswap32(st[6]), __builtin_bswap32(st[7]));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) prev[j] = st[j];
+  }
+}
+
+// SIMDs of the current device (four per compute unit on CDNA), cached per
+// device.
+hipError_t device_simds(int *out) {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && cache[dev].load(std::memory_order_relaxed) > 0) {
+    *out = cache[dev].load(std::memory_order_relaxed);
+    return hipSuccess;
+  }
+  int cus = 0;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  *out = 4 * (cus > 0 ? cus : 1);
+  if (dev >= 0 && dev < 64) cache[dev].store(*out, std::memory_order_relaxed);
+  return hipSuccess;
+}
+
 }  // namespace
 
 hipError_t launch_sha256_midstates(const int32_t *d_tokens,
@@ -256,10 +338,21 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid,
   if (n_seqs <= 0) return hipSuccess;
   // message = 4b token bytes + 32 key bytes
   const uint32_t len_bits = (uint32_t)(8u * (4u * (uint32_t)block_tokens + 32u));
-  const int blocks = (n_seqs + 31) / 32;
+  int lanes = 0;
+  if (const char *f = std::getenv("EA_HASH_LANES")) lanes = std::atoi(f);  // 1 or 2 forces a form
+  if (lanes != 1 && lanes != 2) {
+    int simds = 0;
+    const hipError_t e = device_simds(&simds);
+    if (e != hipSuccess) return e;
+    lanes = (int64_t)n_seqs > 32 * (int64_t)simds ? 1 : 2;  // 32 sequences per two-lane wave
+  }
   (void)hipGetLastError();  // report this launch's status only
-  hipLaunchKernelGGL(sha256_chain, dim3(blocks), dim3(64), 0, stream, d_mid,
-                     d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
+  if (lanes == 1)
+    hipLaunchKernelGGL(sha256_chain_lane, dim3((n_seqs + 255) / 256), dim3(256), 0, stream,
+                       d_mid, d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
+  else
+    hipLaunchKernelGGL(sha256_chain, dim3((n_seqs + 31) / 32), dim3(64), 0, stream, d_mid,
+                       d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
   return hipGetLastError();
 }
 

@@ -107,3 +107,30 @@ def test_device_calls_back_to_back():
     torch.cuda.synchronize()
     for (_, out), okeys in zip(outs, want):
         assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+@pytest.mark.parametrize("lanes", ["1", "2"])
+def test_both_chain_forms(lanes, monkeypatch):
+    # the chained compression runs two lanes per sequence, or one lane per
+    # sequence for large batches; each form forced on ragged chains, parents,
+    # chunk-sized blocks and the extreme token values
+    monkeypatch.setenv("EA_HASH_LANES", lanes)
+    r = W.rng(90 + int(lanes))
+    check(list(r.integers(0, 900, size=300)), 16, parents=True, seed=91)
+    check([0, 15, 16, 17, 1024 * 3 + 5, 2048], 1024, parents=True, seed=92)
+    check([65536], 16, seed=93)
+    lengths = [5 * 16 + 7, 0, 48, 11 * 16 + 1]
+    toks = r.integers(-2**31, 2**31, size=sum(lengths), dtype=np.int64).astype(np.int32)
+    toks[:4] = [-2**31, 2**31 - 1, -1, 0]
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    keys, koffs = api.hash_blocks(toks, offs, 16)
+    okeys, okoffs = oracle.hash_blocks(toks, offs, 16)
+    assert np.array_equal(koffs, okoffs) and np.array_equal(keys, okeys)
+
+
+def test_batch_past_the_one_lane_threshold():
+    # more sequences than two-lane waves fit one per SIMD (32 per SIMD):
+    # the library picks the one-lane chain by itself; ragged lengths, parents
+    r = W.rng(95)
+    check(list(r.integers(0, 160, size=40000)), 16, parents=True, seed=95)
+    check([64] * 40000, 16, seed=96)
