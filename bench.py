@@ -597,11 +597,92 @@ def run_tiny(args):
 def _short(name):
     for key, short in (("copy_host_link<0", "store"), ("copy_host_link<1", "load"),
                        ("copy_hbm<0", "gather"), ("copy_hbm<1", "scatter"),
+                       ("sha256_chain_lane", "sha256_chain_lane"),
                        ("sha256_chain", "sha256_chain"), ("sha256_midstates", "sha256_midstates"),
                        ("copyBuffer", "rocclr_copyBuffer")):
         if key in name:
             return short
     return None
+
+
+SIDE_WORKLOADS = ("layered_fp8", "dense_scattered", "tp8_shard", "load_cost", "agent_pool",
+                  "agent_pool_chunked")
+WORKLOADS_SUMMARY = os.path.join(ROOT, "profiles", "side_workloads_kernel_trace.md")
+
+
+def summarize_workloads(d):
+    """Write the kernel-trace summary of the side workloads from directory d:
+    for each workload w, d/w.json (its bench line) and d/w/w_kernel_trace.csv
+    (rocprofv3 --kernel-trace --output-format csv of that bench run)."""
+    cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d bench_out/prof_wl/{w} -o {w} "
+           "-- python3 bench.py --workload {w} --detail bench_out/prof_wl/{w}/detail.json "
+           "> bench_out/prof_wl/{w}.json")
+    lines = ["# Kernel durations of the side workloads (kernel traces)", "",
+             "Commands (from the repository root on the MI355X), for each workload `{w}` of "
+             + ", ".join(f"`{w}`" for w in SIDE_WORKLOADS) + ":", "", "    " + cmd,
+             "    python3 bench.py --summarize-workloads bench_out/prof_wl", "",
+             f"kernel_source_sha256: {kernel_source_hash()}", "",
+             "Each table lists the kernels of the run (library kernels by role, others by "
+             "name) by launched workgroups: dispatches, median, 99th percentile, mean and "
+             "total duration.  `store`/`load` are `copy_host_link` (direct plan), `gather`/"
+             "`scatter` `copy_hbm`.  A host-link kernel launches its working workgroups times "
+             "the XCD count over the XCDs of its direction's mask, and the workgroups that land "
+             "on other XCDs return at once: 32 launched for the 8 working workgroups of a store "
+             "or load, 64 for the 16 of a layer of the layered load.  Untimed set-up (filling "
+             "the synthetic cache, pre-storing prefixes, the one-time XCD probe `xcd_probe`) "
+             "is included.", ""]
+    for w in SIDE_WORKLOADS:
+        line = json.load(open(os.path.join(d, f"{w}.json")))
+        groups = {}
+        for x in csv.DictReader(open(os.path.join(d, w, f"{w}_kernel_trace.csv"))):
+            k = _short(x["Kernel_Name"]) or _plain_name(x["Kernel_Name"])
+            wg = int(x["Grid_Size_X"]) // max(1, int(x["Workgroup_Size_X"]))
+            dur = (int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3
+            groups.setdefault((k, wg), []).append(dur)
+        lines += [f"## {w}", "", f"Bench line: {line['value']} {line['unit']}"
+                  + (f", {line['ms_per_step']} ms per step" if line.get("ms_per_step") else "")
+                  + f" ({line['config']['workload']}).", "",
+                  "| kernel | workgroups | dispatches | median µs | p99 µs | mean µs | total ms |",
+                  "|---|---|---|---|---|---|---|"]
+        order = sorted(groups.items(), key=lambda kv: -sum(kv[1]))
+        for (k, wg), v in order[:12]:
+            a = np.array(v)
+            lines.append(f"| {k} | {wg:,} | {len(a):,} | {np.median(a):.1f} | "
+                         f"{np.percentile(a, 99):.1f} | {a.mean():.1f} | {a.sum() / 1e3:.1f} |")
+        if len(order) > 12:
+            rest = sum(sum(v) for _, v in order[12:])
+            lines.append(f"| {len(order) - 12} other kernels | | | | | | {rest / 1e3:.1f} |")
+        lines.append("")
+        if w == "layered_fp8":
+            from paper_2609_33762_amd import workloads as W
+            n_pages, piece = W.LAYERED_PREFIX_PAGES, W.LAYERED.piece_bytes
+            v = np.array(max((vals for (k, _), vals in groups.items() if k == "load"), key=len))
+            layer_bytes = n_pages * (piece + 8)
+            lines += [f"One layer's kernel moves {n_pages:,} pieces of {piece:,} B "
+                      f"plus 8 B of scales each ({layer_bytes / 1e6:.2f} MB): "
+                      f"{layer_bytes / (np.median(v) * 1e-6) / GB:.1f} GB/s at the median "
+                      f"duration; the bench's event time per layer is "
+                      f"{line['layered']['per_layer_ms'] * 1e3:.1f} µs.", ""]
+        if w == "dense_scattered":
+            lat = line["latency_ms"]
+            moved = 10000 * lat["mean_bytes_per_call"]
+            ks = sum(sum(v) for (k, _), v in groups.items() if k in ("store", "load"))
+            lines += [f"The run makes two series of 10,000 calls, one kernel each (one call at a "
+                      f"time for the latencies, then back to back), {moved / 1e9:.1f} GB per "
+                      f"series (mean {lat['mean_bytes_per_call'] / 1e6:.2f} MB per call).  Over "
+                      f"the summed durations of the store and load kernels ({ks / 1e3:.1f} ms) "
+                      f"that is {2 * moved / (ks * 1e-6) / GB:.1f} GB/s of kernel time, against "
+                      f"{line['value']} GB/s end to end back to back and a p50 latency of "
+                      f"{lat['p50'] * 1e3:.0f} µs per call from enqueue to completion.", ""]
+    open(WORKLOADS_SUMMARY, "w").write("\n".join(lines))
+    print(f"wrote {WORKLOADS_SUMMARY}")
+
+
+def _plain_name(name):
+    """A kernel's name without return type, namespaces and arguments."""
+    n = name.replace("(anonymous namespace)::", "")
+    n = n.split("(")[0].split("<")[0].strip()
+    return n.split(" ")[-1].split("::")[-1][:48]
 
 
 def summarize_profiles(d):
@@ -1030,6 +1111,7 @@ def main():
     ap.add_argument("--isolated-only", action="store_true")
     ap.add_argument("--summarize-profiles", metavar="DIR")
     ap.add_argument("--summarize-plans", metavar="DIR")
+    ap.add_argument("--summarize-workloads", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
                              "load_cost", "tp8_shard", "hash", "agent_pool_chunked", "plans"])
@@ -1041,6 +1123,9 @@ def main():
         return
     if args.summarize_plans:
         summarize_plans(args.summarize_plans)
+        return
+    if args.summarize_workloads:
+        summarize_workloads(args.summarize_workloads)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
