@@ -166,7 +166,9 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  *
  * Both entry points run the chained compression two lanes per sequence, or
  * one lane per sequence when there are more than 32 sequences per SIMD of
- * the device (the keys are the same); EA_HASH_LANES=1 or 2 forces a form. */
+ * the device (the keys are the same); EA_HASH_LANES=1 or 2 forces a form.
+ * Sequence and key offsets travel to the kernels as 32-bit values when all
+ * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter. */
 int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,
                           int32_t n_seqs, int32_t block_tokens,
                           const uint8_t *d_parents, uint8_t *d_keys_out,

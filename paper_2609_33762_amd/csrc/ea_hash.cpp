@@ -2,6 +2,9 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
+#include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -137,6 +140,42 @@ int ensure_mid(uint32_t **mid, int64_t *cap, int64_t keys) {
   return EA_OK;
 }
 
+// Key offsets [n+1] then token offsets [n] for the kernels, written at h as
+// int32 when `wide` is false (every value below 2^31: half the bytes to
+// upload) and int64 otherwise.  Token offsets are toff[s], or koff[s] * b
+// for tokens packed block after block (toff null).  Returns the bytes
+// written, rounded up to 16.
+template <typename Off>
+void write_offsets(uint8_t *h, const int64_t *koff, const int64_t *toff, int64_t b,
+                   int32_t n) {
+  Off *k = reinterpret_cast<Off *>(h);
+  Off *t = k + n + 1;
+  for (int32_t s = 0; s <= n; ++s) k[s] = (Off)koff[s];
+  if (toff)
+    for (int32_t s = 0; s < n; ++s) t[s] = (Off)toff[s];
+  else
+    for (int32_t s = 0; s < n; ++s) t[s] = (Off)(koff[s] * b);
+}
+
+// EA_HASH_OFFSETS=64 keeps 64-bit offsets even where 32 bits would do.
+bool force_wide() {
+  const char *v = std::getenv("EA_HASH_OFFSETS");
+  return v && std::strcmp(v, "64") == 0;
+}
+
+int64_t offsets_bytes(int32_t n, bool wide) {
+  return ((2 * (int64_t)n + 1) * (wide ? 8 : 4) + 15) / 16 * 16;
+}
+
+int64_t put_offsets(uint8_t *h, const int64_t *koff, const int64_t *toff, int64_t b, int32_t n,
+                    bool wide) {
+  if (wide)
+    write_offsets<int64_t>(h, koff, toff, b, n);
+  else
+    write_offsets<int32_t>(h, koff, toff, b, n);
+  return offsets_bytes(n, wide);
+}
+
 }  // namespace
 
 extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
@@ -154,34 +193,31 @@ extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
   if ((rc = prepare(w)) != EA_OK) return rc;
   // pack the full-block tokens of every sequence contiguously
   const int64_t tok_bytes = total * block_tokens * 4;
-  const int64_t meta_bytes = (2 * (int64_t)n_seqs + 1) * 8 + (parents ? 32 * (int64_t)n_seqs : 0);
+  const bool wide = total * block_tokens > INT32_MAX || force_wide();
+  const int64_t off_bytes = offsets_bytes(n_seqs, wide);
+  const int64_t meta_bytes = off_bytes + (parents ? 32 * (int64_t)n_seqs : 0);
   if ((rc = grow_pair(&w.h_tok, &w.d_tok, &w.cap_tok, tok_bytes)) != EA_OK) return rc;
   if ((rc = grow_pair(&w.h_meta, &w.d_meta, &w.cap_meta, meta_bytes)) != EA_OK) return rc;
   if ((rc = grow_pair(&w.h_keys, &w.d_keys, &w.cap_keys, total * 32)) != EA_OK) return rc;
   if ((rc = ensure_mid(&w.d_mid, &w.cap_mid, total)) != EA_OK) return rc;
 
-  int64_t *koff = reinterpret_cast<int64_t *>(w.h_meta);
-  int64_t *toff = koff + n_seqs + 1;
-  uint8_t *par = reinterpret_cast<uint8_t *>(toff + n_seqs);
-  int64_t packed = 0;
   for (int32_t s = 0; s < n_seqs; ++s) {
-    koff[s] = key_offsets_out[s];
-    toff[s] = packed;
     const int64_t nt = (key_offsets_out[s + 1] - key_offsets_out[s]) * block_tokens;
-    std::memcpy(w.h_tok + packed * 4, tokens + seq_offsets[s], (size_t)nt * 4);
-    packed += nt;
+    std::memcpy(w.h_tok + key_offsets_out[s] * block_tokens * 4, tokens + seq_offsets[s],
+                (size_t)nt * 4);
   }
-  koff[n_seqs] = key_offsets_out[n_seqs];
-  if (parents) std::memcpy(par, parents, (size_t)n_seqs * 32);
+  put_offsets(w.h_meta, key_offsets_out, nullptr, block_tokens, n_seqs, wide);
+  if (parents) std::memcpy(w.h_meta + off_bytes, parents, (size_t)n_seqs * 32);
 
   HS_HIP(hipMemcpyAsync(w.d_tok, w.h_tok, (size_t)tok_bytes, hipMemcpyHostToDevice, stream));
   HS_HIP(hipMemcpyAsync(w.d_meta, w.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
-  const int64_t *d_koff = reinterpret_cast<const int64_t *>(w.d_meta);
-  const int64_t *d_toff = d_koff + n_seqs + 1;
-  const uint8_t *d_par = parents ? reinterpret_cast<const uint8_t *>(d_toff + n_seqs) : nullptr;
+  const uint8_t *d_koff = w.d_meta;
+  const uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
+  const uint8_t *d_par = parents ? w.d_meta + off_bytes : nullptr;
   HS_HIP(ea::launch_sha256_midstates(reinterpret_cast<const int32_t *>(w.d_tok), d_koff,
-                                     d_toff, n_seqs, total, block_tokens, w.d_mid, stream));
-  HS_HIP(ea::launch_sha256_chain(w.d_mid, d_koff, n_seqs, block_tokens, d_par, w.d_keys,
+                                     d_toff, wide, n_seqs, total, block_tokens, w.d_mid,
+                                     stream));
+  HS_HIP(ea::launch_sha256_chain(w.d_mid, d_koff, wide, n_seqs, block_tokens, d_par, w.d_keys,
                                  stream));
   HS_HIP(hipMemcpyAsync(w.h_keys, w.d_keys, (size_t)total * 32, hipMemcpyDeviceToHost, stream));
   HS_HIP(hipEventRecord(w.done, stream));
@@ -211,18 +247,18 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq
   w.next ^= 1;
   if (d.used) HS_HIP(hipEventSynchronize(d.done));  // the call two back is done
   if (!d.done) HS_HIP(hipEventCreateWithFlags(&d.done, hipEventDisableTiming));
-  const int64_t meta_bytes = (2 * (int64_t)n_seqs + 1) * 8;
+  // token offsets are the caller's sequence starts, all at most seq_offsets[n]
+  const bool wide = seq_offsets[n_seqs] > INT32_MAX || total > INT32_MAX || force_wide();
+  const int64_t meta_bytes = offsets_bytes(n_seqs, wide);
   if ((rc = grow_pair(&d.h_meta, &d.d_meta, &d.cap_meta, meta_bytes)) != EA_OK) return rc;
   if ((rc = ensure_mid(&d.d_mid, &d.cap_mid, total)) != EA_OK) return rc;
-  int64_t *koff = reinterpret_cast<int64_t *>(d.h_meta);
-  int64_t *toff = koff + n_seqs + 1;
-  std::memcpy(koff, key_offsets_out, (size_t)(n_seqs + 1) * 8);
-  std::memcpy(toff, seq_offsets, (size_t)n_seqs * 8);
+  put_offsets(d.h_meta, key_offsets_out, seq_offsets, 0, n_seqs, wide);
   HS_HIP(hipMemcpyAsync(d.d_meta, d.h_meta, (size_t)meta_bytes, hipMemcpyHostToDevice, stream));
-  const int64_t *d_koff = reinterpret_cast<const int64_t *>(d.d_meta);
-  HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_koff + n_seqs + 1, n_seqs, total,
+  const uint8_t *d_koff = d.d_meta;
+  const uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
+  HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_toff, wide, n_seqs, total,
                                      block_tokens, d.d_mid, stream));
-  HS_HIP(ea::launch_sha256_chain(d.d_mid, d_koff, n_seqs, block_tokens, d_parents,
+  HS_HIP(ea::launch_sha256_chain(d.d_mid, d_koff, wide, n_seqs, block_tokens, d_parents,
                                  d_keys_out, stream));
   HS_HIP(hipEventRecord(d.done, stream));
   d.used = true;

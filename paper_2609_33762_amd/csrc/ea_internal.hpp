@@ -81,16 +81,15 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
 
 // SHA-256 chained keys.
 //  mid:  device [n_keys][8] words scratch
-//  key_seq_begin: device int64[n_seqs+1] key offsets; tok_begin: device
-//  int64[n_seqs] token offset of each sequence.
-hipError_t launch_sha256_midstates(const int32_t *d_tokens,
-                                   const int64_t *d_key_offsets,
-                                   const int64_t *d_tok_offsets, int32_t n_seqs,
-                                   int64_t n_keys, int32_t block_tokens,
-                                   uint32_t *d_mid, hipStream_t stream);
-hipError_t launch_sha256_chain(const uint32_t *d_mid,
-                               const int64_t *d_key_offsets, int32_t n_seqs,
-                               int32_t block_tokens, const uint8_t *d_parents,
+//  d_key_offsets: device [n_seqs+1] key offsets; d_tok_offsets: device
+//  [n_seqs] token offset of each sequence; both int32 when `wide` is false
+//  (every offset below 2^31), int64 when it is true.
+hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_offsets,
+                                   const void *d_tok_offsets, bool wide, int32_t n_seqs,
+                                   int64_t n_keys, int32_t block_tokens, uint32_t *d_mid,
+                                   hipStream_t stream);
+hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets, bool wide,
+                               int32_t n_seqs, int32_t block_tokens, const uint8_t *d_parents,
                                uint8_t *d_keys, hipStream_t stream);
 
 }  // namespace ea

@@ -98,8 +98,8 @@ __device__ __forceinline__ void compress(uint32_t st[8], uint32_t w[16]) {
 }
 
 // index of the sequence owning key g: largest s with key_off[s] <= g
-__device__ __forceinline__ int32_t owner(const int64_t *key_off, int32_t n_seqs,
-                                         int64_t g) {
+template <typename Off>
+__device__ __forceinline__ int32_t owner(const Off *key_off, int32_t n_seqs, int64_t g) {
   int32_t lo = 0, hi = n_seqs - 1;
   while (lo < hi) {
     const int32_t mid = (lo + hi + 1) >> 1;
@@ -124,15 +124,18 @@ __device__ __forceinline__ void parent_words(const uint8_t *parents, int32_t s,
   }
 }
 
+// Offsets (Off) are 32-bit when every key and token offset fits, which
+// halves their upload; 64-bit otherwise.
+template <typename Off>
 __global__ __launch_bounds__(256) void sha256_midstates(
-    const int32_t *__restrict__ tokens, const int64_t *__restrict__ key_off,
-    const int64_t *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys,
+    const int32_t *__restrict__ tokens, const Off *__restrict__ key_off,
+    const Off *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys,
     int32_t block_tokens, uint32_t *__restrict__ mid) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= n_keys) return;
   const int32_t s = owner(key_off, n_seqs, g);
-  const int64_t i = g - key_off[s];
-  const int32_t *tok = tokens + tok_off[s] + i * block_tokens;
+  const int64_t i = g - (int64_t)key_off[s];
+  const int32_t *tok = tokens + (int64_t)tok_off[s] + i * block_tokens;
   uint32_t st[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) st[j] = kInit[j];
@@ -167,8 +170,9 @@ __device__ __forceinline__ uint32_t dpp_from(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
 }
 
+template <typename Off>
 __global__ __launch_bounds__(64) void sha256_chain(
-    const uint32_t *__restrict__ mid, const int64_t *__restrict__ key_off,
+    const uint32_t *__restrict__ mid, const Off *__restrict__ key_off,
     int32_t n_seqs, uint32_t len_bits, const uint8_t *__restrict__ parents,
     uint8_t *__restrict__ keys) {
   const int lane = threadIdx.x;
@@ -254,8 +258,9 @@ __global__ __launch_bounds__(64) void sha256_chain(
 // One lane per sequence: the working state and the message schedule of a
 // chained compression all in one lane.  Message words 8..15 are the fixed
 // padding of a 32-byte parent (the 0x80 byte, zeros, the bit length).
+template <typename Off>
 __global__ __launch_bounds__(256) void sha256_chain_lane(
-    const uint32_t *__restrict__ mid, const int64_t *__restrict__ key_off,
+    const uint32_t *__restrict__ mid, const Off *__restrict__ key_off,
     int32_t n_seqs, uint32_t len_bits, const uint8_t *__restrict__ parents,
     uint8_t *__restrict__ keys) {
   const int32_t s = blockIdx.x * 256 + threadIdx.x;
@@ -317,23 +322,44 @@ hipError_t device_simds(int *out) {
 
 }  // namespace
 
-hipError_t launch_sha256_midstates(const int32_t *d_tokens,
-                                   const int64_t *d_key_offsets,
-                                   const int64_t *d_tok_offsets, int32_t n_seqs,
-                                   int64_t n_keys, int32_t block_tokens,
-                                   uint32_t *d_mid, hipStream_t stream) {
+hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_offsets,
+                                   const void *d_tok_offsets, bool wide, int32_t n_seqs,
+                                   int64_t n_keys, int32_t block_tokens, uint32_t *d_mid,
+                                   hipStream_t stream) {
   if (n_keys <= 0) return hipSuccess;
   const int64_t blocks = (n_keys + 255) / 256;
   (void)hipGetLastError();  // report this launch's status only
-  hipLaunchKernelGGL(sha256_midstates, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     d_tokens, d_key_offsets, d_tok_offsets, n_seqs, n_keys,
-                     block_tokens, d_mid);
+  if (wide)
+    hipLaunchKernelGGL(sha256_midstates<int64_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       d_tokens, static_cast<const int64_t *>(d_key_offsets),
+                       static_cast<const int64_t *>(d_tok_offsets), n_seqs, n_keys,
+                       block_tokens, d_mid);
+  else
+    hipLaunchKernelGGL(sha256_midstates<int32_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       d_tokens, static_cast<const int32_t *>(d_key_offsets),
+                       static_cast<const int32_t *>(d_tok_offsets), n_seqs, n_keys,
+                       block_tokens, d_mid);
   return hipGetLastError();
 }
 
-hipError_t launch_sha256_chain(const uint32_t *d_mid,
-                               const int64_t *d_key_offsets, int32_t n_seqs,
-                               int32_t block_tokens, const uint8_t *d_parents,
+namespace {
+
+template <typename Off>
+void launch_chain(int lanes, const uint32_t *d_mid, const Off *d_koff, int32_t n_seqs,
+                  uint32_t len_bits, const uint8_t *d_parents, uint8_t *d_keys,
+                  hipStream_t stream) {
+  if (lanes == 1)
+    hipLaunchKernelGGL(sha256_chain_lane<Off>, dim3((n_seqs + 255) / 256), dim3(256), 0, stream,
+                       d_mid, d_koff, n_seqs, len_bits, d_parents, d_keys);
+  else
+    hipLaunchKernelGGL(sha256_chain<Off>, dim3((n_seqs + 31) / 32), dim3(64), 0, stream, d_mid,
+                       d_koff, n_seqs, len_bits, d_parents, d_keys);
+}
+
+}  // namespace
+
+hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets, bool wide,
+                               int32_t n_seqs, int32_t block_tokens, const uint8_t *d_parents,
                                uint8_t *d_keys, hipStream_t stream) {
   if (n_seqs <= 0) return hipSuccess;
   // message = 4b token bytes + 32 key bytes
@@ -347,12 +373,12 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid,
     lanes = (int64_t)n_seqs > 32 * (int64_t)simds ? 1 : 2;  // 32 sequences per two-lane wave
   }
   (void)hipGetLastError();  // report this launch's status only
-  if (lanes == 1)
-    hipLaunchKernelGGL(sha256_chain_lane, dim3((n_seqs + 255) / 256), dim3(256), 0, stream,
-                       d_mid, d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
+  if (wide)
+    launch_chain(lanes, d_mid, static_cast<const int64_t *>(d_key_offsets), n_seqs, len_bits,
+                 d_parents, d_keys, stream);
   else
-    hipLaunchKernelGGL(sha256_chain, dim3((n_seqs + 31) / 32), dim3(64), 0, stream, d_mid,
-                       d_key_offsets, n_seqs, len_bits, d_parents, d_keys);
+    launch_chain(lanes, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
+                 d_parents, d_keys, stream);
   return hipGetLastError();
 }
 

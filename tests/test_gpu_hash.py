@@ -134,3 +134,23 @@ def test_batch_past_the_one_lane_threshold():
     r = W.rng(95)
     check(list(r.integers(0, 160, size=40000)), 16, parents=True, seed=95)
     check([64] * 40000, 16, seed=96)
+
+
+@pytest.mark.parametrize("lanes", ["1", "2"])
+def test_64_bit_offsets(lanes, monkeypatch):
+    # offsets travel as 32-bit values when they fit; the 64-bit form (used
+    # past 2^31 tokens or keys) forced on ragged sequences, both entry points
+    torch = need_gpu()
+    monkeypatch.setenv("EA_HASH_OFFSETS", "64")
+    monkeypatch.setenv("EA_HASH_LANES", lanes)
+    r = W.rng(97)
+    check(list(r.integers(0, 700, size=200)), 16, parents=True, seed=97)
+    check([0, 1023, 1024, 5000], 1024, seed=98)
+    toks, offs = W.sequences(99, [100, 0, 513, 1024, 16])
+    d_tok = torch.as_tensor(toks, device="cuda")
+    okeys, okoffs = oracle.hash_blocks(toks, offs, 16)
+    out = torch.zeros((len(okeys), 32), dtype=torch.uint8, device="cuda")
+    koffs = api.hash_blocks_device(d_tok, offs, 16, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(koffs, okoffs)
+    assert np.array_equal(out.cpu().numpy(), okeys)
