@@ -93,20 +93,22 @@ int64_t grid_link(int dir) {
 }
 
 // XCDs of the device (workgroups are dispatched round-robin over them) and
-// whether kernels may place work by the XCD the hardware reports: a probe
-// at the device's first use checks that dispatches go round-robin over the
-// reported XCDs.  EA_XCD_PLACEMENT=index keeps the index-based placement.
+// whether kernels may place work by the XCD the hardware reports: a probe,
+// run once per device when a cache first asks for hardware placement,
+// checks that dispatches go round-robin over the reported XCDs (hw: -1 not
+// probed yet, 0 no, 1 yes).
 struct XcdInfo {
   int num = 0;
-  bool hw = false;
+  int hw = -1;
 };
 
-XcdInfo device_xcds(int dev) {
+XcdInfo device_xcds(int dev, bool want_hw) {
   static std::mutex mu;
   static XcdInfo known[64];
   std::lock_guard<std::mutex> lk(mu);
-  if (dev < 0 || dev >= 64) return XcdInfo{1, false};
-  if (known[dev].num == 0) {
+  if (dev < 0 || dev >= 64) return XcdInfo{1, 0};
+  XcdInfo &k = known[dev];
+  if (k.num == 0) {
     int v = 0, cus = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess) v = 1;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -114,14 +116,22 @@ XcdInfo device_xcds(int dev) {
     // a value that cannot be right (or a runtime without the attribute)
     // falls back to one XCD: no placement, every workgroup works
     if (v < 1 || v > 16 || cus <= 0 || cus % v != 0) v = 1;
-    bool hw = false;
-    const char *pl = std::getenv("EA_XCD_PLACEMENT");
-    if (v > 1 && !(pl && std::strcmp(pl, "index") == 0)) {
-      if (ea::probe_xcd_round_robin(v, &hw) != hipSuccess) hw = false;
-    }
-    known[dev] = XcdInfo{v, hw};
+    k.num = v;
+    if (v == 1) k.hw = 0;
   }
-  return known[dev];
+  if (want_hw && k.hw < 0) {
+    bool ok = false;
+    if (ea::probe_xcd_round_robin(k.num, &ok) != hipSuccess) ok = false;
+    k.hw = ok ? 1 : 0;
+  }
+  return k;
+}
+
+// EA_XCD_PLACEMENT=index: caches created while it is set place work by
+// workgroup index instead of the XCD the hardware reports.
+bool placement_by_index() {
+  const char *pl = std::getenv("EA_XCD_PLACEMENT");
+  return pl && std::strcmp(pl, "index") == 0;
 }
 
 uint32_t all_xcds(int n) { return n >= 32 ? 0xffffffffu : ((1u << n) - 1u); }
@@ -551,9 +561,10 @@ int ea_cache_create(const ea_cache_desc *desc, ea_cache **out) {
   if (!c) return EA_ENOMEM;
   c->d = *desc;
   c->device = dev;
-  const XcdInfo xi = device_xcds(dev);
+  const bool want_hw = !placement_by_index();
+  const XcdInfo xi = device_xcds(dev, want_hw);
   c->num_xcd = xi.num;
-  c->hw_xcd = xi.hw ? 1 : 0;
+  c->hw_xcd = want_hw && xi.hw == 1 ? 1 : 0;
   c->piece = 2LL * desc->page_tokens * desc->num_kv_heads * desc->head_dim * desc->elem_bytes;
   c->page = c->piece * desc->num_layers;
   c->trailer = desc->scale_base ? ((int64_t)desc->num_layers * 8 + 255) / 256 * 256 : 0;

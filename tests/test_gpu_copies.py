@@ -236,17 +236,22 @@ def test_failed_tier_allocation_leaves_the_library_usable():
     p.close()
 
 
+@pytest.mark.parametrize("placement", ["hardware", "index"])
 @pytest.mark.parametrize("masks", [(0x1, 0x2), (0x80, 0x40), (0x3, 0xC), (0xFF, 0xFF),
                                    (0x11, 0x22), (0x7F, 0x1)])
-def test_any_xcd_masks_copy_every_piece(masks):
-    # Work goes only to workgroups on the XCDs of the store and load masks;
-    # whatever the masks, every piece is copied exactly once.
-    os.environ["EA_XCD_STORE"], os.environ["EA_XCD_LOAD"] = hex(masks[0]), hex(masks[1])
-    try:
-        p = tiny_pair(seed=40 + masks[0], slots=256)
-    finally:
-        os.environ.pop("EA_XCD_STORE")
-        os.environ.pop("EA_XCD_LOAD")
+def test_any_xcd_masks_copy_every_piece(masks, placement, monkeypatch):
+    # Work goes only to workgroups on the XCDs of the store and load masks
+    # (the XCD the hardware reports, or the workgroup index when the probe
+    # fails or EA_XCD_PLACEMENT=index); whatever the masks and the placement,
+    # every piece is copied exactly once.
+    monkeypatch.setenv("EA_XCD_STORE", hex(masks[0]))
+    monkeypatch.setenv("EA_XCD_LOAD", hex(masks[1]))
+    if placement == "index":
+        monkeypatch.setenv("EA_XCD_PLACEMENT", "index")
+    p = tiny_pair(seed=40 + masks[0], slots=256)
+    monkeypatch.delenv("EA_XCD_STORE")
+    monkeypatch.delenv("EA_XCD_LOAD")
+    monkeypatch.delenv("EA_XCD_PLACEMENT", raising=False)
     r = W.rng(masks[0] * 7 + masks[1])
     for n in (5, 120):  # kernel arguments, then the index ring
         src = W.distinct(r, W.TINY.num_pages, n)
