@@ -8,7 +8,6 @@
 #include "ea_tier_meta.hpp"
 
 #include <algorithm>
-#include <unordered_set>
 
 namespace ea {
 
@@ -52,8 +51,17 @@ void TierMeta::trim() {
   if (!have_clock_) return;
   const __int128 old = (__int128)clock_ - keep_time_;
   if (log_.size() > kTrimAt)
-    while ((int64_t)log_.size() > keep_count_ && (__int128)log_.front().time <= old)
+    while ((int64_t)log_.size() > keep_count_ && (__int128)log_.front().time <= old) {
+      if (win_len_ >= 0 && log_base_ >= win_first_) {
+        // still counted in the activity window: it would leave at the next
+        // decision anyway, since its time is at or before clock - keep_time_
+        auto it = win_tasks_.find(log_.front().task);
+        if (--it->second == 0) win_tasks_.erase(it);
+        win_first_ = log_base_ + 1;
+      }
       log_.pop_front();
+      ++log_base_;
+    }
   if (evict_stamps_.size() > kTrimAt)
     while (!evict_stamps_.empty() && (__int128)evict_stamps_.front() <= old)
       evict_stamps_.pop_front();
@@ -111,7 +119,8 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
   if (r.decided >= 0) {
     save = r.decided;  // a later lookup of the request keeps the first choice
   } else {
-    log_.push_back(Lookup{now, r.task_id, r.n_tokens});
+    log_cum_ += r.n_tokens;
+    log_.push_back(Lookup{now, r.task_id, r.n_tokens, log_cum_});
     clock_ = now;
     have_clock_ = true;
     keep_time_ = std::max(keep_time_, p.activity_window);
@@ -119,17 +128,14 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
     const int64_t horizon = now - p.activity_window;
 
     // A_t: distinct tasks whose first lookup falls inside the window
-    std::unordered_set<int64_t> tasks;
-    for (auto it = log_.rbegin(); it != log_.rend() && it->time > horizon; ++it)
-      tasks.insert(it->task);
-    const int64_t active = (int64_t)tasks.size();
+    const int64_t active = active_tasks(p.activity_window, horizon);
 
     // N_t: mean prompt length of the last length_window first lookups
-    int64_t cnt = 0, sum = 0;
-    for (auto it = log_.rbegin(); it != log_.rend() && cnt < p.length_window; ++it) {
-      sum += it->n;
-      ++cnt;
-    }
+    const int64_t size = (int64_t)log_.size();
+    const int64_t cnt = std::min<int64_t>(p.length_window, size);
+    const int64_t before = cnt < size ? log_[(size_t)(size - 1 - cnt)].cum
+                                      : log_.front().cum - log_.front().n;
+    const int64_t sum = log_.back().cum - before;
 
     // [C_reuse > C_H], C_reuse = (A_t - 1) * (sum / cnt) * beta (Eq. 5),
     // compared exactly as (A_t - 1) * sum * beta > C_H * cnt
@@ -176,6 +182,30 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
     mask_out[i] = (uint8_t)(save && !registered(Key::from(keys + 32 * i)));
   *save_out = save;
   return EA_OK;
+}
+
+int64_t TierMeta::active_tasks(int64_t window, int64_t horizon) {
+  const int64_t end = log_base_ + (int64_t)log_.size();  // one past the newest
+  auto at = [&](int64_t i) -> const Lookup & { return log_[(size_t)(i - log_base_)]; };
+  if (window != win_len_) {
+    // a window length not seen last time: count it from scratch
+    win_tasks_.clear();
+    int64_t i = end;
+    while (i > log_base_ && at(i - 1).time > horizon) {
+      --i;
+      win_tasks_[at(i).task] += 1;
+    }
+    win_first_ = i;
+    win_len_ = window;
+  } else {
+    win_tasks_[at(end - 1).task] += 1;  // this decision's own lookup
+    while (win_first_ < end && at(win_first_).time <= horizon) {
+      auto it = win_tasks_.find(at(win_first_).task);
+      if (--it->second == 0) win_tasks_.erase(it);
+      ++win_first_;
+    }
+  }
+  return (int64_t)win_tasks_.size();
 }
 
 int TierMeta::publish(int64_t now, int64_t window, ea_tier_report *out) {

@@ -105,10 +105,25 @@ class TierMeta {
   int64_t registered_ = 0, resident_ = 0;
   std::deque<int64_t> evict_stamps_;
   int64_t evictions_total_ = 0;
+  // First lookups in time order; cum is the prompt tokens of every first
+  // lookup up to and including this one, so a mean over the last L is one
+  // subtraction.
   struct Lookup {
-    int64_t time, task, n;
+    int64_t time, task, n, cum;
   };
   std::deque<Lookup> log_;
+  int64_t log_base_ = 0;  // lookups dropped from the front so far
+  int64_t log_cum_ = 0;
+  // The tasks of the activity window, kept incrementally for one window
+  // length (win_len_, -1 before the first decision): the lookups from index
+  // win_first_ (counting dropped ones) to the newest, counted per task.  A
+  // decision adds its own lookup and drops those that left the window, so A_t
+  // costs amortized constant time per request; a new window length rebuilds
+  // the counts once.
+  int64_t win_len_ = -1;
+  int64_t win_first_ = 0;
+  std::unordered_map<int64_t, int64_t> win_tasks_;
+  int64_t active_tasks(int64_t window, int64_t horizon);
   int64_t keep_time_ = 0;   // largest activity or report window used
   int64_t keep_count_ = 1;  // largest length window used
   int64_t clock_ = 0;

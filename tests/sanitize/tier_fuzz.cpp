@@ -117,6 +117,14 @@ void fuzz_tier(uint64_t seed, int64_t requests) {
   bool have_rep = false;
   ea_tier_report rep{};
   for (int64_t t = 0; t < requests; ++t) {
+    if (requests <= 20000 && coin(r, 0.05)) {
+      // a caller may change the windows between requests (the tier then
+      // recounts the activity window); the long stream keeps them, since
+      // windows larger than any before could reach history the tier dropped
+      p.activity_window = uniform(r, 0, 30);
+      p.length_window = (int32_t)uniform(r, 1, 40);
+      std::memcpy(&q, &p, sizeof p);
+    }
     const int a = (int)uniform(r, 0, n_agents - 1);
     auto &pk = prompt[a];
     if (!pk.empty() && coin(r, 0.1)) {  // an edit rekeys the rest of the prompt
