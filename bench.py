@@ -598,6 +598,7 @@ def _short(name):
     for key, short in (("copy_host_link<0", "store"), ("copy_host_link<1", "load"),
                        ("copy_hbm<0", "gather"), ("copy_hbm<1", "scatter"),
                        ("sha256_chain_lane", "sha256_chain_lane"),
+                       ("sha256_chain_split", "sha256_chain_split"),
                        ("sha256_chain", "sha256_chain"), ("sha256_midstates", "sha256_midstates"),
                        ("copyBuffer", "rocclr_copyBuffer")):
         if key in name:
@@ -743,7 +744,7 @@ def summarize_profiles(d):
         c, a = stats.get(k, (0, float("nan")))
         lines.append(f"| {k} | {len(ds)} | {avg:.4f} | {ev[k]:.4f} | "
                      f"{alg[k] / (avg * 1e-3) / GB:.1f} | {c}, {a:.4f} |")
-    for k in ("sha256_midstates", "sha256_chain"):
+    for k in ("sha256_midstates", "sha256_chain_split", "sha256_chain", "sha256_chain_lane"):
         if k in stats:
             c, a = stats[k]
             lines.append(f"| {k} | {c} | {a:.4f} | - | - | {c}, {a:.4f} |")
@@ -1057,11 +1058,12 @@ def run_hash(args):
     """Chained keys (16-token blocks) on the device, tokens already in HBM:
     the turn's 56k-token prompt (one 3,500-key chain, and in 1,024-token
     chunks: 54 keys of 64 token blocks each), one 64k-token sequence, 64
-    such sequences, 16,384 sequences of 1,024 tokens (the two-lane chain
-    kernel then has 512 waves for the 1,024 SIMDs) and 65,536 of 256 tokens
-    (more than 32 sequences per SIMD, so the chain runs one lane per
-    sequence: 1,024 waves); every run checked against the host entry point's
-    keys.  The roofline is taken on the last."""
+    such sequences (these three in the two-wave form, one workgroup per
+    sequence), 16,384 sequences of 1,024 tokens (the two-lane chain kernel
+    then has 512 waves for the 1,024 SIMDs) and 65,536 of 256 tokens (more
+    than 32 sequences per SIMD, so the chain runs one lane per sequence:
+    1,024 waves); every run checked against the host entry point's keys.
+    The roofline is taken on the last."""
     import torch
     from paper_2609_33762_amd import api, workloads as W
     torch.cuda.set_device(0)

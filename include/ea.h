@@ -164,9 +164,11 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  * int64[n_seqs+1], filled before return).  Asynchronous: the keys are valid
  * once the work enqueued on `stream` completes.
  *
- * Both entry points run the chained compression two lanes per sequence, or
- * one lane per sequence when there are more than 32 sequences per SIMD of
- * the device (the keys are the same); EA_HASH_LANES=1 or 2 forces a form.
+ * Both entry points run the chained compression in one of three forms (the
+ * keys are the same): a workgroup of two waves per sequence while there is
+ * at most one sequence per compute unit, two lanes per sequence up to 32
+ * sequences per SIMD, one lane per sequence beyond; EA_HASH_CHAIN=split,
+ * pair or lane forces a form.
  * Sequence and key offsets travel to the kernels as 32-bit values when all
  * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter. */
 int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,

@@ -12,7 +12,9 @@
 //                     words 0..7 (the serial part: one compression per key);
 //   sha256_chain_lane: the same with one lane per sequence, for batches of
 //                     sequences large enough to give every SIMD more than
-//                     one wave of the two-lane form.
+//                     one wave of the two-lane form;
+//   sha256_chain_split: the same for up to one sequence per compute unit,
+//                     with the message schedule moved to a second wave.
 // A lone chain runs at the issue rate of one wave, so the instructions per
 // compression set its speed: rotations are v_alignbit_b32, every
 // three-input XOR and Ch/Maj one v_bitop3_b32 (gfx950's three-input logic
@@ -29,6 +31,7 @@
 
 #include <atomic>
 #include <cstdlib>
+#include <cstring>
 
 #include "ea_internal.hpp"
 
@@ -255,6 +258,173 @@ __global__ __launch_bounds__(64) void sha256_chain(
   }
 }
 
+// One round of the two-lane form with W_t + K_t given (both lanes).
+__device__ __forceinline__ void pair_round(uint32_t &s0, uint32_t &s1, uint32_t &s2,
+                                           uint32_t &s3, uint32_t wk, uint32_t r1c,
+                                           uint32_t r2c, uint32_t r3c, uint32_t m,
+                                           bool e_side) {
+  const uint32_t S = bitop3<kXor3>(__builtin_amdgcn_alignbit(s0, s0, r1c),
+                                   __builtin_amdgcn_alignbit(s0, s0, r2c),
+                                   __builtin_amdgcn_alignbit(s0, s0, r3c));
+  const uint32_t F = bitop3<kCh>(bitop3<kXorAnd>(s0, s2, m), s1, s2);
+  const uint32_t U = S + F;
+  const uint32_t T1 = U + s3 + wk;
+  const uint32_t dA = dpp_from<kPermFromA>(s3);
+  const uint32_t Q = e_side ? dA : U;
+  const uint32_t nw = dpp_from<kPermFromE>(T1) + Q;
+  s3 = s2; s2 = s1; s1 = s0; s0 = nw;
+}
+
+// W_T0 .. W_T0+15 of the rolling schedule w, each stored as W_t + K_t.
+template <int T0>
+__device__ __forceinline__ void schedule16(uint32_t w[16], uint32_t out[16]) {
+#pragma unroll
+  for (int t = T0; t < T0 + 16; ++t) {
+    const uint32_t a = w[(t - 2) & 15], b = w[(t - 15) & 15];
+    const uint32_t s1 = bitop3<kXor3>(rotr(a, 17), rotr(a, 19), a >> 10);
+    const uint32_t s0 = bitop3<kXor3>(rotr(b, 7), rotr(b, 18), b >> 3);
+    const uint32_t wt = s1 + w[(t - 7) & 15] + s0 + w[t & 15];
+    w[t & 15] = wt;
+    out[t - T0] = wt + kRound[t];
+  }
+}
+
+// One sequence per workgroup of two waves.  Wave 0 runs the 64 rounds in
+// the two-lane form; wave 1 computes the message schedule from the
+// previous key (words 16..63, with K_t added) and hands it over through LDS
+// in three parts of 16 words, so the rounds wave no longer issues the
+// schedule's instructions.  Per key: wave 0 runs rounds 0..15 from the key
+// it holds while wave 1 computes words 16..31; a barrier; rounds 16..31
+// while wave 1 computes 32..47; a barrier; rounds 32..47 while it computes
+// 48..63; a barrier; rounds 48..63, then wave 0 writes the key to memory
+// and to LDS; a barrier, after which wave 1 reads it.  Both waves run the
+// same loop (the workgroup's one sequence), so every barrier is reached by
+// both.  Every lane pair of wave 0 computes the sequence; lanes 0 and 1
+// write it.
+template <typename Off>
+__global__ __launch_bounds__(128) void sha256_chain_split(
+    const uint32_t *__restrict__ mid, const Off *__restrict__ key_off, int32_t n_seqs,
+    uint32_t len_bits, const uint8_t *__restrict__ parents, uint8_t *__restrict__ keys) {
+  __shared__ uint4 wk4[12];   // W_t + K_t for t = 16..63
+  __shared__ uint4 key4[2];   // the key just written, as state words
+  const int32_t s = blockIdx.x;
+  if (s >= n_seqs) return;  // the whole workgroup
+  const bool rounds_wave = threadIdx.x < 64;
+  const int lane = threadIdx.x & 63;
+  const bool e_side = lane & 1;
+  const int64_t k0 = key_off[s], k1 = key_off[s + 1];
+  const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
+  const uint32_t m = e_side ? 0u : 0xffffffffu;
+  const uint32_t pad8 = e_side ? 0x80000000u : 0u;   // (W8, W9)
+  const uint32_t pad14 = e_side ? 0u : len_bits;      // (W14, W15)
+  uint32_t prev[8];
+  parent_words(parents, s, prev);
+  // rounds wave: the previous key in pairs, x[j] = (W_2j, W_2j+1) as
+  // (e-lane, a-lane), and the next midstate half
+  uint32_t x[4] = {e_side ? prev[0] : prev[1], e_side ? prev[2] : prev[3],
+                   e_side ? prev[4] : prev[5], e_side ? prev[6] : prev[7]};
+  const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
+  uint4 nx = make_uint4(0, 0, 0, 0);
+  if (rounds_wave && k0 < k1) nx = mh[2 * k0 + (e_side ? 1 : 0)];
+  // first midstate taken before the loop, as in the two-lane form
+  asm volatile("" ::"v"(nx.x), "v"(nx.y), "v"(nx.z), "v"(nx.w));
+  uint32_t w[16];  // schedule wave: the rolling message schedule
+  uint32_t s0 = 0, s1 = 0, s2 = 0, s3 = 0;
+  uint4 h0 = make_uint4(0, 0, 0, 0);
+  for (int64_t k = k0; k < k1; ++k) {
+    if (rounds_wave) {
+      h0 = nx;
+      if (k + 1 < k1) nx = mh[2 * (k + 1) + (e_side ? 1 : 0)];
+      s0 = h0.x; s1 = h0.y; s2 = h0.z; s3 = h0.w;
+      const uint32_t X[8] = {x[0], x[1], x[2], x[3], pad8, 0u, 0u, pad14};
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[t >> 1]) : X[t >> 1];
+        pair_round(s0, s1, s2, s3, kRound[t] + wt, r1c, r2c, r3c, m, e_side);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w[j] = prev[j];
+      w[8] = 0x80000000u;
+#pragma unroll
+      for (int j = 9; j < 15; ++j) w[j] = 0u;
+      w[15] = len_bits;
+      uint32_t o[16];
+      schedule16<16>(w, o);
+      if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          wk4[i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+    }
+    __syncthreads();
+    if (rounds_wave) {
+      uint32_t q[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4 v = wk4[i];
+        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+    } else {
+      uint32_t o[16];
+      schedule16<32>(w, o);
+      if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          wk4[4 + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+    }
+    __syncthreads();
+    if (rounds_wave) {
+      uint32_t q[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4 v = wk4[4 + i];
+        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+    } else {
+      uint32_t o[16];
+      schedule16<48>(w, o);
+      if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          wk4[8 + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+    }
+    __syncthreads();
+    if (rounds_wave) {
+      uint32_t q[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4 v = wk4[8 + i];
+        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+      const uint32_t o0 = h0.x + s0, o1 = h0.y + s1, o2 = h0.z + s2, o3 = h0.w + s3;
+      if (lane < 2) {
+        uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k + (e_side ? 16 : 0));
+        *out = make_uint4(__builtin_bswap32(o0), __builtin_bswap32(o1), __builtin_bswap32(o2),
+                          __builtin_bswap32(o3));
+        key4[e_side ? 1 : 0] = make_uint4(o0, o1, o2, o3);
+      }
+      const uint32_t a0 = dpp_from<kPermFromA>(o0), a2 = dpp_from<kPermFromA>(o2);
+      const uint32_t e1 = dpp_from<kPermFromE>(o1), e3 = dpp_from<kPermFromE>(o3);
+      x[0] = e_side ? a0 : o1;
+      x[1] = e_side ? a2 : o3;
+      x[2] = e_side ? o0 : e1;
+      x[3] = e_side ? o2 : e3;
+    }
+    __syncthreads();
+    if (!rounds_wave) {
+      const uint4 ka = key4[0], kb = key4[1];
+      prev[0] = ka.x; prev[1] = ka.y; prev[2] = ka.z; prev[3] = ka.w;
+      prev[4] = kb.x; prev[5] = kb.y; prev[6] = kb.z; prev[7] = kb.w;
+    }
+  }
+}
+
 // One lane per sequence: the working state and the message schedule of a
 // chained compression all in one lane.  Message words 8..15 are the fixed
 // padding of a 32-byte parent (the 0x80 byte, zeros, the bit length).
@@ -301,9 +471,8 @@ __global__ __launch_bounds__(256) void sha256_chain_lane(
   }
 }
 
-// SIMDs of the current device (four per compute unit on CDNA), cached per
-// device.
-hipError_t device_simds(int *out) {
+// Compute units of the current device, cached per device.
+hipError_t device_cus(int *out) {
   static std::atomic<int> cache[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -315,7 +484,7 @@ hipError_t device_simds(int *out) {
   int cus = 0;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
-  *out = 4 * (cus > 0 ? cus : 1);
+  *out = cus > 0 ? cus : 1;
   if (dev >= 0 && dev < 64) cache[dev].store(*out, std::memory_order_relaxed);
   return hipSuccess;
 }
@@ -344,13 +513,18 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_of
 
 namespace {
 
+enum ChainForm { kChainPair = 0, kChainLane = 1, kChainSplit = 2 };
+
 template <typename Off>
-void launch_chain(int lanes, const uint32_t *d_mid, const Off *d_koff, int32_t n_seqs,
+void launch_chain(int form, const uint32_t *d_mid, const Off *d_koff, int32_t n_seqs,
                   uint32_t len_bits, const uint8_t *d_parents, uint8_t *d_keys,
                   hipStream_t stream) {
-  if (lanes == 1)
+  if (form == kChainLane)
     hipLaunchKernelGGL(sha256_chain_lane<Off>, dim3((n_seqs + 255) / 256), dim3(256), 0, stream,
                        d_mid, d_koff, n_seqs, len_bits, d_parents, d_keys);
+  else if (form == kChainSplit)
+    hipLaunchKernelGGL(sha256_chain_split<Off>, dim3(n_seqs), dim3(128), 0, stream, d_mid,
+                       d_koff, n_seqs, len_bits, d_parents, d_keys);
   else
     hipLaunchKernelGGL(sha256_chain<Off>, dim3((n_seqs + 31) / 32), dim3(64), 0, stream, d_mid,
                        d_koff, n_seqs, len_bits, d_parents, d_keys);
@@ -364,20 +538,29 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   if (n_seqs <= 0) return hipSuccess;
   // message = 4b token bytes + 32 key bytes
   const uint32_t len_bits = (uint32_t)(8u * (4u * (uint32_t)block_tokens + 32u));
-  int lanes = 0;
-  if (const char *f = std::getenv("EA_HASH_LANES")) lanes = std::atoi(f);  // 1 or 2 forces a form
-  if (lanes != 1 && lanes != 2) {
-    int simds = 0;
-    const hipError_t e = device_simds(&simds);
+  int form = -1;
+  if (const char *f = std::getenv("EA_HASH_CHAIN")) {  // forces a form
+    if (std::strcmp(f, "pair") == 0) form = kChainPair;
+    if (std::strcmp(f, "lane") == 0) form = kChainLane;
+    if (std::strcmp(f, "split") == 0) form = kChainSplit;
+  }
+  if (form < 0) {
+    // Up to one sequence per compute unit: the split form (a workgroup per
+    // sequence, 20% less time per key for a lone chain).  Up to 32
+    // sequences per SIMD (four per compute unit): two lanes per sequence.
+    // Beyond: one lane per sequence.
+    int cus = 0;
+    const hipError_t e = device_cus(&cus);
     if (e != hipSuccess) return e;
-    lanes = (int64_t)n_seqs > 32 * (int64_t)simds ? 1 : 2;  // 32 sequences per two-lane wave
+    form = n_seqs <= cus ? kChainSplit
+                         : ((int64_t)n_seqs > 128 * (int64_t)cus ? kChainLane : kChainPair);
   }
   (void)hipGetLastError();  // report this launch's status only
   if (wide)
-    launch_chain(lanes, d_mid, static_cast<const int64_t *>(d_key_offsets), n_seqs, len_bits,
+    launch_chain(form, d_mid, static_cast<const int64_t *>(d_key_offsets), n_seqs, len_bits,
                  d_parents, d_keys, stream);
   else
-    launch_chain(lanes, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
+    launch_chain(form, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
                  d_parents, d_keys, stream);
   return hipGetLastError();
 }

@@ -109,13 +109,14 @@ def test_device_calls_back_to_back():
         assert np.array_equal(out.cpu().numpy(), okeys)
 
 
-@pytest.mark.parametrize("lanes", ["1", "2"])
-def test_both_chain_forms(lanes, monkeypatch):
-    # the chained compression runs two lanes per sequence, or one lane per
-    # sequence for large batches; each form forced on ragged chains, parents,
-    # chunk-sized blocks and the extreme token values
-    monkeypatch.setenv("EA_HASH_LANES", lanes)
-    r = W.rng(90 + int(lanes))
+@pytest.mark.parametrize("form", ["pair", "lane", "split"])
+def test_every_chain_form(form, monkeypatch):
+    # the chained compression runs two lanes per sequence, one lane per
+    # sequence (large batches) or a workgroup of two waves per sequence (up
+    # to one sequence per compute unit); each form forced on ragged chains,
+    # parents, chunk-sized blocks, a long chain and the extreme token values
+    monkeypatch.setenv("EA_HASH_CHAIN", form)
+    r = W.rng(90 + len(form))
     check(list(r.integers(0, 900, size=300)), 16, parents=True, seed=91)
     check([0, 15, 16, 17, 1024 * 3 + 5, 2048], 1024, parents=True, seed=92)
     check([65536], 16, seed=93)
@@ -136,13 +137,13 @@ def test_batch_past_the_one_lane_threshold():
     check([64] * 40000, 16, seed=96)
 
 
-@pytest.mark.parametrize("lanes", ["1", "2"])
-def test_64_bit_offsets(lanes, monkeypatch):
+@pytest.mark.parametrize("form", ["pair", "lane", "split"])
+def test_64_bit_offsets(form, monkeypatch):
     # offsets travel as 32-bit values when they fit; the 64-bit form (used
     # past 2^31 tokens or keys) forced on ragged sequences, both entry points
     torch = need_gpu()
     monkeypatch.setenv("EA_HASH_OFFSETS", "64")
-    monkeypatch.setenv("EA_HASH_LANES", lanes)
+    monkeypatch.setenv("EA_HASH_CHAIN", form)
     r = W.rng(97)
     check(list(r.integers(0, 700, size=200)), 16, parents=True, seed=97)
     check([0, 1023, 1024, 5000], 1024, seed=98)
@@ -154,3 +155,12 @@ def test_64_bit_offsets(lanes, monkeypatch):
     torch.cuda.synchronize()
     assert np.array_equal(koffs, okoffs)
     assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+def test_few_long_chains_take_the_split_form():
+    # up to one sequence per compute unit the library picks the two-wave form
+    # by itself: ragged long chains with parents, a chain of one key, empty
+    # sequences
+    r = W.rng(101)
+    lengths = [int(x) for x in r.integers(0, 20000, size=40)] + [16, 0, 15]
+    check(lengths, 16, parents=True, seed=101)
