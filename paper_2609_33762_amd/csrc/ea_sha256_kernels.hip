@@ -7,6 +7,8 @@
 // splits in two kernels:
 //   sha256_midstates: one lane per key, compresses the b/16 token blocks
 //                     from the initial hash value (fully parallel);
+//   sha256_midstates_split: the same for few keys of several blocks, a
+//                     workgroup of two waves per key;
 //   sha256_chain:     two lanes per sequence, run the final compression of
 //                     each key in order, feeding key_{i-1} in as message
 //                     words 0..7 (the serial part: one compression per key);
@@ -289,6 +291,72 @@ __device__ __forceinline__ void schedule16(uint32_t w[16], uint32_t out[16]) {
   }
 }
 
+// Midstates of few keys with several token blocks each: one key per
+// workgroup of two waves.  The token blocks of a key are compressed one
+// after the other, but their message schedules depend on the tokens alone,
+// so wave 1 prepares block c + 1's 64 words (W_t + K_t) in one half of an
+// LDS double buffer while wave 0 runs block c's 64 rounds in the two-lane
+// form from the other half; one barrier per block.  Both waves run the
+// same loop over the key's blocks, so every barrier is reached by both.
+template <typename Off>
+__global__ __launch_bounds__(128) void sha256_midstates_split(
+    const int32_t *__restrict__ tokens, const Off *__restrict__ key_off,
+    const Off *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys, int32_t block_tokens,
+    uint32_t *__restrict__ mid) {
+  __shared__ uint4 wk4[2][16];  // W_t + K_t of two blocks
+  const int64_t g = blockIdx.x;
+  if (g >= n_keys) return;  // the whole workgroup
+  const bool rounds_wave = threadIdx.x < 64;
+  const int lane = threadIdx.x & 63;
+  const bool e_side = lane & 1;
+  const int32_t s = owner(key_off, n_seqs, g);
+  const int32_t *tok = tokens + (int64_t)tok_off[s] + (g - (int64_t)key_off[s]) * block_tokens;
+  const int32_t blocks = block_tokens / 16;
+  const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
+  const uint32_t m = e_side ? 0u : 0xffffffffu;
+  // schedule wave: block c's 64 words into half c & 1
+  auto prepare = [&](int32_t c) {
+    uint32_t w[16], o[64];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {  // LE32 token bytes read as a big-endian word
+      w[j] = __builtin_bswap32((uint32_t)tok[16 * c + j]);
+      o[j] = w[j] + kRound[j];
+    }
+    schedule16<16>(w, o + 16);
+    schedule16<32>(w, o + 32);
+    schedule16<48>(w, o + 48);
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        wk4[c & 1][i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+  };
+  if (!rounds_wave) prepare(0);
+  __syncthreads();
+  // rounds wave: this lane's half of the state (a..d on the a-lane, e..h on
+  // the e-lane)
+  uint32_t h0 = e_side ? kInit[4] : kInit[0], h1 = e_side ? kInit[5] : kInit[1];
+  uint32_t h2 = e_side ? kInit[6] : kInit[2], h3 = e_side ? kInit[7] : kInit[3];
+  for (int32_t c = 0; c < blocks; ++c) {
+    if (rounds_wave) {
+      uint32_t s0 = h0, s1 = h1, s2 = h2, s3 = h3;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint4 v = wk4[c & 1][i];
+        pair_round(s0, s1, s2, s3, v.x, r1c, r2c, r3c, m, e_side);
+        pair_round(s0, s1, s2, s3, v.y, r1c, r2c, r3c, m, e_side);
+        pair_round(s0, s1, s2, s3, v.z, r1c, r2c, r3c, m, e_side);
+        pair_round(s0, s1, s2, s3, v.w, r1c, r2c, r3c, m, e_side);
+      }
+      h0 += s0; h1 += s1; h2 += s2; h3 += s3;
+    } else if (c + 1 < blocks) {
+      prepare(c + 1);
+    }
+    __syncthreads();
+  }
+  if (rounds_wave && lane < 2)
+    reinterpret_cast<uint4 *>(mid + 8 * g)[e_side ? 1 : 0] = make_uint4(h0, h1, h2, h3);
+}
+
 // One sequence per workgroup of two waves.  Wave 0 runs the 64 rounds in
 // the two-lane form; wave 1 computes the message schedule from the
 // previous key (words 16..63, with K_t added) and hands it over through LDS
@@ -496,9 +564,32 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_of
                                    int64_t n_keys, int32_t block_tokens, uint32_t *d_mid,
                                    hipStream_t stream) {
   if (n_keys <= 0) return hipSuccess;
-  const int64_t blocks = (n_keys + 255) / 256;
+  // Keys of several blocks, at most one per compute unit: a workgroup of
+  // two waves per key (the schedule on its own wave); otherwise one lane
+  // per key.  EA_HASH_MID=lane or split forces a form.
+  bool split = false;
+  const char *f = std::getenv("EA_HASH_MID");
+  if (f && std::strcmp(f, "split") == 0) {
+    split = true;
+  } else if (!(f && std::strcmp(f, "lane") == 0) && block_tokens >= 32) {
+    int cus = 0;
+    const hipError_t e = device_cus(&cus);
+    if (e != hipSuccess) return e;
+    split = n_keys <= cus;
+  }
   (void)hipGetLastError();  // report this launch's status only
-  if (wide)
+  const int64_t blocks = (n_keys + 255) / 256;
+  if (split && wide)
+    hipLaunchKernelGGL(sha256_midstates_split<int64_t>, dim3((unsigned)n_keys), dim3(128), 0,
+                       stream, d_tokens, static_cast<const int64_t *>(d_key_offsets),
+                       static_cast<const int64_t *>(d_tok_offsets), n_seqs, n_keys,
+                       block_tokens, d_mid);
+  else if (split)
+    hipLaunchKernelGGL(sha256_midstates_split<int32_t>, dim3((unsigned)n_keys), dim3(128), 0,
+                       stream, d_tokens, static_cast<const int32_t *>(d_key_offsets),
+                       static_cast<const int32_t *>(d_tok_offsets), n_seqs, n_keys,
+                       block_tokens, d_mid);
+  else if (wide)
     hipLaunchKernelGGL(sha256_midstates<int64_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        d_tokens, static_cast<const int64_t *>(d_key_offsets),
                        static_cast<const int64_t *>(d_tok_offsets), n_seqs, n_keys,

@@ -164,3 +164,16 @@ def test_few_long_chains_take_the_split_form():
     r = W.rng(101)
     lengths = [int(x) for x in r.integers(0, 20000, size=40)] + [16, 0, 15]
     check(lengths, 16, parents=True, seed=101)
+
+
+@pytest.mark.parametrize("form", ["lane", "split"])
+@pytest.mark.parametrize("b", [32, 1024])
+def test_midstate_forms(form, b, monkeypatch):
+    # the token blocks of a key are compressed by one lane, or for few keys
+    # of several blocks by a workgroup of two waves; each form forced on
+    # ragged sequences with parents, a single key, and many keys
+    monkeypatch.setenv("EA_HASH_MID", form)
+    r = W.rng(110 + b)
+    check([0, b - 1, b, b + 1, 7 * b + 3, 3 * b], b, parents=True, seed=111)
+    check([b], b, seed=112)
+    check(list(r.integers(0, 20 * b, size=30)), b, parents=True, seed=113)
