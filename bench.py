@@ -510,13 +510,9 @@ def run_dense_scattered(args):
                  W.DENSE_CALLS, extra)
 
 
-def run_layered(args):
-    """64k-token fp8 prefix (4,096 pages, 48 layers, per-page scales) loaded
-    one layer at a time, each layer signalled by an event."""
-    import torch
-    from paper_2609_33762_amd import api, workloads as W
-    torch.cuda.set_device(0)
-    sh = W.LAYERED
+def _layered_once(torch, api, W, sh, steps):
+    """Load the 4,096-page prefix of shape sh one layer at a time, `steps`
+    timed repetitions after one untimed; returns the bench figures."""
     L, P = sh.num_layers, sh.num_pages
     kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
     W.fill_random_bytes(kv, W.SEED_DATA)
@@ -532,7 +528,7 @@ def run_layered(args):
     tier.store(cache, src, np.arange(n))
     _, copy_s = copy_streams(torch)
     res = []
-    for rep in range(args.steps + 1):
+    for rep in range(steps + 1):
         start = torch.cuda.Event(enable_timing=True)
         events = [torch.cuda.Event(enable_timing=True) for _ in range(L)]
         torch.cuda.synchronize()
@@ -544,14 +540,33 @@ def run_layered(args):
     res = np.array(res)
     total_ms = float(np.median(res[:, -1]))
     moved = n * tier.slot_bytes
-    extra = {"layered": {"time_to_first_layer_ms": round(float(np.median(res[:, 0])), 4),
-                         "per_layer_ms": round(float(np.median(np.diff(res, axis=1))), 4),
-                         "layer_done_ms": [round(float(x), 3) for x in np.median(res, axis=0)]}}
+    out = {"gbs": round(moved / (total_ms * 1e-3) / GB, 3), "ms": round(total_ms, 3),
+           "slot_bytes": tier.slot_bytes,
+           "time_to_first_layer_ms": round(float(np.median(res[:, 0])), 4),
+           "per_layer_ms": round(float(np.median(np.diff(res, axis=1))), 4),
+           "layer_done_ms": [round(float(x), 3) for x in np.median(res, axis=0)]}
     tier.close()
     cache.close()
+    del kv, sc
+    return out
+
+
+def run_layered(args):
+    """64k-token fp8 prefix (4,096 pages, 48 layers, per-page scales) loaded
+    one layer at a time, each layer signalled by an event; then the same
+    prefix on one TP8 rank's share (1 KV head, 4 KiB pieces)."""
+    import torch
+    from paper_2609_33762_amd import api, workloads as W
+    torch.cuda.set_device(0)
+    full = _layered_once(torch, api, W, W.LAYERED, args.steps)
+    log(f"layered 4 heads: {full['gbs']} GB/s, {full['per_layer_ms']} ms per layer")
+    torch.cuda.empty_cache()
+    shard = _layered_once(torch, api, W, W.LAYERED_TP8, args.steps)
+    log(f"layered 1 head (TP8 shard): {shard['gbs']} GB/s, {shard['per_layer_ms']} ms per layer")
+    extra = {"layered": {k: v for k, v in full.items() if k not in ("gbs", "ms")},
+             "tp8_shard": shard}
     return _line("layered_fp8: 64k-token prefix, 48 layers x 4 heads x d128 fp8 + scales",
-                 round(moved / (total_ms * 1e-3) / GB, 3), "GB/s", round(total_ms, 3),
-                 args.steps, extra)
+                 full["gbs"], "GB/s", full["ms"], args.steps, extra)
 
 
 def run_tiny(args):

@@ -67,6 +67,9 @@ DENSE_CALLS = 10000
 # Layer-pipelined fp8 prefix load: 64k tokens = 4,096 pages, per-page scales.
 LAYERED = Shape("layered_fp8", 48, 4, 128, 1, 16, 8192, has_scales=True, dtype="fp8_e4m3")
 LAYERED_PREFIX_PAGES = 4096
+# The same prefix on one rank of TP8: 1 KV head, 4 KiB pieces.
+LAYERED_TP8 = Shape("layered_fp8_tp8_shard", 48, 1, 128, 1, 16, 8192, has_scales=True,
+                    dtype="fp8_e4m3")
 
 
 def rng(seed):

@@ -150,9 +150,10 @@ def test_hbm_gather_and_scatter_full_size():
     release(torch)
 
 
-def test_layered_fp8_prefix_full_size():
+@pytest.mark.parametrize("sh", [W.LAYERED, W.LAYERED_TP8], ids=lambda sh: sh.name)
+def test_layered_fp8_prefix_full_size(sh):
+    # the 64k-token fp8 prefix, and the same on one TP8 rank (1 KV head)
     torch = need_gpu()
-    sh = W.LAYERED
     L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
     kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
     W.fill_random_bytes(kv, W.SEED_DATA)
