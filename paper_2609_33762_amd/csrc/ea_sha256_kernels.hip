@@ -539,6 +539,10 @@ __global__ __launch_bounds__(256) void sha256_chain_lane(
   }
 }
 
+// The split forms launch one workgroup per sequence or key; forcing them on
+// more than this many falls back to the other forms.
+constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
+
 // Compute units of the current device, cached per device.
 hipError_t device_cus(int *out) {
   static std::atomic<int> cache[64];
@@ -570,7 +574,7 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_of
   bool split = false;
   const char *f = std::getenv("EA_HASH_MID");
   if (f && std::strcmp(f, "split") == 0) {
-    split = true;
+    split = n_keys <= kMaxSplitGroups;
   } else if (!(f && std::strcmp(f, "lane") == 0) && block_tokens >= 32) {
     int cus = 0;
     const hipError_t e = device_cus(&cus);
@@ -635,6 +639,7 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
     if (std::strcmp(f, "lane") == 0) form = kChainLane;
     if (std::strcmp(f, "split") == 0) form = kChainSplit;
   }
+  if (form == kChainSplit && n_seqs > kMaxSplitGroups) form = kChainPair;  // grid bound
   if (form < 0) {
     // Up to one sequence per compute unit: the split form (a workgroup per
     // sequence, 20% less time per key for a lone chain).  Up to 32
