@@ -80,6 +80,9 @@ def lib():
             "eao_sha256_constants": (None, [P, P]),
             "eao_beta_rank": (I64, [I64, I64, I64, I64, I64]),
             "eao_working_set_bytes": (C.c_double, [C.c_double, C.c_double, C.c_double]),
+            "eao_restore_time": (C.c_double, [C.c_double] * 4),
+            "eao_obr": (C.c_double, [C.c_double] * 5),
+            "eao_obr_limit": (C.c_double, [C.c_double] * 3),
             "eao_tier_chunks": (I64, [I64, I64, I64]),
             "eao_piece_bytes": (I64, [P]), "eao_page_bytes": (I64, [P]),
             "eao_trailer_bytes": (I64, [P]), "eao_slot_bytes": (I64, [P]),
@@ -149,6 +152,21 @@ def working_set_bytes(active_pool, mean_prompt_tokens, beta):
 
 def tier_chunks(capacity_bytes, block_tokens, beta):
     return lib().eao_tier_chunks(capacity_bytes, block_tokens, beta)
+
+
+def restore_time(n, beta, b_eff, tau):
+    """Eq. 2: T_load(n) = n * beta / B_eff + tau."""
+    return lib().eao_restore_time(n, beta, b_eff, tau)
+
+
+def obr(n, beta, b_eff, tau, t_pf):
+    """Eq. 2: OBR(n) = 1 - T_load(n) / (n * t_pf)."""
+    return lib().eao_obr(n, beta, b_eff, tau, t_pf)
+
+
+def obr_limit(beta, b_eff, t_pf):
+    """OBR for long prefixes: 1 - beta / (B_eff * t_pf)."""
+    return lib().eao_obr_limit(beta, b_eff, t_pf)
 
 
 def make_shape(num_pages, num_layers, page_tokens, num_kv_heads, head_dim,

@@ -142,6 +142,21 @@ int64_t eao_tier_chunks(int64_t capacity_bytes, int64_t block_tokens,
   return capacity_bytes / (block_tokens * beta_rank);
 }
 
+double eao_restore_time(double n, double beta_rank, double b_eff, double tau_load) {
+  /* Eq. 2: T_load(n) = n beta_rank / B_eff + tau_load */
+  return n * beta_rank / b_eff + tau_load;
+}
+
+double eao_obr(double n, double beta_rank, double b_eff, double tau_load, double t_pf) {
+  /* Eq. 2: OBR(n) = 1 - T_load(n) / T_rec(n), T_rec(n) = n t_pf */
+  return 1.0 - eao_restore_time(n, beta_rank, b_eff, tau_load) / (n * t_pf);
+}
+
+double eao_obr_limit(double beta_rank, double b_eff, double t_pf) {
+  /* n -> infinity: tau_load / n vanishes */
+  return 1.0 - beta_rank / (b_eff * t_pf);
+}
+
 int64_t eao_piece_bytes(const eao_shape *sh) {
   return 2LL * sh->page_tokens * sh->num_kv_heads * sh->head_dim * sh->elem_bytes;
 }

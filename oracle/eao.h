@@ -34,8 +34,10 @@
  * restatements of the layout; the tier by a brute-force model, Lemma 1 and
  * Proposition 1 on random streams, the Eq. 6 truth table with its endpoints
  * and the paper's closed forms (footprints, working sets, K_H); the
- * reference models by brute-force distinct counts and the round-robin closed
- * form.  Parity unpinned: byte compatibility of the keys with LMCache or
+ * restore cost and OBR of Eq. 2 by the paper's H20 numbers (0.86 us per
+ * token, a 5.6 us prefill bound, OBR above 0.84) and the definition's
+ * limits; the reference models by brute-force distinct counts and the
+ * round-robin closed form.  Parity unpinned: byte compatibility of the keys with LMCache or
  * vLLM, which this definition does not claim.
  */
 #ifndef EAO_H
@@ -84,6 +86,22 @@ double eao_working_set_bytes(double active_pool, double mean_prompt_tokens,
  * (section 4, "Which writes a tier can decline"; survival bound of Eq. 4). */
 int64_t eao_tier_chunks(int64_t capacity_bytes, int64_t block_tokens,
                         int64_t beta_rank);
+
+/* ------------------------------------------- restore versus recompute (Eq. 2) */
+
+/* Time to restore a prefix of n tokens from the host tier,
+ * T_load(n) = n * beta_rank / B_eff + tau_load, in the units of tau_load
+ * and of beta_rank / B_eff (section 3.1, Eq. 2). */
+double eao_restore_time(double n, double beta_rank, double b_eff, double tau_load);
+
+/* Offload Benefit Ratio OBR(n) = 1 - T_load(n) / T_rec(n) with
+ * T_rec(n) = n * t_pf (section 3.1, Eq. 2). */
+double eao_obr(double n, double beta_rank, double b_eff, double tau_load, double t_pf);
+
+/* Its limit for long prefixes, where tau_load is amortized:
+ * 1 - beta_rank / (B_eff * t_pf) (App. "Offload Cost and Prefix-Survival
+ * Model", the per-token cost t_load(n) = beta_rank / B_eff + tau_load / n). */
+double eao_obr_limit(double beta_rank, double b_eff, double t_pf);
 
 /* ------------------------------------------------------------------ layout */
 

@@ -90,3 +90,39 @@ def test_heads_per_rank_round_up_when_tp_does_not_divide():
     # Eq. 1 takes ceil(H_kv / TP): 6 heads over 4 ranks leave 2 heads on some rank
     assert oracle.beta_rank(10, 64, 2, 6, 4) == 2 * 10 * 64 * 2 * 2
     assert oracle.beta_rank(10, 64, 2, 3, 2) == 2 * 10 * 64 * 2 * 2
+
+
+def test_restore_cost_and_obr_on_h20(paper):
+    # the paper's H20 numbers: 24 KiB per token at the median 26.6 GiB/s is
+    # 0.86 us per token; 6.6 GFLOP per token on eight GPUs at 148 TFLOPS is
+    # at least 5.6 us; so OBR for long prefixes is at least 0.84 (Eq. 2)
+    h = paper["restore_cost_h20"]
+    b_eff = h["restore_median_gib_s"] * GIB
+    t_load = oracle.restore_time(1, h["beta_rank"], b_eff, 0.0)
+    assert round(t_load * 1e6, 2) == h["restore_us_per_token_2dp"]
+    t_pf = h["gflop_per_token"] * 1e9 / (h["gpus"] * h["peak_tflops_per_gpu"] * 1e12)
+    assert round(t_pf * 1e6, 1) == h["prefill_bound_us_per_token_1dp"]
+    lim = oracle.obr_limit(h["beta_rank"], b_eff, t_pf)
+    assert lim > h["obr_limit_at_least"]
+    # the paper's own rounding of the same bound: 1 - 0.86 / 5.6 > 0.84
+    assert 1 - h["restore_us_per_token_2dp"] / h["prefill_bound_us_per_token_1dp"] > 0.84
+    assert abs(lim - (1 - t_load / t_pf)) < 1e-12
+
+
+def test_obr_definition_and_limit():
+    # OBR(n) = 1 - (n beta / B + tau) / (n t_pf): zero when restoring costs as
+    # much as recomputing, the limit from below as n grows, the limit itself
+    # when tau = 0, and the fixed overhead amortized as tau / n
+    beta, B, tau, t_pf = 24576.0, 50e9, 20e-6, 2e-6
+    lim = oracle.obr_limit(beta, B, t_pf)
+    assert abs(lim - (1 - beta / (B * t_pf))) < 1e-15
+    prev = -1e9
+    for n in (1, 10, 100, 1000, 10 ** 4, 10 ** 6):
+        v = oracle.obr(n, beta, B, tau, t_pf)
+        assert prev < v < lim
+        assert abs((1 - v) * n * t_pf - oracle.restore_time(n, beta, B, tau)) < 1e-12
+        prev = v
+    assert abs(oracle.obr(10 ** 9, beta, B, tau, t_pf) - lim) < 1e-6
+    assert abs(oracle.obr(7, beta, B, 0.0, t_pf) - lim) < 1e-15
+    n_even = tau / (t_pf - beta / B)  # T_load(n) = T_rec(n)
+    assert abs(oracle.obr(n_even, beta, B, tau, t_pf)) < 1e-12
