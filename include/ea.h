@@ -44,6 +44,25 @@
  *  - A tier is internally locked; one tier may be used from several threads.
  *    Calls are bound to the device that was current when the cache or tier
  *    was created.
+ *
+ * Environment variables (tuning and testing; the defaults are the measured
+ * best on MI355X, and every setting gives the same bytes and keys)
+ * -------------------------------------------------------------------------
+ *  EA_TRANSFER=direct|staged   transfer plan of tiers left at EA_PLAN_AUTO
+ *  EA_LINK_WG, EA_LINK_WG_STORE, EA_LINK_WG_LOAD
+ *                              working workgroups of a direct store / load (8)
+ *  EA_LINK_WG_LAYERED          workgroups of one layer of a layered load (16)
+ *  EA_XCD_STORE, EA_XCD_LOAD   XCD masks of the two directions (0x5, 0xA
+ *                              with four or more XCDs); read at tier creation
+ *  EA_XCD_PLACEMENT=index      place work by workgroup index, not by the XCD
+ *                              the hardware reports; read at cache creation
+ *  EA_GRID_HBM, EA_GRID_GATHER, EA_GRID_SCATTER
+ *                              workgroups of the HBM gather (512) / scatter (256)
+ *  EA_STAGING_MB               HBM staging of the staged plan per direction (512)
+ *  EA_HOST_COHERENT=0          non-coherent pinned memory for new tiers
+ *  EA_HASH_CHAIN=split|pair|lane, EA_HASH_MID=split|lane
+ *                              force a form of the hash kernels
+ *  EA_HASH_OFFSETS=64          64-bit offsets for the hash kernels
  */
 #ifndef EA_H
 #define EA_H
