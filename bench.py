@@ -650,8 +650,17 @@ def summarize_workloads(d):
     for w in SIDE_WORKLOADS:
         line = json.load(open(os.path.join(d, f"{w}.json")))
         groups = {}
-        for x in csv.DictReader(open(os.path.join(d, w, f"{w}_kernel_trace.csv"))):
+        rows = sorted(csv.DictReader(open(os.path.join(d, w, f"{w}_kernel_trace.csv"))),
+                      key=lambda x: int(x["Start_Timestamp"]))
+        n_layer_loads = sum(1 for x in rows if _short(x["Kernel_Name"]) == "load")
+        seen_loads = 0
+        for x in rows:
             k = _short(x["Kernel_Name"]) or _plain_name(x["Kernel_Name"])
+            if w == "layered_fp8" and k == "load":
+                # the run loads the 4-head prefix, then the 1-head (TP8) one,
+                # the same number of layer kernels each
+                k = "load, 4 heads" if seen_loads < n_layer_loads // 2 else "load, 1 head"
+                seen_loads += 1
             wg = int(x["Grid_Size_X"]) // max(1, int(x["Workgroup_Size_X"]))
             dur = (int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3
             groups.setdefault((k, wg), []).append(dur)
@@ -671,14 +680,18 @@ def summarize_workloads(d):
         lines.append("")
         if w == "layered_fp8":
             from paper_2609_33762_amd import workloads as W
-            n_pages, piece = W.LAYERED_PREFIX_PAGES, W.LAYERED.piece_bytes
-            v = np.array(max((vals for (k, _), vals in groups.items() if k == "load"), key=len))
-            layer_bytes = n_pages * (piece + 8)
-            lines += [f"One layer's kernel moves {n_pages:,} pieces of {piece:,} B "
-                      f"plus 8 B of scales each ({layer_bytes / 1e6:.2f} MB): "
-                      f"{layer_bytes / (np.median(v) * 1e-6) / GB:.1f} GB/s at the median "
-                      f"duration; the bench's event time per layer is "
-                      f"{line['layered']['per_layer_ms'] * 1e3:.1f} µs.", ""]
+            n_pages = W.LAYERED_PREFIX_PAGES
+            for label, shape, ev in (("4 heads", W.LAYERED, line["layered"]),
+                                     ("1 head", W.LAYERED_TP8, line["tp8_shard"])):
+                v = np.array([x for (k, _), vals in groups.items() if k == "load, " + label
+                              for x in vals])
+                piece = shape.piece_bytes
+                layer_bytes = n_pages * (piece + 8)
+                lines += [f"{label}: one layer's kernel moves {n_pages:,} pieces of {piece:,} B "
+                          f"plus 8 B of scales each ({layer_bytes / 1e6:.2f} MB): "
+                          f"{layer_bytes / (np.median(v) * 1e-6) / GB:.1f} GB/s at the median "
+                          f"duration of {np.median(v):.1f} µs; the bench's event time per layer "
+                          f"is {ev['per_layer_ms'] * 1e3:.1f} µs.", ""]
         if w == "dense_scattered":
             lat = line["latency_ms"]
             moved = 10000 * lat["mean_bytes_per_call"]
