@@ -177,3 +177,12 @@ def test_midstate_forms(form, b, monkeypatch):
     check([0, b - 1, b, b + 1, 7 * b + 3, 3 * b], b, parents=True, seed=111)
     check([b], b, seed=112)
     check(list(r.integers(0, 20 * b, size=30)), b, parents=True, seed=113)
+
+
+def test_longest_contexts():
+    # the paper's longest contexts: the 262,144-token maximum of the serving
+    # configuration and the 238,105-token prompt it reports, in 16-token
+    # blocks and in 1,024-token chunks (ragged tails)
+    check([262144], 16, seed=121)
+    check([238105], 16, seed=122)
+    check([238105, 262144], 1024, parents=True, seed=123)

@@ -16,6 +16,9 @@
 * Agent pool (64 agents, 64 GiB tier, 6 turns each): every turn's lookup,
   admission, allocation and the tier's full metadata are compared with the
   oracle, and every loaded page is checked against its key's pattern.
+* The longest context of the serving configuration (262,144 tokens) as one
+  TP8 rank's prefix: 16,384 pages stored and loaded back, every page equal
+  to its source, sampled pages and slots against the oracle.
 """
 import gc
 
@@ -405,4 +408,46 @@ def test_agent_pool_in_1024_token_chunks():
     tier.close()
     cache.close()
     del kv
+    release(torch)
+
+
+def test_longest_prefix_on_one_tp8_rank():
+    # a 262,144-token prefix (the serving configuration's maximum context),
+    # 16,384 pages of one TP8 rank's share (384 KiB each, 6 GiB), stored and
+    # loaded back into other pages: every page equal to its source, sampled
+    # pages and slots against the oracle
+    torch = need_gpu()
+    sh = W.Shape("tp8_shard_long", 48, 1, 128, 2, 16, 2 * 16384 + 64)
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    n = 16384
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    kv3 = kv.view(L, P, piece)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes)
+    tier = api.Tier(cache, n * L * piece)
+    assert tier.capacity == n
+    r = W.rng(131)
+    src = W.distinct(r, P, n)
+    dst = W.distinct(r, P, n, exclude=src)
+    slots = r.permutation(n).astype(np.int64)
+    tier.store(cache, src, slots)
+    tier.load(cache, slots, dst)
+    torch.cuda.synchronize()
+    d, s_ = torch.as_tensor(dst, device="cuda"), torch.as_tensor(src, device="cuda")
+    assert torch.equal(kv3[:, d], kv3[:, s_])
+    host = tier.host_view()
+    pick = W.distinct(r, n, 12)
+    o = oshape_of(sh, num_pages=len(pick))
+    ocache = kv3[:, torch.as_tensor(src[pick], device="cuda")].cpu().numpy().copy()
+    otier = np.zeros((len(pick), tier.slot_bytes), np.uint8)
+    oracle.store_blocks(o, ocache.reshape(-1), None, otier,
+                        np.arange(len(pick), dtype=np.int32), np.arange(len(pick)))
+    assert np.array_equal(host[slots[pick]], otier)
+    oback = np.zeros_like(ocache)
+    oracle.load_blocks(o, otier, oback.reshape(-1), None, np.arange(len(pick)),
+                       np.arange(len(pick), dtype=np.int32))
+    assert np.array_equal(kv3[:, torch.as_tensor(dst[pick], device="cuda")].cpu().numpy(), oback)
+    tier.close()
+    cache.close()
+    del kv, kv3
     release(torch)
