@@ -361,10 +361,10 @@ __global__ __launch_bounds__(128) void sha256_midstates_split(
 // the two-lane form; wave 1 computes the message schedule from the
 // previous key (words 16..63, with K_t added) and hands it over through LDS
 // in three parts of 16 words, so the rounds wave no longer issues the
-// schedule's instructions.  Per key: wave 0 runs rounds 0..15 from the key
-// it holds while wave 1 computes words 16..31; a barrier; rounds 16..31
-// while wave 1 computes 32..47; a barrier; rounds 32..47 while it computes
-// 48..63; a barrier; rounds 48..63, then wave 0 writes the key to memory
+// schedule's instructions.  Per key: wave 0 runs rounds 0..11 from the key
+// it holds while wave 1 computes words 16..31; a barrier; rounds 12..27
+// while wave 1 computes 32..47; a barrier; rounds 28..43 while it computes
+// 48..63; a barrier; rounds 44..63, then wave 0 writes the key to memory
 // and to LDS; a barrier, after which wave 1 reads it.  Both waves run the
 // same loop (the workgroup's one sequence), so every barrier is reached by
 // both.  Every lane pair of wave 0 computes the sequence; lanes 0 and 1
@@ -399,14 +399,34 @@ __global__ __launch_bounds__(128) void sha256_chain_split(
   uint32_t w[16];  // schedule wave: the rolling message schedule
   uint32_t s0 = 0, s1 = 0, s2 = 0, s3 = 0;
   uint4 h0 = make_uint4(0, 0, 0, 0);
+  uint32_t X[8];
+  uint32_t qa[16], qb[16];  // rounds wave: two parts of the schedule in hand
+  // Each barrier comes four rounds before the rounds wave needs the part
+  // it releases: the wave issues the LDS reads and runs four rounds from
+  // words it already holds while they arrive.
+  auto read_part = [&](int part, uint32_t q[16]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint4 v = wk4[4 * part + i];
+      q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+    }
+  };
+  auto write_part = [&](int part, const uint32_t o[16]) {
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        wk4[4 * part + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+  };
   for (int64_t k = k0; k < k1; ++k) {
+    // rounds 0..11 | words 16..31
     if (rounds_wave) {
       h0 = nx;
       if (k + 1 < k1) nx = mh[2 * (k + 1) + (e_side ? 1 : 0)];
       s0 = h0.x; s1 = h0.y; s2 = h0.z; s3 = h0.w;
-      const uint32_t X[8] = {x[0], x[1], x[2], x[3], pad8, 0u, 0u, pad14};
+      X[0] = x[0]; X[1] = x[1]; X[2] = x[2]; X[3] = x[3];
+      X[4] = pad8; X[5] = 0u; X[6] = 0u; X[7] = pad14;
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
+      for (int t = 0; t < 12; ++t) {
         const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[t >> 1]) : X[t >> 1];
         pair_round(s0, s1, s2, s3, kRound[t] + wt, r1c, r2c, r3c, m, e_side);
       }
@@ -419,57 +439,45 @@ __global__ __launch_bounds__(128) void sha256_chain_split(
       w[15] = len_bits;
       uint32_t o[16];
       schedule16<16>(w, o);
-      if (lane == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          wk4[i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+      write_part(0, o);
     }
     __syncthreads();
+    // rounds 12..27 | words 32..47
     if (rounds_wave) {
-      uint32_t q[16];
+      read_part(0, qa);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint4 v = wk4[i];
-        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+      for (int t = 12; t < 16; ++t) {
+        const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[t >> 1]) : X[t >> 1];
+        pair_round(s0, s1, s2, s3, kRound[t] + wt, r1c, r2c, r3c, m, e_side);
       }
 #pragma unroll
-      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+      for (int t = 16; t < 28; ++t) pair_round(s0, s1, s2, s3, qa[t - 16], r1c, r2c, r3c, m, e_side);
     } else {
       uint32_t o[16];
       schedule16<32>(w, o);
-      if (lane == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          wk4[4 + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+      write_part(1, o);
     }
     __syncthreads();
+    // rounds 28..43 | words 48..63
     if (rounds_wave) {
-      uint32_t q[16];
+      read_part(1, qb);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint4 v = wk4[4 + i];
-        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
-      }
+      for (int t = 28; t < 32; ++t) pair_round(s0, s1, s2, s3, qa[t - 16], r1c, r2c, r3c, m, e_side);
 #pragma unroll
-      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+      for (int t = 32; t < 44; ++t) pair_round(s0, s1, s2, s3, qb[t - 32], r1c, r2c, r3c, m, e_side);
     } else {
       uint32_t o[16];
       schedule16<48>(w, o);
-      if (lane == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          wk4[8 + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+      write_part(2, o);
     }
     __syncthreads();
+    // rounds 44..63 and the key | idle
     if (rounds_wave) {
-      uint32_t q[16];
+      read_part(2, qa);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint4 v = wk4[8 + i];
-        q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
-      }
+      for (int t = 44; t < 48; ++t) pair_round(s0, s1, s2, s3, qb[t - 32], r1c, r2c, r3c, m, e_side);
 #pragma unroll
-      for (int t = 0; t < 16; ++t) pair_round(s0, s1, s2, s3, q[t], r1c, r2c, r3c, m, e_side);
+      for (int t = 48; t < 64; ++t) pair_round(s0, s1, s2, s3, qa[t - 48], r1c, r2c, r3c, m, e_side);
       const uint32_t o0 = h0.x + s0, o1 = h0.y + s1, o2 = h0.z + s2, o3 = h0.w + s3;
       if (lane < 2) {
         uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k + (e_side ? 16 : 0));
