@@ -253,7 +253,13 @@ typedef struct {
  *   p_t  = [C_reuse > C_H] and [registered >= theta K_H and e_t > 0]
  *          (the second factor is dropped when telemetry == 0),
  *   save = not (p_t and u > kappa),
- *   mask_out[i] = save and key i is not registered in the tier.
+ *   mask_out[i] = save and the tier holds no slot under key i (pending or
+ *                 resident: deduplication sees allocations whose store is
+ *                 not issued yet).
+ * registered counts the chunks whose store has been issued (a store
+ * allocates its buffers before it registers the chunks, App. "Runtime
+ * Admission Details"), so another request's pending allocation does not
+ * raise the occupancy o_t.
  * e_t counts evictions made to allocate inside the window.  n_keys must be
  * floor(n/b); keys host uint8[n_keys][32]; mask_out host uint8[n_keys]. */
 int ea_admission_fill(ea_tier *tier, const ea_policy *policy,
@@ -269,7 +275,10 @@ int ea_admission_fill(ea_tier *tier, const ea_policy *policy,
  * a fresh report the working-set estimate alone decides. */
 typedef struct {
   int64_t time;            /* clock value the report was taken at             */
-  int64_t registered;      /* pending + resident chunks                       */
+  int64_t registered;      /* chunks whose store has been issued: the o_t
+                              numerator (a store allocates its buffers before
+                              it registers its chunks, so pending allocations
+                              do not count)                                   */
   int64_t capacity_slots;  /* K_H                                             */
   int64_t evictions;       /* e_t: evictions made to allocate with a stamp in
                               (time - window, time]                           */
@@ -351,12 +360,12 @@ int ea_controller_decide(ea_controller *ctl, int64_t n_tokens, int64_t h_tokens,
 int ea_controller_get_status(ea_controller *ctl, ea_controller_status *out);
 
 /* Allocate host slots for the keys with mask[i] != 0 (mask NULL = all) that
- * are not already registered: the lowest-numbered free slot, else the
- * least-recent resident slot that no lookup, allocation or transfer pins (an
+ * the tier does not hold yet (pending or resident): the lowest-numbered free
+ * slot, else the least-recent resident slot that no lookup, allocation or transfer pins (an
  * eviction inside allocation, App. "Runtime Admission Details").  New slots
  * are registered under their key, go to the most-recent end in increasing
- * position order, and carry one pin; they become visible to lookups once
- * ea_store_blocks has been issued for them.  slots_out[i] = -1 where no slot
+ * position order, and carry one pin; they become visible to lookups, and
+ * count as registered chunks, once ea_store_blocks has been issued for them.  slots_out[i] = -1 where no slot
  * was allocated; once no victim is left every later block gets -1 (not an
  * error).  *allocated gets the number of slots allocated. */
 int ea_tier_alloc(ea_tier *tier, const uint8_t *keys, const uint8_t *mask,
@@ -369,8 +378,8 @@ int ea_tier_unpin(ea_tier *tier, const int64_t *slots, int64_t n);
 
 typedef struct {
   int64_t capacity_slots;   /* K_H                                          */
-  int64_t registered;       /* allocated + resident slots                   */
-  int64_t resident;
+  int64_t allocated;        /* slots holding a key: pending + resident      */
+  int64_t registered;       /* resident chunks (store issued): o_t numerator*/
   int64_t pinned;           /* slots with at least one pin                  */
   int64_t evictions_total;  /* evictions made to allocate                   */
   int64_t evictions_window; /* of those, inside the last decision's window  */
@@ -393,7 +402,7 @@ int ea_tier_stats_get(const ea_tier *tier, ea_tier_stats *stats);
 enum { EA_SLOT_FREE = 0, EA_SLOT_PENDING = 1, EA_SLOT_RESIDENT = 2 };
 
 /* Full metadata image: per slot its state, pin count and key (zeros when
- * free), and the registered slots from least to most recent in lru_out
+ * free), and the pending and resident slots from least to most recent in lru_out
  * (*n_lru entries).  Host arrays of K_H entries. */
 int ea_tier_export(const ea_tier *tier, uint8_t *state_out, int32_t *pins_out,
                    uint8_t *keys_out, int64_t *lru_out, int64_t *n_lru);

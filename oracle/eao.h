@@ -209,8 +209,9 @@ typedef struct {
 
 typedef struct {
   int64_t capacity_slots;   /* K_H                                            */
-  int64_t registered;       /* pending + resident slots                       */
-  int64_t resident;
+  int64_t allocated;        /* slots holding a key: pending + resident        */
+  int64_t registered;       /* resident chunks (store issued): the occupancy
+                               o_t = registered / K_H of Eq. 10               */
   int64_t pinned;           /* slots with a pin count > 0                     */
   int64_t evictions_total;  /* evictions made to allocate                     */
   int64_t evictions_window; /* of those, within the activity window at clock  */
@@ -243,7 +244,8 @@ int eao_tier_lookup(eao_tier *t, const uint8_t *keys, int64_t n,
 
 /* Write admission (section 4, Eq. 6; App. "Runtime Admission Details",
  * Eq. 10) plus copy-time deduplication: save_out gets save(r), and
- * mask_out[i] = save && key_i is not registered in the tier. */
+ * mask_out[i] = save && the tier holds no slot under key_i (pending or
+ * resident: deduplication also sees allocations whose store is not issued). */
 int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
                        const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
                        int32_t *save_out);
@@ -253,7 +255,8 @@ int eao_admission_fill(eao_tier *t, const eao_policy *p, const eao_request *r,
  * evictions made to allocate in the last window). */
 typedef struct {
   int64_t time;            /* clock value the report was taken at           */
-  int64_t registered;      /* pending + resident chunks                     */
+  int64_t registered;      /* resident chunks (store issued); a pending
+                              allocation is not registered yet             */
   int64_t capacity_slots;  /* K_H                                           */
   int64_t evictions;       /* e_t: evictions stamped in (time - window, time] */
 } eao_tier_report;
@@ -273,11 +276,12 @@ int eao_admission_fill_report(eao_tier *t, const eao_policy *p, const eao_reques
                               const uint8_t *keys, int64_t n_keys, uint8_t *mask_out,
                               int32_t *save_out);
 
-/* Allocate a slot for every i with mask[i] != 0 whose key is not already
- * registered: the lowest-numbered free slot, else the least-recent resident
- * unpinned slot (an eviction).  New slots are PENDING, registered under the
- * key, placed at the most-recent end in increasing position order, and
- * pinned.  slots_out[i] = -1 where nothing was allocated; once no victim is
+/* Allocate a slot for every i with mask[i] != 0 whose key the tier does not
+ * hold yet (pending or resident): the lowest-numbered free slot, else the
+ * least-recent resident unpinned slot (an eviction).  New slots are PENDING
+ * under the key, placed at the most-recent end in increasing position order,
+ * and pinned; they count as registered (occupancy) only once their store is
+ * issued (eao_tier_mark_stored).  slots_out[i] = -1 where nothing was allocated; once no victim is
  * left, every later admitted block gets -1.  *allocated gets the count. */
 int eao_tier_alloc(eao_tier *t, const uint8_t *keys, const uint8_t *mask,
                    int64_t n, int64_t *slots_out, int64_t *allocated);
@@ -288,7 +292,7 @@ int eao_tier_mark_stored(eao_tier *t, const int64_t *slots,
                          const uint8_t *mask, int64_t n);
 
 /* Drop one pin from each slot; a PENDING slot whose last pin goes away is
- * abandoned: its key is unregistered and the slot becomes free. */
+ * abandoned: its key is dropped and the slot becomes free. */
 int eao_tier_unpin(eao_tier *t, const int64_t *slots, int64_t n);
 
 int eao_tier_stats_get(const eao_tier *t, eao_tier_stats *s);

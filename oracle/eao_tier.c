@@ -2,11 +2,11 @@
  * eao_tier.c -- CPU oracle: host-tier metadata (key map, LRU recency, pins)
  * and working-set-aware write admission.  TEST INFRASTRUCTURE ONLY.
  *
- * Recency follows the paper's description of the LRU host tier (App.
- * "Runtime Admission Details", "Recency order of the host tier"): an
- * insertion goes to the most-recent end, a lookup hit moves the matched
- * prefix chunks there, and eviction happens only inside allocation, from the
- * least-recent end, skipping chunks a pending lookup or transfer pins.
+ * The LRU host tier of App. "Runtime Admission Details" and "Recency order
+ * of the host tier": new chunks join at the tail of a recency list; a lookup
+ * promotes only its leading hits to the tail; nothing leaves except when an
+ * allocation finds no free slot, which then takes the first unpinned
+ * resident chunk from the head.
  */
 #include "eao.h"
 
@@ -26,7 +26,10 @@ struct eao_tier {
   int64_t nbuckets;
   int64_t *bucket;        /* [nbuckets] first slot or -1                      */
   int64_t *chain;         /* [K] next slot in the same bucket or -1           */
-  int64_t registered, resident;
+  /* allocated: slots holding a key (pending + resident); registered: chunks
+   * whose store has been issued, the numerator of the occupancy o_t (a store
+   * allocates its buffers before it registers its chunks) */
+  int64_t allocated, registered;
   /* eviction log (clock stamps), only the last stamp and the count matter */
   int64_t evictions_total;
   int64_t *evict_stamp;   /* growing array of stamps                          */
@@ -336,7 +339,7 @@ int eao_tier_alloc(eao_tier *t, const uint8_t *keys, const uint8_t *mask,
     slots_out[i] = -1;
     if (mask && !mask[i]) continue;
     if (exhausted) continue;
-    if (map_find(t, keys + 32 * i) >= 0) continue;  /* already registered */
+    if (map_find(t, keys + 32 * i) >= 0) continue;  /* held: pending or resident */
     /* lowest-numbered free slot */
     int64_t s = -1;
     for (int64_t c = 0; c < t->K; ++c)
@@ -352,8 +355,8 @@ int eao_tier_alloc(eao_tier *t, const uint8_t *keys, const uint8_t *mask,
       lru_unlink(t, v);
       t->state[v] = EAO_SLOT_FREE;
       memset(t->keys + 32 * v, 0, 32);
+      t->allocated -= 1;
       t->registered -= 1;
-      t->resident -= 1;
       s = v;
     }
     memcpy(t->keys + 32 * s, keys + 32 * i, 32);
@@ -361,7 +364,7 @@ int eao_tier_alloc(eao_tier *t, const uint8_t *keys, const uint8_t *mask,
     t->pins[s] += 1;
     map_insert(t, s);
     lru_push_recent(t, s);
-    t->registered += 1;
+    t->allocated += 1;  /* not registered until its store is issued */
     slots_out[i] = s;
     ++count;
   }
@@ -381,7 +384,7 @@ int eao_tier_mark_stored(eao_tier *t, const int64_t *slots,
     if (mask && !mask[i]) continue;
     if (t->state[slots[i]] == EAO_SLOT_PENDING) {
       t->state[slots[i]] = EAO_SLOT_RESIDENT;
-      t->resident += 1;
+      t->registered += 1;
     }
   }
   return EAO_OK;
@@ -412,7 +415,7 @@ int eao_tier_unpin(eao_tier *t, const int64_t *slots, int64_t n) {
       lru_unlink(t, s);
       t->state[s] = EAO_SLOT_FREE;
       memset(t->keys + 32 * s, 0, 32);
-      t->registered -= 1;
+      t->allocated -= 1;
     }
   }
   return EAO_OK;
@@ -422,8 +425,8 @@ int eao_tier_stats_get(const eao_tier *t, eao_tier_stats *s) {
   if (!t || !s) return EAO_EINVAL;
   memset(s, 0, sizeof *s);
   s->capacity_slots = t->K;
+  s->allocated = t->allocated;
   s->registered = t->registered;
-  s->resident = t->resident;
   for (int64_t i = 0; i < t->K; ++i) s->pinned += t->pins[i] > 0;
   s->evictions_total = t->evictions_total;
   for (int64_t i = t->evictions_total - 1; i >= 0; --i) {

@@ -49,8 +49,8 @@ class Request(C.Structure):
 
 
 class TierStats(C.Structure):
-    _fields_ = [("capacity_slots", C.c_int64), ("registered", C.c_int64),
-                ("resident", C.c_int64), ("pinned", C.c_int64),
+    _fields_ = [("capacity_slots", C.c_int64), ("allocated", C.c_int64),
+                ("registered", C.c_int64), ("pinned", C.c_int64),
                 ("evictions_total", C.c_int64), ("evictions_window", C.c_int64),
                 ("clock", C.c_int64), ("active_tasks", C.c_int64),
                 ("mean_prompt", C.c_double), ("working_set", C.c_double),

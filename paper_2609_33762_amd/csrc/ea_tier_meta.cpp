@@ -1,10 +1,10 @@
 // Host-tier metadata and write admission (see ea_tier_meta.hpp).
 //
-// Recency follows the LRU host tier the paper describes (App. "Runtime
-// Admission Details", "Recency order of the host tier"): insertions go to the
-// most-recent end, a lookup hit moves the matched prefix there, and eviction
-// happens only inside allocation, from the least-recent end, skipping chunks
-// that a pending lookup, an allocation or a transfer pins.
+// The LRU host tier of App. "Runtime Admission Details" and "Recency order
+// of the host tier": a recency list with new chunks appended at the tail; a
+// lookup promotes only its leading hits to the tail; chunks leave only when an
+// allocation finds no free slot, which then takes the first resident chunk
+// from the head that no lookup, allocation or transfer pins.
 #include "ea_tier_meta.hpp"
 
 #include <algorithm>
@@ -72,7 +72,7 @@ void TierMeta::release_slot(int64_t s) {
   lru_remove(s);
   state_[s] = EA_SLOT_FREE;
   keys_[s] = Key{{0, 0, 0, 0}};
-  registered_ -= 1;
+  allocated_ -= 1;  // only pending slots are released here
   returned_.push(s);
 }
 
@@ -179,7 +179,7 @@ int TierMeta::admission(const ea_policy &p, const ea_request &r,
   }
   // copy-time deduplication: chunks the tier already holds are not copied
   for (int64_t i = 0; i < n_keys; ++i)
-    mask_out[i] = (uint8_t)(save && !registered(Key::from(keys + 32 * i)));
+    mask_out[i] = (uint8_t)(save && !held(Key::from(keys + 32 * i)));
   *save_out = save;
   return EA_OK;
 }
@@ -238,7 +238,7 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
     slots_out[i] = -1;
     if ((mask && !mask[i]) || exhausted) continue;
     const Key k = Key::from(keys + 32 * i);
-    if (registered(k)) continue;
+    if (held(k)) continue;
     int64_t s = take_free_slot();
     if (s < 0) {
       // evict the least-recent resident chunk nothing pins
@@ -253,8 +253,8 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
       map_.erase(keys_[v]);
       lru_remove(v);
       state_[v] = EA_SLOT_FREE;
+      allocated_ -= 1;
       registered_ -= 1;
-      resident_ -= 1;
       s = v;
     }
     keys_[s] = k;
@@ -262,7 +262,7 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
     pins_[s] += 1;
     map_.emplace(k, s);
     lru_append(s);
-    registered_ += 1;
+    allocated_ += 1;  // registered once its store is issued (mark_stored)
     slots_out[i] = s;
     ++count;
   }
@@ -274,7 +274,7 @@ int TierMeta::alloc(const uint8_t *keys, const uint8_t *mask, int64_t n,
 void TierMeta::mark_stored(int64_t slot) {
   if (state_[slot] == EA_SLOT_PENDING) {
     state_[slot] = EA_SLOT_RESIDENT;
-    resident_ += 1;
+    registered_ += 1;
   }
 }
 
@@ -295,8 +295,8 @@ int TierMeta::unpin(const int64_t *slots, int64_t n) {
 
 void TierMeta::stats(ea_tier_stats *s) const {
   s->capacity_slots = K_;
+  s->allocated = allocated_;
   s->registered = registered_;
-  s->resident = resident_;
   int64_t pinned = 0;
   for (int32_t p : pins_) pinned += p > 0;
   s->pinned = pinned;

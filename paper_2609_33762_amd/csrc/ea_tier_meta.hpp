@@ -77,7 +77,8 @@ class TierMeta {
   }
 
  private:
-  bool registered(const Key &k) const { return map_.find(k) != map_.end(); }
+  // the tier holds a slot under k: pending or resident (deduplication)
+  bool held(const Key &k) const { return map_.find(k) != map_.end(); }
   int64_t take_free_slot();
   void release_slot(int64_t s);
   void lru_remove(int64_t s);
@@ -102,7 +103,10 @@ class TierMeta {
   // keep_count_ lookups enter a mean.
   void trim();
 
-  int64_t registered_ = 0, resident_ = 0;
+  // allocated_: slots holding a key (pending + resident); registered_:
+  // chunks whose store has been issued, the numerator of the occupancy o_t
+  // (a store allocates its chunk buffers before it registers the chunks)
+  int64_t allocated_ = 0, registered_ = 0;
   std::deque<int64_t> evict_stamps_;
   int64_t evictions_total_ = 0;
   // First lookups in time order; cum is the prompt tokens of every first

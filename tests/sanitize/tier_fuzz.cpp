@@ -74,7 +74,7 @@ void compare_state(ea::TierMeta &m, eao_tier *o, int64_t K, int64_t at) {
   eao_tier_stats b;
   CHECK(eao_tier_stats_get(o, &b) == 0, "stats", at);
   CHECK(a.capacity_slots == b.capacity_slots && a.registered == b.registered &&
-            a.resident == b.resident && a.pinned == b.pinned &&
+            a.allocated == b.allocated && a.pinned == b.pinned &&
             a.evictions_total == b.evictions_total &&
             a.evictions_window == b.evictions_window && a.clock == b.clock &&
             a.active_tasks == b.active_tasks && a.last_pressure == b.last_pressure &&
@@ -112,7 +112,8 @@ void fuzz_tier(uint64_t seed, int64_t requests) {
 
   const int n_agents = (int)uniform(r, 1, 10);
   std::vector<std::vector<Key32>> prompt(n_agents);
-  std::vector<int64_t> held;  // slots still pinned (pins drop later)
+  std::vector<int64_t> held;      // slots still pinned (pins drop later)
+  std::vector<int64_t> deferred;  // allocated slots whose store comes later
   int64_t now = 0;
   bool have_rep = false;
   ea_tier_report rep{};
@@ -191,6 +192,12 @@ void fuzz_tier(uint64_t seed, int64_t requests) {
     std::vector<int64_t> got;
     for (int64_t i = 0; i < n; ++i)
       if (a1[i] >= 0) got.push_back(a1[i]);
+    if (coin(r, 0.25)) {
+      // the store is issued some requests later: decisions and reports in
+      // between see these slots allocated but not registered
+      deferred.insert(deferred.end(), got.begin(), got.end());
+      got.clear();
+    }
     for (int64_t s : got)
       if (coin(r, 0.9)) {
         m.mark_stored(s);
@@ -202,6 +209,14 @@ void fuzz_tier(uint64_t seed, int64_t requests) {
       } else {
         held.push_back(s);
       }
+    }
+    if (!deferred.empty() && coin(r, 0.3)) {
+      for (int64_t s : deferred) {
+        m.mark_stored(s);
+        CHECK(eao_tier_mark_stored(o, &s, nullptr, 1) == 0, "deferred store", t);
+        CHECK(m.unpin(&s, 1) == 0 && eao_tier_unpin(o, &s, 1) == 0, "deferred unpin", t);
+      }
+      deferred.clear();
     }
     for (int64_t i = 0; i < h1; ++i) {
       if (coin(r, 0.8)) {

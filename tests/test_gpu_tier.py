@@ -14,7 +14,7 @@ from gpu_common import Pair
 
 pytestmark = pytest.mark.gpu
 
-STAT_KEYS = ["capacity_slots", "registered", "resident", "pinned", "evictions_total",
+STAT_KEYS = ["capacity_slots", "allocated", "registered", "pinned", "evictions_total",
              "evictions_window", "clock", "active_tasks", "last_pressure", "last_save"]
 
 
@@ -144,4 +144,72 @@ def test_long_stream_with_bounded_history_matches_the_oracle():
             compare(p.tier, ot, f"request {t}")
     st = p.tier.stats()
     assert st["evictions_total"] > 65_536
+    p.close()
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_decisions_between_alloc_and_store(seed):
+    # App. 'Runtime Admission Details': a store allocates its chunks' buffers
+    # before it registers them, so the occupancy o_t counts stored chunks
+    # only.  Requests here allocate, then other requests look up, decide and
+    # publish before the first one's store is issued (on the GPU, through
+    # ea_store_blocks); every decision, report, statistic and metadata image
+    # must equal the oracle's, and a decision must differ from what counting
+    # the pending allocations would give at least once.
+    K = 10
+    p = Pair(64, 2, 16, 1, 32, 2, K, seed=seed)  # 4 KiB slots
+    ot = oracle.Tier(p.oshape, K * p.sizes["slot"])
+    beta = 2 * 2 * 32 * 2
+    kw = dict(kappa=0, block_tokens=16, activity_window=1000, length_window=64,
+              mode=N.EA_ADMIT_CONDITIONED, telemetry=1)
+    pol_p = api.make_policy(beta_rank=beta, **kw)
+    pol_o = oracle.make_policy(beta=beta, **kw)
+    r = W.rng(300 + seed)
+    serial = [0]
+
+    def fresh(nb):
+        keys = np.zeros((nb, 32), np.uint8)
+        for j in range(nb):
+            serial[0] += 1
+            keys[j, :8] = np.frombuffer(serial[0].to_bytes(8, "little"), np.uint8)
+        return keys
+
+    pending = []  # (keys, slots) allocated, store not issued yet
+    differs = 0
+    for t in range(200):
+        keys = fresh(int(r.integers(1, 3)))
+        nb = len(keys)
+        h, hs = p.tier.lookup(keys)
+        oh, ohs = ot.lookup(keys)
+        assert h == oh and np.array_equal(hs, ohs), t
+        st = ot.stats()
+        full_alloc = st["allocated"] * 10**6 >= 950000 * K
+        full_reg = st["registered"] * 10**6 >= 950000 * K
+        save, mask = p.tier.admission(pol_p, 16 * nb, 16 * h, t % 8, t, keys)
+        osave, omask = ot.admission(pol_o, 16 * nb, 16 * h, t % 8, t, keys)
+        assert save == osave and np.array_equal(mask, omask), t
+        after = ot.stats()
+        over = after["working_set"] > K * p.sizes["slot"]
+        differs += int(over and full_alloc and not full_reg and after["evictions_window"] > 0)
+        cnt, slots = p.tier.alloc(keys, mask)
+        ocnt, oslots = ot.alloc(keys, mask)
+        assert cnt == ocnt and np.array_equal(slots, oslots), t
+        got = slots[slots >= 0]
+        if len(got):
+            pending.append(got)
+        rp, ro = p.tier.publish(t, 1000), ot.publish(t, 1000)
+        assert (rp.registered, rp.capacity_slots, rp.evictions) == \
+            (ro.registered, ro.capacity_slots, ro.evictions), t
+        # issue the stores of some earlier allocations, later than their alloc
+        while pending and (len(pending) > 3 or r.random() < 0.3):
+            sl = pending.pop(0)
+            p.tier.store(p.cache, W.distinct(r, 64, len(sl)), sl)
+            ot.mark_stored(sl)
+            p.tier.unpin(sl)
+            ot.unpin(sl)
+        if h:
+            p.tier.unpin(hs)
+            ot.unpin(ohs)
+        compare(p.tier, ot, f"request {t}")
+    assert differs > 0, "no decision fell where pending allocations matter"
     p.close()

@@ -289,7 +289,7 @@ def test_agent_pool_metadata_and_bytes():
             for k in ("state", "pins", "keys", "lru"):
                 assert np.array_equal(a[k], b[k]), (t, k)
         sa, sb = tier.stats(), ot.stats()
-        for k in ("registered", "resident", "evictions_total", "active_tasks", "last_pressure"):
+        for k in ("allocated", "registered", "evictions_total", "active_tasks", "last_pressure"):
             assert sa[k] == sb[k], (t, k)
         evicted = sa["evictions_total"]
     # the run crosses the capacity transition: the tier evicts and declines refills

@@ -236,6 +236,48 @@ def test_decision_holds_for_the_request_and_dedup():
     assert t.stats()["clock"] == 0
 
 
+def test_pending_allocations_are_not_registered():
+    # App. 'Runtime Admission Details': a store allocates the buffers of all
+    # its chunks before it registers them, so an allocation can fail while
+    # fewer chunks are registered than the tier holds; the occupancy o_t of
+    # Eq. 10 is the registered chunks over K_H.  A decision or report that
+    # falls between another request's allocation and its store therefore
+    # sees the allocation's victim gone and the new chunk not yet counted.
+    K = 10
+    t = build_state(full=True, evicting=False, K=K)    # 10 of 10 registered
+    n, s = t.alloc(key_of(5000))                       # evicts one chunk
+    assert n == 1
+    st = t.stats()
+    assert (st["registered"], st["allocated"], st["evictions_total"]) == (K - 1, K, 1)
+    rep = t.publish(0, 10)
+    assert (rep.registered, rep.capacity_slots, rep.evictions) == (K - 1, K, 1)
+    # over the capacity and evicting, but o_t = 0.9 < theta = 0.95: no pressure
+    save, mask = decide(t, oracle.ADMIT_CONDITIONED, 1, over=True, u=3)
+    assert save == 1 and mask.sum() == N
+    # the report taken in between says the same
+    save, _ = t.admission_report(oracle.make_policy(kappa=2, block_tokens=1, beta=BETA,
+                                                    activity_window=10),
+                                 N, N - 3, 4, 1, np.stack([key_of(7000 + i)[0] for i in range(N)]),
+                                 rep, 5)
+    assert save == 1
+    # the pending key is still deduplicated: it is not copied a second time
+    pol = oracle.make_policy(kappa=2, block_tokens=1, beta=BETA, activity_window=10)
+    _, mask = t.admission(pol, 3, 0, 4, 1, np.concatenate([key_of(4999), key_of(5000),
+                                                             key_of(5001)]), decided=1)
+    assert list(mask) == [1, 0, 1]
+    # once its store is issued the chunk is registered: full and evicting
+    t.mark_stored(s)
+    assert t.stats()["registered"] == K and t.publish(1, 10).registered == K
+    save, _ = decide(t, oracle.ADMIT_CONDITIONED, 1, over=True, u=3, now=2)
+    assert save == 0
+    # an abandoned allocation never counted
+    t2 = build_state(full=True, evicting=False, K=K)
+    n, s2 = t2.alloc(key_of(6000))
+    t2.unpin(s2)
+    st = t2.stats()
+    assert (st["registered"], st["allocated"]) == (K - 1, K - 1)
+
+
 # ------------------------------------------------ brute-force tier model
 
 class Model:
@@ -346,6 +388,9 @@ def test_tier_matches_brute_force_model(seed):
         assert list(ex["lru"]) == m.order
         st = t.stats()
         assert st["evictions_total"] == m.evictions
+        # occupancy counts stored chunks only; allocations hold keys too
+        assert st["registered"] == m.state.count(Model.RESIDENT)
+        assert st["allocated"] == K - m.state.count(Model.FREE)
         for s in range(K):
             if m.keys[s] is None:
                 assert not ex["keys"][s].any()
