@@ -1104,25 +1104,39 @@ def run_hash(args):
                              ("batch_65536x256", [256] * 65536, 16)):
         toks, offs = W.sequences(W.SEED_TOKENS, lengths)
         d_tok = torch.as_tensor(toks, device="cuda")
+        d_offs = torch.as_tensor(offs, device="cuda")
+        d_koffs = torch.empty(len(offs), dtype=torch.int64, device="cuda")
         nk = int(sum(n // b for n in lengths))
         d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
-        call = lambda: api.hash_blocks_device(d_tok, offs, b, d_keys, stream=cur)  # noqa: E731
-        # untimed calls for 0.3 s first: a GPU left idle or lightly loaded runs
-        # at lower clocks and takes a while to rise (successive single chains
-        # measured 2.8 down to 2.1 us per key)
-        t_warm = time.perf_counter() + 0.3
-        while time.perf_counter() < t_warm:
-            call()
-            torch.cuda.synchronize()
-        ms = event_ms(torch, call, cur, 20, warm=2)
         host, _ = api.hash_blocks(toks, offs, b)
-        assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32))
-        out[name] = {"ms": round(ms, 4), "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
+        # tokens and offsets resident in HBM (the key offsets from the scan
+        # kernel), and for comparison host offsets uploaded by each call
+        calls = {"device_offsets": lambda: api.hash_blocks_device_offsets(  # noqa: E731
+                     d_tok, d_offs, b, d_keys, d_koffs, stream=cur),
+                 "host_offsets": lambda: api.hash_blocks_device(  # noqa: E731
+                     d_tok, offs, b, d_keys, stream=cur)}
+        res = {}
+        for kind, call in calls.items():
+            # untimed calls for 0.3 s first: a GPU left idle or lightly loaded
+            # runs at lower clocks and takes a while to rise (successive single
+            # chains measured 2.8 down to 2.1 us per key)
+            t_warm = time.perf_counter() + 0.3
+            while time.perf_counter() < t_warm:
+                call()
+                torch.cuda.synchronize()
+            d_keys.zero_()
+            ms = event_ms(torch, call, cur, 20, warm=2)
+            assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32)), (name, kind)
+            res[kind] = ms
+        ms = res["device_offsets"]
+        out[name] = {"ms": round(ms, 4), "ms_host_offsets": round(res["host_offsets"], 4),
+                     "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
                      "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1)}
         log(f"hash {name}: {out[name]}")
     b = out["batch_65536x256"]
     achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
-    roof = {"bound": "alu", "kernel": "sha256_midstates + sha256_chain_lane (65,536 x 256 tokens)",
+    roof = {"bound": "alu", "kernel": "hash_key_offsets + sha256_midstates + sha256_chain_lane "
+                                      "(65,536 x 256 tokens, offsets in HBM)",
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
             "traffic": None}

@@ -177,11 +177,14 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
                    const uint8_t *parents, uint8_t *keys_out,
                    int64_t *key_offsets_out, hipStream_t stream);
 
-/* The same keys from DEVICE-resident tokens: d_tokens (device int32),
- * seq_offsets (HOST int64[n_seqs+1]), d_parents (device uint8[n_seqs][32] or
- * NULL), d_keys_out (device uint8[...][32]) and key_offsets_out (HOST
- * int64[n_seqs+1], filled before return).  Asynchronous: the keys are valid
- * once the work enqueued on `stream` completes.
+/* The same keys from DEVICE-resident tokens: d_tokens (device int32, n_tokens
+ * of them), seq_offsets (HOST int64[n_seqs+1]; seq_offsets[n_seqs] <=
+ * n_tokens), d_parents (device uint8[n_seqs][32] or NULL), d_keys_out
+ * (device uint8[keys_capacity][32], 16-byte aligned) and key_offsets_out
+ * (HOST int64[n_seqs+1], filled before return).  EA_EINVAL, nothing
+ * launched, when the offsets run past n_tokens or the keys would not fit in
+ * keys_capacity.  Asynchronous: the keys are valid once the work enqueued on
+ * `stream` completes.
  *
  * Both entry points run the chained compression in one of three forms (the
  * keys are the same): a workgroup of two waves per sequence while there is
@@ -189,11 +192,31 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  * sequences per SIMD, one lane per sequence beyond; EA_HASH_CHAIN=split,
  * pair or lane forces a form.
  * Sequence and key offsets travel to the kernels as 32-bit values when all
- * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter. */
-int ea_hash_blocks_device(const int32_t *d_tokens, const int64_t *seq_offsets,
-                          int32_t n_seqs, int32_t block_tokens,
-                          const uint8_t *d_parents, uint8_t *d_keys_out,
+ * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter.
+ * Buffers are kept per (device, stream): calls on different streams run
+ * concurrently, from any threads. */
+int ea_hash_blocks_device(const int32_t *d_tokens, int64_t n_tokens,
+                          const int64_t *seq_offsets, int32_t n_seqs,
+                          int32_t block_tokens, const uint8_t *d_parents,
+                          uint8_t *d_keys_out, int64_t keys_capacity,
                           int64_t *key_offsets_out, hipStream_t stream);
+
+/* The same with the sequence offsets on the DEVICE too, so that nothing
+ * crosses the host link: d_seq_offsets (device int64[n_seqs+1], 8-byte
+ * aligned) and d_key_offsets_out (device int64[n_seqs+1]).  A kernel derives
+ * the key offsets on the device (key_offsets[s] = sum over earlier
+ * sequences of floor(len/b)).  The host cannot see the offsets, so
+ * malformed ones (a negative start, a decrease, an end past n_tokens) or
+ * more keys than keys_capacity are reported on the device: the call then
+ * sets d_key_offsets_out[0] = -1 and writes no key.  On success
+ * d_key_offsets_out[0] = 0 and d_key_offsets_out[n_seqs] is the key count.
+ * Keys need the first lookup of a request at once (App. "Runtime Admission
+ * Details"); this form suits callers whose prompts already sit in HBM. */
+int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_tokens,
+                                  const int64_t *d_seq_offsets, int32_t n_seqs,
+                                  int32_t block_tokens, const uint8_t *d_parents,
+                                  uint8_t *d_keys_out, int64_t keys_capacity,
+                                  int64_t *d_key_offsets_out, hipStream_t stream);
 
 /* ------------------------------------------------- lookup and admission */
 
@@ -372,8 +395,11 @@ int ea_tier_alloc(ea_tier *tier, const uint8_t *keys, const uint8_t *mask,
                   int64_t n, int64_t *slots_out, int64_t *allocated);
 
 /* Drop one pin from each listed slot (pins from ea_tier_lookup or
- * ea_tier_alloc).  A slot allocated but never stored whose last pin goes away
- * is released.  EA_EINVAL (and no change) if any slot would drop below zero. */
+ * ea_tier_alloc): the end of a pending lookup or transfer, after which App.
+ * "Runtime Admission Details" lets eviction take the chunk again.  A slot
+ * allocated but never stored whose last pin goes away is released (the
+ * paper does not say what happens to an abandoned allocation).  EA_EINVAL
+ * (and no change) if any slot would drop below zero. */
 int ea_tier_unpin(ea_tier *tier, const int64_t *slots, int64_t n);
 
 typedef struct {
@@ -432,25 +458,31 @@ int ea_store_blocks(ea_cache *cache, ea_tier *tier, const int32_t *block_ids,
 int ea_load_blocks(ea_tier *tier, ea_cache *cache, const int64_t *host_slots,
                    const int32_t *dst_pages, int32_t n, hipStream_t stream);
 
-/* Layer-pipelined load: the same end state as ea_load_blocks, issued one
- * layer at a time on copy_stream; after layer l's copy the library records
- * layer_done[l] (caller-created events, num_layers of them) on copy_stream,
- * so a consumer stream can hipStreamWaitEvent(layer_done[l]) and use layer l
- * of every destination page while later layers are still in flight. */
+/* Layer-pipelined load (not in the paper, which restores a prefix as one
+ * transfer; it gives the same end state as ea_load_blocks, the restore of
+ * Eq. 2, issued one layer at a time so that attention over layer l can
+ * start before later layers arrive): on copy_stream, after layer l's copy
+ * the library records layer_done[l] (caller-created events; n_events must
+ * equal the cache's num_layers, else EA_EINVAL), so a consumer stream can
+ * hipStreamWaitEvent(layer_done[l]) and use layer l of every destination
+ * page while later layers are still in flight. */
 int ea_load_blocks_layered(ea_tier *tier, ea_cache *cache,
                            const int64_t *host_slots, const int32_t *dst_pages,
                            int32_t n, hipStream_t copy_stream,
-                           hipEvent_t *layer_done);
+                           hipEvent_t *layer_done, int32_t n_events);
 
 /* Paged gather / scatter between the cache and a DEVICE buffer in the slot
- * layout of one page per slot (the HBM half of a staged transfer, also
- * usable on its own):
+ * layout of one page per slot.  Not in the paper: they are the HBM half of
+ * the staged transfer plan (the GPU-side copy of "KV copied from GPU to
+ * host and back", section 2), also usable on their own.
  * gather writes page block_ids[i] (with scales) to d_dst + i*slot_bytes;
  * scatter writes d_src + i*slot_bytes into page dst_pages[i] (destinations
- * distinct).  slot_bytes is that of a tier of the same shape with C = 1. */
+ * distinct).  slot_bytes is that of a tier of the same shape with C = 1;
+ * dst_bytes / src_bytes give the device buffer's size, which must hold n
+ * slots (EA_EINVAL otherwise, nothing launched). */
 int ea_gather_blocks(ea_cache *cache, const int32_t *block_ids, int32_t n,
-                     void *d_dst, hipStream_t stream);
-int ea_scatter_blocks(ea_cache *cache, const void *d_src,
+                     void *d_dst, int64_t dst_bytes, hipStream_t stream);
+int ea_scatter_blocks(ea_cache *cache, const void *d_src, int64_t src_bytes,
                       const int32_t *dst_pages, int32_t n, hipStream_t stream);
 
 /* How stores and loads cross the host link:
@@ -464,7 +496,9 @@ enum { EA_DIR_STORE = 0, EA_DIR_LOAD = 1, EA_DIR_BOTH = 2 };
 int ea_tier_set_plan(ea_tier *tier, int direction, int plan);
 int ea_tier_get_plan(const ea_tier *tier, int direction, int *plan);
 
-/* Pinned-copy peak of the host link: hipMemcpyAsync of `bytes` contiguous
+/* Pinned-copy peak of the host link (not in the paper, which quotes the
+ * nominal PCIe rate per direction, App. "Offload Cost and Prefix-Survival
+ * Model"; here it is the denominator of the host-link fractions): hipMemcpyAsync of `bytes` contiguous
  * bytes between d_buf (device, >= bytes; for EA_DIR_BOTH >= 2*bytes) and the
  * tier's pinned memory, best of `reps`, in GB/s (1e9 bytes/s).  direction:
  * EA_DIR_STORE (device to host), EA_DIR_LOAD (host to device) or EA_DIR_BOTH

@@ -90,7 +90,8 @@ SIGNATURES = {
     "ea_tier_destroy": (_INT, [_P]),
     "ea_tier_get_info": (_INT, [_P, _P]),
     "ea_hash_blocks": (_INT, [_P, _P, _I32, _I32, _P, _P, _P, _P]),
-    "ea_hash_blocks_device": (_INT, [_P, _P, _I32, _I32, _P, _P, _P, _P]),
+    "ea_hash_blocks_device": (_INT, [_P, _I64, _P, _I32, _I32, _P, _P, _I64, _P, _P]),
+    "ea_hash_blocks_device_offsets": (_INT, [_P, _I64, _P, _I32, _I32, _P, _P, _I64, _P, _P]),
     "ea_tier_lookup": (_INT, [_P, _P, _I64, _P, _P]),
     "ea_admission_fill": (_INT, [_P, _P, _P, _P, _I64, _P, _P]),
     "ea_admission_fill_report": (_INT, [_P, _P, _P, _P, _I64, _P, _I64, _P, _P]),
@@ -106,9 +107,9 @@ SIGNATURES = {
     "ea_tier_export": (_INT, [_P, _P, _P, _P, _P, _P]),
     "ea_store_blocks": (_INT, [_P, _P, _P, _P, _P, _I32, _P]),
     "ea_load_blocks": (_INT, [_P, _P, _P, _P, _I32, _P]),
-    "ea_load_blocks_layered": (_INT, [_P, _P, _P, _P, _I32, _P, _P]),
-    "ea_gather_blocks": (_INT, [_P, _P, _I32, _P, _P]),
-    "ea_scatter_blocks": (_INT, [_P, _P, _P, _I32, _P]),
+    "ea_load_blocks_layered": (_INT, [_P, _P, _P, _P, _I32, _P, _P, _I32]),
+    "ea_gather_blocks": (_INT, [_P, _P, _I32, _P, _I64, _P]),
+    "ea_scatter_blocks": (_INT, [_P, _P, _I64, _P, _I32, _P]),
     "ea_tier_set_plan": (_INT, [_P, _INT, _INT]),
     "ea_tier_get_plan": (_INT, [_P, _INT, _P]),
     "ea_peak_probe": (_INT, [_P, _P, _I64, _INT, _INT, _P]),

@@ -28,6 +28,19 @@ def _u8(a):
     return np.ascontiguousarray(a, dtype=np.uint8)
 
 
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def _check_offsets(offs, n_tokens):
+    if len(offs) < 1:
+        raise ValueError("seq_offsets needs at least one entry")
+    if len(offs) > 1 and (offs[0] < 0 or (np.diff(offs) < 0).any()):
+        raise ValueError("seq_offsets must be non-decreasing from >= 0")
+    if offs[-1] > n_tokens:
+        raise ValueError(f"seq_offsets end at {offs[-1]}, past the {n_tokens} tokens given")
+
+
 def current_stream():
     import torch
     return torch.cuda.current_stream().cuda_stream
@@ -63,6 +76,9 @@ class Cache:
                                 head_dim, elem_bytes)
         self.num_pages, self.num_layers = num_pages, num_layers
         self.piece_bytes = piece
+        # one page per slot: the layers' pieces, then the scale trailer
+        trailer = (num_layers * 8 + 255) // 256 * 256 if scales is not None else 0
+        self.slot_bytes = num_layers * piece + trailer
         self._h = C.c_void_p()
         N.check("ea_cache_create", lib.ea_cache_create(C.byref(self.desc), C.byref(self._h)))
 
@@ -81,15 +97,24 @@ class Cache:
         except Exception:
             pass
 
+    def _slots_fit(self, buf, n, what):
+        if not buf.is_cuda:
+            raise ValueError(f"{what} must be a device tensor")
+        if _nbytes(buf) < n * self.slot_bytes:
+            raise ValueError(f"{what} holds {_nbytes(buf)} bytes, {n} slots need "
+                             f"{n * self.slot_bytes}")
+
     def gather(self, block_ids, dst, stream=None):
         ids = _i32(block_ids)
+        self._slots_fit(dst, len(ids), "dst")
         N.check("ea_gather_blocks", N.load().ea_gather_blocks(
-            self._h, _ptr(ids), len(ids), dst.data_ptr(), _stream(stream)))
+            self._h, _ptr(ids), len(ids), dst.data_ptr(), _nbytes(dst), _stream(stream)))
 
     def scatter(self, src, dst_pages, stream=None):
         d = _i32(dst_pages)
+        self._slots_fit(src, len(d), "src")
         N.check("ea_scatter_blocks", N.load().ea_scatter_blocks(
-            self._h, src.data_ptr(), _ptr(d), len(d), _stream(stream)))
+            self._h, src.data_ptr(), _nbytes(src), _ptr(d), len(d), _stream(stream)))
 
 
 def make_policy(kappa, block_tokens, beta_rank, theta_ppm=950000, activity_window=64,
@@ -235,13 +260,16 @@ class Tier:
         """layer_events: torch.cuda.Event objects, one per layer."""
         slots, dst = _i64(host_slots), _i32(dst_pages)
         self._pages_per_slot(dst, slots)
+        if len(layer_events) != cache.num_layers:
+            raise ValueError(f"need one event per layer ({cache.num_layers}), "
+                             f"got {len(layer_events)}")
         for e in layer_events:
             if not e.cuda_event:  # torch creates the HIP event at its first record
                 e.record(copy_stream)
         evs = (C.c_void_p * len(layer_events))(*[e.cuda_event for e in layer_events])
         N.check("ea_load_blocks_layered", N.load().ea_load_blocks_layered(
             self._h, cache.handle, _ptr(slots), _ptr(dst), len(slots),
-            _stream(copy_stream), evs))
+            _stream(copy_stream), evs, len(layer_events)))
 
     def peak_probe(self, dev_buf, nbytes, direction, reps=10):
         g = C.c_double()
@@ -254,10 +282,13 @@ def hash_blocks(tokens, seq_offsets, block_tokens, parents=None, stream=None):
     """Chained keys of every full block, computed on the GPU.  Host in, host
     out; returns (keys uint8 [K, 32], key_offsets int64 [n_seqs + 1])."""
     tokens, offs = _i32(tokens), _i64(seq_offsets)
+    _check_offsets(offs, len(tokens))
     n_seqs = len(offs) - 1
     total = int(np.sum(np.diff(offs) // block_tokens)) if n_seqs > 0 and block_tokens > 0 else 0
     keys = np.zeros((max(total, 1), 32), np.uint8)
     koffs = np.zeros(n_seqs + 1, np.int64)
+    if parents is not None and _u8(parents).size != 32 * n_seqs:
+        raise ValueError("parents must hold 32 bytes per sequence")
     par = None if parents is None else _u8(parents).reshape(n_seqs, 32)
     N.check("ea_hash_blocks", N.load().ea_hash_blocks(
         _ptr(tokens) if tokens.size else None, _ptr(offs), n_seqs, block_tokens,
@@ -269,13 +300,50 @@ def hash_blocks_device(d_tokens, seq_offsets, block_tokens, d_keys_out, d_parent
                        stream=None):
     """Asynchronous variant on device tensors; returns key_offsets."""
     offs = _i64(seq_offsets)
+    _check_device_buffers(d_tokens, d_keys_out, d_parents, len(offs) - 1)
+    _check_offsets(offs, d_tokens.numel())
     n_seqs = len(offs) - 1
+    total = int(np.sum(np.diff(offs) // block_tokens)) if n_seqs > 0 and block_tokens > 0 else 0
+    if _nbytes(d_keys_out) < 32 * total:
+        raise ValueError(f"d_keys_out holds {_nbytes(d_keys_out)} bytes, {total} keys need "
+                         f"{32 * total}")
     koffs = np.empty(n_seqs + 1, np.int64)
     N.check("ea_hash_blocks_device", N.load().ea_hash_blocks_device(
-        d_tokens.data_ptr(), _ptr(offs), n_seqs, block_tokens,
+        d_tokens.data_ptr(), d_tokens.numel(), _ptr(offs), n_seqs, block_tokens,
         None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),
-        _ptr(koffs), _stream(stream)))
+        _nbytes(d_keys_out) // 32, _ptr(koffs), _stream(stream)))
     return koffs
+
+
+def hash_blocks_device_offsets(d_tokens, d_seq_offsets, block_tokens, d_keys_out,
+                               d_key_offsets_out, d_parents=None, stream=None):
+    """Fully asynchronous variant: sequence offsets (int64 [n_seqs + 1]) and
+    key offsets (int64 [n_seqs + 1]) are device tensors too; on the device,
+    malformed offsets or too many keys leave d_key_offsets_out[0] = -1."""
+    import torch
+    n_seqs = d_seq_offsets.numel() - 1
+    _check_device_buffers(d_tokens, d_keys_out, d_parents, n_seqs)
+    for t, what in ((d_seq_offsets, "d_seq_offsets"), (d_key_offsets_out, "d_key_offsets_out")):
+        if not t.is_cuda or t.dtype != torch.int64 or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous int64 device tensor")
+    if n_seqs < 0 or d_key_offsets_out.numel() < n_seqs + 1:
+        raise ValueError("need n_seqs + 1 entries in both offset tensors")
+    N.check("ea_hash_blocks_device_offsets", N.load().ea_hash_blocks_device_offsets(
+        d_tokens.data_ptr(), d_tokens.numel(), d_seq_offsets.data_ptr(), n_seqs, block_tokens,
+        None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),
+        _nbytes(d_keys_out) // 32, d_key_offsets_out.data_ptr(), _stream(stream)))
+
+
+def _check_device_buffers(d_tokens, d_keys_out, d_parents, n_seqs):
+    import torch
+    if not (d_tokens.is_cuda and d_keys_out.is_cuda):
+        raise ValueError("tokens and keys must be device tensors")
+    if d_tokens.dtype != torch.int32 or not d_tokens.is_contiguous():
+        raise ValueError("d_tokens must be a contiguous int32 tensor")
+    if not d_keys_out.is_contiguous():
+        raise ValueError("d_keys_out must be contiguous")
+    if d_parents is not None and (not d_parents.is_cuda or _nbytes(d_parents) < 32 * n_seqs):
+        raise ValueError("d_parents must be a device tensor of 32 bytes per sequence")
 
 
 # ------------------------------------------- reuse-distance capacity tool

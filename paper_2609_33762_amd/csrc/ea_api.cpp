@@ -903,9 +903,9 @@ int ea_load_blocks(ea_tier *t, ea_cache *c, const int64_t *host_slots,
 
 int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
                            const int32_t *dst_pages, int32_t n, hipStream_t copy_stream,
-                           hipEvent_t *layer_done) {
+                           hipEvent_t *layer_done, int32_t n_events) {
   try {
-    if (!layer_done) return EA_EINVAL;
+    if (!layer_done || !c || n_events != c->d.num_layers) return EA_EINVAL;
     EA_TRY(validate_load(t, c, host_slots, dst_pages, n));
     for (int32_t l = 0; l < c->d.num_layers; ++l)
       if (!layer_done[l]) return EA_EINVAL;
@@ -959,11 +959,12 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
 // ------------------------------------------------- gather / scatter (HBM)
 
 int ea_gather_blocks(ea_cache *c, const int32_t *block_ids, int32_t n, void *d_dst,
-                     hipStream_t stream) {
+                     int64_t dst_bytes, hipStream_t stream) {
   try {
-    if (!c || n < 0) return EA_EINVAL;
+    if (!c || n < 0 || dst_bytes < 0) return EA_EINVAL;
     if (n == 0) return EA_OK;
     if (!block_ids || !d_dst || !aligned(d_dst, 16)) return EA_EINVAL;
+    if (dst_bytes / c->slot < n) return EA_EINVAL;  // n slots must fit
     for (int32_t i = 0; i < n; ++i)
       if (block_ids[i] < 0 || block_ids[i] >= c->d.num_pages) return EA_EINVAL;
     DeviceScope ds(c->device);
@@ -978,12 +979,13 @@ int ea_gather_blocks(ea_cache *c, const int32_t *block_ids, int32_t n, void *d_d
   }
 }
 
-int ea_scatter_blocks(ea_cache *c, const void *d_src, const int32_t *dst_pages, int32_t n,
-                      hipStream_t stream) {
+int ea_scatter_blocks(ea_cache *c, const void *d_src, int64_t src_bytes,
+                      const int32_t *dst_pages, int32_t n, hipStream_t stream) {
   try {
-    if (!c || n < 0) return EA_EINVAL;
+    if (!c || n < 0 || src_bytes < 0) return EA_EINVAL;
     if (n == 0) return EA_OK;
     if (!dst_pages || !d_src || !aligned(d_src, 16)) return EA_EINVAL;
+    if (src_bytes / c->slot < n) return EA_EINVAL;  // n slots must be there
     for (int32_t i = 0; i < n; ++i)
       if (dst_pages[i] < 0 || dst_pages[i] >= c->d.num_pages) return EA_EINVAL;
     if (!all_distinct(dst_pages, n)) return EA_EINVAL;

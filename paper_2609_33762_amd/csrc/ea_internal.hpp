@@ -92,4 +92,19 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
                                int32_t n_seqs, int32_t block_tokens, const uint8_t *d_parents,
                                uint8_t *d_keys, hipStream_t stream);
 
+// Key offsets from device sequence offsets d_seq_offsets [n_seqs+1], in two
+// kernels: d_key_offsets_out [n_seqs+1] (int64) and the hash kernels'
+// copies d_koff [n_seqs+1], d_toff [n_seqs] (int32 unless wide).  On
+// invalid offsets, or more than keys_cap keys, d_key_offsets_out[0] = -1
+// and d_koff is all zero (the hash kernels then write nothing).  d_state:
+// hash_scan_state_bytes(n_seqs) bytes of device memory whose first 8 bytes
+// are zero before the call (the kernels leave them zero again).
+hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
+                                   int64_t n_tokens, int32_t block_tokens, int64_t keys_cap,
+                                   int64_t *d_key_offsets_out, bool wide, void *d_koff,
+                                   void *d_toff, void *d_state, hipStream_t stream);
+int64_t hash_scan_groups(int32_t n_seqs);
+inline int64_t hash_scan_state_bytes(int32_t n_seqs) { return 64 + 16 * hash_scan_groups(n_seqs); }
+
+
 }  // namespace ea

@@ -31,6 +31,7 @@
 // SIMD) take 83 us against 72 us.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdlib>
 #include <cstring>
@@ -137,7 +138,9 @@ __global__ __launch_bounds__(256) void sha256_midstates(
     const Off *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys,
     int32_t block_tokens, uint32_t *__restrict__ mid) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= n_keys) return;
+  // n_keys bounds the grid; the offsets hold the keys there are (fewer when
+  // the offsets were derived on the device from a bound)
+  if (g >= n_keys || g >= (int64_t)key_off[n_seqs]) return;
   const int32_t s = owner(key_off, n_seqs, g);
   const int64_t i = g - (int64_t)key_off[s];
   const int32_t *tok = tokens + (int64_t)tok_off[s] + i * block_tokens;
@@ -305,7 +308,7 @@ __global__ __launch_bounds__(128) void sha256_midstates_split(
     uint32_t *__restrict__ mid) {
   __shared__ uint4 wk4[2][16];  // W_t + K_t of two blocks
   const int64_t g = blockIdx.x;
-  if (g >= n_keys) return;  // the whole workgroup
+  if (g >= n_keys || g >= (int64_t)key_off[n_seqs]) return;  // the whole workgroup
   const bool rounds_wave = threadIdx.x < 64;
   const int lane = threadIdx.x & 63;
   const bool e_side = lane & 1;
@@ -547,6 +550,174 @@ __global__ __launch_bounds__(256) void sha256_chain_lane(
   }
 }
 
+// Key offsets from device-resident sequence offsets, in two kernels.  A
+// workgroup owns kScanSeqs consecutive sequences, kScanRun per thread
+// (thread t the t-th run), so its loads cover one contiguous range.
+//   hash_offsets_partials: each workgroup counts the full blocks of its
+//     sequences and checks them; the last workgroup to finish (a ticket
+//     counter, reset by that workgroup) turns the per-workgroup totals into
+//     exclusive prefixes, the grand total and an error flag.
+//   hash_offsets_write: each workgroup scans its own counts from its prefix
+//     and writes key_off_out (int64, the caller's) and the kernels' copies
+//     koff / toff in Off.
+// Invalid offsets (a negative start, a decrease, an end past n_tokens) or
+// more keys than keys_cap: key_off_out[0] = -1 and koff all zero, so the
+// hash kernels that follow write nothing.
+constexpr int kScanThreads = 256;
+constexpr int kScanRun = 8;
+constexpr int64_t kScanSeqs = (int64_t)kScanThreads * kScanRun;
+
+// Scan state in device memory: [0] ticket counter (zero between calls),
+// [1] grand total, [2] error flag, then per workgroup its total and, after
+// the last workgroup's pass, its exclusive prefix.
+struct ScanState {
+  uint64_t *ticket;
+  int64_t *total;
+  int64_t *bad;
+  int64_t *part;    // [groups]
+  int64_t *prefix;  // [groups]
+};
+
+__device__ __forceinline__ int64_t full_blocks(int64_t len, int32_t block_tokens, int32_t shift) {
+  return shift >= 0 ? (len >> shift) : len / block_tokens;
+}
+
+// This thread's run: sequences [s0, s1), their offsets loaded together.
+struct Run {
+  int64_t s0, s1;
+  int64_t off[kScanRun + 1];
+};
+
+__device__ __forceinline__ void load_run(const int64_t *seq_off, int32_t n_seqs, Run &r) {
+  r.s0 = min((int64_t)blockIdx.x * kScanSeqs + (int64_t)threadIdx.x * kScanRun, (int64_t)n_seqs);
+  r.s1 = min(r.s0 + kScanRun, (int64_t)n_seqs);
+#pragma unroll
+  for (int j = 0; j <= kScanRun; ++j) r.off[j] = r.s0 + j <= r.s1 ? seq_off[r.s0 + j] : 0;
+}
+
+// Sum over the workgroup of v (every thread returns it).
+__device__ __forceinline__ int64_t group_sum(int64_t v, int64_t *lds) {
+  lds[threadIdx.x] = v;
+  __syncthreads();
+  for (int d = kScanThreads / 2; d > 0; d >>= 1) {
+    if ((int)threadIdx.x < d) lds[threadIdx.x] += lds[threadIdx.x + d];
+    __syncthreads();
+  }
+  const int64_t r = lds[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kScanThreads) void hash_offsets_partials(
+    const int64_t *__restrict__ seq_off, int32_t n_seqs, int64_t n_tokens, int32_t block_tokens,
+    int32_t shift, ScanState st) {
+  __shared__ int64_t lds[kScanThreads];
+  __shared__ bool last;
+  Run r;
+  load_run(seq_off, n_seqs, r);
+  bool ok = !(blockIdx.x == 0 && threadIdx.x == 0) || (r.off[0] >= 0 && r.off[0] <= n_tokens);
+  int64_t count = 0;
+#pragma unroll
+  for (int j = 0; j < kScanRun; ++j)
+    if (r.s0 + j < r.s1) {
+      const int64_t a = r.off[j], e = r.off[j + 1];
+      ok = ok && e >= a && e <= n_tokens;
+      count += ok ? full_blocks(e - a, block_tokens, shift) : 0;
+    }
+  const int64_t sum = group_sum(count, lds);
+  const int64_t nbad = group_sum(ok ? 0 : 1, lds);
+  if (threadIdx.x == 0) {
+    st.part[blockIdx.x] = nbad ? -1 : sum;
+    // publish this workgroup's total, then take a ticket; the last ticket
+    // sees every total (release / acquire at device scope)
+    const uint64_t t = __hip_atomic_fetch_add(st.ticket, 1ull, __ATOMIC_ACQ_REL,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+    last = t == gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  // the last workgroup: exclusive prefixes of the totals, in order
+  const int64_t groups = gridDim.x;
+  const int64_t per = (groups + kScanThreads - 1) / kScanThreads;
+  const int64_t g0 = min((int64_t)threadIdx.x * per, groups), g1 = min(g0 + per, groups);
+  int64_t mine = 0, bad = 0;
+  for (int64_t g = g0; g < g1; ++g) {
+    const int64_t v = __hip_atomic_load(st.part + g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    bad |= v < 0;
+    mine += v < 0 ? 0 : v;
+  }
+  lds[threadIdx.x] = mine;
+  __syncthreads();
+  for (int d = 1; d < kScanThreads; d <<= 1) {  // inclusive scan of the thread sums
+    const int64_t add = (int)threadIdx.x >= d ? lds[threadIdx.x - d] : 0;
+    __syncthreads();
+    lds[threadIdx.x] += add;
+    __syncthreads();
+  }
+  int64_t run = lds[threadIdx.x] - mine;
+  const int64_t total = lds[kScanThreads - 1];
+  for (int64_t g = g0; g < g1; ++g) {
+    st.prefix[g] = run;
+    const int64_t v = __hip_atomic_load(st.part + g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    run += v < 0 ? 0 : v;
+  }
+  __syncthreads();  // every thread has read the scan before lds is reused
+  const int64_t any_bad = group_sum(bad, lds);
+  if (threadIdx.x == kScanThreads - 1) {
+    *st.total = total;
+    *st.bad = any_bad;
+    // ready for the next call (stream order keeps calls apart)
+    __hip_atomic_store(st.ticket, 0ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+template <typename Off>
+__global__ __launch_bounds__(kScanThreads) void hash_offsets_write(
+    const int64_t *__restrict__ seq_off, int32_t n_seqs, int32_t block_tokens, int32_t shift,
+    int64_t keys_cap, ScanState st, int64_t *__restrict__ key_off_out, Off *__restrict__ koff,
+    Off *__restrict__ toff) {
+  __shared__ int64_t lds[kScanThreads];
+  Run r;
+  load_run(seq_off, n_seqs, r);
+  const int64_t total = *st.total;
+  const bool failed = *st.bad != 0 || total > keys_cap;
+  const bool tail = blockIdx.x == gridDim.x - 1 && threadIdx.x == kScanThreads - 1;
+  if (failed) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) key_off_out[0] = -1;
+    for (int64_t s = r.s0; s < r.s1; ++s) koff[s] = 0;
+    if (tail) koff[n_seqs] = 0;
+    return;
+  }
+  int64_t cnt[kScanRun];
+  int64_t mine = 0;
+#pragma unroll
+  for (int j = 0; j < kScanRun; ++j) {
+    cnt[j] = r.s0 + j < r.s1 ? full_blocks(r.off[j + 1] - r.off[j], block_tokens, shift) : 0;
+    mine += cnt[j];
+  }
+  lds[threadIdx.x] = mine;
+  __syncthreads();
+  for (int d = 1; d < kScanThreads; d <<= 1) {
+    const int64_t add = (int)threadIdx.x >= d ? lds[threadIdx.x - d] : 0;
+    __syncthreads();
+    lds[threadIdx.x] += add;
+    __syncthreads();
+  }
+  int64_t run = st.prefix[blockIdx.x] + lds[threadIdx.x] - mine;
+#pragma unroll
+  for (int j = 0; j < kScanRun; ++j)
+    if (r.s0 + j < r.s1) {
+      key_off_out[r.s0 + j] = run;
+      koff[r.s0 + j] = (Off)run;
+      toff[r.s0 + j] = (Off)r.off[j];
+      run += cnt[j];
+    }
+  if (tail) {
+    key_off_out[n_seqs] = total;
+    koff[n_seqs] = (Off)total;
+  }
+}
+
 // The split forms launch one workgroup per sequence or key; forcing them on
 // more than this many falls back to the other forms.
 constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
@@ -666,6 +837,36 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   else
     launch_chain(form, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
                  d_parents, d_keys, stream);
+  return hipGetLastError();
+}
+
+int64_t hash_scan_groups(int32_t n_seqs) {
+  return std::max<int64_t>(1, ((int64_t)n_seqs + kScanSeqs - 1) / kScanSeqs);
+}
+
+hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
+                                   int64_t n_tokens, int32_t block_tokens, int64_t keys_cap,
+                                   int64_t *d_key_offsets_out, bool wide, void *d_koff,
+                                   void *d_toff, void *d_state, hipStream_t stream) {
+  const int shift = (block_tokens & (block_tokens - 1)) == 0 ? __builtin_ctz(block_tokens) : -1;
+  const int64_t groups = hash_scan_groups(n_seqs);
+  uint8_t *base = static_cast<uint8_t *>(d_state);
+  ScanState st{reinterpret_cast<uint64_t *>(base), reinterpret_cast<int64_t *>(base + 8),
+               reinterpret_cast<int64_t *>(base + 16), reinterpret_cast<int64_t *>(base + 64),
+               reinterpret_cast<int64_t *>(base + 64) + groups};
+  (void)hipGetLastError();  // report this launch's status only
+  hipLaunchKernelGGL(hash_offsets_partials, dim3((unsigned)groups), dim3(kScanThreads), 0, stream,
+                     d_seq_offsets, n_seqs, n_tokens, block_tokens, shift, st);
+  if (wide)
+    hipLaunchKernelGGL(hash_offsets_write<int64_t>, dim3((unsigned)groups), dim3(kScanThreads), 0,
+                       stream, d_seq_offsets, n_seqs, block_tokens, shift, keys_cap, st,
+                       d_key_offsets_out, static_cast<int64_t *>(d_koff),
+                       static_cast<int64_t *>(d_toff));
+  else
+    hipLaunchKernelGGL(hash_offsets_write<int32_t>, dim3((unsigned)groups), dim3(kScanThreads), 0,
+                       stream, d_seq_offsets, n_seqs, block_tokens, shift, keys_cap, st,
+                       d_key_offsets_out, static_cast<int32_t *>(d_koff),
+                       static_cast<int32_t *>(d_toff));
   return hipGetLastError();
 }
 

@@ -74,3 +74,86 @@ class Pair:
     def close(self):
         self.tier.close()
         self.cache.close()
+
+
+# ----------------------------------------------- full-size image checks
+
+POISON = 0xC3
+
+
+def poison_tier(host, value=POISON):
+    """Fill every host slot with one byte value (viewed as 64-bit words)."""
+    host.reshape(-1).view(np.uint64)[:] = np.uint64(int.from_bytes(bytes([value]) * 8, "little"))
+
+
+def assert_poisoned_except(host, written, value=POISON, chunk=256):
+    """Every slot not listed in `written` still holds the poison bytes."""
+    word = np.uint64(int.from_bytes(bytes([value]) * 8, "little"))
+    keep = np.setdiff1d(np.arange(host.shape[0]), np.asarray(written))
+    for i in range(0, len(keep), chunk):
+        idx = keep[i:i + chunk]
+        lo, hi = idx[0], idx[-1] + 1
+        if hi - lo == len(idx):   # a contiguous run: compare in place
+            ok = (host[lo:hi].reshape(-1).view(np.uint64) == word).all()
+        else:
+            ok = (host[idx].reshape(-1).view(np.uint64) == word).all()
+        assert ok, f"an unwritten slot among {idx[:4]}... lost its poison"
+
+
+def pages_to_host(torch, kv3, pages, chunk=512):
+    """[L][n][piece] host copy of the listed pages, in the listed order."""
+    L, _, piece = kv3.shape
+    pages = np.asarray(pages)
+    out = np.empty((L, len(pages), piece), np.uint8)
+    for i in range(0, len(pages), chunk):
+        idx = torch.as_tensor(pages[i:i + chunk], device=kv3.device, dtype=torch.int64)
+        out[:, i:i + len(idx)] = kv3[:, idx].cpu().numpy()
+    return out
+
+
+def oracle_mini_shape(sh, n):
+    return oracle.make_shape(n, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                             sh.elem_bytes, sh.has_scales)
+
+
+def oracle_slots(sh, mini, mini_scales=None):
+    """The oracle's store of pages 0..n-1 of a [L][n][piece] host cache (and
+    [L][n][8] scales) into slots 0..n-1: [n][slot_bytes]."""
+    n = mini.shape[1]
+    o = oracle_mini_shape(sh, n)
+    want = np.zeros((n, oracle.sizes(o)["slot"]), np.uint8)
+    oracle.store_blocks(o, np.ascontiguousarray(mini).reshape(-1),
+                        None if mini_scales is None else np.ascontiguousarray(mini_scales).reshape(-1),
+                        want, np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int64))
+    return want
+
+
+def oracle_pages(sh, slots_img, with_scales=False):
+    """The oracle's load of slots 0..n-1 into pages 0..n-1 of a fresh host
+    cache: [L][n][piece] (and [L][n][8] scales)."""
+    n = slots_img.shape[0]
+    o = oracle_mini_shape(sh, n)
+    out = np.zeros((sh.num_layers, n, sh.piece_bytes), np.uint8)
+    sc = np.zeros((sh.num_layers, n, 8), np.uint8) if with_scales else None
+    oracle.load_blocks(o, np.ascontiguousarray(slots_img), out.reshape(-1),
+                       None if sc is None else sc.reshape(-1), np.arange(n, dtype=np.int64),
+                       np.arange(n, dtype=np.int32))
+    return (out, sc) if with_scales else out
+
+
+def changed_pages(torch, kv3, before3, chunk=512):
+    """Pages (any layer) whose bytes differ between two [L][P][piece] device
+    images."""
+    P = kv3.shape[1]
+    out = []
+    for p0 in range(0, P, chunk):
+        p1 = min(P, p0 + chunk)
+        d = (kv3[:, p0:p1] != before3[:, p0:p1]).any(dim=2).any(dim=0)
+        out.append((torch.nonzero(d).flatten() + p0).cpu().numpy())
+    return np.concatenate(out)
+
+
+def assert_rows_equal(got, want, what):
+    if not np.array_equal(got, want):
+        bad = np.nonzero((got.reshape(len(got), -1) != want.reshape(len(want), -1)).any(axis=1))[0]
+        raise AssertionError(f"{what}: {len(bad)} of {len(got)} rows differ, first {bad[:8]}")

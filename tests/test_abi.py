@@ -129,3 +129,43 @@ def test_kernel_source_sha_constants_match_the_oracles_derivation():
     h = [int(x, 16) for x in re.findall(r"0x([0-9a-f]{8})u", src.split("kInit[8] = {")[1].split("};")[0])]
     K, H = oracle.sha256_constants()
     assert k == list(K) and h == list(H)
+
+
+def test_buffer_sizes_are_checked_before_any_gpu_work(lib):
+    # device buffers carry their sizes across the boundary: offsets past the
+    # tokens given, or more keys than the output holds, are refused before
+    # anything is launched (no GPU is needed to see it)
+    offs = (C.c_int64 * 3)(0, 32, 64)       # 64 tokens, 4 keys of 16
+    koffs = (C.c_int64 * 3)()
+    fake = C.c_void_p(0x10000)               # never dereferenced
+    assert lib.ea_hash_blocks_device(fake, 63, offs, 2, 16, None, fake, 4, koffs,
+                                     None) == N.EA_EINVAL          # tokens too short
+    assert lib.ea_hash_blocks_device(fake, 64, offs, 2, 16, None, fake, 3, koffs,
+                                     None) == N.EA_EINVAL          # keys do not fit
+    assert lib.ea_hash_blocks_device(fake, 64, offs, 2, 8, None, fake, 8, koffs,
+                                     None) == N.EA_ENOTSUP
+    assert lib.ea_hash_blocks_device_offsets(fake, 64, None, 2, 16, None, fake, 4, fake,
+                                             None) == N.EA_EINVAL  # no offsets
+    assert lib.ea_hash_blocks_device_offsets(fake, 64, C.c_void_p(0x10004), 2, 16, None, fake,
+                                             4, fake, None) == N.EA_EINVAL  # misaligned
+    assert lib.ea_hash_blocks_device_offsets(fake, -1, fake, 2, 16, None, fake, 4, fake,
+                                             None) == N.EA_EINVAL
+    assert lib.ea_hash_blocks_device_offsets(fake, 64, fake, 2, 24, None, fake, 4, fake,
+                                             None) == N.EA_ENOTSUP
+    assert lib.ea_gather_blocks(None, None, 1, fake, 1 << 20, None) == N.EA_EINVAL
+    assert lib.ea_scatter_blocks(None, fake, 1 << 20, None, 1, None) == N.EA_EINVAL
+    evs = (C.c_void_p * 2)()
+    assert lib.ea_load_blocks_layered(None, None, None, None, 0, None, evs, 2) == N.EA_EINVAL
+
+
+def test_host_hash_checks_the_token_range():
+    # the binding refuses offsets that run past the token array
+    import numpy as np
+    from paper_2609_33762_amd import api
+    with pytest.raises(ValueError):
+        api.hash_blocks(np.zeros(31, np.int32), np.array([0, 32]), 16)
+    with pytest.raises(ValueError):
+        api.hash_blocks(np.zeros(32, np.int32), np.array([0, 32]), 16,
+                        parents=np.zeros(31, np.uint8))
+    with pytest.raises(ValueError):
+        api.hash_blocks(np.zeros(32, np.int32), np.array([16, 8]), 16)

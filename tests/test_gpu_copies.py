@@ -263,3 +263,83 @@ def test_any_xcd_masks_copy_every_piece(masks, placement, monkeypatch):
         p.o_load(slots, dst)
         p.assert_equal(f"masks {masks} n={n}")
     p.close()
+
+
+@pytest.mark.parametrize("placement", ["hardware", "index"])
+def test_one_workgroup_runs_many_index_batches(placement, monkeypatch):
+    # Kernels fetch page and slot indices 64 units per wave at a time.  With
+    # one working workgroup (four waves) on one XCD, 600 pages of 4 layers
+    # give each wave about 600 units: ten index batches, the last one
+    # partial.  Store, load, layered load, gather and scatter, full images
+    # against the oracle.
+    torch = need_gpu()
+    for k, v in {"EA_LINK_WG": "1", "EA_LINK_WG_LAYERED": "1", "EA_XCD_STORE": "0x1",
+                 "EA_XCD_LOAD": "0x1", "EA_GRID_GATHER": "1", "EA_GRID_SCATTER": "1",
+                 "EA_GRID_HBM": "1"}.items():
+        monkeypatch.setenv(k, v)
+    if placement == "index":
+        monkeypatch.setenv("EA_XCD_PLACEMENT", "index")
+    L, P, S, n = 4, 2000, 640, 600
+    p = Pair(P, L, 16, 1, 32, 2, S, scales=True, seed=61)  # 2 KiB pieces
+    r = W.rng(61)
+    src = W.distinct(r, P, n)
+    dst = W.distinct(r, P, n, exclude=src)
+    slots = W.distinct(r, S, n)
+    p.tier.store(p.cache, src, slots)
+    p.o_store(src, slots)
+    p.assert_equal("store, one workgroup")
+    p.tier.load(p.cache, slots, dst)
+    p.o_load(slots, dst)
+    p.assert_equal("load, one workgroup")
+    dst2 = W.distinct(r, P, n, exclude=np.concatenate([src, dst]))
+    copy_s = torch.cuda.Stream()
+    events = [torch.cuda.Event() for _ in range(L)]
+    p.tier.load_layered(p.cache, slots, dst2, copy_s, events)
+    torch.cuda.synchronize()
+    p.o_load(slots, dst2)
+    p.assert_equal("layered load, one workgroup")
+    slot = p.sizes["slot"]
+    buf = torch.full((n * slot,), 0x5A, dtype=torch.uint8, device="cuda")
+    p.cache.gather(src, buf)
+    want = np.full((n, slot), 0x5A, np.uint8)
+    oracle.store_blocks(p.oshape, p.o_cache, p.o_sc, want, src, np.arange(n))
+    torch.cuda.synchronize()
+    assert np.array_equal(buf.cpu().numpy().reshape(n, slot), want)
+    dst3 = np.setdiff1d(np.arange(P), src)[:n]
+    p.cache.scatter(buf, dst3)
+    oracle.load_blocks(p.oshape, want, p.o_cache, p.o_sc, np.arange(n), dst3)
+    p.assert_equal("scatter, one workgroup")
+    p.close()
+
+
+def test_device_buffer_sizes_are_checked():
+    # gather / scatter buffers and layer events must match the call; a short
+    # one is refused and nothing is launched
+    torch = need_gpu()
+    import ctypes as C
+    p = tiny_pair(seed=62)
+    slot = p.sizes["slot"]
+    n = 10
+    buf = torch.full((n * slot - 16,), 0x5A, dtype=torch.uint8, device="cuda")
+    ids = np.arange(n, dtype=np.int32)
+    with pytest.raises(ValueError):
+        p.cache.gather(ids, buf)
+    with pytest.raises(ValueError):
+        p.cache.scatter(buf, ids)
+    lib = N.load()
+    assert lib.ea_gather_blocks(p.cache.handle, ids.ctypes.data, n, buf.data_ptr(),
+                                buf.numel(), None) == N.EA_EINVAL
+    assert lib.ea_scatter_blocks(p.cache.handle, buf.data_ptr(), buf.numel(), ids.ctypes.data,
+                                 n, None) == N.EA_EINVAL
+    torch.cuda.synchronize()
+    assert (buf.cpu().numpy() == 0x5A).all()
+    slots = np.arange(4, dtype=np.int64)
+    p.tier.store(p.cache, ids[:4], slots)
+    events = [torch.cuda.Event() for _ in range(W.TINY.num_layers - 1)]
+    with pytest.raises(ValueError):
+        p.tier.load_layered(p.cache, slots, ids[4:8], torch.cuda.Stream(), events)
+    evs = (C.c_void_p * 1)()
+    dst = ids[4:8].copy()
+    assert lib.ea_load_blocks_layered(p.tier._h, p.cache.handle, slots.ctypes.data,
+                                      dst.ctypes.data, 4, None, evs, 1) == N.EA_EINVAL
+    p.close()

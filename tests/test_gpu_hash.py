@@ -186,3 +186,126 @@ def test_longest_contexts():
     check([262144], 16, seed=121)
     check([238105], 16, seed=122)
     check([238105, 262144], 1024, parents=True, seed=123)
+
+
+def device_offsets_case(torch, lengths, b, seed, parents=False, keys_capacity=None,
+                        tokens_pad=0):
+    toks, offs = W.sequences(seed, lengths)
+    par = W.host_bytes(seed + 1, 32 * len(lengths)).reshape(-1, 32) if parents else None
+    okeys, okoffs = oracle.hash_blocks(toks, offs, b, par)
+    d_tok = torch.as_tensor(np.concatenate([toks, np.zeros(tokens_pad, np.int32)]),
+                            device="cuda")
+    d_offs = torch.as_tensor(offs, device="cuda")
+    cap = len(okeys) if keys_capacity is None else keys_capacity
+    out = torch.full((max(cap, 1), 32), 0xEE, dtype=torch.uint8, device="cuda")
+    d_koffs = torch.full((len(offs),), -7, dtype=torch.int64, device="cuda")
+    d_par = None if par is None else torch.as_tensor(par, device="cuda")
+    api.hash_blocks_device_offsets(d_tok, d_offs, b, out[:cap] if cap else out[:0], d_koffs,
+                                   d_parents=d_par)
+    return okeys, okoffs, out, d_koffs
+
+
+@pytest.mark.parametrize("b", [16, 32, 1024])
+def test_device_offsets_variant(b):
+    # sequence offsets on the device too: the key offsets come from a scan
+    # kernel; ragged sequences, empty ones, parents, tokens past the last
+    # sequence (ignored)
+    torch = need_gpu()
+    lengths = [0, b - 1, b, b + 1, 7 * b + 3, 1, 3 * b, 0]
+    for parents in (False, True):
+        okeys, okoffs, out, d_koffs = device_offsets_case(torch, lengths, b, 60 + b, parents,
+                                                          tokens_pad=5 * b)
+        torch.cuda.synchronize()
+        assert np.array_equal(d_koffs.cpu().numpy(), okoffs)
+        assert np.array_equal(out[:len(okeys)].cpu().numpy(), okeys)
+        assert (out[len(okeys):].cpu().numpy() == 0xEE).all()
+
+
+def test_device_offsets_many_sequences_and_forms(monkeypatch):
+    # more sequences than the scan's 1,024 threads (several runs each), and
+    # every chain form
+    torch = need_gpu()
+    r = W.rng(71)
+    lengths = list(r.integers(0, 300, size=5000))
+    for form in ["pair", "lane", "split", None]:
+        if form:
+            monkeypatch.setenv("EA_HASH_CHAIN", form)
+        else:
+            monkeypatch.delenv("EA_HASH_CHAIN", raising=False)
+        okeys, okoffs, out, d_koffs = device_offsets_case(torch, lengths, 16, 72, True)
+        torch.cuda.synchronize()
+        assert np.array_equal(d_koffs.cpu().numpy(), okoffs), form
+        assert np.array_equal(out.cpu().numpy()[:len(okeys)], okeys), form
+
+
+def test_device_offsets_batch_workload_size():
+    # the batch of the hash benchmark: 65,536 sequences of 256 tokens
+    torch = need_gpu()
+    n, L = 65536, 256
+    r = W.rng(73)
+    toks = r.integers(0, W.VOCAB, size=n * L, dtype=np.int64).astype(np.int32)
+    offs = np.arange(0, n * L + 1, L, dtype=np.int64)
+    okeys, okoffs = oracle.hash_blocks(toks, offs, 16)
+    d_tok = torch.as_tensor(toks, device="cuda")
+    out = torch.zeros((len(okeys), 32), dtype=torch.uint8, device="cuda")
+    d_koffs = torch.zeros(n + 1, dtype=torch.int64, device="cuda")
+    api.hash_blocks_device_offsets(d_tok, torch.as_tensor(offs, device="cuda"), 16, out, d_koffs)
+    torch.cuda.synchronize()
+    assert np.array_equal(d_koffs.cpu().numpy(), okoffs)
+    assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+def test_device_offsets_errors_are_reported_on_the_device():
+    # malformed device offsets or too small an output: key_offsets[0] = -1
+    # and no key is written; a later good call on the same stream works
+    torch = need_gpu()
+    cases = [
+        ([0, 32, 16, 48], 64, None),     # a decrease
+        ([-16, 0, 32], 64, None),        # a negative start
+        ([0, 32, 80], 64, None),         # past the 64 tokens given
+        ([0, 32, 64], 64, 3),            # 4 keys, room for 3
+    ]
+    for offs, n_tok, cap in cases:
+        d_tok = torch.zeros(n_tok, dtype=torch.int32, device="cuda")
+        out = torch.full((cap or 8, 32), 0xEE, dtype=torch.uint8, device="cuda")
+        d_koffs = torch.full((len(offs),), 5, dtype=torch.int64, device="cuda")
+        api.hash_blocks_device_offsets(d_tok, torch.tensor(offs, dtype=torch.int64,
+                                                           device="cuda"), 16, out, d_koffs)
+        torch.cuda.synchronize()
+        assert d_koffs[0].item() == -1, offs
+        assert (out.cpu().numpy() == 0xEE).all(), offs
+    okeys, okoffs, out, d_koffs = device_offsets_case(torch, [64, 48], 16, 74)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+def test_device_offsets_no_sequences():
+    torch = need_gpu()
+    d_koffs = torch.full((1,), 9, dtype=torch.int64, device="cuda")
+    out = torch.zeros((1, 32), dtype=torch.uint8, device="cuda")
+    api.hash_blocks_device_offsets(torch.zeros(16, dtype=torch.int32, device="cuda"),
+                                   torch.zeros(1, dtype=torch.int64, device="cuda"), 16, out,
+                                   d_koffs)
+    torch.cuda.synchronize()
+    assert d_koffs.item() == 0 and not out.any()
+
+
+def test_device_variant_size_checks():
+    # the sizes of device buffers cross the boundary: too few tokens or too
+    # small an output is refused before anything runs
+    torch = need_gpu()
+    from paper_2609_33762_amd import _native as N
+    import ctypes as C
+    d_tok = torch.zeros(40, dtype=torch.int32, device="cuda")
+    out = torch.full((2, 32), 0xEE, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError):
+        api.hash_blocks_device(d_tok, np.array([0, 48]), 16, out)     # 48 > 40 tokens
+    with pytest.raises(ValueError):
+        api.hash_blocks_device(d_tok, np.array([0, 16, 40]), 16, out[:1])  # 2 keys, room 1
+    offs = (C.c_int64 * 2)(0, 48)
+    koffs = (C.c_int64 * 2)()
+    rc = N.load().ea_hash_blocks_device(d_tok.data_ptr(), 40, offs, 1, 16, None,
+                                        out.data_ptr(), 2, koffs, None)
+    assert rc == N.EA_EINVAL
+    torch.cuda.synchronize()
+    assert (out.cpu().numpy() == 0xEE).all()

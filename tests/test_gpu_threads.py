@@ -139,3 +139,49 @@ def test_threads_share_one_cache_and_tier():
                 p.o_load(x, y)
     p.assert_equal("threads")
     p.close()
+
+
+def test_hashing_on_two_streams_runs_concurrently():
+    # Hash buffers are kept per (device, stream) and no lock is held across
+    # a wait for the GPU, so two threads hashing on two streams do not queue
+    # behind each other.  Each thread hashes a 3,500-key chain (one serial
+    # chain takes milliseconds and occupies one compute unit), synchronously
+    # and asynchronously; keys equal the oracle's, and the two threads
+    # together take well under twice one thread's time.
+    import time
+    torch = need_gpu()
+    n = 56000
+    seqs = [W.sequences(800 + i, [n]) for i in range(2)]
+    want = [oracle.hash_blocks(t, o, B)[0] for t, o in seqs]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    d_toks = [torch.as_tensor(t, device="cuda") for t, _ in seqs]
+    outs = [torch.zeros((n // B, 32), dtype=torch.uint8, device="cuda") for _ in range(2)]
+    got, errors = [None, None], []
+
+    def work(i, reps):
+        try:
+            for _ in range(reps):
+                got[i], _ = api.hash_blocks(seqs[i][0], seqs[i][1], B, stream=streams[i])
+                api.hash_blocks_device(d_toks[i], seqs[i][1], B, outs[i], stream=streams[i])
+                streams[i].synchronize()
+        except Exception as e:
+            errors.append(e)
+
+    work(0, 1)  # warm up both paths and the workspace of stream 0
+    work(1, 1)
+    t0 = time.perf_counter()
+    work(0, 3)
+    alone = time.perf_counter() - t0
+    threads = [threading.Thread(target=work, args=(i, 3)) for i in range(2)]
+    t0 = time.perf_counter()
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    both = time.perf_counter() - t0
+    assert not errors, errors
+    for i in range(2):
+        assert np.array_equal(got[i], want[i]), i
+        assert np.array_equal(outs[i].cpu().numpy(), want[i]), i
+    print(f"one thread {alone * 1e3:.1f} ms, two threads {both * 1e3:.1f} ms")
+    assert both < 1.5 * alone, (alone, both)

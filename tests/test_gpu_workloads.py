@@ -1,15 +1,17 @@
-"""GPU parity at the workloads' full sizes.
+"""GPU parity at the workloads' full sizes, on complete images.
+
+Every written slot and every written page is compared with the oracle's
+result, byte for byte; the whole cache is snapshotted in HBM before the
+operation, and afterwards only destination pages may differ; host slots
+that nothing writes are poisoned beforehand and must keep the poison.
 
 * One Qwen3-30B-A3B turn (20,000-page cache, 16 GiB tier, 2,000 pages stored,
-  1,500 loaded), both transfer plans: round-trip identity on every page,
-  sampled pages and slots against the oracle one by one, sampled untouched
-  pages and slots.
-* The HBM gather and scatter of 2,000 pages in one launch each, as measured:
-  round trip on every page, sampled slots against the oracle.
+  1,500 loaded at the same time on two streams), both transfer plans.
+* The HBM gather and scatter of 2,000 pages in one launch each, as measured.
 * Layer-pipelined fp8 prefix load (64k tokens = 4,096 pages, 48 layers,
-  per-page scales): a consumer stream snapshots each layer right after its
-  event; every snapshot and the end state match the source pages, sampled
-  entries match the oracle's per-layer load.
+  per-page scales), also on one TP8 rank's share: a consumer stream
+  snapshots each layer right after its event, and each snapshot must
+  already hold the layer's final bytes.
 * Dense scattered batches (4,096-page cache, 4,096-slot tier, 10,000 calls of
   1-8 non-adjacent pages): the oracle replays every call on full host images
   and the final cache and tier images must be equal byte for byte.
@@ -17,8 +19,7 @@
   admission, allocation and the tier's full metadata are compared with the
   oracle, and every loaded page is checked against its key's pattern.
 * The longest context of the serving configuration (262,144 tokens) as one
-  TP8 rank's prefix: 16,384 pages stored and loaded back, every page equal
-  to its source, sampled pages and slots against the oracle.
+  TP8 rank's prefix: 16,384 pages stored to shuffled slots and loaded back.
 """
 import gc
 
@@ -28,7 +29,8 @@ import pytest
 import oracle
 from paper_2609_33762_amd import api, drivers, _native as N, workloads as W
 
-from gpu_common import need_gpu
+from gpu_common import (POISON, assert_poisoned_except, assert_rows_equal, changed_pages,
+                        need_gpu, oracle_pages, oracle_slots, pages_to_host, poison_tier)
 
 pytestmark = pytest.mark.gpu
 
@@ -61,11 +63,7 @@ def test_qwen3_turn_full_size(plan):
     store_pages = W.distinct(r, P, n_s, exclude=prefix_pages)
     dst = W.distinct(r, P, n_l, exclude=np.concatenate([prefix_pages, store_pages]))
     host = tier.host_view()
-    # poison a sample of slots that nothing writes, and snapshot sampled pages
-    never = W.distinct(r, tier.capacity, 64, exclude=np.arange(n_l + n_s))
-    host[never] = 0xC3
-    keep_pages = W.distinct(r, P, 64, exclude=dst)
-    keep_before = drivers.read_pages(torch, kv3, keep_pages).cpu().numpy()
+    poison_tier(host)  # every slot, so that any stray write shows
 
     toks = W.tokens(W.SEED_TOKENS, n_l * sh.page_tokens)
     pkeys, _ = api.hash_blocks(toks, np.array([0, len(toks)]), sh.page_tokens)
@@ -76,6 +74,8 @@ def test_qwen3_turn_full_size(plan):
     rkeys = W.rng(7).integers(0, 256, size=(n_s, 32), dtype=np.uint8)
     cnt, sslots = tier.alloc(rkeys)
     assert cnt == n_s
+    torch.cuda.synchronize()
+    before = kv.clone()  # the whole 29 GiB cache, kept in HBM
     s_store, s_load = torch.cuda.Stream(), torch.cuda.Stream()
     h, hslots = tier.lookup(pkeys)
     assert h == n_l
@@ -85,27 +85,22 @@ def test_qwen3_turn_full_size(plan):
     tier.unpin(sslots)
     tier.unpin(hslots)
 
-    # round trip on every page: destination pages hold the prefix pages
-    assert torch.equal(kv3[:, torch.as_tensor(dst, device="cuda")],
-                       kv3[:, torch.as_tensor(prefix_pages, device="cuda")])
-    # sampled entries against the oracle, one by one
-    sample = W.distinct(r, n_s, 48)
-    o = oshape_of(sh, num_pages=len(sample))
-    mini = drivers.read_pages(torch, kv3, store_pages[sample]).cpu().numpy()
-    mini_cache = np.ascontiguousarray(mini.reshape(len(sample), L, piece).transpose(1, 0, 2))
-    want = np.zeros((len(sample), tier.slot_bytes), np.uint8)
-    oracle.store_blocks(o, mini_cache.reshape(-1), None, want, np.arange(len(sample)),
-                        np.arange(len(sample)))
-    assert np.array_equal(host[sslots[sample]], want)
-    lsample = W.distinct(r, n_l, 48)
-    lo = np.zeros((L, len(lsample), piece), np.uint8)
-    oracle.load_blocks(o, host[pslots[lsample]].copy(), lo.reshape(-1), None,
-                       np.arange(len(lsample)), np.arange(len(lsample)))
-    got = drivers.read_pages(torch, kv3, dst[lsample]).cpu().numpy()
-    assert np.array_equal(got, lo.transpose(1, 0, 2).reshape(len(lsample), -1))
-    # untouched pages and slots
-    assert np.array_equal(drivers.read_pages(torch, kv3, keep_pages).cpu().numpy(), keep_before)
-    assert (host[never] == 0xC3).all()
+    # every written slot is the oracle's store of its source page
+    want_p = oracle_slots(sh, pages_to_host(torch, kv3, prefix_pages))
+    assert_rows_equal(host[pslots], want_p, "prefix slots")
+    want_s = oracle_slots(sh, pages_to_host(torch, kv3, store_pages))
+    assert_rows_equal(host[sslots], want_s, "refill slots")
+    del want_s
+    # every loaded page is the oracle's load of the oracle's slot image
+    want_l = oracle_pages(sh, want_p)
+    got_l = pages_to_host(torch, kv3, dst)
+    assert_rows_equal(got_l.transpose(1, 0, 2), want_l.transpose(1, 0, 2), "loaded pages")
+    del want_l, got_l, want_p
+    # nothing else in HBM changed, and every slot nobody wrote kept its poison
+    changed = changed_pages(torch, kv3, before.view(L, P, piece))
+    assert np.isin(changed, dst).all(), np.setdiff1d(changed, dst)[:8]
+    del before
+    assert_poisoned_except(host, np.concatenate([pslots, sslots]))
     tier.close()
     cache.close()
     del kv, kv3
@@ -116,8 +111,8 @@ def test_hbm_gather_and_scatter_full_size():
     # The measured HBM launches: one gather of 2,000 random pages of the
     # 20,000-page Qwen3 cache into a slot-layout device buffer, one scatter of
     # that buffer into 2,000 other pages (the default grids).  Every gathered
-    # slot is the oracle's store of its page (sampled one by one) and every
-    # scattered page equals its source page.
+    # slot is the oracle's store of its page, every scattered page the
+    # oracle's load of that slot, and no other page changes.
     torch = need_gpu()
     sh = W.QWEN3
     L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
@@ -129,27 +124,23 @@ def test_hbm_gather_and_scatter_full_size():
     n = W.QWEN3_STORE_PAGES
     src = W.distinct(r, P, n)
     dst = W.distinct(r, P, n, exclude=src)
-    keep = W.distinct(r, P, 64, exclude=dst)
-    keep_before = drivers.read_pages(torch, kv3, keep).cpu().numpy()
     slot = L * piece
-    staging = torch.empty(n * slot, dtype=torch.uint8, device="cuda")
+    staging = torch.full((n * slot,), POISON, dtype=torch.uint8, device="cuda")
+    before = kv.clone()
     cache.gather(src, staging)
     cache.scatter(staging, dst)
     torch.cuda.synchronize()
-    assert torch.equal(kv3[:, torch.as_tensor(dst, device="cuda")],
-                       kv3[:, torch.as_tensor(src, device="cuda")])
-    sample = W.distinct(r, n, 48)
-    o = oshape_of(sh, num_pages=len(sample))
-    mini = drivers.read_pages(torch, kv3, src[sample]).cpu().numpy()
-    mini_cache = np.ascontiguousarray(mini.reshape(len(sample), L, piece).transpose(1, 0, 2))
-    want = np.zeros((len(sample), slot), np.uint8)
-    oracle.store_blocks(o, mini_cache.reshape(-1), None, want, np.arange(len(sample)),
-                        np.arange(len(sample)))
-    got = staging.view(n, slot)[torch.as_tensor(sample, device="cuda")].cpu().numpy()
-    assert np.array_equal(got, want)
-    assert np.array_equal(drivers.read_pages(torch, kv3, keep).cpu().numpy(), keep_before)
+    want = oracle_slots(sh, pages_to_host(torch, kv3, src))
+    assert_rows_equal(staging.view(n, slot).cpu().numpy(), want, "gathered slots")
+    want_l = oracle_pages(sh, want)
+    del want
+    got_l = pages_to_host(torch, kv3, dst)
+    assert_rows_equal(got_l.transpose(1, 0, 2), want_l.transpose(1, 0, 2), "scattered pages")
+    del want_l, got_l
+    changed = changed_pages(torch, kv3, before.view(L, P, piece))
+    assert np.isin(changed, dst).all(), np.setdiff1d(changed, dst)[:8]
     cache.close()
-    del kv, kv3, staging
+    del kv, kv3, staging, before
     release(torch)
 
 
@@ -184,6 +175,7 @@ def test_layered_fp8_prefix_full_size(sh):
     kv3[:, d] = 0xA5
     sc3[:, d] = 0x5A
     torch.cuda.synchronize()
+    before3, before_sc3 = kv3.clone(), sc3.clone()
     h, hslots = tier.lookup(keys)
     assert h == n
     copy_s, cons_s = torch.cuda.Stream(), torch.cuda.Stream()
@@ -200,21 +192,28 @@ def test_layered_fp8_prefix_full_size(sh):
         assert torch.equal(snaps[l][0], kv3[l].index_select(0, s_)), l
         assert torch.equal(snaps[l][1], sc3[l].index_select(0, s_)), l
     assert torch.equal(kv3[:, d], kv3[:, s_]) and torch.equal(sc3[:, d], sc3[:, s_])
-    # sampled entries against the oracle's per-layer load
+    # every slot is the oracle's store of its source page (with scales), and
+    # every destination page the oracle's layer-by-layer load of that image
     host = tier.host_view()
-    pick = W.distinct(r, n, 16)
-    o = oshape_of(sh, num_pages=len(pick))
-    ocache = np.zeros((L, len(pick), piece), np.uint8)
-    osc = np.zeros((L, len(pick), 8), np.uint8)
+    src_pages = pages_to_host(torch, kv3, src)
+    src_sc = sc3[:, s_].cpu().numpy()
+    want = oracle_slots(sh, src_pages, src_sc)
+    assert_rows_equal(host[hslots], want, "stored slots")
+    o = oshape_of(sh, num_pages=n)
+    ocache = np.zeros((L, n, piece), np.uint8)
+    osc = np.zeros((L, n, 8), np.uint8)
     for l in range(L):
-        oracle.load_layer(o, host[hslots[pick]].copy(), ocache.reshape(-1), osc.reshape(-1),
-                          np.arange(len(pick)), np.arange(len(pick)), l)
-    pd = torch.as_tensor(dst[pick], device="cuda")
-    assert np.array_equal(kv3[:, pd].cpu().numpy(), ocache)
-    assert np.array_equal(sc3[:, pd].cpu().numpy(), osc)
+        oracle.load_layer(o, want, ocache.reshape(-1), osc.reshape(-1), np.arange(n),
+                          np.arange(n, dtype=np.int32), l)
+    got = pages_to_host(torch, kv3, dst)
+    assert_rows_equal(got.transpose(1, 0, 2), ocache.transpose(1, 0, 2), "loaded pages")
+    assert np.array_equal(sc3[:, d].cpu().numpy(), osc)
+    # only destination pages changed since the poison was written
+    assert np.isin(changed_pages(torch, kv3, before3), dst).all()
+    assert np.isin(changed_pages(torch, sc3, before_sc3), dst).all()
     tier.close()
     cache.close()
-    del kv, sc, kv3, sc3
+    del kv, sc, kv3, sc3, before3, before_sc3
     release(torch)
 
 
@@ -413,9 +412,9 @@ def test_agent_pool_in_1024_token_chunks():
 
 def test_longest_prefix_on_one_tp8_rank():
     # a 262,144-token prefix (the serving configuration's maximum context),
-    # 16,384 pages of one TP8 rank's share (384 KiB each, 6 GiB), stored and
-    # loaded back into other pages: every page equal to its source, sampled
-    # pages and slots against the oracle
+    # 16,384 pages of one TP8 rank's share (384 KiB each, 6 GiB), stored to
+    # shuffled slots and loaded back into other pages: every slot and every
+    # loaded page against the oracle, no other page changed
     torch = need_gpu()
     sh = W.Shape("tp8_shard_long", 48, 1, 128, 2, 16, 2 * 16384 + 64)
     L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
@@ -430,24 +429,20 @@ def test_longest_prefix_on_one_tp8_rank():
     src = W.distinct(r, P, n)
     dst = W.distinct(r, P, n, exclude=src)
     slots = r.permutation(n).astype(np.int64)
+    before = kv.clone()
     tier.store(cache, src, slots)
     tier.load(cache, slots, dst)
     torch.cuda.synchronize()
-    d, s_ = torch.as_tensor(dst, device="cuda"), torch.as_tensor(src, device="cuda")
-    assert torch.equal(kv3[:, d], kv3[:, s_])
     host = tier.host_view()
-    pick = W.distinct(r, n, 12)
-    o = oshape_of(sh, num_pages=len(pick))
-    ocache = kv3[:, torch.as_tensor(src[pick], device="cuda")].cpu().numpy().copy()
-    otier = np.zeros((len(pick), tier.slot_bytes), np.uint8)
-    oracle.store_blocks(o, ocache.reshape(-1), None, otier,
-                        np.arange(len(pick), dtype=np.int32), np.arange(len(pick)))
-    assert np.array_equal(host[slots[pick]], otier)
-    oback = np.zeros_like(ocache)
-    oracle.load_blocks(o, otier, oback.reshape(-1), None, np.arange(len(pick)),
-                       np.arange(len(pick), dtype=np.int32))
-    assert np.array_equal(kv3[:, torch.as_tensor(dst[pick], device="cuda")].cpu().numpy(), oback)
+    want = oracle_slots(sh, pages_to_host(torch, kv3, src))
+    assert_rows_equal(host[slots], want, "stored slots")
+    want_l = oracle_pages(sh, want)
+    del want
+    got = pages_to_host(torch, kv3, dst)
+    assert_rows_equal(got.transpose(1, 0, 2), want_l.transpose(1, 0, 2), "loaded pages")
+    del want_l, got
+    assert np.isin(changed_pages(torch, kv3, before.view(L, P, piece)), dst).all()
     tier.close()
     cache.close()
-    del kv, kv3
+    del kv, kv3, before
     release(torch)
