@@ -383,7 +383,7 @@ extern "C" int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_
   const int64_t scan_bytes = ea::hash_scan_state_bytes(n_seqs);
   if (scan_bytes > w.cap_scan) {
     if ((rc = grow_device(w, &w.d_scan, &w.cap_scan, scan_bytes)) != EA_OK) return rc;
-    HS_HIP(hipMemsetAsync(w.d_scan, 0, 64, stream));  // a fresh ticket counter
+    HS_HIP(ea::launch_hash_scan_reset(w.d_scan, stream));  // a fresh ticket counter
   }
   if ((rc = ensure_mid(w, &w.d_mid, &w.cap_mid, std::max<int64_t>(bound, 1))) != EA_OK) return rc;
   uint8_t *d_koff = w.d_off;

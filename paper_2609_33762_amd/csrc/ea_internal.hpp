@@ -104,6 +104,9 @@ hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
                                    int64_t *d_key_offsets_out, bool wide, void *d_koff,
                                    void *d_toff, void *d_state, hipStream_t stream);
 int64_t hash_scan_groups(int32_t n_seqs);
+// Zero the first 8 bytes of a scan state on `stream` (a fill kernel).
+hipError_t launch_hash_scan_reset(void *d_state, hipStream_t stream);
+
 inline int64_t hash_scan_state_bytes(int32_t n_seqs) { return 64 + 16 * hash_scan_groups(n_seqs); }
 
 

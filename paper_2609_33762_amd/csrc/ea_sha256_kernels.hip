@@ -35,6 +35,7 @@
 #include <atomic>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "ea_internal.hpp"
 
@@ -143,6 +144,7 @@ __global__ __launch_bounds__(256) void sha256_midstates(
   if (g >= n_keys || g >= (int64_t)key_off[n_seqs]) return;
   const int32_t s = owner(key_off, n_seqs, g);
   const int64_t i = g - (int64_t)key_off[s];
+  if (i < 0 || g >= (int64_t)key_off[s + 1]) return;  // offsets not increasing: nothing to do
   const int32_t *tok = tokens + (int64_t)tok_off[s] + i * block_tokens;
   uint32_t st[8];
 #pragma unroll
@@ -313,6 +315,7 @@ __global__ __launch_bounds__(128) void sha256_midstates_split(
   const int lane = threadIdx.x & 63;
   const bool e_side = lane & 1;
   const int32_t s = owner(key_off, n_seqs, g);
+  if (g < (int64_t)key_off[s] || g >= (int64_t)key_off[s + 1]) return;  // the whole workgroup
   const int32_t *tok = tokens + (int64_t)tok_off[s] + (g - (int64_t)key_off[s]) * block_tokens;
   const int32_t blocks = block_tokens / 16;
   const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
@@ -718,6 +721,12 @@ __global__ __launch_bounds__(kScanThreads) void hash_offsets_write(
   }
 }
 
+// Zero the scan's ticket counter (a fill kernel rather than a memset, so
+// that a captured graph replays it safely).
+__global__ __launch_bounds__(64) void hash_scan_reset(uint64_t *ticket) {
+  if (threadIdx.x == 0) *ticket = 0;
+}
+
 // The split forms launch one workgroup per sequence or key; forcing them on
 // more than this many falls back to the other forms.
 constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
@@ -837,6 +846,13 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   else
     launch_chain(form, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
                  d_parents, d_keys, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_scan_reset(void *d_state, hipStream_t stream) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(hash_scan_reset, dim3(1), dim3(64), 0, stream,
+                     static_cast<uint64_t *>(d_state));
   return hipGetLastError();
 }
 
