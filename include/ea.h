@@ -218,6 +218,22 @@ int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_tokens,
                                   uint8_t *d_keys_out, int64_t keys_capacity,
                                   int64_t *d_key_offsets_out, hipStream_t stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): ea_hash_blocks_device_
+ * offsets with every buffer of its own in fixed device memory that the
+ * library reserves per device (48 MiB, held until the process ends), so the
+ * call allocates nothing.  Same arguments and results.  Limits: at most
+ * 1,048,576 keys (min(keys_capacity, n_tokens / block_tokens)) and
+ * 1,048,576 sequences per call, else EA_EINVAL with nothing launched.  All
+ * calls on one device share that memory and each leaves it as it found it:
+ * two calls that overlap on one device (on different streams, not ordered
+ * by events) race and may compute wrong keys; order them. */
+int ea_hash_blocks_device_offsets_noalloc(const int32_t *d_tokens, int64_t n_tokens,
+                                          const int64_t *d_seq_offsets, int32_t n_seqs,
+                                          int32_t block_tokens, const uint8_t *d_parents,
+                                          uint8_t *d_keys_out, int64_t keys_capacity,
+                                          int64_t *d_key_offsets_out, hipStream_t stream);
+
 /* ------------------------------------------------- lookup and admission */
 
 /* Consecutive-prefix lookup (section 3.2; App. "Prefix coverage from a

@@ -92,6 +92,8 @@ SIGNATURES = {
     "ea_hash_blocks": (_INT, [_P, _P, _I32, _I32, _P, _P, _P, _P]),
     "ea_hash_blocks_device": (_INT, [_P, _I64, _P, _I32, _I32, _P, _P, _I64, _P, _P]),
     "ea_hash_blocks_device_offsets": (_INT, [_P, _I64, _P, _I32, _I32, _P, _P, _I64, _P, _P]),
+    "ea_hash_blocks_device_offsets_noalloc": (_INT, [_P, _I64, _P, _I32, _I32, _P, _P, _I64, _P,
+                                                     _P]),
     "ea_tier_lookup": (_INT, [_P, _P, _I64, _P, _P]),
     "ea_admission_fill": (_INT, [_P, _P, _P, _P, _I64, _P, _P]),
     "ea_admission_fill_report": (_INT, [_P, _P, _P, _P, _I64, _P, _I64, _P, _P]),

@@ -316,10 +316,12 @@ def hash_blocks_device(d_tokens, seq_offsets, block_tokens, d_keys_out, d_parent
 
 
 def hash_blocks_device_offsets(d_tokens, d_seq_offsets, block_tokens, d_keys_out,
-                               d_key_offsets_out, d_parents=None, stream=None):
+                               d_key_offsets_out, d_parents=None, stream=None, noalloc=False):
     """Fully asynchronous variant: sequence offsets (int64 [n_seqs + 1]) and
     key offsets (int64 [n_seqs + 1]) are device tensors too; on the device,
-    malformed offsets or too many keys leave d_key_offsets_out[0] = -1."""
+    malformed offsets or too many keys leave d_key_offsets_out[0] = -1.
+    noalloc=True calls the entry point that allocates nothing (fixed device
+    memory per device; calls must not overlap on one device)."""
     import torch
     n_seqs = d_seq_offsets.numel() - 1
     _check_device_buffers(d_tokens, d_keys_out, d_parents, n_seqs)
@@ -328,7 +330,8 @@ def hash_blocks_device_offsets(d_tokens, d_seq_offsets, block_tokens, d_keys_out
             raise ValueError(f"{what} must be a contiguous int64 device tensor")
     if n_seqs < 0 or d_key_offsets_out.numel() < n_seqs + 1:
         raise ValueError("need n_seqs + 1 entries in both offset tensors")
-    N.check("ea_hash_blocks_device_offsets", N.load().ea_hash_blocks_device_offsets(
+    name = "ea_hash_blocks_device_offsets" + ("_noalloc" if noalloc else "")
+    N.check(name, getattr(N.load(), name)(
         d_tokens.data_ptr(), d_tokens.numel(), d_seq_offsets.data_ptr(), n_seqs, block_tokens,
         None if d_parents is None else d_parents.data_ptr(), d_keys_out.data_ptr(),
         _nbytes(d_keys_out) // 32, d_key_offsets_out.data_ptr(), _stream(stream)))

@@ -396,3 +396,28 @@ extern "C" int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_
     return rc;
   return release(w, stream);
 }
+
+extern "C" int ea_hash_blocks_device_offsets_noalloc(
+    const int32_t *d_tokens, int64_t n_tokens, const int64_t *d_seq_offsets, int32_t n_seqs,
+    int32_t block_tokens, const uint8_t *d_parents, uint8_t *d_keys_out, int64_t keys_capacity,
+    int64_t *d_key_offsets_out, hipStream_t stream) {
+  int64_t bound = 0;
+  int rc = check_device_offsets(d_tokens, n_tokens, d_seq_offsets, n_seqs, block_tokens,
+                                d_keys_out, keys_capacity, d_key_offsets_out, &bound);
+  if (rc != EA_OK) return rc;
+  // the fixed scratch holds this many keys and sequences
+  if (bound > ea::kScratchKeys || (int64_t)n_seqs > ea::kScratchSeqs) return EA_EINVAL;
+  void *scratch = nullptr;
+  HS_HIP(ea::hash_scratch(stream, &scratch));
+  uint8_t *base = static_cast<uint8_t *>(scratch);
+  const bool wide = n_tokens > INT32_MAX || bound > INT32_MAX || force_wide();
+  uint8_t *d_koff = base + ea::kScratchOffsets;
+  uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
+  HS_HIP(ea::launch_hash_key_offsets(d_seq_offsets, n_seqs, n_tokens, block_tokens, bound,
+                                     d_key_offsets_out, wide, d_koff, d_toff,
+                                     base + ea::kScratchState, stream));
+  if (bound > 0 && n_seqs > 0)
+    return run_kernels(d_tokens, d_koff, d_toff, wide, n_seqs, bound, block_tokens,
+                       reinterpret_cast<uint32_t *>(base), d_parents, d_keys_out, stream);
+  return EA_OK;
+}

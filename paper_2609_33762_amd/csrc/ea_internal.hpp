@@ -107,6 +107,20 @@ int64_t hash_scan_groups(int32_t n_seqs);
 // Zero the first 8 bytes of a scan state on `stream` (a fill kernel).
 hipError_t launch_hash_scan_reset(void *d_state, hipStream_t stream);
 
+// The fixed device memory of the hashing entry point that allocates
+// nothing, per device: midstates of up to kScratchKeys keys, the kernels'
+// key and token offsets (64-bit) of up to kScratchSeqs sequences, then the
+// scan state.  48 MiB in all.
+constexpr int64_t kScratchKeys = int64_t(1) << 20;
+constexpr int64_t kScratchSeqs = int64_t(1) << 20;
+constexpr int64_t kScratchOffsets = 32 * kScratchKeys;  // byte offsets in the scratch
+constexpr int64_t kScratchState = kScratchOffsets + (8 * (2 * kScratchSeqs + 1) + 255) / 256 * 256;
+constexpr int64_t kScratchBytes = kScratchState + 64 + 16 * ((kScratchSeqs + 2047) / 2048);
+// The scratch's address on the current device: resolved with
+// hipGetSymbolAddress the first time a device asks (that device current),
+// then kept; the first resolution also zeroes the scan's ticket counter
+// with a fill kernel on `stream`.
+hipError_t hash_scratch(hipStream_t stream, void **ptr);
 inline int64_t hash_scan_state_bytes(int32_t n_seqs) { return 64 + 16 * hash_scan_groups(n_seqs); }
 
 

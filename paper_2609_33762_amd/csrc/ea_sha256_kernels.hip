@@ -886,4 +886,33 @@ hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
   return hipGetLastError();
 }
 
+// Fixed device memory for the hashing entry point that allocates nothing
+// (layout in ea_internal.hpp).  Each device holds its own copy for the
+// life of the process.  In host code the array's name is not a device
+// address: the address comes from hipGetSymbolAddress, once per device with
+// that device current, and only that address is passed to kernels.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+hipError_t hash_scratch(hipStream_t stream, void **ptr) {
+  static std::mutex mu;
+  static void *known[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (known[dev] == nullptr) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    // the scan's ticket counter must start at zero; each call leaves it so
+    e = launch_hash_scan_reset(static_cast<uint8_t *>(p) + kScratchState, stream);
+    if (e != hipSuccess) return e;
+    known[dev] = p;
+  }
+  *ptr = known[dev];
+  return hipSuccess;
+}
+
 }  // namespace ea
