@@ -348,6 +348,89 @@ def _line(workload, value, unit, ms, steps, extra, higher=True):
             "config": {"workload": workload}, **extra}
 
 
+def _pinned_one_core(fn):
+    """Run fn() on one core (the first of this process's), then restore."""
+    prev = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {sorted(prev)[0]})
+    try:
+        return fn()
+    finally:
+        os.sched_setaffinity(0, prev)
+
+
+def _pool_cpu_baseline(records, sh, chunk_pages, tier_bytes, kappa, window, mode=0):
+    """The oracle on one core replays every turn's metadata (lookup, write
+    rule, allocation, store marks, unpins) from the run's records and checks
+    each result against the library's; then it times host copies of 256
+    slots each way at the pool's slot size."""
+    import oracle
+    C = chunk_pages
+    b = sh.page_tokens * C
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    oshape = oracle.make_shape(sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                               sh.head_dim, sh.elem_bytes, chunk_pages=C)
+    opol = oracle.make_policy(kappa=kappa, block_tokens=b, beta=beta, activity_window=window,
+                              mode=mode)
+
+    def replay():
+        ot = oracle.Tier(oshape, tier_bytes)
+        ok = True
+        t0 = time.perf_counter()
+        for rec in records:
+            h, hs = ot.lookup(rec.keys)
+            ok &= bool(h == rec.hit and np.array_equal(hs, rec.hit_slots))
+            save, mask = ot.admission(opol, rec.n_tokens, rec.hit * b, rec.agent, rec.turn,
+                                      rec.keys)
+            ok &= bool(save == rec.save and np.array_equal(mask, rec.mask))
+            _, slots = ot.alloc(rec.keys, mask)
+            ok &= bool(np.array_equal(slots, rec.alloc_slots))
+            good = slots >= 0
+            ot.mark_stored(slots[good])
+            if good.any():
+                ot.unpin(slots[good])
+            if h:
+                ot.unpin(hs)
+        return ok, time.perf_counter() - t0
+
+    ok, replay_s = _pinned_one_core(replay)
+    # copies: 256 pages (in slots of C pages) stored from and loaded back
+    # into a host cache of those pages
+    n = max(1, 256 // C)
+    mini = oracle.make_shape(n * C, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                             sh.elem_bytes, chunk_pages=C)
+    sz = oracle.sizes(mini)
+    cache = np.tile(W_host_bytes(sz["piece"]), sh.num_layers * n * C)
+    otier = np.zeros((n, sz["slot"]), np.uint8)
+    ids = np.arange(n * C, dtype=np.int32)
+    sl = np.arange(n, dtype=np.int64)
+
+    def copies():
+        ts, tl = [], []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            oracle.store_blocks(mini, cache, None, otier, ids, sl)
+            t1 = time.perf_counter()
+            oracle.load_blocks(mini, otier, cache, None, sl, ids)
+            tl.append(time.perf_counter() - t1)
+            ts.append(t1 - t0)
+        return float(np.median(ts)), float(np.median(tl))
+
+    t_s, t_l = _pinned_one_core(copies)
+    moved = n * sz["slot"]
+    return {"value": round(2 * moved / (t_s + t_l) / GB, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle", "store_gbs": round(moved / t_s / GB, 3),
+            "load_gbs": round(moved / t_l / GB, 3),
+            "metadata_replay_s": round(replay_s, 3), "turns_replayed": len(records),
+            "oracle_replay_ok": ok,
+            "sample": f"metadata of all {len(records)} turns replayed on the oracle's tier; "
+                      f"copies of {n} slots of {sz['slot']} B each way, median of 5"}
+
+
+def W_host_bytes(n):
+    from paper_2609_33762_amd import workloads as W
+    return W.host_bytes(W.SEED_DATA, n)
+
+
 def run_agent_pool(args):
     """64 agents round-robin, 24 turns each (1,536 turns), 64 GiB tier."""
     import torch
@@ -398,6 +481,10 @@ def run_agent_pool(args):
     log(f"reference model: {extra['pool']['reference_model']}")
     tier.close()
     cache.close()
+    if not args.no_cpu_baseline:
+        extra["cpu_baseline"] = _pool_cpu_baseline(records, sh, 1, W.POOL_TIER_BYTES, 256,
+                                                   W.POOL_AGENTS)
+        log(f"cpu baseline: {extra['cpu_baseline']}")
     return _line("agent_pool: 64 agents x %d turns, contexts 8k->64k, 64 GiB tier"
                  % args.turns_per_agent, round(moved / el / GB, 3), "GB/s",
                  round(el / turns * 1e3, 3), turns, extra)
@@ -444,6 +531,9 @@ def run_agent_pool_chunked(args):
         total_s += el
         rep = drivers.stack_report(records, tier.capacity, tier.slot_bytes)
         rep.pop("hits_tier_order_per_request")
+        replay = None
+        if not args.no_cpu_baseline:
+            replay = _pool_cpu_baseline(records, sh, C, gib << 30, 8, agents, mode)
         runs[f"{gib}GiB_{mname}"] = {
             "K_H": tier.capacity, "gbs": round(moved / el / GB, 2),
             "ms_per_turn": round(el / turns * 1e3, 3),
@@ -451,7 +541,9 @@ def run_agent_pool_chunked(args):
             "prompt_chunks": int(sum(len(r.keys) for r in records)),
             "stored_chunks": int(sum(r.stored for r in records)),
             "declined_requests": int(sum(not r.save for r in records)),
-            "evictions": st["evictions_total"], "reference_model": rep}
+            "evictions": st["evictions_total"], "reference_model": rep,
+            "oracle_replay_ok": None if replay is None else replay["oracle_replay_ok"],
+            "oracle_metadata_replay_s": None if replay is None else replay["metadata_replay_s"]}
         r = runs[f"{gib}GiB_{mname}"]
         log(f"chunked pool {gib} GiB {mname}: hit {r['hit_chunks']} of {r['prompt_chunks']}, "
             f"stored {r['stored_chunks']}, declined {r['declined_requests']}, evictions "
@@ -459,10 +551,56 @@ def run_agent_pool_chunked(args):
             f"{rep['declined_meeting_condition']}, tier-order model {rep['hits_model_tier_order']}")
         tier.close()
     cache.close()
+    extra = {"pool_chunked": runs}
+    if not args.no_cpu_baseline:
+        extra["cpu_baseline"] = dict(replay, oracle_replay_ok=all(
+            r["oracle_replay_ok"] for r in runs.values()))
+        extra["cpu_baseline"]["sample"] = ("metadata of every turn of all nine runs replayed on "
+                                           "the oracle's tier (replay time of the last run); "
+                                           + replay["sample"].split("; ", 1)[1])
     return _line("agent_pool_chunked: one TP8 rank, 1,024-token chunks, 16 agents x %d turns, "
                  "5/10/40 GiB tiers x 3 admission modes" % args.turns_per_agent,
                  round(total_moved / total_s / GB, 3), "GB/s",
-                 round(total_s / (9 * turns) * 1e3, 3), 9 * turns, {"pool_chunked": runs})
+                 round(total_s / (9 * turns) * 1e3, 3), 9 * turns, extra)
+
+
+def _dense_cpu_baseline(sh, calls=2000):
+    """The oracle on one core: `calls` alternating store / load calls of 1-8
+    random non-adjacent pages between a 256-page host cache and a 256-slot
+    host tier of the dense shape (2 MiB pages); per-call time."""
+    import oracle
+    from paper_2609_33762_amd import drivers, workloads as W
+    n_pages = 256
+    o = oracle.make_shape(n_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                          sh.elem_bytes)
+    sz = oracle.sizes(o)
+    cache = np.tile(W.host_bytes(W.SEED_DATA, sz["piece"]), sh.num_layers * n_pages)
+    otier = np.zeros((n_pages, sz["slot"]), np.uint8)
+    r = W.rng(W.SEED_WORKLOAD)
+    plan = []
+    for i in range(calls):
+        k = int(r.integers(1, 9))
+        plan.append((i % 2, drivers.non_adjacent_pages(r, n_pages, k).astype(np.int32),
+                     r.choice(n_pages, size=k, replace=False).astype(np.int64)))
+
+    def run():
+        ts, moved = [], 0
+        for op, pages, slots in plan:
+            t0 = time.perf_counter()
+            if op == 0:
+                oracle.store_blocks(o, cache, None, otier, pages, slots)
+            else:
+                oracle.load_blocks(o, otier, cache, None, slots, pages)
+            ts.append(time.perf_counter() - t0)
+            moved += len(pages) * sz["page"]
+        return np.array(ts), moved
+
+    ts, moved = _pinned_one_core(run)
+    return {"value": round(moved / ts.sum() / GB, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle", "per_call_ms_p50": round(float(np.percentile(ts, 50)) * 1e3, 4),
+            "per_call_ms_p99": round(float(np.percentile(ts, 99)) * 1e3, 4),
+            "sample": f"{calls} alternating store/load calls of 1-8 pages of {sz['page']} B on "
+                      f"a {n_pages}-page host cache and tier"}
 
 
 def run_dense_scattered(args):
@@ -505,14 +643,20 @@ def run_dense_scattered(args):
              "calls_per_s": round(W.DENSE_CALLS / el, 1)}
     tier.close()
     cache.close()
+    if not args.no_cpu_baseline:
+        extra["cpu_baseline"] = _dense_cpu_baseline(sh)
+        log(f"cpu baseline: {extra['cpu_baseline']}")
     return _line("dense_scattered: 32 layers x 8 heads x d128 bf16, 10,000 calls of 1-8 pages",
                  round(moved2 / el / GB, 3), "GB/s", round(el / W.DENSE_CALLS * 1e3, 4),
                  W.DENSE_CALLS, extra)
 
 
-def _layered_once(torch, api, W, sh, steps):
+def _layered_once(torch, api, W, sh, steps, cpu=True):
     """Load the 4,096-page prefix of shape sh one layer at a time, `steps`
-    timed repetitions after one untimed; returns the bench figures."""
+    timed repetitions after one untimed; a consumer stream waits on each
+    layer's event and checksums that layer of every destination page (the
+    stand-in for attention over the layer).  Returns the bench figures, with
+    the oracle's check of the consumer's checksums and its timing."""
     L, P = sh.num_layers, sh.num_pages
     kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
     W.fill_random_bytes(kv, W.SEED_DATA)
@@ -526,29 +670,80 @@ def _layered_once(torch, api, W, sh, steps):
     src = W.distinct(r, P, n)
     dst = np.setdiff1d(np.arange(P), src)
     tier.store(cache, src, np.arange(n))
-    _, copy_s = copy_streams(torch)
-    res = []
+    cons_s, copy_s = copy_streams(torch)
+    sums = torch.zeros((L, n), dtype=torch.int64, device="cuda")
+    res, cons = [], []
     for rep in range(steps + 1):
         start = torch.cuda.Event(enable_timing=True)
         events = [torch.cuda.Event(enable_timing=True) for _ in range(L)]
+        done = [torch.cuda.Event(enable_timing=True) for _ in range(L)]
         torch.cuda.synchronize()
         start.record(copy_s)
         tier.load_layered(cache, np.arange(n), dst, copy_s, events)
+        for l in range(L):
+            cons_s.wait_event(events[l])
+            cache.layer_checksum(l, dst, sums[l], stream=cons_s)
+            done[l].record(cons_s)
         torch.cuda.synchronize()
         if rep:
             res.append([start.elapsed_time(e) for e in events])
-    res = np.array(res)
+            cons.append([start.elapsed_time(e) for e in done])
+    res, cons = np.array(res), np.array(cons)
     total_ms = float(np.median(res[:, -1]))
     moved = n * tier.slot_bytes
     out = {"gbs": round(moved / (total_ms * 1e-3) / GB, 3), "ms": round(total_ms, 3),
            "slot_bytes": tier.slot_bytes,
            "time_to_first_layer_ms": round(float(np.median(res[:, 0])), 4),
            "per_layer_ms": round(float(np.median(np.diff(res, axis=1))), 4),
-           "layer_done_ms": [round(float(x), 3) for x in np.median(res, axis=0)]}
+           "layer_done_ms": [round(float(x), 3) for x in np.median(res, axis=0)],
+           "consumer": {
+               "kernel": "ea_layer_checksum: XOR of each destination page's layer piece",
+               "done_ms": [round(float(x), 3) for x in np.median(cons, axis=0)],
+               "finish_after_last_layer_ms": round(float(np.median(cons[:, -1] - res[:, -1])), 4),
+               "lag_per_layer_ms": round(float(np.median(cons - res)), 4),
+               "layers_consumed_before_load_done": int(np.median((cons < res[:, -1:]).sum(1)))}}
+    if cpu:
+        out["cpu_baseline"] = _layered_cpu_baseline(sh, tier, dst, sums.cpu().numpy())
     tier.close()
     cache.close()
     del kv, sc
     return out
+
+
+def _layered_cpu_baseline(sh, tier, dst, sums):
+    """The oracle on one core: the layer-by-layer load of the tier's image
+    into a host cache of the destination pages, then each layer's checksum
+    (compared with the consumer's), timed per layer."""
+    import oracle
+    n, L = len(dst), sh.num_layers
+    o = oracle.make_shape(n, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes,
+                          True)
+    host = tier.host_view()
+    ocache = np.zeros(L * n * sh.piece_bytes, np.uint8)
+    osc = np.zeros(L * n * 8, np.uint8)
+    idx = np.arange(n, dtype=np.int32)
+    prev = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {sorted(prev)[0]})
+    t_load, t_sum, ok = [], [], True
+    try:
+        for l in range(L):
+            t0 = time.perf_counter()
+            oracle.load_layer(o, host, ocache, osc, np.arange(n, dtype=np.int64), idx, l)
+            t1 = time.perf_counter()
+            want = oracle.layer_checksum(o, ocache, osc, l, idx)
+            t2 = time.perf_counter()
+            t_load.append(t1 - t0)
+            t_sum.append(t2 - t1)
+            ok &= bool(np.array_equal(sums[l].view(np.uint64), want))
+    finally:
+        os.sched_setaffinity(0, prev)
+    moved = n * tier.slot_bytes
+    return {"value": round(moved / sum(t_load) / GB, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle", "layer_checksum_ms": round(float(np.median(t_sum)) * 1e3, 2),
+            "load_layer_ms": round(float(np.median(t_load)) * 1e3, 2),
+            "consumer_checksums_match_oracle": ok,
+            "sample": f"the whole prefix: {L} layers of {n} pages, each loaded from the tier "
+                      f"image and checksummed"}
 
 
 def run_layered(args):
@@ -561,10 +756,11 @@ def run_layered(args):
     full = _layered_once(torch, api, W, W.LAYERED, args.steps)
     log(f"layered 4 heads: {full['gbs']} GB/s, {full['per_layer_ms']} ms per layer")
     torch.cuda.empty_cache()
-    shard = _layered_once(torch, api, W, W.LAYERED_TP8, args.steps)
+    shard = _layered_once(torch, api, W, W.LAYERED_TP8, args.steps, cpu=False)
     log(f"layered 1 head (TP8 shard): {shard['gbs']} GB/s, {shard['per_layer_ms']} ms per layer")
+    cpu = full.pop("cpu_baseline")
     extra = {"layered": {k: v for k, v in full.items() if k not in ("gbs", "ms")},
-             "tp8_shard": shard}
+             "tp8_shard": shard, "cpu_baseline": cpu}
     return _line("layered_fp8: 64k-token prefix, 48 layers x 4 heads x d128 fp8 + scales",
                  full["gbs"], "GB/s", full["ms"], args.steps, extra)
 
@@ -602,9 +798,49 @@ def run_tiny(args):
     moved = 2 * 32 * tier.info["page_bytes"] * steps
     tier.close()
     cache.close()
+    extra = {}
+    if not args.no_cpu_baseline:
+        extra["cpu_baseline"] = _tiny_cpu_baseline(sh, W, src, dst, slots, toks, offs)
+        log(f"cpu baseline: {extra['cpu_baseline']}")
     return _line("tiny: 2 layers x 2 heads x d64 bf16, 32 pages stored and loaded, 4 x 512 "
                  "tokens hashed", round(moved / el / GB, 3), "GB/s", round(el / steps * 1e3, 4),
-                 steps, {})
+                 steps, extra)
+
+
+def _tiny_cpu_baseline(sh, W, src, dst, slots, toks, offs):
+    """The oracle on one core running the tiny step on host arrays (hash
+    4 x 512 tokens, store 32 pages, load them into 32 others), repeated for
+    about two seconds; medians per phase."""
+    import oracle
+    o = oracle.make_shape(sh.num_pages, sh.num_layers, sh.page_tokens, sh.num_kv_heads,
+                          sh.head_dim, sh.elem_bytes)
+    sz = oracle.sizes(o)
+    cache = np.tile(W.host_bytes(W.SEED_DATA, sz["piece"]), sh.num_layers * sh.num_pages)
+    otier = np.zeros((W.TINY_TIER_SLOTS, sz["slot"]), np.uint8)
+
+    def run():
+        t = {"hash": [], "store": [], "load": []}
+        end = time.perf_counter() + 2.0
+        while time.perf_counter() < end or len(t["hash"]) < 5:
+            t0 = time.perf_counter()
+            oracle.hash_blocks(toks, offs, sh.page_tokens)
+            t1 = time.perf_counter()
+            oracle.store_blocks(o, cache, None, otier, src, slots)
+            t2 = time.perf_counter()
+            oracle.load_blocks(o, otier, cache, None, slots, dst)
+            t3 = time.perf_counter()
+            t["hash"].append(t1 - t0)
+            t["store"].append(t2 - t1)
+            t["load"].append(t3 - t2)
+        return {k: float(np.median(v)) for k, v in t.items()}, len(t["hash"])
+
+    med, reps = _pinned_one_core(run)
+    moved = 2 * 32 * sz["page"]
+    step = sum(med.values())
+    return {"value": round(moved / step / GB, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "ms_per_step": round(step * 1e3, 4),
+            "hash_tokens_per_s": round(int(offs[-1]) / med["hash"], 1),
+            "sample": f"the tiny step on host arrays, medians over {reps} runs"}
 
 
 # ------------------------------------------------------------ profiles
@@ -863,24 +1099,7 @@ def run_load_cost(args):
         src = W.distinct(r, sh.num_pages, top * C)
         tier.store(cache, src, np.arange(top), stream=cur)
         torch.cuda.synchronize()
-        pts = []
-        for n in sizes:
-            reps = 40 if n * C <= 64 else (10 if n * C <= 512 else 5)
-            dev_ms, wall_ms = [], []
-            for _ in range(reps):
-                slots = W.distinct(r, top, n)
-                dst = W.distinct(r, sh.num_pages, n * C)
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                e0.record(cur)
-                tier.load(cache, slots, dst, stream=cur)
-                e1.record(cur)
-                e1.synchronize()
-                wall_ms.append((time.perf_counter() - t0) * 1e3)
-                dev_ms.append(e0.elapsed_time(e1))
-            pts.append([n * C * sh.page_tokens, n * tier.slot_bytes, float(np.median(dev_ms)),
-                        float(np.median(wall_ms))])
+        pts = drivers.load_cost_sweep(torch, cache, tier, sh, sizes, cur, r)
         tier.close()
         cache.close()
         del kv
@@ -901,6 +1120,47 @@ def run_load_cost(args):
     return _line("load_cost: load sweeps, T_load(n) = n beta / B_eff + tau_load fitted at "
                  "96/128/24 KiB per token and 1,024-token chunks", head["B_eff_gbs"], "GB/s",
                  None, sum(len(x[3]) for x in setups), {"load_cost": res})
+
+
+RESTORE_FIT_SIZES = [1, 4, 16, 64, 256, 1024, 1500]
+RESTORE_FIT_REPS = 5
+RESTORE_FIT_LOADS = len(RESTORE_FIT_SIZES) * RESTORE_FIT_REPS
+
+
+def restore_fit(peak_h2d):
+    """Eq. 2's restore cost on one TP8 rank's shard of the Qwen3 KV (1 KV
+    head, 24 KiB per token), the per-rank setting of the paper's H20 figure:
+    a short sweep of loads (1 to 1,500 random resident slots into random
+    free pages, medians of 5) fitted to T_load(n) = n beta / B_eff + tau."""
+    import torch
+    from paper_2609_33762_amd import api, drivers, workloads as W
+    sh = W.QWEN3_TP8
+    cur = torch.cuda.current_stream()
+    kv, cache = _quiet_cache(torch, api, sh)
+    beta = sh.num_layers * sh.piece_bytes // sh.page_tokens
+    sizes = RESTORE_FIT_SIZES
+    top = max(sizes)
+    tier = api.Tier(cache, top * sh.num_layers * sh.piece_bytes + 4096)
+    r = W.rng(W.SEED_IDS)
+    tier.store(cache, W.distinct(r, sh.num_pages, top), np.arange(top), stream=cur)
+    torch.cuda.synchronize()
+    rows = drivers.load_cost_sweep(torch, cache, tier, sh, sizes, cur, r, reps=RESTORE_FIT_REPS)
+    tier.close()
+    cache.close()
+    del kv
+    torch.cuda.empty_cache()
+    tok = np.array([x[0] for x in rows], np.float64)
+    out = {"shape": "Qwen3-30B-A3B KV on one TP8 rank: 1 KV head, 24 KiB per token, "
+                    "16-token slots of 384 KiB",
+           "sweep_pages": sizes}
+    for k, col in (("device", 2), ("end_to_end", 3)):
+        B, tau, resid = drivers.fit_load_cost(tok * beta, np.array([x[col] for x in rows]) * 1e-3)
+        out[k] = {"B_eff_gbs": round(B / GB, 2), "tau_load_us": round(tau * 1e6, 1),
+                  "us_per_token_per_rank": round(beta / B * 1e6, 4),
+                  "frac_of_h2d_peak": round(B / GB / peak_h2d, 4),
+                  "max_rel_residual": round(resid, 3)}
+    out["context_h20_us_per_token_per_rank"] = 0.86
+    return out
 
 
 def run_plans(args):
@@ -1140,9 +1400,36 @@ def run_hash(args):
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
             "traffic": None}
+    extra = {"hash": out, "roofline": roof}
+    if not args.no_cpu_baseline:
+        extra["cpu_baseline"] = _hash_cpu_baseline(W)
+        log(f"cpu baseline: {extra['cpu_baseline']}")
     return _line("hash: chained SHA-256 keys of 16-token blocks, tokens in HBM",
-                 round(b["tokens_per_s"] / 1e9, 3), "G tokens/s", b["ms"], 20,
-                 {"hash": out, "roofline": roof})
+                 round(b["tokens_per_s"] / 1e9, 3), "G tokens/s", b["ms"], 20, extra)
+
+
+def _hash_cpu_baseline(W):
+    """The oracle on one core: the turn's 56,000-token prompt as one chain,
+    and 1,024 of the batch's 256-token sequences (medians of 5)."""
+    import oracle
+
+    def run():
+        res = {}
+        for name, lengths in (("turn_56k_prompt", [56000]), ("batch_1024x256", [256] * 1024)):
+            toks, offs = W.sequences(W.SEED_TOKENS, lengths)
+            ts = []
+            for _ in range(5):
+                t0 = time.perf_counter()
+                oracle.hash_blocks(toks, offs, 16)
+                ts.append(time.perf_counter() - t0)
+            res[name] = sum(lengths) / float(np.median(ts))
+        return res
+
+    res = _pinned_one_core(run)
+    return {"value": round(res["batch_1024x256"] / 1e9, 5), "unit": "G tokens/s", "cores": 1,
+            "kind": "oracle", "turn_56k_prompt_ms": round(56000 / res["turn_56k_prompt"] * 1e3, 3),
+            "sample": "the turn's 56,000-token prompt as one chain, and 1,024 sequences of 256 "
+                      "tokens (a 64th of the batch), medians of 5"}
 
 
 def main():
@@ -1202,6 +1489,9 @@ def main():
     plan_name = {N.EA_PLAN_DIRECT: "direct", N.EA_PLAN_STAGED: "staged"}
     plans = {"store": plan_name[tier.get_plan(N.EA_DIR_STORE)],
              "load": plan_name[tier.get_plan(N.EA_DIR_LOAD)]}
+    log("restore-cost fit (Eq. 2) on one TP8 rank's shard ...")
+    fit = restore_fit(ctx["peak"]["h2d"])
+    log(f"restore fit: {fit['device']}")
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle, one core) ...")
@@ -1258,15 +1548,18 @@ def main():
                       "frac_load": round(iso["load_gbs"] / peak["h2d"], 4),
                       "duplex_step_gbs": round(steps["gbs"], 2),
                       "frac_duplex_of_bidir": round(steps["gbs"] / peak["bidir"], 4)},
+        "restore_fit": fit,
         "cpu_baseline": cpu,
     }
     # launch order of each copy kernel in this run, for the profile summary:
     # the setup's prefix store, the warmup and timed steps, then the
     # isolated series (one untimed call before each)
+    # (then the restore fit's one store and its loads)
     dispatches = {
         "store": {"before": 1 + args.warmup, "timed": args.steps,
-                  "after": 1 + 3 + 1 + N_ISO["store"]},
-        "load": {"before": args.warmup, "timed": args.steps, "after": 1 + 3 + 1 + N_ISO["load"]},
+                  "after": 1 + 3 + 1 + N_ISO["store"] + 1},
+        "load": {"before": args.warmup, "timed": args.steps,
+                 "after": 1 + 3 + 1 + N_ISO["load"] + RESTORE_FIT_LOADS},
     }
     json.dump({"line": out, "steps": steps, "isolated": iso, "peak": peak,
                "dispatches": dispatches, "argv": sys.argv[1:]}, open(args.detail, "w"),

@@ -501,6 +501,18 @@ int ea_gather_blocks(ea_cache *cache, const int32_t *block_ids, int32_t n,
 int ea_scatter_blocks(ea_cache *cache, const void *d_src, int64_t src_bytes,
                       const int32_t *dst_pages, int32_t n, hipStream_t stream);
 
+/* Consumer stand-in for the layered load (not in the paper: it stands in
+ * for the attention over layer `layer` that a layered restore lets start
+ * early).  For each i < n, d_out[i] (device uint64, out_capacity >= n
+ * entries, 8-byte aligned) = the XOR of the little-endian 64-bit words of
+ * page pages[i]'s piece of that layer, XOR'd with its 8-byte scale word
+ * when the cache has scales.  pages: host int32[n] in [0, P), read before
+ * return.  Asynchronous on `stream`, which may wait on a layer_done event
+ * of ea_load_blocks_layered first. */
+int ea_layer_checksum(ea_cache *cache, int32_t layer, const int32_t *pages,
+                      int32_t n, uint64_t *d_out, int64_t out_capacity,
+                      hipStream_t stream);
+
 /* How stores and loads cross the host link:
  *  EA_PLAN_DIRECT: one kernel reads/writes the mapped pinned slots;
  *  EA_PLAN_STAGED: gather/scatter through an HBM staging buffer plus DMA

@@ -92,6 +92,7 @@ def lib():
             "eao_store_blocks": (C.c_int, [P, P, P, P, I64, P, P, U8, I32]),
             "eao_load_blocks": (C.c_int, [P, P, I64, P, P, P, P, I32]),
             "eao_load_layer": (C.c_int, [P, P, I64, P, P, P, P, I32, I32]),
+            "eao_layer_checksum": (C.c_int, [P, P, P, I32, P, I32, P]),
             "eao_tier_create": (C.c_int, [P, I64, P]),
             "eao_tier_destroy": (C.c_int, [P]),
             "eao_tier_capacity": (I64, [P]),
@@ -243,6 +244,17 @@ def load_layer(shape, tier, cache, scales, host_slots, dst_pages, layer):
                               _ptr(cache), _ptr(scales), _ptr(host_slots),
                               _ptr(dst_pages), len(host_slots), layer)
     _check("eao_load_layer", rc)
+
+
+def layer_checksum(shape, cache, scales, layer, pages):
+    """uint64 [n]: XOR of the 64-bit words of each page's layer piece (and
+    its scale word)."""
+    pages = np.ascontiguousarray(pages, dtype=np.int32)
+    out = np.zeros(max(len(pages), 1), np.uint64)
+    rc = lib().eao_layer_checksum(C.byref(shape), _ptr(cache), _ptr(scales), layer,
+                                  _ptr(pages), len(pages), _ptr(out))
+    _check("eao_layer_checksum", rc)
+    return out[:len(pages)]
 
 
 # --------------------------------------------------------------------- tier

@@ -359,3 +359,37 @@ int eao_load_layer(const eao_shape *sh, const uint8_t *tier,
   load_one_layer(sh, tier, cache, scales, host_slots, dst_pages, n, layer);
   return EAO_OK;
 }
+
+/* Consumer stand-in of the layered load: for each listed page, the XOR of
+ * the little-endian 64-bit words of its piece of layer `layer`, XOR'd with
+ * its 8-byte scale word when the shape has scales.  Not in the paper (it
+ * stands in for the attention that reads layer l once it has arrived). */
+int eao_layer_checksum(const eao_shape *sh, const uint8_t *cache,
+                       const uint8_t *scales, int32_t layer,
+                       const int32_t *pages, int32_t n, uint64_t *out) {
+  if (!shape_ok(sh) || !cache || n < 0 || (n > 0 && (!pages || !out)))
+    return EAO_EINVAL;
+  if (layer < 0 || layer >= sh->num_layers) return EAO_EINVAL;
+  if (sh->has_scales && !scales) return EAO_EINVAL;
+  const int64_t piece = eao_piece_bytes(sh);
+  const int64_t P = sh->num_pages;
+  for (int32_t i = 0; i < n; ++i)
+    if (pages[i] < 0 || pages[i] >= P) return EAO_EINVAL;
+  for (int32_t i = 0; i < n; ++i) {
+    const uint8_t *p = cache + ((int64_t)layer * P + pages[i]) * piece;
+    uint64_t x = 0;
+    for (int64_t w = 0; w < piece / 8; ++w) {
+      uint64_t v = 0;
+      for (int b = 0; b < 8; ++b) v |= (uint64_t)p[8 * w + b] << (8 * b);
+      x ^= v;
+    }
+    if (sh->has_scales) {
+      const uint8_t *s = scales + ((int64_t)layer * P + pages[i]) * 8;
+      uint64_t v = 0;
+      for (int b = 0; b < 8; ++b) v |= (uint64_t)s[b] << (8 * b);
+      x ^= v;
+    }
+    out[i] = x;
+  }
+  return EAO_OK;
+}

@@ -172,6 +172,13 @@ int eao_load_layer(const eao_shape *sh, const uint8_t *tier,
                    const int64_t *host_slots, const int32_t *dst_pages,
                    int32_t n, int32_t layer);
 
+/* Consumer stand-in of the layered load (not in the paper): out[i] = XOR
+ * of the little-endian 64-bit words of page pages[i]'s piece of `layer`,
+ * XOR'd with its 8-byte scale word when the shape has scales. */
+int eao_layer_checksum(const eao_shape *sh, const uint8_t *cache,
+                       const uint8_t *scales, int32_t layer,
+                       const int32_t *pages, int32_t n, uint64_t *out);
+
 /* ---------------------------------------------------- host tier metadata */
 
 /* Slot states. */

@@ -112,6 +112,7 @@ SIGNATURES = {
     "ea_load_blocks_layered": (_INT, [_P, _P, _P, _P, _I32, _P, _P, _I32]),
     "ea_gather_blocks": (_INT, [_P, _P, _I32, _P, _I64, _P]),
     "ea_scatter_blocks": (_INT, [_P, _P, _I64, _P, _I32, _P]),
+    "ea_layer_checksum": (_INT, [_P, _I32, _P, _I32, _P, _I64, _P]),
     "ea_tier_set_plan": (_INT, [_P, _INT, _INT]),
     "ea_tier_get_plan": (_INT, [_P, _INT, _P]),
     "ea_peak_probe": (_INT, [_P, _P, _I64, _INT, _INT, _P]),

@@ -116,6 +116,17 @@ class Cache:
         N.check("ea_scatter_blocks", N.load().ea_scatter_blocks(
             self._h, src.data_ptr(), _nbytes(src), _ptr(d), len(d), _stream(stream)))
 
+    def layer_checksum(self, layer, pages, d_out, stream=None):
+        """d_out (device uint64 tensor, >= len(pages) entries) gets the XOR
+        checksum of each page's piece of `layer` (and its scale word)."""
+        import torch
+        p = _i32(pages)
+        if not d_out.is_cuda or d_out.dtype not in (torch.int64, torch.uint64) or \
+                not d_out.is_contiguous() or d_out.numel() < len(p):
+            raise ValueError("d_out must be a contiguous 64-bit device tensor of len(pages)")
+        N.check("ea_layer_checksum", N.load().ea_layer_checksum(
+            self._h, layer, _ptr(p), len(p), d_out.data_ptr(), d_out.numel(), _stream(stream)))
+
 
 def make_policy(kappa, block_tokens, beta_rank, theta_ppm=950000, activity_window=64,
                 length_window=256, mode=N.EA_ADMIT_CONDITIONED, telemetry=1):

@@ -1001,6 +1001,32 @@ int ea_scatter_blocks(ea_cache *c, const void *d_src, int64_t src_bytes,
   }
 }
 
+// ------------------------------------------- consumer stand-in (checksum)
+
+int ea_layer_checksum(ea_cache *c, int32_t layer, const int32_t *pages, int32_t n,
+                      uint64_t *d_out, int64_t out_capacity, hipStream_t stream) {
+  try {
+    if (!c || n < 0 || layer < 0 || layer >= c->d.num_layers) return EA_EINVAL;
+    if (n == 0) return EA_OK;
+    if (!pages || !d_out || !aligned(d_out, 8) || out_capacity < n) return EA_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+      if (pages[i] < 0 || pages[i] >= c->d.num_pages) return EA_EINVAL;
+    DeviceScope ds(c->device);
+    EA_TRY(ds.status());
+    std::lock_guard<std::mutex> lk(c->mu);
+    const int64_t *unused = nullptr;
+    const int32_t *d_pages = nullptr;
+    int region;
+    EA_TRY(c->ring.upload(nullptr, pages, n, &unused, &d_pages, &region));
+    EA_HIP(ea::launch_layer_checksum(static_cast<const uint8_t *>(c->d.base),
+                                     static_cast<const uint8_t *>(c->d.scale_base),
+                                     c->d.num_pages, c->piece, layer, d_pages, n, d_out, stream));
+    return c->ring.release(region, stream);
+  } catch (const std::bad_alloc &) {
+    return EA_ENOMEM;
+  }
+}
+
 // --------------------------------------------------------------- peak probe
 
 int ea_peak_probe(ea_tier *t, void *d_buf, int64_t bytes, int direction, int reps,

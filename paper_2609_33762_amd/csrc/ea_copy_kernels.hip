@@ -152,6 +152,43 @@ __global__ __launch_bounds__(kThreads) void copy_hbm(PieceCopy a, const int32_t 
   piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, inl);
 }
 
+// Consumer stand-in of the layered load: wave w of the grid folds the
+// pieces of pages w, w + waves, ... of one layer into the XOR of their
+// little-endian 64-bit words (and the page's scale word), one 16-byte
+// vector per lane per step, then across the wave by lane swaps.
+__global__ __launch_bounds__(kThreads) void layer_checksum(
+    const uint8_t *__restrict__ cache, const uint8_t *__restrict__ scales, int64_t num_pages,
+    int64_t piece_bytes, int32_t layer, const int32_t *__restrict__ pages, int32_t n,
+    uint64_t *__restrict__ out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
+  const int64_t first = (int64_t)blockIdx.x * (kThreads / kWave) +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t nvec = piece_bytes >> 4;
+  for (int64_t i = first; i < n; i += waves) {
+    const int64_t page = pages[i];
+    const u32x4 *src =
+        reinterpret_cast<const u32x4 *>(cache + ((int64_t)layer * num_pages + page) * piece_bytes);
+    uint32_t lo = 0, hi = 0;
+    for (int64_t v = lane; v < nvec; v += kWave) {
+      const u32x4 x = src[v];
+      lo ^= x.x ^ x.z;
+      hi ^= x.y ^ x.w;
+    }
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      lo ^= (uint32_t)__shfl_xor((int)lo, d, kWave);
+      hi ^= (uint32_t)__shfl_xor((int)hi, d, kWave);
+    }
+    if (lane == 0) {
+      uint64_t x = ((uint64_t)hi << 32) | lo;
+      if (scales != nullptr)
+        x ^= *reinterpret_cast<const uint64_t *>(scales + ((int64_t)layer * num_pages + page) * 8);
+      out[i] = x;
+    }
+  }
+}
+
 // One workgroup of one wave per entry: out[b] = the XCD of workgroup b.
 __global__ __launch_bounds__(64) void xcd_probe(int32_t *__restrict__ out) {
   if (threadIdx.x == 0) out[blockIdx.x] = (int32_t)(__builtin_amdgcn_s_getreg(kXccIdReg) & 0xFu);
@@ -217,6 +254,19 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok) {
   (void)hipStreamDestroy(s);
   if (e == hipSuccess) *ok = good;
   return e;
+}
+
+hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,
+                                 int64_t piece_bytes, int32_t layer, const int32_t *pages,
+                                 int32_t n, uint64_t *out, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t waves_per_group = kThreads / kWave;
+  int64_t grid = (n + waves_per_group - 1) / waves_per_group;
+  if (grid > 1024) grid = 1024;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(layer_checksum, dim3((unsigned)grid), dim3(kThreads), 0, stream, cache,
+                     scales, num_pages, piece_bytes, layer, pages, n, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,

@@ -79,6 +79,11 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok);
 hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
                              int64_t workgroups, hipStream_t stream);
 
+// XOR checksum of one layer's piece of each of n pages (device page ids).
+hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,
+                                 int64_t piece_bytes, int32_t layer, const int32_t *pages,
+                                 int32_t n, uint64_t *out, hipStream_t stream);
+
 // SHA-256 chained keys.
 //  mid:  device [n_keys][8] words scratch
 //  d_key_offsets: device [n_seqs+1] key offsets; d_tok_offsets: device

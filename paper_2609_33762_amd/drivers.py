@@ -349,3 +349,33 @@ def fit_load_cost(nbytes, seconds):
     a, tau = np.polyfit(x, y, 1)
     resid = np.abs(a * x + tau - y) / y
     return 1.0 / a, tau, float(resid.max())
+
+
+def load_cost_sweep(torch, cache, tier, sh, sizes, stream, rng, reps=None):
+    """Loads of n random resident slots into random free pages for each n in
+    `sizes` (slots 0..max(sizes)-1 of `tier` must hold stored chunks).
+    Returns rows [tokens, bytes, device ms, end-to-end ms], each the median
+    over its repetitions: device time between HIP events on the load's
+    stream, end to end from the call to completion on the host clock."""
+    C = tier.chunk_pages
+    top = max(sizes)
+    rows = []
+    for n in sizes:
+        k = reps or (40 if n * C <= 64 else (10 if n * C <= 512 else 5))
+        dev_ms, wall_ms = [], []
+        for _ in range(k):
+            slots = W.distinct(rng, top, n)
+            dst = W.distinct(rng, sh.num_pages, n * C)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            e0.record(stream)
+            tier.load(cache, slots, dst, stream=stream)
+            e1.record(stream)
+            e1.synchronize()
+            wall_ms.append((time.perf_counter() - t0) * 1e3)
+            dev_ms.append(e0.elapsed_time(e1))
+        rows.append([n * C * sh.page_tokens, n * tier.slot_bytes, float(np.median(dev_ms)),
+                     float(np.median(wall_ms))])
+    return rows

@@ -343,3 +343,24 @@ def test_device_buffer_sizes_are_checked():
     assert lib.ea_load_blocks_layered(p.tier._h, p.cache.handle, slots.ctypes.data,
                                       dst.ctypes.data, 4, None, evs, 1) == N.EA_EINVAL
     p.close()
+
+
+@pytest.mark.parametrize("scales", [False, True])
+@pytest.mark.parametrize("n", [1, 37, 300])
+def test_layer_checksum_matches_the_oracle(scales, n):
+    # the consumer stand-in of the layered load, on random bytes (fp8 NaN
+    # patterns included), ragged page lists with repeats
+    torch = need_gpu()
+    L, P = 3, 400
+    p = Pair(P, L, 16, 2, 64, 1, 8, scales=scales, seed=70 + n)
+    r = W.rng(70 + n)
+    pages = r.integers(0, P, size=n).astype(np.int32)
+    out = torch.full((n + 3,), 7, dtype=torch.int64, device="cuda")
+    for layer in range(L):
+        p.cache.layer_checksum(layer, pages, out)
+        want = oracle.layer_checksum(p.oshape, p.o_cache, p.o_sc, layer, pages)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().view(np.uint64)
+        assert np.array_equal(got[:n], want), layer
+        assert (got[n:] == 7).all()
+    p.close()

@@ -1,0 +1,68 @@
+"""The restore cost of Eq. 2 measured and fitted on one TP8 rank's shard of
+the Qwen3-30B-A3B KV (24 KiB per token, the per-rank setting of the paper's
+0.86 us per token): loads of 1 to 1,500 random resident slots into random
+free pages, fitted to T_load(n) = n beta / B_eff + tau_load by least squares
+(App. "Offload Cost and Prefix-Survival Model", Eq. 2).
+
+* The oracle's Eq. 2 with the fitted B_eff and tau_load reproduces every
+  measured point within 15% (the smallest loads take about 20 us, where a
+  microsecond or two of launch jitter is 5-10%).
+* B_eff cannot exceed the measured pinned-copy peak of the host link.
+* The loads in the sweep move the right bytes (a load after the sweep is
+  compared with the oracle)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_33762_amd import _native as N, api, drivers, workloads as W
+
+from gpu_common import need_gpu, oracle_pages, oracle_slots, pages_to_host
+
+pytestmark = pytest.mark.gpu
+
+TOLERANCE = 0.15
+
+
+def test_restore_fit_on_one_tp8_rank():
+    torch = need_gpu()
+    sh = W.QWEN3_TP8
+    L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
+    beta = L * piece // sh.page_tokens
+    assert beta == 24576
+    kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+    W.fill_bf16_normal(kv, W.SEED_DATA)
+    kv3 = kv.view(L, P, piece)
+    cache = api.Cache(kv, P, L, sh.page_tokens, sh.num_kv_heads, sh.head_dim, sh.elem_bytes)
+    sizes = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 1500]
+    tier = api.Tier(cache, 2800 * L * piece)  # room for the 1 GiB peak probe
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    peak = tier.peak_probe(buf, 1 << 30, N.EA_DIR_LOAD, reps=5)
+    del buf
+    r = W.rng(W.SEED_IDS)
+    top = max(sizes)
+    src = W.distinct(r, P, top)
+    cur = torch.cuda.current_stream()
+    tier.store(cache, src, np.arange(top), stream=cur)
+    torch.cuda.synchronize()
+    src_bytes = pages_to_host(torch, kv3, src)  # the sweep's loads may land on source pages
+    rows = np.array(drivers.load_cost_sweep(torch, cache, tier, sh, sizes, cur, r))
+    tok, sec = rows[:, 0], rows[:, 2] * 1e-3
+    B, tau, resid = drivers.fit_load_cost(tok * beta, sec)
+    print(f"B_eff {B / 1e9:.2f} GB/s, tau_load {tau * 1e6:.1f} us, "
+          f"{beta / B * 1e6:.3f} us per token, peak {peak:.2f} GB/s, residual {resid:.3f}")
+    for n, s in zip(tok, sec):
+        pred = oracle.restore_time(float(n), float(beta), float(B), float(tau))
+        assert abs(pred - s) / s <= TOLERANCE, (n, s, pred)
+    assert 0 < B <= peak * 1e9 * 1.01
+    assert tau > 0
+    # the sweep's loads move the right bytes
+    slots = W.distinct(r, top, 64)
+    dst = W.distinct(r, P, 64)
+    tier.load(cache, slots, dst, stream=cur)
+    torch.cuda.synchronize()
+    want = oracle_pages(sh, oracle_slots(sh, src_bytes[:, slots]))
+    assert np.array_equal(pages_to_host(torch, kv3, dst), want)
+    tier.close()
+    cache.close()
+    del kv, kv3
+    torch.cuda.empty_cache()

@@ -180,12 +180,14 @@ def test_layered_fp8_prefix_full_size(sh):
     assert h == n
     copy_s, cons_s = torch.cuda.Stream(), torch.cuda.Stream()
     events = [torch.cuda.Event() for _ in range(L)]
+    sums = torch.zeros((L, n), dtype=torch.int64, device="cuda")
     tier.load_layered(cache, hslots, dst, copy_s, events)
     snaps = []
     with torch.cuda.stream(cons_s):
         for l in range(L):
             cons_s.wait_event(events[l])
             snaps.append((kv3[l].index_select(0, d).clone(), sc3[l].index_select(0, d).clone()))
+            cache.layer_checksum(l, dst, sums[l], stream=cons_s)  # the consumer stand-in
     torch.cuda.synchronize()
     tier.unpin(hslots)
     for l in range(L):
@@ -208,6 +210,14 @@ def test_layered_fp8_prefix_full_size(sh):
     got = pages_to_host(torch, kv3, dst)
     assert_rows_equal(got.transpose(1, 0, 2), ocache.transpose(1, 0, 2), "loaded pages")
     assert np.array_equal(sc3[:, d].cpu().numpy(), osc)
+    # the consumer's per-layer checksums, taken right after each event, equal
+    # the oracle's checksums of its own load
+    o_full = oshape_of(sh, num_pages=n)
+    got_sums = sums.cpu().numpy().view(np.uint64)
+    for l in range(L):
+        want_l = oracle.layer_checksum(o_full, ocache.reshape(-1), osc.reshape(-1), l,
+                                       np.arange(n, dtype=np.int32))
+        assert np.array_equal(got_sums[l], want_l), l
     # only destination pages changed since the poison was written
     assert np.isin(changed_pages(torch, kv3, before3), dst).all()
     assert np.isin(changed_pages(torch, sc3, before_sc3), dst).all()
