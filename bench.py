@@ -46,7 +46,7 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_33762_amd", "csrc", "ea_copy_kernels.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_hbm_bytes.md")
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", "piece_copy_qwen3_turn_kernel_trace.md")
-PLANS_SUMMARY = os.path.join(ROOT, "profiles", "transfer_plans_qwen3_turn.md")
+PLANS_SUMMARY = os.path.join(ROOT, "profiles", "transfer_plans_size_classes.md")
 N_ISO = {"store": 5, "load": 5, "gather": 20, "scatter": 20}
 
 
@@ -1061,6 +1061,109 @@ def summarize_profiles(d):
     print(open(TRAFFIC_SUMMARY).read())
 
 
+HBM_COUNTER_PASSES = {
+    "wr1": "TCC_EA0_WRREQ_sum TCC_EA0_WRREQ_64B_sum TCC_EA0_WRREQ_STALL_sum "
+           "TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum GRBM_GUI_ACTIVE",
+    "wr2": "TCC_EA0_WRREQ_LEVEL_sum TCC_TOO_MANY_EA_WRREQS_STALL_sum TCC_EA0_WRREQ_WRITE_DRAM_sum "
+           "TCC_EA0_WRREQ_WRITE_GMI_32B_sum",
+    "rd": "TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_LEVEL_sum TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum "
+          "TCC_TAG_STALL_sum",
+    "tcp": "TCP_TCC_WRITE_REQ_LATENCY_sum TCP_TCC_WRITE_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum "
+           "TCP_TCC_READ_REQ_sum",
+    "tlb": "TCP_UTCL1_TRANSLATION_MISS_sum TCP_UTCL1_TRANSLATION_HIT_sum "
+           "TCP_UTCL1_STALL_UTCL2_REQ_OUT_OF_CREDITS_sum TCP_PENDING_STALL_CYCLES_sum",
+}
+HBM_COUNTERS_SUMMARY = os.path.join(ROOT, "profiles", "hbm_gather_scatter_counters.md")
+
+
+def summarize_hbm_counters(d):
+    """Write the gather-versus-scatter counter summary from directory d:
+    for each unit order (entry, layer) one rocprofv3 --pmc run per pass of
+    HBM_COUNTER_PASSES over `bench.py --isolated-only`; the isolated gather
+    and scatter series (their last N_ISO launches) are averaged."""
+    cmd = ("EA_HBM_ORDER={o} rocprofv3 --pmc {c} --output-format csv -d bench_out/hbm_{o}_{p} "
+           "-o {p} -- python3 bench.py --isolated-only --no-cpu-baseline "
+           "--detail bench_out/hbm_{o}_{p}.json")
+    per = {}
+    iso = {}
+    for order in ("entry", "layer"):
+        for p in HBM_COUNTER_PASSES:
+            f = os.path.join(d, f"hbm_{order}_{p}", f"{p}_counter_collection.csv")
+            if not os.path.exists(f):
+                continue
+            vals = {}
+            for x in csv.DictReader(open(f)):
+                k = _short(x["Kernel_Name"])
+                if k in ("gather", "scatter"):
+                    key = (k, x["Counter_Name"])
+                    vals.setdefault(key, {}).setdefault(x.get("Dispatch_Id", len(vals)), 0.0)
+                    vals[key][x.get("Dispatch_Id")] += float(x["Counter_Value"])
+            for (k, c), disp in vals.items():
+                v = list(disp.values())[-N_ISO[k]:]
+                per[(order, k, c)] = float(np.mean(v))
+            det = os.path.join(d, f"hbm_{order}_{p}.json")
+            if os.path.exists(det):
+                iso.setdefault(order, []).append(json.load(open(det))["isolated"])
+    lines = ["# HBM gather versus scatter: what the write path does", "",
+             "Qwen3-30B-A3B turn shape: 2,000 random pages of 1.5 MiB (48 pieces of 32 KiB each) "
+             "gathered into a slot-layout HBM buffer and scattered back, 256 (scatter) and 512 "
+             "(gather) workgroups.  Per launch averages over the isolated series "
+             f"({N_ISO['gather']} launches each).", "",
+             "Commands (from the repository root on the MI355X), one run per pass and order:", ""]
+    for p, c in HBM_COUNTER_PASSES.items():
+        lines.append("    " + cmd.format(o="entry", c=c, p=p))
+    lines += ["", "and the same with EA_HBM_ORDER=layer; then "
+              "`python3 bench.py --summarize-hbm-counters bench_out`.", "",
+              f"kernel_source_sha256: {kernel_source_hash()}", ""]
+    if iso:
+        lines += ["| order | gather TB/s | scatter TB/s (HIP events, the same runs) |",
+                  "|---|---|---|"]
+        for o, runs in iso.items():
+            g = [x["gather_gbs"] / 1e3 for x in runs]
+            sc = [x["scatter_gbs"] / 1e3 for x in runs]
+            lines.append(f"| {o} | {min(g):.2f}-{max(g):.2f} | {min(sc):.2f}-{max(sc):.2f} |")
+        lines.append("")
+
+    def v(o, k, c):
+        return per.get((o, k, c), float("nan"))
+
+    rows = [("EA write requests", "TCC_EA0_WRREQ_sum", None),
+            ("of them 64-byte", "TCC_EA0_WRREQ_64B_sum", None),
+            ("write requests to DRAM", "TCC_EA0_WRREQ_WRITE_DRAM_sum", None),
+            ("32-byte writes over GMI", "TCC_EA0_WRREQ_WRITE_GMI_32B_sum", None),
+            ("avg EA write latency (cycles)", "TCC_EA0_WRREQ_LEVEL_sum", "TCC_EA0_WRREQ_sum"),
+            ("write stall cycles", "TCC_EA0_WRREQ_STALL_sum", None),
+            ("  of them out of DRAM credits", "TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum", None),
+            ("  at the pending-write limit", "TCC_TOO_MANY_EA_WRREQS_STALL_sum", None),
+            ("EA read requests", "TCC_EA0_RDREQ_sum", None),
+            ("avg EA read latency (cycles)", "TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_RDREQ_sum"),
+            ("read stall cycles, out of DRAM credits", "TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum", None),
+            ("L2 tag stall cycles", "TCC_TAG_STALL_sum", None),
+            ("avg L1-to-L2 write latency (cycles)", "TCP_TCC_WRITE_REQ_LATENCY_sum",
+             "TCP_TCC_WRITE_REQ_sum"),
+            ("avg L1-to-L2 read latency (cycles)", "TCP_TCC_READ_REQ_LATENCY_sum",
+             "TCP_TCC_READ_REQ_sum"),
+            ("address translation misses (L1 TLB)", "TCP_UTCL1_TRANSLATION_MISS_sum", None),
+            ("address translation hits", "TCP_UTCL1_TRANSLATION_HIT_sum", None),
+            ("stalls waiting on L2 TLB credits", "TCP_UTCL1_STALL_UTCL2_REQ_OUT_OF_CREDITS_sum",
+             None),
+            ("L1 pending stall cycles", "TCP_PENDING_STALL_CYCLES_sum", None),
+            ("GPU busy cycles (GRBM_GUI_ACTIVE)", "GRBM_GUI_ACTIVE", None)]
+    orders = [o for o in ("entry", "layer") if any(key[0] == o for key in per)]
+    head = "| per launch | " + " | ".join(f"gather ({o})" for o in orders) + " | " + \
+        " | ".join(f"scatter ({o})" for o in orders) + " |"
+    lines += [head, "|---|" + "---|" * (2 * len(orders))]
+    for label, c, denom in rows:
+        cells = []
+        for k in ("gather", "scatter"):
+            for o in orders:
+                x = v(o, k, c) / v(o, k, denom) if denom else v(o, k, c)
+                cells.append(f"{x:,.1f}" if denom else f"{x:,.0f}")
+        lines.append(f"| {label} | " + " | ".join(cells) + " |")
+    open(HBM_COUNTERS_SUMMARY, "w").write("\n".join(lines) + "\n")
+    print(open(HBM_COUNTERS_SUMMARY).read())
+
+
 def _quiet_cache(torch, api, sh, num_pages=None):
     """A cache of shape sh (contents irrelevant for timing: left unfilled)."""
     P = num_pages or sh.num_pages
@@ -1163,47 +1266,74 @@ def restore_fit(peak_h2d):
     return out
 
 
+PLAN_CASES = (
+    # name, shape, chunk pages, pages per call (store / load), calls timed
+    ("qwen3_turn", "QWEN3", 1, 2000, 1500, 3),
+    ("tp8_shard", "QWEN3_TP8", 1, 2000, 1500, 3),
+    ("tp8_chunks_1024_tokens", "QWEN3_TP8", 64, 31, 23, 3),
+    ("layered_fp8_prefix", "LAYERED", 1, 4096, 4096, 3),
+    ("dense_8_pages", "DENSE", 1, 8, 8, 50),
+    ("dense_4_pages", "DENSE", 1, 4, 4, 50),
+    ("dense_1_page", "DENSE", 1, 1, 1, 50),
+)
+
+
 def run_plans(args):
-    """The turn's store (2,000 pages) and load (1,500 pages) alone under one
-    transfer plan (--plan direct or staged), first to consecutive slots and
-    then to random ones.  Direct: one kernel between the cache and the mapped
-    pinned slots.  Staged: a paged gather or scatter through an HBM staging
-    buffer plus hipMemcpyAsync of each run of consecutive slots.  Each
-    operation is one untimed call and three timed ones between HIP events.
-    The cache is left unfilled (contents do not change the timing), so the
-    only copy kernels in the process are the plan's own: a rocprofv3 run of
-    this command attributes its kernels and byte counters to the plan."""
+    """Stores and loads alone under one transfer plan (--plan direct or
+    staged) for each size class the workloads use: the Qwen3 turn (2,000 /
+    1,500 pages of 1.5 MiB), one TP8 rank's turn (384 KiB pages, and the
+    paper's 1,024-token chunks of 24 MiB), the layered fp8 prefix (768 KiB
+    pages with scales) and the dense model's calls of 8, 4 and 1 pages of
+    2 MiB; each first to consecutive slots, then to random ones.  Direct:
+    one kernel between the cache and the mapped pinned slots.  Staged: a
+    paged gather or scatter through an HBM staging buffer plus
+    hipMemcpyAsync of each run of consecutive slots.  Each operation is one
+    untimed call and then the timed ones between HIP events.  Caches are
+    left unfilled (contents do not change the timing), so the only copy
+    kernels in the process are the plan's own: a rocprofv3 run of this
+    command attributes its kernels and byte counters to the plan."""
     import torch
     from paper_2609_33762_amd import api, _native as N, workloads as W
     torch.cuda.set_device(0)
     plan_name = "staged" if args.plan == "staged" else "direct"
     plan = N.EA_PLAN_STAGED if plan_name == "staged" else N.EA_PLAN_DIRECT
-    sh = W.QWEN3
-    kv, cache = _quiet_cache(torch, api, sh)
-    r = W.rng(W.SEED_IDS)
-    n_s, n_l = W.QWEN3_STORE_PAGES, W.QWEN3_LOAD_PAGES
-    tier = api.Tier(cache, W.QWEN3_TIER_BYTES)
-    tier.set_plan(N.EA_DIR_BOTH, plan)
-    src = W.distinct(r, sh.num_pages, n_s)
-    dst = W.distinct(r, sh.num_pages, n_l, exclude=src)
-    page = tier.info["page_bytes"]
     cur = torch.cuda.current_stream()
-    out, reps, link = {}, 3, 0
-    for slots_name, slots in (("consecutive", np.arange(n_s, dtype=np.int64)),
-                              ("random", W.distinct(r, tier.capacity, n_s))):
-        st = event_ms(torch, lambda: tier.store(cache, src, slots, stream=cur), cur, reps)
-        ld = event_ms(torch, lambda: tier.load(cache, slots[:n_l], dst, stream=cur), cur, reps)
-        out[slots_name] = {"store_ms": round(st, 4), "store_gbs": round(n_s * page / st / 1e6, 2),
-                           "load_ms": round(ld, 4), "load_gbs": round(n_l * page / ld / 1e6, 2)}
-        link += (1 + reps) * (n_s + n_l) * page
-        log(f"plan {plan_name}, {slots_name} slots: {out[slots_name]}")
-    torch.cuda.synchronize()
-    tier.close()
-    cache.close()
-    del kv
-    torch.cuda.empty_cache()
-    return _line(f"plans: the Qwen3 turn's store and load alone, {plan_name} plan, consecutive and "
-                 "random slots", out["random"]["store_gbs"], "GB/s", None, reps,
+    out, link = {}, 0
+    for name, shape, C, n_s, n_l, reps in PLAN_CASES:
+        sh = getattr(W, shape)
+        r = W.rng(W.SEED_IDS)
+        P = sh.num_pages
+        kv = torch.empty(sh.cache_bytes, dtype=torch.uint8, device="cuda")
+        sc = torch.empty(sh.num_layers * P * 8, dtype=torch.uint8, device="cuda") \
+            if sh.has_scales else None
+        cache = api.Cache(kv, P, sh.num_layers, sh.page_tokens, sh.num_kv_heads, sh.head_dim,
+                          sh.elem_bytes, scales=sc)
+        slot_pages = sh.num_layers * sh.piece_bytes * C + (4096 if sh.has_scales else 0)
+        cap_slots = max(2 * n_s, 64)
+        tier = api.Tier(cache, cap_slots * slot_pages, chunk_pages=C)
+        tier.set_plan(N.EA_DIR_BOTH, plan)
+        src = W.distinct(r, P, n_s * C)
+        dst = W.distinct(r, P, n_l * C, exclude=src)
+        page = tier.slot_bytes
+        res = {}
+        for slots_name, slots in (("consecutive", np.arange(n_s, dtype=np.int64)),
+                                  ("random", W.distinct(r, tier.capacity, n_s))):
+            st = event_ms(torch, lambda: tier.store(cache, src, slots, stream=cur), cur, reps)
+            ld = event_ms(torch, lambda: tier.load(cache, slots[:n_l], dst, stream=cur), cur,
+                          reps)
+            res[slots_name] = {"store_ms": round(st, 4),
+                               "store_gbs": round(n_s * page / st / 1e6, 2),
+                               "load_ms": round(ld, 4), "load_gbs": round(n_l * page / ld / 1e6, 2)}
+            link += (1 + reps) * (n_s + n_l) * page
+        out[name] = {"slot_bytes": page, "store_slots": n_s, "load_slots": n_l, **res}
+        log(f"plan {plan_name}, {name}: {res}")
+        torch.cuda.synchronize()
+        tier.close()
+        cache.close()
+        del kv, sc
+        torch.cuda.empty_cache()
+    return _line(f"plans: stores and loads alone per size class, {plan_name} plan, consecutive and "
+                 "random slots", out["qwen3_turn"]["random"]["store_gbs"], "GB/s", None, 3,
                  {"plan": plan_name, "plans": out, "link_bytes_all_calls": link})
 
 
@@ -1215,8 +1345,8 @@ def summarize_plans(d):
     m = re.search(r"FETCH_SIZE is scaled by ([0-9.]+) and WRITE_SIZE by ([0-9]+\.[0-9]+)",
                   open(TRAFFIC_SUMMARY).read())
     cal_f, cal_w = float(m.group(1)), float(m.group(2))
-    lines = ["# Transfer plans: direct kernels against HBM staging plus hipMemcpyAsync, "
-             "Qwen3-30B-A3B turn", "",
+    lines = ["# Transfer plans: direct kernels against HBM staging plus hipMemcpyAsync, per "
+             "size class", "",
              "Commands (from the repository root on the MI355X), for P in direct and staged:", "",
              "    rocprofv3 --kernel-trace --memory-copy-trace --stats --output-format csv "
              "-d bench_out/plans_P/trace -o trace -- python3 bench.py --workload plans --plan P",
@@ -1226,19 +1356,28 @@ def summarize_plans(d):
              "-- python3 bench.py --workload plans --plan P",
              "    python3 bench.py --summarize-plans bench_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
-             "Each process runs one plan: the turn's 2,000-page store and 1,500-page load alone, "
-             "to consecutive slots and then to random ones, one untimed and three timed calls "
-             "each.  Every copy kernel in a process belongs to its plan, apart from the few "
+             "Each process runs one plan over every size class: stores and loads alone, to "
+             "consecutive slots and then to random ones, one untimed call and then the timed "
+             "ones.  Every copy kernel in a process belongs to its plan, apart from the few "
              "bytes the library's one-time XCD probe copies back.  Byte counters are "
              f"scaled as in the piece-copy summary (FETCH_SIZE x{cal_f:.3f}, WRITE_SIZE "
              f"x{cal_w:.3f}) and include the host-memory side.", ""]
+    both = {plan: json.load(open(os.path.join(d, f"plans_{plan}", "line.json")))["plans"]
+            for plan in ("direct", "staged")}
+    lines += ["## Rates per size class (HIP events, GB/s; store / load)", "",
+              "| case | slot bytes | slots per call (store / load) | direct, consecutive | "
+              "staged, consecutive | direct, random | staged, random |", "|---|---|---|---|---|---|---|"]
+    for case, v in both["direct"].items():
+        w = both["staged"][case]
+        cell = lambda x, k: f"{x[k]['store_gbs']} / {x[k]['load_gbs']}"  # noqa: E731
+        lines.append(f"| {case} | {v['slot_bytes']} | {v['store_slots']} / {v['load_slots']} | "
+                     f"{cell(v, 'consecutive')} | {cell(w, 'consecutive')} | "
+                     f"{cell(v, 'random')} | {cell(w, 'random')} |")
+    lines.append("")
     for plan in ("direct", "staged"):
         base = os.path.join(d, f"plans_{plan}")
         res = json.load(open(os.path.join(base, "line.json")))
-        lines += [f"## {plan}", "", "| slots | store GB/s (HIP events) | load GB/s (HIP events) |",
-                  "|---|---|---|"]
-        for k, v in res["plans"].items():
-            lines.append(f"| {k} | {v['store_gbs']} | {v['load_gbs']} |")
+        lines += [f"## {plan}", ""]
         lines += ["", "| kernel | calls | total ms | avg ms |", "|---|---|---|---|"]
         for x in csv.DictReader(open(os.path.join(base, "trace", "trace_kernel_stats.csv"))):
             name = x["Name"]
@@ -1249,11 +1388,21 @@ def summarize_plans(d):
                              f"{float(x['AverageNs']) / 1e6:.4f} |")
         mc = os.path.join(base, "trace", "trace_memory_copy_trace.csv")
         copies = list(csv.DictReader(open(mc))) if os.path.exists(mc) else []
+        lost = None
+        log_f = os.path.join(d, f"trace_{plan}.log")
+        if os.path.exists(log_f):
+            m2 = re.search(r"(\d+) completion callbacks were not delivered", open(log_f).read())
+            lost = int(m2.group(1)) if m2 else None
         if copies:
             dur = sum(int(x["End_Timestamp"]) - int(x["Start_Timestamp"]) for x in copies) / 1e6
+            dirs = sorted({x["Direction"] for x in copies})
             lines += ["", f"Copies the runtime ran on its copy engines (not kernels, so absent "
-                      f"from the kernel table and the byte counters): {len(copies)} copies, "
-                      f"{dur:.2f} ms in total."]
+                      f"from the kernel table and the byte counters): {len(copies)} copies "
+                      f"({', '.join(dirs)}), {dur:.2f} ms in total."]
+            if lost:
+                lines += [f"The copy trace is incomplete: rocprofv3 reported {lost} completion "
+                          "callbacks of the copies never delivered, so these counts and times "
+                          "are lower bounds."]
         elif plan == "staged":
             lines += ["", "No copy ran on the copy engines: every hipMemcpyAsync was a blit "
                       "kernel."]
@@ -1443,6 +1592,7 @@ def main():
     ap.add_argument("--summarize-profiles", metavar="DIR")
     ap.add_argument("--summarize-plans", metavar="DIR")
     ap.add_argument("--summarize-workloads", metavar="DIR")
+    ap.add_argument("--summarize-hbm-counters", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
                              "load_cost", "tp8_shard", "hash", "agent_pool_chunked", "plans"])
@@ -1457,6 +1607,9 @@ def main():
         return
     if args.summarize_workloads:
         summarize_workloads(args.summarize_workloads)
+        return
+    if args.summarize_hbm_counters:
+        summarize_hbm_counters(args.summarize_hbm_counters)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "

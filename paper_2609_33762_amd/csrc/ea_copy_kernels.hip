@@ -43,14 +43,23 @@ __device__ __forceinline__ int this_xcd(const PieceCopy &a) {
 __device__ __forceinline__ u32x4 load_nt(const u32x4 *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void store_nt(u32x4 *p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
-// Copy unit u: layer layer_begin + (u mod layer_count) of entry i, whose
-// page and slot the caller has made wave-uniform.  The entry's piece sits at
-// chunk position c = i mod C of layer l inside the slot.
+// Unit u is (entry i, layer l): entry-major (u = i * layer_count + l - b,
+// a page's layers one after the other) or, with a.layer_major, layer-major
+// (u = (l - b) * n + i, every entry of one layer first); b = layer_begin.
+__device__ __forceinline__ int64_t unit_entry(const PieceCopy &a, int64_t u) {
+  return a.layer_major ? u % a.n : u / a.layer_count;
+}
+__device__ __forceinline__ int64_t unit_layer(const PieceCopy &a, int64_t u, int64_t i) {
+  return a.layer_begin + (a.layer_major ? u / a.n : u - i * a.layer_count);
+}
+
+// Copy the piece of layer l of entry i, whose page and slot the caller has
+// made wave-uniform.  The entry's piece sits at chunk position c = i mod C
+// of layer l inside the slot.
 template <int DIR, bool INLINE, int VEC>
-__device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t i, int64_t page,
+__device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t l, int64_t i, int64_t page,
                                           int64_t slot, int lane) {
   const int64_t nvec = a.piece_bytes >> 4;
-  const int64_t l = a.layer_begin + (u - i * a.layer_count);
   const int64_t c = a.chunk == 1 ? 0 : (int64_t)((uint32_t)i % (uint32_t)a.chunk);
   const int64_t at = l * a.chunk + c;  // piece index inside the slot
   uint8_t *cache_piece = a.cache + (l * a.num_pages + page) * a.piece_bytes;
@@ -58,6 +67,15 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t
   uint8_t *slot_piece = slot_base + at * a.piece_bytes;
   const u32x4 *src = reinterpret_cast<const u32x4 *>(DIR == kToSlots ? cache_piece : slot_piece);
   u32x4 *dst = reinterpret_cast<u32x4 *>(DIR == kToSlots ? slot_piece : cache_piece);
+  // The scale word is read before the piece, so that its round trip (over
+  // the host link for a load) overlaps the piece's instead of following it.
+  uint64_t *cs = nullptr, *ss = nullptr;
+  uint64_t scale = 0;
+  if (a.scales != nullptr) {
+    cs = reinterpret_cast<uint64_t *>(a.scales + (l * a.num_pages + page) * 8);
+    ss = reinterpret_cast<uint64_t *>(slot_base + a.payload_bytes + at * 8);
+    if (lane == 0) scale = DIR == kToSlots ? *cs : *ss;
+  }
   for (int64_t base = 0; base < nvec; base += (int64_t)kWave * VEC) {
     u32x4 r[VEC];
 #pragma unroll
@@ -72,10 +90,8 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t u, int64_t
     }
   }
   if (a.scales != nullptr) {
-    uint64_t *cs = reinterpret_cast<uint64_t *>(a.scales + (l * a.num_pages + page) * 8);
-    uint64_t *ss = reinterpret_cast<uint64_t *>(slot_base + a.payload_bytes + at * 8);
     if (lane == 0) {
-      if (DIR == kToSlots) *ss = *cs; else *cs = *ss;
+      if (DIR == kToSlots) *ss = scale; else *cs = scale;
     }
     if (DIR == kToSlots && at == 0) {  // once per slot
       const int64_t pad_begin = a.payload_bytes + 8 * (int64_t)a.num_layers * a.chunk;
@@ -104,8 +120,8 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
   if constexpr (INLINE) {
     // indices from the kernel arguments (scalar loads, u is wave-uniform)
     for (int64_t u = first; u < units; u += waves) {
-      const int64_t i = u / a.layer_count;
-      copy_unit<DIR, INLINE, VEC>(a, u, i, inl.pages[i], inl.slots[i], lane);
+      const int64_t i = unit_entry(a, u);
+      copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, inl.pages[i], inl.slots[i], lane);
     }
   } else {
     // The index arrays live in pinned host memory that the kernel reads
@@ -119,18 +135,19 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
       int32_t vpage = 0;
       int64_t vslot = 0;
       if (ul < units) {
-        const int64_t il = ul / a.layer_count;
+        const int64_t il = unit_entry(a, ul);
         vpage = pages[il];
         vslot = a.identity_slots ? (int64_t)((uint32_t)il / (uint32_t)a.chunk) : slot_idx[il];
       }
       for (int k = 0; k < kWave; ++k) {
         const int64_t u = u0 + (int64_t)k * waves;
         if (u >= units) break;
-        const int64_t i = u / a.layer_count;
+        const int64_t i = unit_entry(a, u);
         const int64_t page = __builtin_amdgcn_readlane(vpage, k);
         const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)vslot, k);
         const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)vslot >> 32), k);
-        copy_unit<DIR, INLINE, VEC>(a, u, i, page, (int64_t)(((uint64_t)hi << 32) | lo), lane);
+        copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, page,
+                                    (int64_t)(((uint64_t)hi << 32) | lo), lane);
       }
     }
   }

@@ -34,6 +34,7 @@ struct PieceCopy {
   int32_t layer_begin;
   int32_t layer_count;
   int32_t identity_slots;    // slot of entry i is i / C (staging buffers)
+  int32_t layer_major;       // units ordered layer by layer, else entry by entry
   // Only workgroups on XCDs in xcd_mask do work.  Workgroups of a dispatch
   // go round-robin over the XCDs starting at an offset the hardware chooses
   // (workgroup b runs on XCD (b + offset) % num_xcd), so the workgroup's
