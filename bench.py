@@ -1670,6 +1670,12 @@ def main():
         "traffic_algorithmic": 2 * ctx["n_store"] * ctx["page"],
         "timing": f"HIP events on the store's stream around each of the {args.steps} timed "
                   f"launches",
+        # the restore beside it, which has priority on the link (the store's
+        # waves yield while it runs)
+        "load_in_step": {"kernel": "copy_host_link<load> (1,500 pages, beside the store)",
+                         "achieved": round(steps["load_gbs_in_step"], 2),
+                         "peak": round(peak["h2d"], 2), "unit": "GB/s",
+                         "frac": round(steps["load_gbs_in_step"] / peak["h2d"], 4)},
     }
     roofline_hbm = {
         "bound": "hbm", "kernel": "copy_hbm<gather> (paged gather of 2,000 pages to HBM)",

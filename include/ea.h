@@ -50,7 +50,12 @@
  * -------------------------------------------------------------------------
  *  EA_TRANSFER=direct|staged   transfer plan of tiers left at EA_PLAN_AUTO
  *  EA_LINK_WG, EA_LINK_WG_STORE, EA_LINK_WG_LOAD
- *                              working workgroups of a direct store / load (8)
+ *                              working workgroups of a direct store / load
+ *                              (8 / 9; EA_LINK_WG sets both)
+ *  EA_LOAD_PRIORITY            sleeps (x 127 x 64 cycles) a direct store's
+ *                              waves take after each piece while a load of
+ *                              the same tier runs (4; 0 = off); read at tier
+ *                              creation
  *  EA_LINK_WG_LAYERED          workgroups of one layer of a layered load (16)
  *  EA_XCD_STORE, EA_XCD_LOAD   XCD masks of the two directions (0x5, 0xA
  *                              with four or more XCDs); read at tier creation
@@ -58,8 +63,14 @@
  *                              the hardware reports; read at cache creation
  *  EA_GRID_HBM, EA_GRID_GATHER, EA_GRID_SCATTER
  *                              workgroups of the HBM gather (512) / scatter (256)
+ *  EA_HBM_ORDER, EA_GATHER_ORDER, EA_SCATTER_ORDER = entry|layer
+ *                              unit order of the HBM gather / scatter: each
+ *                              page's layers in turn (entry, the default) or
+ *                              one layer of every page at a time
  *  EA_STAGING_MB               HBM staging of the staged plan per direction (512)
  *  EA_HOST_COHERENT=0          non-coherent pinned memory for new tiers
+ *  EA_HOST_ALLOC_WAIT_MS       how long a tier's failed pinned allocation is
+ *                              retried (5000; 0 = fail at once)
  *  EA_HASH_CHAIN=split|pair|lane, EA_HASH_MID=split|lane
  *                              force a form of the hash kernels
  *  EA_HASH_OFFSETS=64          64-bit offsets for the hash kernels
@@ -132,7 +143,11 @@ typedef struct {
  * any cache of the same shape).  numa_node >= 0 binds the allocation to that
  * NUMA node; -1 uses the runtime's default placement.  capacity_bytes is also
  * the C_H the write rule compares the working-set estimate with.  Fails with
- * EA_EINVAL if K_H < 1, EA_ENOMEM if the pinned allocation fails. */
+ * EA_EINVAL if K_H < 1, EA_ENOMEM if the pinned allocation fails.  The driver
+ * returns the pages of a freed tier to its pool only after a delay, so an
+ * out-of-memory failure is retried with growing waits for up to
+ * EA_HOST_ALLOC_WAIT_MS (5 s by default) before EA_ENOMEM; a request beyond
+ * the machine's physical memory fails at once. */
 int ea_tier_create(const ea_cache *shape, int64_t capacity_bytes,
                    int numa_node, ea_tier **out);
 

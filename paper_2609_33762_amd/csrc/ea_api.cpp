@@ -67,6 +67,29 @@ int env_int(const char *name, int dflt) {
   return v && *v ? std::atoi(v) : dflt;
 }
 
+// Pinned, device-mapped host memory.  The driver hands the pages of a
+// buffer freed moments earlier back to its pool only some time later (on
+// MI355X, 64 GiB freed by one tier became allocatable again 2.6 s after the
+// free), so a tier created right after another was destroyed can fail for a
+// while.  An out-of-memory failure is retried with growing waits for up to
+// EA_HOST_ALLOC_WAIT_MS milliseconds (default 5000, 0 = no retry); a request
+// larger than the machine's physical memory fails at once.
+hipError_t host_alloc_retry(void **p, size_t bytes, unsigned flags) {
+  hipError_t e = hipHostMalloc(p, bytes, flags);
+  const long pages = sysconf(_SC_PHYS_PAGES), page = sysconf(_SC_PAGESIZE);
+  if (e != hipErrorOutOfMemory || pages <= 0 || page <= 0 ||
+      bytes > (size_t)pages * (size_t)page)
+    return e;
+  long budget_ms = std::max(0, env_int("EA_HOST_ALLOC_WAIT_MS", 5000));
+  for (long wait_ms = 50; e == hipErrorOutOfMemory && budget_ms > 0; wait_ms *= 2) {
+    const long ms = std::min(wait_ms, budget_ms);
+    usleep((useconds_t)(ms * 1000));
+    budget_ms -= ms;
+    e = hipHostMalloc(p, bytes, flags);
+  }
+  return e;
+}
+
 // Workgroups for the HBM-bound kernels, measured best on MI355X (256 CUs):
 // the gather (random reads, sequential writes) peaks with 2 workgroups per
 // CU, the scatter (sequential reads, random writes) with one per CU: more
@@ -96,9 +119,15 @@ int64_t grid_hbm(int dir) {
 // lowered both.  The store runs on XCDs 0 and 2 and the load on 1 and 3 by
 // default (EA_XCD_STORE / EA_XCD_LOAD override the masks).  EA_LINK_WG sets
 // both directions' workgroups, EA_LINK_WG_STORE / EA_LINK_WG_LOAD one each.
+//
+// Loads get one workgroup more than stores (9 against 8): with a store
+// yielding the link (EA_LOAD_PRIORITY below) the load's extra reads in
+// flight carry it to 94% of the pinned host-to-device peak during the turn's
+// duplex, against 84% with 8.
 int64_t grid_link(int dir) {
-  const int both = std::max(1, env_int("EA_LINK_WG", 8));
-  return std::max(1, env_int(dir == ea::kToSlots ? "EA_LINK_WG_STORE" : "EA_LINK_WG_LOAD", both));
+  const int both = env_int("EA_LINK_WG", 0);
+  const int dflt = both > 0 ? both : (dir == ea::kToSlots ? 8 : 9);
+  return std::max(1, env_int(dir == ea::kToSlots ? "EA_LINK_WG_STORE" : "EA_LINK_WG_LOAD", dflt));
 }
 
 // XCDs of the device (workgroups are dispatched round-robin over them) and
@@ -283,11 +312,20 @@ struct DirRes {
   bool used[2] = {};
 };
 
+// The end of one transfer call: its event, the stream it was recorded on
+// and the call's sequence number (0: never used).
 struct EvRec {
-  hipEvent_t ev;
-  hipStream_t stream;
-  int32_t refs;
+  hipEvent_t ev = nullptr;
+  hipStream_t stream = nullptr;
+  int64_t seq = 0;
 };
+
+// Transfer events per tier.  Events are a bounded resource of the driver
+// (each one holds a kernel event slot, a few thousand per process), so a
+// tier keeps a ring of this many and never one per slot: call q uses entry
+// q mod kTransferEvents, after the host has seen call q - kTransferEvents
+// complete.
+constexpr int64_t kTransferEvents = 64;
 
 }  // namespace
 
@@ -304,13 +342,17 @@ struct ea_tier {
   std::unique_ptr<ea::TierMeta> meta;
   int plan[2] = {EA_PLAN_AUTO, EA_PLAN_AUTO};
   DirRes res[2];
-  std::vector<int32_t> slot_ev;  // last transfer event of each slot, -1 none
-  std::vector<EvRec> evs;
-  std::vector<int32_t> free_evs;
+  std::vector<int64_t> slot_seq;  // sequence number of each slot's last transfer, 0 none
+  EvRec evs[kTransferEvents];
+  int64_t seq = 0;                // transfer calls so far
   int64_t bytes_stored = 0, bytes_loaded = 0, store_calls = 0, load_calls = 0;
   int64_t grid_store = 8, grid_load = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
+  // loads have priority on the host link when yield_sleeps > 0: direct
+  // stores sleep between units while d_busy (queued or running loads) > 0
+  uint32_t *d_busy = nullptr;
+  int32_t yield_sleeps = 0;
   int32_t controllers = 0;  // attached admission controllers (guarded by mu)
   int32_t steady_users = 0; // attached steady-clock controllers (guarded by mu)
 };
@@ -331,6 +373,16 @@ int resolve_plan(const ea_tier *t, int dir) {
   return EA_PLAN_DIRECT;
 }
 
+int device_copy_stream(int dev, hipStream_t *out) {
+  static std::mutex mu;
+  static hipStream_t streams[64];
+  if (dev < 0 || dev >= 64) return EA_EINVAL;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!streams[dev]) EA_HIP(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking));
+  *out = streams[dev];
+  return EA_OK;
+}
+
 int ensure_staging(ea_tier *t, int dir) {
   DirRes &R = t->res[dir];
   if (R.staging) return EA_OK;
@@ -341,70 +393,54 @@ int ensure_staging(ea_tier *t, int dir) {
     if (!R.ready[h]) EA_HIP(hipEventCreateWithFlags(&R.ready[h], hipEventDisableTiming));
     if (!R.done[h]) EA_HIP(hipEventCreateWithFlags(&R.done[h], hipEventDisableTiming));
   }
-  // only loads copy on a stream of their own (see copy_staged)
-  if (dir == EA_DIR_LOAD && !R.dma) EA_HIP(hipStreamCreateWithFlags(&R.dma, hipStreamNonBlocking));
+  // only loads copy on a stream of their own (see copy_staged): one per
+  // device for the life of the process, shared by every tier (streams are
+  // a runtime resource: creating one per tier and destroying it with the
+  // tier churns them)
+  if (dir == EA_DIR_LOAD && !R.dma) EA_TRY(device_copy_stream(t->device, &R.dma));
   EA_HIP(hipMalloc((void **)&R.staging, (size_t)(2 * per_half * t->slot)));
   R.per_half = per_half;
   return EA_OK;
 }
 
-int32_t new_event(ea_tier *t, hipStream_t s) {
-  int32_t e;
-  if (!t->free_evs.empty()) {
-    e = t->free_evs.back();
-    t->free_evs.pop_back();
-  } else {
-    hipEvent_t ev;
-    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return -1;
-    t->evs.push_back(EvRec{ev, nullptr, 0});
-    e = (int32_t)t->evs.size() - 1;
-  }
-  t->evs[e].stream = s;
-  t->evs[e].refs = 0;
-  return e;
-}
-
-void unref_event(ea_tier *t, int32_t e) {
-  if (e < 0) return;
-  if (--t->evs[e].refs == 0) t->free_evs.push_back(e);
-}
-
 // Order `s` after earlier transfers on other streams that touch these slots.
+// A slot whose last transfer is older than the ring holds is complete: the
+// host saw it finish before its event was used again.
 int wait_slot_hazards(ea_tier *t, const int64_t *slots, int64_t n, hipStream_t s) {
-  std::vector<int32_t> waits;
+  std::vector<int64_t> waits;
   for (int64_t i = 0; i < n; ++i) {
-    const int32_t e = t->slot_ev[slots[i]];
-    if (e < 0 || t->evs[e].stream == s) continue;
-    if (std::find(waits.begin(), waits.end(), e) == waits.end()) waits.push_back(e);
+    const int64_t q = t->slot_seq[slots[i]];
+    if (q == 0 || q <= t->seq - kTransferEvents) continue;
+    const EvRec &r = t->evs[q % kTransferEvents];
+    if (r.stream == s) continue;
+    if (std::find(waits.begin(), waits.end(), q) == waits.end()) waits.push_back(q);
   }
-  for (int32_t e : waits) {
-    const hipError_t q = hipEventQuery(t->evs[e].ev);
-    if (q == hipSuccess) continue;
-    if (q != hipErrorNotReady) {
-      g_last_hip = (int)q;
+  for (int64_t q : waits) {
+    hipEvent_t ev = t->evs[q % kTransferEvents].ev;
+    const hipError_t e = hipEventQuery(ev);
+    if (e == hipSuccess) continue;
+    if (e != hipErrorNotReady) {
+      g_last_hip = (int)e;
       return EA_EHIP;
     }
-    EA_HIP(hipStreamWaitEvent(s, t->evs[e].ev, 0));
+    EA_HIP(hipStreamWaitEvent(s, ev, 0));
   }
   return EA_OK;
 }
 
 // Record the end of this call's transfer on `s` as the slots' last event.
 int note_slot_transfer(ea_tier *t, const int64_t *slots, int64_t n, hipStream_t s) {
-  const int32_t e = new_event(t, s);
-  if (e < 0) {
-    g_last_hip = (int)hipErrorOutOfMemory;
-    return EA_EHIP;
-  }
-  EA_HIP(hipEventRecord(t->evs[e].ev, s));
-  for (int64_t i = 0; i < n; ++i) {
-    int32_t &cur = t->slot_ev[slots[i]];
-    if (cur == e) continue;
-    unref_event(t, cur);
-    cur = e;
-    t->evs[e].refs += 1;
-  }
-  if (t->evs[e].refs == 0) t->free_evs.push_back(e);
+  const int64_t q = t->seq + 1;
+  EvRec &r = t->evs[q % kTransferEvents];
+  if (!r.ev) EA_HIP(hipEventCreateWithFlags(&r.ev, hipEventDisableTiming));
+  // the entry's previous call (kTransferEvents calls ago) must be done
+  // before its event is recorded again; it normally finished long ago
+  if (r.seq != 0) EA_HIP(hipEventSynchronize(r.ev));
+  EA_HIP(hipEventRecord(r.ev, s));
+  r.stream = s;
+  r.seq = q;
+  t->seq = q;
+  for (int64_t i = 0; i < n; ++i) t->slot_seq[slots[i]] = q;
   return EA_OK;
 }
 
@@ -464,8 +500,18 @@ int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
   a.slots = t->dev;
   a.xcd_mask = dir == ea::kToSlots ? t->xcd_store : t->xcd_load;
   const int res_dir = dir == ea::kToSlots ? EA_DIR_STORE : EA_DIR_LOAD;
-  return launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir, ea::kRouteHostLink,
-                        dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
+  const bool mark = t->d_busy != nullptr && dir == ea::kToPages;
+  if (t->d_busy != nullptr && dir == ea::kToSlots) {
+    a.yield_flag = t->d_busy;
+    a.yield_sleeps = t->yield_sleeps;
+  }
+  if (mark) EA_HIP(ea::launch_link_busy_add(t->d_busy, 1, s));
+  const int rc = launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir,
+                                ea::kRouteHostLink,
+                                dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
+  // the counter drops again whatever happened to the copy
+  if (mark) EA_HIP(ea::launch_link_busy_add(t->d_busy, -1, s));
+  return rc;
 }
 
 // Staged plan: HBM staging + DMA copies of runs of consecutive slots.
@@ -689,7 +735,7 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
       numa_set = syscall(SYS_set_mempolicy, 1, &mask, 64) == 0;
       if (numa_set) flags |= hipHostMallocNumaUser;
     }
-    hipError_t e = hipHostMalloc((void **)&t->host, (size_t)(K * t->slot), flags);
+    hipError_t e = host_alloc_retry((void **)&t->host, (size_t)(K * t->slot), flags);
     if (numa_set) (void)syscall(SYS_set_mempolicy, 0, nullptr, 0);
     if (e != hipSuccess) {
       g_last_hip = (int)e;
@@ -701,12 +747,32 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
       g_last_hip = (int)e;
       return EA_EHIP;
     }
+    // Loads first on the host link: a restore is the T_load of Eq. 2 that a
+    // waiting request pays, a store is background write-back.  While a load
+    // of this tier is queued or running, each wave of a direct store sleeps
+    // 4 x 127 x 64 cycles after every piece.  Measured on the Qwen3 turn
+    // (2,000-page store beside a 1,500-page load): the load's in-step rate
+    // rose from 42.4-42.9 to 54.0 GB/s and the duplex fell from 87.5-87.8 to
+    // 85.2 GB/s; 3 sleeps did not shift the share, 5 or more cut the duplex
+    // to 79 GB/s and below.  EA_LOAD_PRIORITY=0 turns it off.
+    t->yield_sleeps = std::max(0, env_int("EA_LOAD_PRIORITY", 4));
+    if (t->yield_sleeps > 0) {
+      e = hipMalloc((void **)&t->d_busy, 256);
+      if (e == hipSuccess) e = hipMemset(t->d_busy, 0, 256);
+      if (e != hipSuccess) {
+        if (t->d_busy) (void)hipFree(t->d_busy);
+        (void)hipHostFree(t->host);
+        g_last_hip = (int)e;
+        return EA_EHIP;
+      }
+    }
     t->meta.reset(new (std::nothrow) ea::TierMeta(K, capacity_bytes));
     if (!t->meta) {
+      if (t->d_busy) (void)hipFree(t->d_busy);
       (void)hipHostFree(t->host);
       return EA_ENOMEM;
     }
-    t->slot_ev.assign((size_t)K, -1);
+    t->slot_seq.assign((size_t)K, 0);
     *out = t.release();
     return EA_OK;
   } catch (const std::bad_alloc &) {
@@ -723,16 +789,15 @@ int ea_tier_destroy(ea_tier *t) {
   {
     DeviceScope ds(t->device);
     std::lock_guard<std::mutex> lk(t->mu);
-    for (auto &ev : t->evs) {
-      (void)hipEventSynchronize(ev.ev);
-      (void)hipEventDestroy(ev.ev);
-    }
+    for (auto &ev : t->evs)
+      if (ev.ev) {
+        (void)hipEventSynchronize(ev.ev);
+        (void)hipEventDestroy(ev.ev);
+      }
     for (auto &R : t->res) {
       R.ring.destroy();
-      if (R.dma) {
-        (void)hipStreamSynchronize(R.dma);
-        (void)hipStreamDestroy(R.dma);
-      }
+      // the device's copy stream outlives the tier; its events below
+      // cover this tier's copies on it
       for (hipEvent_t e : {R.start, R.ready[0], R.ready[1], R.done[0], R.done[1]})
         if (e) {
           (void)hipEventSynchronize(e);
@@ -741,6 +806,7 @@ int ea_tier_destroy(ea_tier *t) {
       if (R.staging) (void)hipFree(R.staging);
     }
     if (t->host) (void)hipHostFree(t->host);
+    if (t->d_busy) (void)hipFree(t->d_busy);
   }
   delete t;
   return EA_OK;
@@ -996,12 +1062,17 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
     } else {
       EA_TRY(ring.upload(each.data(), dst_pages, m, &a.slot_idx, &a.pages, &region));
     }
-    for (int32_t l = 0; l < c->d.num_layers; ++l) {
+    if (t->d_busy) EA_HIP(ea::launch_link_busy_add(t->d_busy, 1, copy_stream));
+    hipError_t e = hipSuccess;
+    for (int32_t l = 0; l < c->d.num_layers && e == hipSuccess; ++l) {
       a.layer_begin = l;
-      EA_HIP(ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
-                                   copy_stream));
-      EA_HIP(hipEventRecord(layer_done[l], copy_stream));
+      e = ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
+                                copy_stream);
+      if (e == hipSuccess) e = hipEventRecord(layer_done[l], copy_stream);
     }
+    // the counter drops again whatever happened to the copies
+    if (t->d_busy) EA_HIP(ea::launch_link_busy_add(t->d_busy, -1, copy_stream));
+    EA_HIP(e);
     if (region >= 0) EA_TRY(ring.release(region, copy_stream));
     EA_TRY(note_slot_transfer(t, host_slots, n, copy_stream));
     t->bytes_loaded += (int64_t)n * t->slot;
@@ -1098,7 +1169,8 @@ int ea_peak_probe(ea_tier *t, void *d_buf, int64_t bytes, int direction, int rep
   std::lock_guard<std::mutex> lk(t->mu);
   // the probe overwrites the first slots: refuse while any of them is in use
   if (!t->meta->slots_free(0, (need + t->slot - 1) / t->slot)) return EA_EINVAL;
-  for (auto &ev : t->evs) EA_HIP(hipEventSynchronize(ev.ev));
+  for (auto &ev : t->evs)
+    if (ev.ev) EA_HIP(hipEventSynchronize(ev.ev));
   hipStream_t s[2] = {nullptr, nullptr};
   hipEvent_t e0[2] = {nullptr, nullptr}, e1[2] = {nullptr, nullptr};
   int rc = EA_OK;

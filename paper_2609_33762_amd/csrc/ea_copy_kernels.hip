@@ -102,6 +102,20 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t l, int64_t
   }
 }
 
+// A store that yields the host link to loads: while the tier's load
+// counter is non-zero (a load kernel of the same tier is queued or running)
+// the wave sleeps a.yield_sleeps times 127 x 64 cycles after each unit.  The
+// counter is read before the unit and acted on after it, so its round trip
+// overlaps the copy.
+__device__ __forceinline__ uint32_t link_busy(const PieceCopy &a) {
+  if (a.yield_flag == nullptr) return 0;
+  return __hip_atomic_load(a.yield_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void yield_link(const PieceCopy &a, uint32_t busy) {
+  if (__builtin_amdgcn_readfirstlane(busy) != 0)
+    for (int32_t k = 0; k < a.yield_sleeps; ++k) __builtin_amdgcn_s_sleep(127);
+}
+
 template <int DIR, bool INLINE, int VEC>
 __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__restrict__ pages,
                                            const int64_t *__restrict__ slot_idx,
@@ -121,7 +135,9 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
     // indices from the kernel arguments (scalar loads, u is wave-uniform)
     for (int64_t u = first; u < units; u += waves) {
       const int64_t i = unit_entry(a, u);
+      const uint32_t busy = link_busy(a);
       copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, inl.pages[i], inl.slots[i], lane);
+      yield_link(a, busy);
     }
   } else {
     // The index arrays live in pinned host memory that the kernel reads
@@ -146,8 +162,10 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
         const int64_t page = __builtin_amdgcn_readlane(vpage, k);
         const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)vslot, k);
         const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)vslot >> 32), k);
+        const uint32_t busy = link_busy(a);
         copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, page,
                                     (int64_t)(((uint64_t)hi << 32) | lo), lane);
+        yield_link(a, busy);
       }
     }
   }
@@ -204,6 +222,13 @@ __global__ __launch_bounds__(kThreads) void layer_checksum(
       out[i] = x;
     }
   }
+}
+
+// Add delta to a tier's load counter (one lane; launched on a load's
+// stream right before and right after its copy kernels).
+__global__ __launch_bounds__(64) void link_busy_add(uint32_t *flag, int32_t delta) {
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(flag, (uint32_t)delta, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // One workgroup of one wave per entry: out[b] = the XCD of workgroup b.
@@ -271,6 +296,12 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok) {
   (void)hipStreamDestroy(s);
   if (e == hipSuccess) *ok = good;
   return e;
+}
+
+hipError_t launch_link_busy_add(uint32_t *flag, int32_t delta, hipStream_t stream) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(link_busy_add, dim3(1), dim3(64), 0, stream, flag, delta);
+  return hipGetLastError();
 }
 
 hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,

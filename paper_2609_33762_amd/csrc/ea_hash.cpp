@@ -219,6 +219,11 @@ void put_offsets(uint8_t *h, const int64_t *koff, const int64_t *toff, int64_t b
 int run_kernels(const int32_t *d_tokens, const uint8_t *d_koff, const uint8_t *d_toff, bool wide,
                 int32_t n_seqs, int64_t key_bound, int32_t block_tokens, uint32_t *d_mid,
                 const uint8_t *d_parents, uint8_t *d_keys, hipStream_t stream) {
+  if (ea::hash_fused(n_seqs)) {
+    HS_HIP(ea::launch_sha256_fused(d_tokens, d_koff, d_toff, wide, n_seqs, block_tokens,
+                                   d_parents, d_keys, stream));
+    return EA_OK;
+  }
   HS_HIP(ea::launch_sha256_midstates(d_tokens, d_koff, d_toff, wide, n_seqs, key_bound,
                                      block_tokens, d_mid, stream));
   HS_HIP(ea::launch_sha256_chain(d_mid, d_koff, wide, n_seqs, block_tokens, d_parents, d_keys,

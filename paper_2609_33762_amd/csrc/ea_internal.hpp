@@ -35,6 +35,11 @@ struct PieceCopy {
   int32_t layer_count;
   int32_t identity_slots;    // slot of entry i is i / C (staging buffers)
   int32_t layer_major;       // units ordered layer by layer, else entry by entry
+  // a store that yields the link: sleep yield_sleeps x 127 x 64 cycles after
+  // each unit while *yield_flag (the tier's count of queued or running loads)
+  // is non-zero; nullptr = never
+  const uint32_t *yield_flag;
+  int32_t yield_sleeps;
   // Only workgroups on XCDs in xcd_mask do work.  Workgroups of a dispatch
   // go round-robin over the XCDs starting at an offset the hardware chooses
   // (workgroup b runs on XCD (b + offset) % num_xcd), so the workgroup's
@@ -80,6 +85,9 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok);
 hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
                              int64_t workgroups, hipStream_t stream);
 
+// Add delta to a tier's load counter on `stream` (a one-lane kernel).
+hipError_t launch_link_busy_add(uint32_t *flag, int32_t delta, hipStream_t stream);
+
 // XOR checksum of one layer's piece of each of n pages (device page ids).
 hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,
                                  int64_t piece_bytes, int32_t layer, const int32_t *pages,
@@ -97,6 +105,16 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_of
 hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets, bool wide,
                                int32_t n_seqs, int32_t block_tokens, const uint8_t *d_parents,
                                uint8_t *d_keys, hipStream_t stream);
+
+// The one-kernel form for large batches (a lane per sequence computes its
+// keys' token blocks and chained blocks in turn): chosen when there are at
+// least 256 sequences per compute unit, or forced with EA_HASH_CHAIN=fused
+// (any other EA_HASH_CHAIN value keeps the two kernels).
+bool hash_fused(int32_t n_seqs);
+hipError_t launch_sha256_fused(const int32_t *d_tokens, const void *d_key_offsets,
+                               const void *d_tok_offsets, bool wide, int32_t n_seqs,
+                               int32_t block_tokens, const uint8_t *d_parents, uint8_t *d_keys,
+                               hipStream_t stream);
 
 // Key offsets from device sequence offsets d_seq_offsets [n_seqs+1], in two
 // kernels: d_key_offsets_out [n_seqs+1] (int64) and the hash kernels'

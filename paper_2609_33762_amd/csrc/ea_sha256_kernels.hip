@@ -727,6 +727,61 @@ __global__ __launch_bounds__(64) void hash_scan_reset(uint64_t *ticket) {
   if (threadIdx.x == 0) *ticket = 0;
 }
 
+// One lane per sequence for the whole key: the token blocks of a key from
+// the initial hash value, then the chained block, key after key, with the
+// next token block loaded while the current one is compressed.  For batches
+// of at least one wave of sequences per SIMD this leaves out the midstates'
+// trip through memory and the second launch.
+template <typename Off>
+__global__ __launch_bounds__(256) void sha256_fused_lane(
+    const int32_t *__restrict__ tokens, const Off *__restrict__ key_off,
+    const Off *__restrict__ tok_off, int32_t n_seqs, int32_t block_tokens, uint32_t len_bits,
+    const uint8_t *__restrict__ parents, uint8_t *__restrict__ keys) {
+  const int32_t s = blockIdx.x * 256 + threadIdx.x;
+  if (s >= n_seqs) return;
+  uint32_t prev[8];
+  parent_words(parents, s, prev);
+  const int64_t k0 = key_off[s], k1 = key_off[s + 1];
+  const int32_t blocks = block_tokens / 16;
+  const int64_t total = (k1 - k0) * blocks;  // token blocks of the sequence
+  const int32_t *tok = tokens + (int64_t)tok_off[s];
+  uint32_t nx[16];
+  if (total > 0)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) nx[j] = (uint32_t)tok[j];
+  int64_t q = 0;  // token blocks consumed
+  for (int64_t k = k0; k < k1; ++k) {
+    uint32_t st[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) st[j] = kInit[j];
+    for (int32_t c = 0; c < blocks; ++c, ++q) {
+      uint32_t w[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)  // LE32 token bytes read as a big-endian word
+        w[j] = __builtin_bswap32(nx[j]);
+      if (q + 1 < total)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) nx[j] = (uint32_t)tok[16 * (q + 1) + j];
+      compress(st, w);
+    }
+    uint32_t w[16];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = prev[j];
+    w[8] = 0x80000000u;
+#pragma unroll
+    for (int j = 9; j < 15; ++j) w[j] = 0u;
+    w[15] = len_bits;
+    compress(st, w);
+    uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k);
+    out[0] = make_uint4(__builtin_bswap32(st[0]), __builtin_bswap32(st[1]),
+                        __builtin_bswap32(st[2]), __builtin_bswap32(st[3]));
+    out[1] = make_uint4(__builtin_bswap32(st[4]), __builtin_bswap32(st[5]),
+                        __builtin_bswap32(st[6]), __builtin_bswap32(st[7]));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) prev[j] = st[j];
+  }
+}
+
 // The split forms launch one workgroup per sequence or key; forcing them on
 // more than this many falls back to the other forms.
 constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
@@ -846,6 +901,36 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   else
     launch_chain(form, d_mid, static_cast<const int32_t *>(d_key_offsets), n_seqs, len_bits,
                  d_parents, d_keys, stream);
+  return hipGetLastError();
+}
+
+bool hash_fused(int32_t n_seqs) {
+  const char *f = std::getenv("EA_HASH_CHAIN");
+  if (f && *f) return std::strcmp(f, "fused") == 0;
+  int cus = 0;
+  if (device_cus(&cus) != hipSuccess) return false;
+  // at least one wave of sequences on every SIMD (four per compute unit)
+  return (int64_t)n_seqs >= 256 * (int64_t)cus;
+}
+
+hipError_t launch_sha256_fused(const int32_t *d_tokens, const void *d_key_offsets,
+                               const void *d_tok_offsets, bool wide, int32_t n_seqs,
+                               int32_t block_tokens, const uint8_t *d_parents, uint8_t *d_keys,
+                               hipStream_t stream) {
+  if (n_seqs <= 0) return hipSuccess;
+  const uint32_t len_bits = (uint32_t)(8u * (4u * (uint32_t)block_tokens + 32u));
+  (void)hipGetLastError();
+  const dim3 g((unsigned)((n_seqs + 255) / 256));
+  if (wide)
+    hipLaunchKernelGGL(sha256_fused_lane<int64_t>, g, dim3(256), 0, stream, d_tokens,
+                       static_cast<const int64_t *>(d_key_offsets),
+                       static_cast<const int64_t *>(d_tok_offsets), n_seqs, block_tokens,
+                       len_bits, d_parents, d_keys);
+  else
+    hipLaunchKernelGGL(sha256_fused_lane<int32_t>, g, dim3(256), 0, stream, d_tokens,
+                       static_cast<const int32_t *>(d_key_offsets),
+                       static_cast<const int32_t *>(d_tok_offsets), n_seqs, block_tokens,
+                       len_bits, d_parents, d_keys);
   return hipGetLastError();
 }
 

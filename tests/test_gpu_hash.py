@@ -109,12 +109,14 @@ def test_device_calls_back_to_back():
         assert np.array_equal(out.cpu().numpy(), okeys)
 
 
-@pytest.mark.parametrize("form", ["pair", "lane", "split"])
+@pytest.mark.parametrize("form", ["pair", "lane", "split", "fused"])
 def test_every_chain_form(form, monkeypatch):
     # the chained compression runs two lanes per sequence, one lane per
-    # sequence (large batches) or a workgroup of two waves per sequence (up
-    # to one sequence per compute unit); each form forced on ragged chains,
-    # parents, chunk-sized blocks, a long chain and the extreme token values
+    # sequence (large batches), a workgroup of two waves per sequence (up to
+    # one sequence per compute unit), or, for the largest batches, one lane
+    # per sequence for token blocks and chain alike (fused); each form forced
+    # on ragged chains, parents, chunk-sized blocks, a long chain and the
+    # extreme token values
     monkeypatch.setenv("EA_HASH_CHAIN", form)
     r = W.rng(90 + len(form))
     check(list(r.integers(0, 900, size=300)), 16, parents=True, seed=91)
@@ -131,10 +133,12 @@ def test_every_chain_form(form, monkeypatch):
 
 def test_batch_past_the_one_lane_threshold():
     # more sequences than two-lane waves fit one per SIMD (32 per SIMD):
-    # the library picks the one-lane chain by itself; ragged lengths, parents
+    # the library picks the one-lane chain by itself; ragged lengths, parents;
+    # past 256 sequences per compute unit it picks the fused form
     r = W.rng(95)
     check(list(r.integers(0, 160, size=40000)), 16, parents=True, seed=95)
     check([64] * 40000, 16, seed=96)
+    check(list(r.integers(0, 400, size=70000)), 16, parents=True, seed=97)
 
 
 @pytest.mark.parametrize("form", ["pair", "lane", "split"])
@@ -227,7 +231,7 @@ def test_device_offsets_many_sequences_and_forms(monkeypatch):
     torch = need_gpu()
     r = W.rng(71)
     lengths = list(r.integers(0, 300, size=5000))
-    for form in ["pair", "lane", "split", None]:
+    for form in ["pair", "lane", "split", "fused", None]:
         if form:
             monkeypatch.setenv("EA_HASH_CHAIN", form)
         else:
