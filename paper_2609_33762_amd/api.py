@@ -151,15 +151,19 @@ class Tier:
         self.chunk_pages = info.chunk_pages
 
     def close(self):
+        """Free the tier; raises EAError (and keeps it) while a Controller is
+        attached to it."""
         if self._h:
-            N.load().ea_tier_destroy(self._h)
+            N.check("ea_tier_destroy", N.load().ea_tier_destroy(self._h))
             self._h = C.c_void_p()
 
     def __del__(self):
         try:
             self.close()
         except Exception:
-            pass
+            # a controller collected in the same cycle still holds it: that
+            # controller frees the tier when it closes
+            self._orphaned = True
 
     def host_view(self):
         """numpy uint8 [K_H, slot_bytes] view of the pinned slots (no copy)."""
@@ -437,11 +441,14 @@ class Controller:
                                  int(bool(manual_clock)), 0)
         N.check("ea_controller_create", N.load().ea_controller_create(
             tier._h, C.byref(policy), C.byref(cfg), C.byref(self._h)))
+        self._tier = tier  # the tier outlives its controllers
 
     def close(self):
         if self._h:
             N.load().ea_controller_destroy(self._h)
             self._h = C.c_void_p()
+            if getattr(self._tier, "_orphaned", False):
+                self._tier.close()
 
     def __del__(self):
         try:

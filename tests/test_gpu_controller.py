@@ -180,12 +180,36 @@ def test_steady_clock_without_a_report_uses_the_estimate_alone():
     st = ctl.status()
     assert st["reports_published"] == 0 and not st["have_seen"]
     assert st["fresh_decisions"] == 0 and st["skips"] == 6
-    # the tier refuses to go while the controller is attached
+    # the tier refuses to go while the controller is attached, and the
+    # binding keeps its handle then
     assert N.load().ea_tier_destroy(tier._h) == N.EA_EINVAL
+    with pytest.raises(N.EAError):
+        tier.close()
+    assert tier._h
     t0 = time.perf_counter()
     ctl.close()  # the publisher waits on a 60 s tick: closing must not wait for it
     assert time.perf_counter() - t0 < 1.0
     tier.close()
+    assert not tier._h
+    cache.close()
+
+
+def test_controller_collected_with_its_tier_frees_the_tier():
+    # a tier and its controller dropped together in one reference cycle:
+    # whichever finaliser runs first, the tier is freed once the controller
+    # is gone
+    torch = need_gpu()
+    kv, cache, tier, slot = make_tier(torch, 24)
+    pol = api.make_policy(kappa=2, block_tokens=B, beta_rank=slot // B)
+    ctl = api.Controller(tier, pol, manual_clock=True)
+    tier._cycle = ctl
+    handle = tier._h.value
+    tier._orphaned = False
+    tier.__del__()  # the tier's finaliser first: the controller still holds it
+    assert tier._orphaned and tier._h.value == handle
+    ctl.close()
+    assert not tier._h
+    del tier._cycle
     cache.close()
 
 
