@@ -984,7 +984,10 @@ def summarize_profiles(d):
     for x in csv.DictReader(open(os.path.join(d, "prof_trace", "trace_kernel_stats.csv"))):
         k = _short(x["Name"])
         if k:
-            stats[k] = (int(x["Calls"]), float(x["AverageNs"]) / 1e6)
+            # one row per instantiation: add calls and total time up
+            c0, t0 = stats.get(k, (0, 0.0))
+            stats[k] = (c0 + int(x["Calls"]), t0 + float(x["TotalDurationNs"]) / 1e6)
+    stats = {k: (c, t / c) for k, (c, t) in stats.items()}
     n_store, n_load, page, slot = 2000, 1500, 1572864, 1572864
     alg = {"store": n_store * page, "load": n_load * page,
            "gather": 2 * n_store * slot, "scatter": 2 * n_store * slot}
