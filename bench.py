@@ -27,6 +27,7 @@ Other modes:
   --summarize-profiles D   turn the rocprofv3 CSVs of the default command
                            under D into the summaries in profiles/
   --summarize-plans D      the same for the two transfer plans
+  --summarize-hash D       the hash workload's kernel trace under D
 """
 import argparse
 import csv
@@ -1167,6 +1168,95 @@ def summarize_hbm_counters(d):
     print(open(HBM_COUNTERS_SUMMARY).read())
 
 
+HASH_SUMMARY = os.path.join(ROOT, "profiles", "sha256_hash_workloads_kernel_trace.md")
+HASH_CASE_NOTES = {
+    "turn_56k_prompt": "the turn's prompt, one chain of 3,500 keys",
+    "turn_56k_prompt_1024_token_chunks": "the same prompt in 1,024-token chunks: 54 keys of "
+                                         "64 token blocks",
+    "one_64k": "one 65,536-token sequence",
+    "pool_64x64k": "64 sequences of 65,536 tokens",
+    "batch_16384x1k": "16,384 sequences of 1,024 tokens",
+    "batch_65536x256": "65,536 sequences of 256 tokens",
+}
+
+
+def _hash_role(name):
+    n = _plain_name(name)
+    return n if ("sha256" in n or "hash_" in n) else None
+
+
+def summarize_hash(d):
+    """Write the hash kernel summary from directory d: the line printed by
+    `bench.py --workload hash` (hash.json) and the kernel trace of the same
+    run (hash_kernel_trace.csv).  The trace is cut into calls (each call
+    ends with its chain or fused kernel), and the calls into the run's
+    series with the counts the line records."""
+    line = json.load(open(os.path.join(d, "hash.json")))
+    rows = sorted(csv.DictReader(open(os.path.join(d, "hash_kernel_trace.csv"))),
+                  key=lambda x: int(x["Start_Timestamp"]))
+    calls, cur = [], []
+    for x in rows:
+        role = _hash_role(x["Kernel_Name"])
+        if role is None:
+            continue
+        wg = int(x["Grid_Size_X"]) // max(1, int(x["Workgroup_Size_X"]))
+        dur = (int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3
+        cur.append((role, wg, int(x["Workgroup_Size_X"]), dur))
+        if "chain" in role or "fused" in role:
+            calls.append(cur)
+            cur = []
+    want = sum(1 + sum(sum(c) for c in case["calls"].values()) for case in line["hash"].values())
+    if len(calls) != want:
+        raise SystemExit(f"{len(calls)} calls in the trace, the run made {want}")
+    lines = ["# Hash kernels on the hash workload (kernel trace)", "",
+             "Command (from the repository root on the MI355X):", "",
+             "    rocprofv3 --kernel-trace --stats --output-format csv -d bench_out/prof_hash "
+             "-o hash -- python3 -u bench.py --workload hash > bench_out/prof_hash/hash.json",
+             "    python3 bench.py --summarize-hash bench_out/prof_hash", "",
+             "`bench.py --workload hash` runs six cases of chained keys (16-token blocks unless "
+             "named otherwise, tokens already in HBM).  Per case it first checks the keys of one "
+             "call of the host entry point, then times two series of 20 back-to-back calls "
+             "between one pair of HIP events, each after 0.3 s of untimed calls: "
+             "`ea_hash_blocks_device_offsets` (sequence offsets in HBM, key offsets from the "
+             "library's scan kernels) and `ea_hash_blocks_device` (host offsets uploaded by each "
+             "call).  The tables give the median duration of each kernel over the 20 timed "
+             "calls, their sum, and the HIP-event time per call the bench reports.  Grids are "
+             "in workgroups (work-items per workgroup in parentheses).", ""]
+    i = 0
+    summary = []
+    for name, case in line["hash"].items():
+        i += 1  # the host entry point's checking call
+        series = {}
+        for kind in ("device_offsets", "host_offsets"):
+            n_untimed, n_timed = case["calls"][kind]
+            i += n_untimed
+            series[kind] = calls[i:i + n_timed]
+            i += n_timed
+        lines += [f"## {name}: {HASH_CASE_NOTES.get(name, name)}, {case['keys']:,} keys", "",
+                  "| series | kernel (grid) | median µs |", "|---|---|---|"]
+        for kind, ev in (("device_offsets", case["ms"]), ("host_offsets", case["ms_host_offsets"])):
+            per = {}
+            for c in series[kind]:
+                for role, wg, wgs, dur in c:
+                    per.setdefault((role, wg, wgs), []).append(dur)
+            tot = float(np.median([sum(x[3] for x in c) for c in series[kind]]))
+            for (role, wg, wgs), v in per.items():
+                lines.append(f"| {kind} | {role} ({wg:,} x {wgs}) | {np.median(v):.1f} |")
+            lines.append(f"| {kind} | kernels of one call | {tot:.1f} |")
+            lines.append(f"| {kind} | one call, HIP events | {ev * 1e3:.1f} |")
+            summary.append((name, kind, tot, ev * 1e3, case["keys"]))
+        lines.append("")
+    lines += ["## Per key", "", "| case | series | kernels µs per key | call µs per key |",
+              "|---|---|---|---|"]
+    for name, kind, tot, ev, keys in summary:
+        lines.append(f"| {name} | {kind} | {tot / keys:.4f} | {ev / keys:.4f} |")
+    roof = line["roofline"]
+    lines += ["", f"Roofline case (the line's `roofline`): {roof['kernel']}: {roof['achieved']} "
+              f"{roof['unit']} against {roof['peak']} ({roof['frac']:.1%}).", ""]
+    open(HASH_SUMMARY, "w").write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def _quiet_cache(torch, api, sh, num_pages=None):
     """A cache of shape sh (contents irrelevant for timing: left unfilled)."""
     P = num_pages or sh.num_pages
@@ -1527,27 +1617,32 @@ def run_hash(args):
                      d_tok, d_offs, b, d_keys, d_koffs, stream=cur),
                  "host_offsets": lambda: api.hash_blocks_device(  # noqa: E731
                      d_tok, offs, b, d_keys, stream=cur)}
-        res = {}
+        res, counts = {}, {}
         for kind, call in calls.items():
             # untimed calls for 0.3 s first: a GPU left idle or lightly loaded
             # runs at lower clocks and takes a while to rise (successive single
             # chains measured 2.8 down to 2.1 us per key)
             t_warm = time.perf_counter() + 0.3
+            n_warm = 0
             while time.perf_counter() < t_warm:
                 call()
                 torch.cuda.synchronize()
+                n_warm += 1
             d_keys.zero_()
             ms = event_ms(torch, call, cur, 20, warm=2)
             assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32)), (name, kind)
             res[kind] = ms
+            # calls in launch order (untimed, timed): a kernel trace of the
+            # run is cut into calls with these counts
+            counts[kind] = [n_warm + 2, 20]
         ms = res["device_offsets"]
         out[name] = {"ms": round(ms, 4), "ms_host_offsets": round(res["host_offsets"], 4),
                      "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
-                     "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1)}
+                     "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1), "calls": counts}
         log(f"hash {name}: {out[name]}")
     b = out["batch_65536x256"]
     achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
-    roof = {"bound": "alu", "kernel": "hash_key_offsets + sha256_midstates + sha256_chain_lane "
+    roof = {"bound": "alu", "kernel": "hash key-offset scan + sha256_fused_lane "
                                       "(65,536 x 256 tokens, offsets in HBM)",
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
@@ -1596,6 +1691,7 @@ def main():
     ap.add_argument("--summarize-plans", metavar="DIR")
     ap.add_argument("--summarize-workloads", metavar="DIR")
     ap.add_argument("--summarize-hbm-counters", metavar="DIR")
+    ap.add_argument("--summarize-hash", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
                              "load_cost", "tp8_shard", "hash", "agent_pool_chunked", "plans"])
@@ -1613,6 +1709,9 @@ def main():
         return
     if args.summarize_hbm_counters:
         summarize_hbm_counters(args.summarize_hbm_counters)
+        return
+    if args.summarize_hash:
+        summarize_hash(args.summarize_hash)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "

@@ -598,23 +598,44 @@ __device__ __forceinline__ void load_run(const int64_t *seq_off, int32_t n_seqs,
   for (int j = 0; j <= kScanRun; ++j) r.off[j] = r.s0 + j <= r.s1 ? seq_off[r.s0 + j] : 0;
 }
 
+constexpr int kScanWaves = kScanThreads / 64;
+
+// Inclusive scan of v over the workgroup: within each wave by lane shifts
+// (no barrier), then across the waves through their totals in lds (one
+// barrier).  *total gets the workgroup's sum.  lds holds kScanWaves
+// entries; the call ends with a barrier, so it can be reused at once.
+__device__ __forceinline__ int64_t group_scan(int64_t v, int64_t *lds, int64_t *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t t = __shfl_up(v, (unsigned)d, 64);
+    if (lane >= d) v += t;
+  }
+  if (lane == 63) lds[wave] = v;
+  __syncthreads();
+  int64_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kScanWaves; ++w) {
+    const int64_t t = lds[w];
+    before += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return v + before;
+}
+
 // Sum over the workgroup of v (every thread returns it).
 __device__ __forceinline__ int64_t group_sum(int64_t v, int64_t *lds) {
-  lds[threadIdx.x] = v;
-  __syncthreads();
-  for (int d = kScanThreads / 2; d > 0; d >>= 1) {
-    if ((int)threadIdx.x < d) lds[threadIdx.x] += lds[threadIdx.x + d];
-    __syncthreads();
-  }
-  const int64_t r = lds[0];
-  __syncthreads();
-  return r;
+  int64_t total;
+  (void)group_scan(v, lds, &total);
+  return total;
 }
 
 __global__ __launch_bounds__(kScanThreads) void hash_offsets_partials(
     const int64_t *__restrict__ seq_off, int32_t n_seqs, int64_t n_tokens, int32_t block_tokens,
     int32_t shift, ScanState st) {
-  __shared__ int64_t lds[kScanThreads];
+  __shared__ int64_t lds[kScanWaves];
   __shared__ bool last;
   Run r;
   load_run(seq_off, n_seqs, r);
@@ -649,22 +670,13 @@ __global__ __launch_bounds__(kScanThreads) void hash_offsets_partials(
     bad |= v < 0;
     mine += v < 0 ? 0 : v;
   }
-  lds[threadIdx.x] = mine;
-  __syncthreads();
-  for (int d = 1; d < kScanThreads; d <<= 1) {  // inclusive scan of the thread sums
-    const int64_t add = (int)threadIdx.x >= d ? lds[threadIdx.x - d] : 0;
-    __syncthreads();
-    lds[threadIdx.x] += add;
-    __syncthreads();
-  }
-  int64_t run = lds[threadIdx.x] - mine;
-  const int64_t total = lds[kScanThreads - 1];
+  int64_t total;
+  int64_t run = group_scan(mine, lds, &total) - mine;  // exclusive prefix of the thread sums
   for (int64_t g = g0; g < g1; ++g) {
     st.prefix[g] = run;
     const int64_t v = __hip_atomic_load(st.part + g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     run += v < 0 ? 0 : v;
   }
-  __syncthreads();  // every thread has read the scan before lds is reused
   const int64_t any_bad = group_sum(bad, lds);
   if (threadIdx.x == kScanThreads - 1) {
     *st.total = total;
@@ -679,7 +691,7 @@ __global__ __launch_bounds__(kScanThreads) void hash_offsets_write(
     const int64_t *__restrict__ seq_off, int32_t n_seqs, int32_t block_tokens, int32_t shift,
     int64_t keys_cap, ScanState st, int64_t *__restrict__ key_off_out, Off *__restrict__ koff,
     Off *__restrict__ toff) {
-  __shared__ int64_t lds[kScanThreads];
+  __shared__ int64_t lds[kScanWaves];
   Run r;
   load_run(seq_off, n_seqs, r);
   const int64_t total = *st.total;
@@ -698,15 +710,8 @@ __global__ __launch_bounds__(kScanThreads) void hash_offsets_write(
     cnt[j] = r.s0 + j < r.s1 ? full_blocks(r.off[j + 1] - r.off[j], block_tokens, shift) : 0;
     mine += cnt[j];
   }
-  lds[threadIdx.x] = mine;
-  __syncthreads();
-  for (int d = 1; d < kScanThreads; d <<= 1) {
-    const int64_t add = (int)threadIdx.x >= d ? lds[threadIdx.x - d] : 0;
-    __syncthreads();
-    lds[threadIdx.x] += add;
-    __syncthreads();
-  }
-  int64_t run = st.prefix[blockIdx.x] + lds[threadIdx.x] - mine;
+  int64_t group_total;
+  int64_t run = st.prefix[blockIdx.x] + group_scan(mine, lds, &group_total) - mine;
 #pragma unroll
   for (int j = 0; j < kScanRun; ++j)
     if (r.s0 + j < r.s1) {
