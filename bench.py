@@ -1170,9 +1170,9 @@ def summarize_hbm_counters(d):
 
 HASH_SUMMARY = os.path.join(ROOT, "profiles", "sha256_hash_workloads_kernel_trace.md")
 HASH_CASE_NOTES = {
-    "turn_56k_prompt": "the turn's prompt, one chain of 3,500 keys",
-    "turn_56k_prompt_1024_token_chunks": "the same prompt in 1,024-token chunks: 54 keys of "
-                                         "64 token blocks",
+    "turn_56k_prompt": "the turn's 56,000-token prompt as one chain",
+    "turn_56k_prompt_1024_token_chunks": "the same prompt in 1,024-token chunks (64 token "
+                                         "blocks per key)",
     "one_64k": "one 65,536-token sequence",
     "pool_64x64k": "64 sequences of 65,536 tokens",
     "batch_16384x1k": "16,384 sequences of 1,024 tokens",
@@ -1232,7 +1232,7 @@ def summarize_hash(d):
             i += n_untimed
             series[kind] = calls[i:i + n_timed]
             i += n_timed
-        lines += [f"## {name}: {HASH_CASE_NOTES.get(name, name)}, {case['keys']:,} keys", "",
+        lines += [f"## {name}: {HASH_CASE_NOTES.get(name, name)} ({case['keys']:,} keys)", "",
                   "| series | kernel (grid) | median µs |", "|---|---|---|"]
         for kind, ev in (("device_offsets", case["ms"]), ("host_offsets", case["ms_host_offsets"])):
             per = {}
@@ -1431,7 +1431,7 @@ def run_plans(args):
 
 
 def summarize_plans(d):
-    """profiles/transfer_plans_qwen3_turn.md from three rocprofv3 runs (kernel
+    """The plan summary in profiles/ from three rocprofv3 runs (kernel
     trace, FETCH_SIZE, WRITE_SIZE) of each plan's `--workload plans` command,
     under d/plans_<plan>/, beside the runs' own JSON lines."""
     import re
