@@ -1482,7 +1482,7 @@ def summarize_plans(d):
         mc = os.path.join(base, "trace", "trace_memory_copy_trace.csv")
         copies = list(csv.DictReader(open(mc))) if os.path.exists(mc) else []
         lost = None
-        log_f = os.path.join(d, f"trace_{plan}.log")
+        log_f = os.path.join(base, "trace.log")
         if os.path.exists(log_f):
             m2 = re.search(r"(\d+) completion callbacks were not delivered", open(log_f).read())
             lost = int(m2.group(1)) if m2 else None
