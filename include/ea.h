@@ -53,9 +53,9 @@
  *                              working workgroups of a direct store / load
  *                              (8 / 9; EA_LINK_WG sets both)
  *  EA_LOAD_PRIORITY            sleeps (x 127 x 64 cycles) a direct store's
- *                              waves take after each piece while a load of
- *                              the same tier runs (4; 0 = off); read at tier
- *                              creation
+ *                              waves take per 32 KiB copied while waves of a
+ *                              direct or layered load of the same tier run
+ *                              (4; 0 = off); read at tier creation
  *  EA_LINK_WG_LAYERED          workgroups of one layer of a layered load (16)
  *  EA_XCD_STORE, EA_XCD_LOAD   XCD masks of the two directions (0x5, 0xA
  *                              with four or more XCDs); read at tier creation

@@ -349,8 +349,8 @@ struct ea_tier {
   int64_t grid_store = 8, grid_load = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
-  // loads have priority on the host link when yield_sleeps > 0: direct
-  // stores sleep between units while d_busy (queued or running loads) > 0
+  // loads have priority on the host link when yield_sleeps > 0: load waves
+  // count themselves in d_busy, and direct stores sleep while it is > 0
   uint32_t *d_busy = nullptr;
   int32_t yield_sleeps = 0;
   int32_t controllers = 0;  // attached admission controllers (guarded by mu)
@@ -500,18 +500,13 @@ int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
   a.slots = t->dev;
   a.xcd_mask = dir == ea::kToSlots ? t->xcd_store : t->xcd_load;
   const int res_dir = dir == ea::kToSlots ? EA_DIR_STORE : EA_DIR_LOAD;
-  const bool mark = t->d_busy != nullptr && dir == ea::kToPages;
-  if (t->d_busy != nullptr && dir == ea::kToSlots) {
-    a.yield_flag = t->d_busy;
+  if (t->d_busy != nullptr) {
+    a.link_flag = t->d_busy;
+    a.link_role = dir == ea::kToSlots ? ea::kLinkYield : ea::kLinkMark;
     a.yield_sleeps = t->yield_sleeps;
   }
-  if (mark) EA_HIP(ea::launch_link_busy_add(t->d_busy, 1, s));
-  const int rc = launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir,
-                                ea::kRouteHostLink,
-                                dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
-  // the counter drops again whatever happened to the copy
-  if (mark) EA_HIP(ea::launch_link_busy_add(t->d_busy, -1, s));
-  return rc;
+  return launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir, ea::kRouteHostLink,
+                        dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
 }
 
 // Staged plan: HBM staging + DMA copies of runs of consecutive slots.
@@ -748,9 +743,9 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
       return EA_EHIP;
     }
     // Loads first on the host link: a restore is the T_load of Eq. 2 that a
-    // waiting request pays, a store is background write-back.  While a load
-    // of this tier is queued or running, each wave of a direct store sleeps
-    // 4 x 127 x 64 cycles after every piece.  Measured on the Qwen3 turn
+    // waiting request pays, a store is background write-back.  While waves
+    // of a load of this tier run, each wave of a direct store sleeps
+    // 4 x 127 x 64 cycles per 32 KiB it copies.  Measured on the Qwen3 turn
     // (2,000-page store beside a 1,500-page load): the load's in-step rate
     // rose from 42.4-42.9 to 54.0 GB/s and the duplex fell from 87.5-87.8 to
     // 85.2 GB/s; 3 sleeps did not shift the share, 5 or more cut the duplex
@@ -1062,7 +1057,10 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
     } else {
       EA_TRY(ring.upload(each.data(), dst_pages, m, &a.slot_idx, &a.pages, &region));
     }
-    if (t->d_busy) EA_HIP(ea::launch_link_busy_add(t->d_busy, 1, copy_stream));
+    if (t->d_busy != nullptr) {
+      a.link_flag = t->d_busy;
+      a.link_role = ea::kLinkMark;
+    }
     hipError_t e = hipSuccess;
     for (int32_t l = 0; l < c->d.num_layers && e == hipSuccess; ++l) {
       a.layer_begin = l;
@@ -1070,8 +1068,6 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
                                 copy_stream);
       if (e == hipSuccess) e = hipEventRecord(layer_done[l], copy_stream);
     }
-    // the counter drops again whatever happened to the copies
-    if (t->d_busy) EA_HIP(ea::launch_link_busy_add(t->d_busy, -1, copy_stream));
     EA_HIP(e);
     if (region >= 0) EA_TRY(ring.release(region, copy_stream));
     EA_TRY(note_slot_transfer(t, host_slots, n, copy_stream));

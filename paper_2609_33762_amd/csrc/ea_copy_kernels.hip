@@ -102,18 +102,32 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t l, int64_t
   }
 }
 
-// A store that yields the host link to loads: while the tier's load
-// counter is non-zero (a load kernel of the same tier is queued or running)
-// the wave sleeps a.yield_sleeps times 127 x 64 cycles after each unit.  The
-// counter is read before the unit and acted on after it, so its round trip
-// overlaps the copy.
+// Loads first on the host link.  Every wave of a load raises the tier's
+// counter for its whole loop.  A store wave reads the counter before each
+// unit and acts on it after the unit (so the read's round trip overlaps the
+// copy): while a load runs it sleeps a.yield_sleeps x 127 x 64 cycles per
+// 32 KiB copied, which holds back small pieces as much as large ones.
+constexpr int64_t kYieldBytes = 32768;
+
 __device__ __forceinline__ uint32_t link_busy(const PieceCopy &a) {
-  if (a.yield_flag == nullptr) return 0;
-  return __hip_atomic_load(a.yield_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.link_role != kLinkYield) return 0;
+  return __hip_atomic_load(a.link_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void yield_link(const PieceCopy &a, uint32_t busy) {
-  if (__builtin_amdgcn_readfirstlane(busy) != 0)
+__device__ __forceinline__ void yield_link(const PieceCopy &a, uint32_t busy, int64_t &debt) {
+  if (a.link_role != kLinkYield) return;
+  debt += a.piece_bytes;
+  if (__builtin_amdgcn_readfirstlane(busy) == 0) {
+    debt = 0;  // nothing to make up once the link is free
+    return;
+  }
+  for (; debt >= kYieldBytes; debt -= kYieldBytes)
     for (int32_t k = 0; k < a.yield_sleeps; ++k) __builtin_amdgcn_s_sleep(127);
+}
+// one lane per wave: +1 before a load wave's loop, -1 after it
+__device__ __forceinline__ void mark_load(const PieceCopy &a, int lane, int32_t delta) {
+  if (a.link_role == kLinkMark && lane == 0)
+    __hip_atomic_fetch_add(a.link_flag, (uint32_t)delta, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int DIR, bool INLINE, int VEC>
@@ -131,13 +145,15 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
   const int64_t waves = groups * (kThreads / kWave);
   const int64_t first =
       group * (kThreads / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  int64_t debt = 0;  // bytes a yielding store has copied since its last sleep
+  mark_load(a, lane, 1);
   if constexpr (INLINE) {
     // indices from the kernel arguments (scalar loads, u is wave-uniform)
     for (int64_t u = first; u < units; u += waves) {
       const int64_t i = unit_entry(a, u);
       const uint32_t busy = link_busy(a);
       copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, inl.pages[i], inl.slots[i], lane);
-      yield_link(a, busy);
+      yield_link(a, busy, debt);
     }
   } else {
     // The index arrays live in pinned host memory that the kernel reads
@@ -165,10 +181,11 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
         const uint32_t busy = link_busy(a);
         copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, page,
                                     (int64_t)(((uint64_t)hi << 32) | lo), lane);
-        yield_link(a, busy);
+        yield_link(a, busy, debt);
       }
     }
   }
+  mark_load(a, lane, -1);
 }
 
 // Two entry points with the same body, so that profiles tell the host-link
@@ -222,13 +239,6 @@ __global__ __launch_bounds__(kThreads) void layer_checksum(
       out[i] = x;
     }
   }
-}
-
-// Add delta to a tier's load counter (one lane; launched on a load's
-// stream right before and right after its copy kernels).
-__global__ __launch_bounds__(64) void link_busy_add(uint32_t *flag, int32_t delta) {
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(flag, (uint32_t)delta, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // One workgroup of one wave per entry: out[b] = the XCD of workgroup b.
@@ -296,12 +306,6 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok) {
   (void)hipStreamDestroy(s);
   if (e == hipSuccess) *ok = good;
   return e;
-}
-
-hipError_t launch_link_busy_add(uint32_t *flag, int32_t delta, hipStream_t stream) {
-  (void)hipGetLastError();
-  hipLaunchKernelGGL(link_busy_add, dim3(1), dim3(64), 0, stream, flag, delta);
-  return hipGetLastError();
 }
 
 hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,

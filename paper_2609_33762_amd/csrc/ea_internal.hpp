@@ -35,10 +35,13 @@ struct PieceCopy {
   int32_t layer_count;
   int32_t identity_slots;    // slot of entry i is i / C (staging buffers)
   int32_t layer_major;       // units ordered layer by layer, else entry by entry
-  // a store that yields the link: sleep yield_sleeps x 127 x 64 cycles after
-  // each unit while *yield_flag (the tier's count of queued or running loads)
-  // is non-zero; nullptr = never
-  const uint32_t *yield_flag;
+  // Loads first on the host link.  link_flag is the tier's count of load
+  // waves at work (nullptr: no priority).  A load (link_role 2) raises it
+  // by one per wave for the wave's whole loop; a store (link_role 1) that
+  // finds it non-zero sleeps yield_sleeps x 127 x 64 cycles per 32 KiB it
+  // has copied since its last sleep.
+  uint32_t *link_flag;
+  int32_t link_role;
   int32_t yield_sleeps;
   // Only workgroups on XCDs in xcd_mask do work.  Workgroups of a dispatch
   // go round-robin over the XCDs starting at an offset the hardware chooses
@@ -73,6 +76,8 @@ void tier_attach_controller(ea_tier *t, int delta);
 
 // Which memory the slot-layout buffer of a piece copy lives in.
 enum Route : int { kRouteHostLink = 0, kRouteHbm = 1 };
+// PieceCopy::link_role
+enum LinkRole : int { kLinkNone = 0, kLinkYield = 1, kLinkMark = 2 };
 
 // Check, with a probe kernel on the current device, that the workgroups of
 // a dispatch go round-robin over num_xcd XCDs as the hardware reports them
@@ -86,7 +91,6 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
                              int64_t workgroups, hipStream_t stream);
 
 // Add delta to a tier's load counter on `stream` (a one-lane kernel).
-hipError_t launch_link_busy_add(uint32_t *flag, int32_t delta, hipStream_t stream);
 
 // XOR checksum of one layer's piece of each of n pages (device page ids).
 hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, int64_t num_pages,
