@@ -450,11 +450,11 @@ typedef struct {
   int64_t bytes_loaded;     /* bytes enqueued device-ward by loads          */
   int64_t store_calls;
   int64_t load_calls;
-} ea_tier_stats;
+} ea_tier_stats_t;
 
 /* Tier telemetry (App. "Runtime Admission Details": registered chunks, K_H,
  * evictions in the window). */
-int ea_tier_stats_get(const ea_tier *tier, ea_tier_stats *stats);
+int ea_tier_stats(const ea_tier *tier, ea_tier_stats_t *stats);
 
 enum { EA_SLOT_FREE = 0, EA_SLOT_PENDING = 1, EA_SLOT_RESIDENT = 2 };
 
@@ -548,7 +548,9 @@ int ea_tier_get_plan(const ea_tier *tier, int direction, int *plan);
  * (both at once on two streams; total bytes over the slower one).  Overwrites
  * the first bytes (2*bytes for BOTH) of the tier's slots, so it returns
  * EA_EINVAL, moving nothing, while any slot in that range is allocated or
- * holds a stored chunk: use it on a tier that holds nothing yet. */
+ * holds a stored chunk: use it on a tier that holds nothing yet.  The device
+ * buffer and the repetition count come from the caller, so the probe
+ * allocates nothing and its cost is the caller's choice. */
 int ea_peak_probe(ea_tier *tier, void *d_buf, int64_t bytes, int direction,
                   int reps, double *gbps);
 

@@ -105,7 +105,7 @@ SIGNATURES = {
     "ea_controller_get_status": (_INT, [_P, _P]),
     "ea_tier_alloc": (_INT, [_P, _P, _P, _I64, _P, _P]),
     "ea_tier_unpin": (_INT, [_P, _P, _I64]),
-    "ea_tier_stats_get": (_INT, [_P, _P]),
+    "ea_tier_stats": (_INT, [_P, _P]),
     "ea_tier_export": (_INT, [_P, _P, _P, _P, _P, _P]),
     "ea_store_blocks": (_INT, [_P, _P, _P, _P, _P, _I32, _P]),
     "ea_load_blocks": (_INT, [_P, _P, _P, _P, _I32, _P]),

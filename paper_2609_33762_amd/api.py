@@ -229,7 +229,7 @@ class Tier:
 
     def stats(self):
         s = N.TierStats()
-        N.check("ea_tier_stats_get", N.load().ea_tier_stats_get(self._h, C.byref(s)))
+        N.check("ea_tier_stats", N.load().ea_tier_stats(self._h, C.byref(s)))
         return {f: getattr(s, f) for f, _ in N.TierStats._fields_}
 
     def export(self):

@@ -911,7 +911,7 @@ int ea_tier_unpin(ea_tier *t, const int64_t *slots, int64_t n) {
   }
 }
 
-int ea_tier_stats_get(const ea_tier *t, ea_tier_stats *s) {
+int ea_tier_stats(const ea_tier *t, ea_tier_stats_t *s) {
   if (!t || !s) return EA_EINVAL;
   std::memset(s, 0, sizeof *s);
   std::lock_guard<std::mutex> lk(const_cast<ea_tier *>(t)->mu);

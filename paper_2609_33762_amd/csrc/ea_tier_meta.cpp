@@ -293,7 +293,7 @@ int TierMeta::unpin(const int64_t *slots, int64_t n) {
   return EA_OK;
 }
 
-void TierMeta::stats(ea_tier_stats *s) const {
+void TierMeta::stats(ea_tier_stats_t *s) const {
   s->capacity_slots = K_;
   s->allocated = allocated_;
   s->registered = registered_;

@@ -65,7 +65,7 @@ class TierMeta {
   // A store was issued to `slot`: an allocated slot becomes resident.
   void mark_stored(int64_t slot);
   int unpin(const int64_t *slots, int64_t n);
-  void stats(ea_tier_stats *s) const;
+  void stats(ea_tier_stats_t *s) const;
   void export_state(uint8_t *state, int32_t *pins, uint8_t *keys, int64_t *lru,
                     int64_t *n_lru) const;
   // True when slots [first, first + count) hold nothing (no allocation, no

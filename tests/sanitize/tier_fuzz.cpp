@@ -68,7 +68,7 @@ void compare_state(ea::TierMeta &m, eao_tier *o, int64_t K, int64_t at) {
   CHECK(p1 == p2, "pins", at);
   CHECK(k1 == k2, "keys", at);
   CHECK(n1 == n2 && std::equal(l1.begin(), l1.begin() + n1, l2.begin()), "LRU order", at);
-  ea_tier_stats a;
+  ea_tier_stats_t a;
   std::memset(&a, 0, sizeof a);
   m.stats(&a);
   eao_tier_stats b;
