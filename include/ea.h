@@ -597,8 +597,8 @@ int ea_lru_simulate(const uint8_t *refs, int64_t n, const uint8_t *declined,
                     int64_t capacity, uint8_t *hits);
 
 /* The host tier's own recency order (App. "Recency order of the host
- * tier": a lookup hit moves only the matched prefix to the most-recent
- * end), request by request, for one capacity: request j (refs
+ * tier"; unlike the reference model, only the leading run of hits is
+ * promoted), request by request, for one capacity: request j (refs
  * req_off[j] .. req_off[j+1]-1, req_off[0] = 0) promotes its leading
  * resident chunks, hit_blocks[j] of them; unless declined[j] != 0 it then
  * inserts every later chunk that is absent at that moment, in order

@@ -363,147 +363,275 @@ __global__ __launch_bounds__(128) void sha256_midstates_split(
     reinterpret_cast<uint4 *>(mid + 8 * g)[e_side ? 1 : 0] = make_uint4(h0, h1, h2, h3);
 }
 
-// One sequence per workgroup of two waves.  Wave 0 runs the 64 rounds in
-// the two-lane form; wave 1 computes the message schedule from the
-// previous key (words 16..63, with K_t added) and hands it over through LDS
-// in three parts of 16 words, so the rounds wave no longer issues the
-// schedule's instructions.  Per key: wave 0 runs rounds 0..11 from the key
-// it holds while wave 1 computes words 16..31; a barrier; rounds 12..27
-// while wave 1 computes 32..47; a barrier; rounds 28..43 while it computes
-// 48..63; a barrier; rounds 44..63, then wave 0 writes the key to memory
-// and to LDS; a barrier, after which wave 1 reads it.  Both waves run the
-// same loop (the workgroup's one sequence), so every barrier is reached by
-// both.  Every lane pair of wave 0 computes the sequence; lanes 0 and 1
-// write it.
+// One sequence per workgroup of two waves: wave 0 runs the rounds, wave 1
+// the message schedule, handed over through LDS.
+//
+// Rounds wave.  Lanes 0..3 of every row of 16 hold the a-side (a, b, c, d)
+// of the working state, lanes 12..15 the e-side (e, f, g, h); lanes 4..11
+// compute values nobody reads.  Writing A_t and E_t for the new a and e of
+// round t, the round is
+//   E_t = Sigma1(E_t-1) + Ch(E_t-1, E_t-2, E_t-3) + (E_t-4 + A_t-4 + K_t + W_t)
+//   A_t = E_t + Sigma0(A_t-1) + Maj(A_t-1, A_t-2, A_t-3) - A_t-4
+// (T1 = E_t - d, A_t = T1 + T2).  Both lanes run one instruction stream
+// with per-lane rotation amounts (Maj(a, b, c) = Ch(a ^ c, b, c), so one
+// v_bitop3 serves both sides): G = Sigma + Ch/Maj + V, where V holds the
+// bracket on the e-side and -A_t-4 on the a-side, and one DPP add gives
+// both lanes their new value: row_shl:12 brings the e-lane's G to the
+// a-lane, and the e-lane, whose source lies outside the row, adds zero.
+// V for the next round takes two instructions that fill the DPP add's
+// wait states: a row_shr:12 add brings A_t-3 to the e-lane (zero to the
+// a-lane) plus K + W (1 on the a-lane), then v_xad_u32 adds E_t-3 on the
+// e-lane and ~A_t-3 on the a-lane (~x + 1 = -x).  Ten instructions per
+// round, no wait states, and every VGPR a DPP instruction reads was
+// written at least two instructions before it.  The rounds sit in asm
+// blocks of up to four (the compiler adds a wait state between blocks);
+// volatile keeps them where they are written relative to the barriers.
+//
+// Schedule wave.  Lane j of a row holds W_T0-16+j and computes W_T0+j for
+// the 16 words of a part: the terms from the previous part in three DPP
+// passes, then seven steps in which lane j takes sigma1 of lane j - 2 and
+// W_t-7 from lane j - 7 (two steps old, hence no wait states); after step s
+// lanes 0 .. 2s + 1 hold final words.
+//
+// Per key: the rounds wave runs rounds 0..11 from the previous key and the
+// fixed padding words while the schedule wave computes words 16..31; a
+// barrier; the rounds wave reads them and runs rounds 12..26 while words
+// 32..47 are computed; a barrier; rounds 27..42 | words 48..63; a barrier;
+// rounds 43..63, the key into LDS; a barrier, after which the schedule
+// wave reads the key, stores the previous one and starts the next key's
+// words.  Each wave runs its own loop with the same four barriers per key.
+#define EA_RND(S0, S1, S2, K, VI, VO, NW)                                                    \
+  "v_alignbit_b32 %[r1], %[" S0 "], %[" S0 "], %[c1]\n\t"                                    \
+  "v_alignbit_b32 %[r2], %[" S0 "], %[" S0 "], %[c2]\n\t"                                    \
+  "v_alignbit_b32 %[r3], %[" S0 "], %[" S0 "], %[c3]\n\t"                                    \
+  "v_bitop3_b32 %[x], %[" S0 "], %[" S2 "], %[m] bitop3:0x78\n\t"                            \
+  "v_bitop3_b32 %[F], %[x], %[" S1 "], %[" S2 "] bitop3:0xca\n\t"                            \
+  "v_bitop3_b32 %[S], %[r1], %[r2], %[r3] bitop3:0x96\n\t"                                   \
+  "v_add3_u32 %[G], %[S], %[F], %[" VI "]\n\t"                                               \
+  "v_add_u32_dpp %[P], %[" S2 "], %[" K "] row_shr:12 row_mask:0xf bank_mask:0xf "           \
+  "bound_ctrl:1\n\t"                                                                         \
+  "v_xad_u32 %[" VO "], %[" S2 "], %[m], %[P]\n\t"                                           \
+  "v_add_u32_dpp %[" NW "], %[G], %[G] row_shl:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+// The last round of a compression: no next V, two wait states instead.
+#define EA_RND_LAST(S0, S1, S2, VI, NW)                                                      \
+  "v_alignbit_b32 %[r1], %[" S0 "], %[" S0 "], %[c1]\n\t"                                    \
+  "v_alignbit_b32 %[r2], %[" S0 "], %[" S0 "], %[c2]\n\t"                                    \
+  "v_alignbit_b32 %[r3], %[" S0 "], %[" S0 "], %[c3]\n\t"                                    \
+  "v_bitop3_b32 %[x], %[" S0 "], %[" S2 "], %[m] bitop3:0x78\n\t"                            \
+  "v_bitop3_b32 %[F], %[x], %[" S1 "], %[" S2 "] bitop3:0xca\n\t"                            \
+  "v_bitop3_b32 %[S], %[r1], %[r2], %[r3] bitop3:0x96\n\t"                                   \
+  "v_add3_u32 %[G], %[S], %[F], %[" VI "]\n\t"                                               \
+  "s_nop 1\n\t"                                                                              \
+  "v_add_u32_dpp %[" NW "], %[G], %[G] row_shl:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+
+// Per-lane constants of the split round: rotation amounts and the side mask.
+struct SplitLane {
+  uint32_t c1, c2, c3, m;
+};
+// Working state of the split round (s3 only feeds the final sum).
+struct SplitState {
+  uint32_t s0, s1, s2, s3, v;
+};
+
+// Four rounds; k0..k3 are K + W of the round after each (1 on a-lanes).
+__device__ __forceinline__ void split_rounds4(SplitState &q, uint32_t k0, uint32_t k1,
+                                              uint32_t k2, uint32_t k3, const SplitLane &c) {
+  uint32_t r1, r2, r3, x, F, S, G, P, v0, v1, v2, vo, n0, n1, n2, n3;
+  asm volatile(EA_RND("s0", "s1", "s2", "k0", "V", "v0", "n0")
+               EA_RND("n0", "s0", "s1", "k1", "v0", "v1", "n1")
+               EA_RND("n1", "n0", "s0", "k2", "v1", "v2", "n2")
+               EA_RND("n2", "n1", "n0", "k3", "v2", "Vo", "n3")
+               : [r1] "=&v"(r1), [r2] "=&v"(r2), [r3] "=&v"(r3), [x] "=&v"(x), [F] "=&v"(F),
+                 [S] "=&v"(S), [G] "=&v"(G), [P] "=&v"(P), [v0] "=&v"(v0), [v1] "=&v"(v1),
+                 [v2] "=&v"(v2), [Vo] "=&v"(vo), [n0] "=&v"(n0), [n1] "=&v"(n1),
+                 [n2] "=&v"(n2), [n3] "=&v"(n3)
+               : [s0] "v"(q.s0), [s1] "v"(q.s1), [s2] "v"(q.s2), [V] "v"(q.v), [k0] "v"(k0),
+                 [k1] "v"(k1), [k2] "v"(k2), [k3] "v"(k3), [c1] "v"(c.c1), [c2] "v"(c.c2),
+                 [c3] "v"(c.c3), [m] "v"(c.m));
+  q.s0 = n3; q.s1 = n2; q.s2 = n1; q.s3 = n0; q.v = vo;
+}
+// Three rounds.
+__device__ __forceinline__ void split_rounds3(SplitState &q, uint32_t k0, uint32_t k1,
+                                              uint32_t k2, const SplitLane &c) {
+  uint32_t r1, r2, r3, x, F, S, G, P, v0, v1, vo, n0, n1, n2;
+  asm volatile(EA_RND("s0", "s1", "s2", "k0", "V", "v0", "n0")
+               EA_RND("n0", "s0", "s1", "k1", "v0", "v1", "n1")
+               EA_RND("n1", "n0", "s0", "k2", "v1", "Vo", "n2")
+               : [r1] "=&v"(r1), [r2] "=&v"(r2), [r3] "=&v"(r3), [x] "=&v"(x), [F] "=&v"(F),
+                 [S] "=&v"(S), [G] "=&v"(G), [P] "=&v"(P), [v0] "=&v"(v0), [v1] "=&v"(v1),
+                 [Vo] "=&v"(vo), [n0] "=&v"(n0), [n1] "=&v"(n1), [n2] "=&v"(n2)
+               : [s0] "v"(q.s0), [s1] "v"(q.s1), [s2] "v"(q.s2), [V] "v"(q.v), [k0] "v"(k0),
+                 [k1] "v"(k1), [k2] "v"(k2), [c1] "v"(c.c1), [c2] "v"(c.c2), [c3] "v"(c.c3),
+                 [m] "v"(c.m));
+  q.s3 = q.s0; q.s0 = n2; q.s1 = n1; q.s2 = n0; q.v = vo;
+}
+// Rounds 62 and 63 (the last): k0 is K + W of round 63.
+__device__ __forceinline__ void split_rounds_end(SplitState &q, uint32_t k0,
+                                                 const SplitLane &c) {
+  uint32_t r1, r2, r3, x, F, S, G, P, v0, n0, n1;
+  asm volatile(EA_RND("s0", "s1", "s2", "k0", "V", "v0", "n0")
+               EA_RND_LAST("n0", "s0", "s1", "v0", "n1")
+               : [r1] "=&v"(r1), [r2] "=&v"(r2), [r3] "=&v"(r3), [x] "=&v"(x), [F] "=&v"(F),
+                 [S] "=&v"(S), [G] "=&v"(G), [P] "=&v"(P), [v0] "=&v"(v0), [n0] "=&v"(n0),
+                 [n1] "=&v"(n1)
+               : [s0] "v"(q.s0), [s1] "v"(q.s1), [s2] "v"(q.s2), [V] "v"(q.v), [k0] "v"(k0),
+                 [c1] "v"(c.c1), [c2] "v"(c.c2), [c3] "v"(c.c3), [m] "v"(c.m));
+  q.s3 = q.s1; q.s2 = q.s0; q.s1 = n0; q.s0 = n1;
+}
+
+// DPP move within a row of 16 lanes; lanes whose source lies outside the
+// row read zero.
+constexpr int kRowShl1 = 0x101, kRowShl9 = 0x109, kRowShl14 = 0x10E;
+constexpr int kRowShr2 = 0x112, kRowShr7 = 0x117, kRowShr12 = 0x11C, kRowShr15 = 0x11F;
+template <int CTRL>
+__device__ __forceinline__ uint32_t row_move(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+__device__ __forceinline__ uint32_t sig0(uint32_t x) {
+  return bitop3<kXor3>(rotr(x, 7), rotr(x, 18), x >> 3);
+}
+__device__ __forceinline__ uint32_t sig1(uint32_t x) {
+  return bitop3<kXor3>(rotr(x, 17), rotr(x, 19), x >> 10);
+}
+
+// Lane j of a row holds W_T0-16+j; returns W_T0+j.
+__device__ __forceinline__ uint32_t split_schedule16(uint32_t wp) {
+  uint32_t q = sig0(row_move<kRowShl1>(wp)) + wp;  // sigma0(W_t-15) + W_t-16 (lane 15: below)
+  q += row_move<kRowShl9>(wp);                      // W_t-7 for j < 7
+  q += sig1(row_move<kRowShl14>(wp));               // sigma1(W_t-2) for j < 2
+  uint32_t w = q;                                   // lanes 0, 1 final
+  q += sig0(row_move<kRowShr15>(w));                // lane 15: sigma0(W_T0)
+  uint32_t w1 = w, w2 = w;
+#pragma unroll
+  for (int s = 1; s < 8; ++s) {
+    // lane j - 7 is final three steps before lane j
+    const uint32_t t7 = row_move<kRowShr7>(w2) + q;
+    w2 = w1; w1 = w;
+    w = sig1(row_move<kRowShr2>(w)) + t7;
+  }
+  return w;
+}
+
 template <typename Off>
 __global__ __launch_bounds__(128) void sha256_chain_split(
     const uint32_t *__restrict__ mid, const Off *__restrict__ key_off, int32_t n_seqs,
     uint32_t len_bits, const uint8_t *__restrict__ parents, uint8_t *__restrict__ keys) {
-  __shared__ uint4 wk4[12];   // W_t + K_t for t = 16..63
-  __shared__ uint4 key4[2];   // the key just written, as state words
+  // words 0..47: K_t + W_t (t = 16..63); 48..95: ones (the a-lanes' K +
+  // W); 96..103 the last key, 104..111 the padding words; 112..367: the
+  // stores of lanes that hold nothing
+  __shared__ __align__(16) uint32_t lds[112 + 4 * 64];
   const int32_t s = blockIdx.x;
   if (s >= n_seqs) return;  // the whole workgroup
-  const bool rounds_wave = threadIdx.x < 64;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const bool e_side = lane & 1;
+  const int j = lane & 15;
+  const bool e_lane = j >= 12;
+  const bool a_lane = j < 4;
   const int64_t k0 = key_off[s], k1 = key_off[s + 1];
-  const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
-  const uint32_t m = e_side ? 0u : 0xffffffffu;
-  const uint32_t pad8 = e_side ? 0x80000000u : 0u;   // (W8, W9)
-  const uint32_t pad14 = e_side ? 0u : len_bits;      // (W14, W15)
   uint32_t prev[8];
   parent_words(parents, s, prev);
-  // rounds wave: the previous key in pairs, x[j] = (W_2j, W_2j+1) as
-  // (e-lane, a-lane), and the next midstate half
-  uint32_t x[4] = {e_side ? prev[0] : prev[1], e_side ? prev[2] : prev[3],
-                   e_side ? prev[4] : prev[5], e_side ? prev[6] : prev[7]};
-  const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
-  uint4 nx = make_uint4(0, 0, 0, 0);
-  if (rounds_wave && k0 < k1) nx = mh[2 * k0 + (e_side ? 1 : 0)];
-  // first midstate taken before the loop, as in the two-lane form
-  asm volatile("" ::"v"(nx.x), "v"(nx.y), "v"(nx.z), "v"(nx.w));
-  uint32_t w[16];  // schedule wave: the rolling message schedule
-  uint32_t s0 = 0, s1 = 0, s2 = 0, s3 = 0;
-  uint4 h0 = make_uint4(0, 0, 0, 0);
-  uint32_t X[8];
-  uint32_t qa[16], qb[16];  // rounds wave: two parts of the schedule in hand
-  // Each barrier comes four rounds before the rounds wave needs the part
-  // it releases: the wave issues the LDS reads and runs four rounds from
-  // words it already holds while they arrive.
-  auto read_part = [&](int part, uint32_t q[16]) {
+  if (wave == 1) {
+    if (lane < 48) lds[48 + lane] = 1u;
+    if (lane < 8) lds[104 + lane] = lane == 0 ? 0x80000000u : (lane == 7 ? len_bits : 0u);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    SplitLane c;
+    c.c1 = e_lane ? 6 : 2;
+    c.c2 = e_lane ? 11 : 13;
+    c.c3 = e_lane ? 25 : 22;
+    c.m = e_lane ? 0u : 0xffffffffu;
+    // K_t (t < 8) and K_t + W_t (t = 8..15, the padding) on e-lanes, 1 on a-lanes
+    uint32_t kc[8], kwc[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint4 v = wk4[4 * part + i];
-      q[4 * i] = v.x; q[4 * i + 1] = v.y; q[4 * i + 2] = v.z; q[4 * i + 3] = v.w;
+    for (int t = 0; t < 8; ++t) kc[t] = e_lane ? kRound[t] : 1u;
+#pragma unroll
+    for (int t = 8; t < 16; ++t) {
+      const uint32_t w = t == 8 ? 0x80000000u : (t == 15 ? len_bits : 0u);
+      kwc[t - 8] = e_lane ? kRound[t] + w : 1u;
     }
-  };
-  auto write_part = [&](int part, const uint32_t o[16]) {
-    if (lane == 0)
+    uint32_t o[4];  // the previous key, this lane's half (a: H0..3, e: H4..7)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        wk4[4 * part + i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
-  };
-  for (int64_t k = k0; k < k1; ++k) {
-    // rounds 0..11 | words 16..31
-    if (rounds_wave) {
-      h0 = nx;
-      if (k + 1 < k1) nx = mh[2 * (k + 1) + (e_side ? 1 : 0)];
-      s0 = h0.x; s1 = h0.y; s2 = h0.z; s3 = h0.w;
-      X[0] = x[0]; X[1] = x[1]; X[2] = x[2]; X[3] = x[3];
-      X[4] = pad8; X[5] = 0u; X[6] = 0u; X[7] = pad14;
+    for (int i = 0; i < 4; ++i) o[i] = e_lane ? prev[4 + i] : prev[i];
+    const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
+    const int half = j >= 8 ? 1 : 0;
+    uint4 nx = make_uint4(0, 0, 0, 0);
+    if (k0 < k1) nx = mh[2 * k0 + half];
+    // The word offsets of the K + W reads and of the key store differ per
+    // lane; hiding them keeps the compiler from reading both arrays and
+    // selecting.
+    uint32_t kbase = e_lane ? 0u : 48u;
+    asm volatile("" : "+v"(kbase));
+    const uint4 *kw4 = reinterpret_cast<const uint4 *>(lds + kbase);
+    uint32_t kst = a_lane ? 96u : (e_lane ? 100u : 112u + 4u * lane);
+    asm volatile("" : "+v"(kst));
+    uint4 *key_dst = reinterpret_cast<uint4 *>(lds + kst);
+    for (int64_t k = k0; k < k1; ++k) {
+      const uint4 h0 = nx;
+      if (k + 1 < k1) nx = mh[2 * (k + 1) + half];
+      SplitState q{h0.x, h0.y, h0.z, h0.w, 0u};
+      uint32_t kw[8];  // K + W of rounds 0..7: the previous key
 #pragma unroll
-      for (int t = 0; t < 12; ++t) {
-        const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[t >> 1]) : X[t >> 1];
-        pair_round(s0, s1, s2, s3, kRound[t] + wt, r1c, r2c, r3c, m, e_side);
-      }
-    } else {
+      for (int t = 0; t < 4; ++t) kw[t] = row_move<kRowShr12>(o[t]) + kc[t];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) w[j] = prev[j];
-      w[8] = 0x80000000u;
-#pragma unroll
-      for (int j = 9; j < 15; ++j) w[j] = 0u;
-      w[15] = len_bits;
-      uint32_t o[16];
-      schedule16<16>(w, o);
-      write_part(0, o);
+      for (int t = 4; t < 8; ++t) kw[t] = e_lane ? o[t - 4] + kc[t] : 1u;
+      q.v = (q.s3 ^ c.m) + (row_move<kRowShr12>(q.s3) + kw[0]);
+      split_rounds4(q, kw[1], kw[2], kw[3], kw[4], c);      // rounds 0..3
+      split_rounds4(q, kw[5], kw[6], kw[7], kwc[0], c);     // 4..7
+      split_rounds4(q, kwc[1], kwc[2], kwc[3], kwc[4], c);  // 8..11
+      __syncthreads();
+      uint4 a0 = kw4[0], a1 = kw4[1], a2 = kw4[2], a3 = kw4[3];  // t = 16..31
+      split_rounds3(q, kwc[5], kwc[6], kwc[7], c);          // 12..14
+      split_rounds4(q, a0.x, a0.y, a0.z, a0.w, c);          // 15..18
+      split_rounds4(q, a1.x, a1.y, a1.z, a1.w, c);          // 19..22
+      split_rounds4(q, a2.x, a2.y, a2.z, a2.w, c);          // 23..26
+      __syncthreads();
+      a0 = kw4[4]; a1 = kw4[5]; a2 = kw4[6];                // t = 32..43
+      const uint4 b3 = kw4[7];                               // t = 44..47
+      split_rounds4(q, a3.x, a3.y, a3.z, a3.w, c);          // 27..30
+      split_rounds4(q, a0.x, a0.y, a0.z, a0.w, c);          // 31..34
+      split_rounds4(q, a1.x, a1.y, a1.z, a1.w, c);          // 35..38
+      split_rounds4(q, a2.x, a2.y, a2.z, a2.w, c);          // 39..42
+      __syncthreads();
+      a0 = kw4[8]; a1 = kw4[9]; a2 = kw4[10]; a3 = kw4[11];  // t = 48..63
+      split_rounds4(q, b3.x, b3.y, b3.z, b3.w, c);          // 43..46
+      split_rounds4(q, a0.x, a0.y, a0.z, a0.w, c);          // 47..50
+      split_rounds4(q, a1.x, a1.y, a1.z, a1.w, c);          // 51..54
+      split_rounds4(q, a2.x, a2.y, a2.z, a2.w, c);          // 55..58
+      split_rounds3(q, a3.x, a3.y, a3.z, c);                // 59..61
+      split_rounds_end(q, a3.w, c);                         // 62, 63
+      o[0] = h0.x + q.s0; o[1] = h0.y + q.s1; o[2] = h0.z + q.s2; o[3] = h0.w + q.s3;
+      *key_dst = make_uint4(o[0], o[1], o[2], o[3]);
+      __syncthreads();
     }
-    __syncthreads();
-    // rounds 12..27 | words 32..47
-    if (rounds_wave) {
-      read_part(0, qa);
-#pragma unroll
-      for (int t = 12; t < 16; ++t) {
-        const uint32_t wt = (t & 1) ? dpp_from<kPermFromA>(X[t >> 1]) : X[t >> 1];
-        pair_round(s0, s1, s2, s3, kRound[t] + wt, r1c, r2c, r3c, m, e_side);
-      }
-#pragma unroll
-      for (int t = 16; t < 28; ++t) pair_round(s0, s1, s2, s3, qa[t - 16], r1c, r2c, r3c, m, e_side);
-    } else {
-      uint32_t o[16];
-      schedule16<32>(w, o);
-      write_part(1, o);
+  } else {
+    // lane j: W_j of the first key's final block (the parent and padding),
+    // read per lane rather than from prev[j], which a per-lane index would
+    // move out of registers
+    uint32_t wp = j == 8 ? 0x80000000u : (j == 15 ? len_bits : 0u);
+    if (j < 8 && parents != nullptr) {
+      const uint8_t *pw = parents + 32 * (int64_t)s + 4 * j;
+      wp = ((uint32_t)pw[0] << 24) | ((uint32_t)pw[1] << 16) | ((uint32_t)pw[2] << 8) | pw[3];
     }
-    __syncthreads();
-    // rounds 28..43 | words 48..63
-    if (rounds_wave) {
-      read_part(1, qb);
-#pragma unroll
-      for (int t = 28; t < 32; ++t) pair_round(s0, s1, s2, s3, qa[t - 16], r1c, r2c, r3c, m, e_side);
-#pragma unroll
-      for (int t = 32; t < 44; ++t) pair_round(s0, s1, s2, s3, qb[t - 32], r1c, r2c, r3c, m, e_side);
-    } else {
-      uint32_t o[16];
-      schedule16<48>(w, o);
-      write_part(2, o);
+    const uint32_t kp0 = kRound[16 + j], kp1 = kRound[32 + j], kp2 = kRound[48 + j];
+    for (int64_t k = k0; k < k1; ++k) {
+      const uint32_t key_prev = wp;  // lanes 0..7: key k - 1
+      uint32_t w = split_schedule16(wp);
+      lds[j] = w + kp0;
+      __syncthreads();
+      if (k > k0 && lane < 8)
+        reinterpret_cast<uint32_t *>(keys + 32 * (k - 1))[lane] = __builtin_bswap32(key_prev);
+      w = split_schedule16(w);
+      lds[16 + j] = w + kp1;
+      __syncthreads();
+      w = split_schedule16(w);
+      lds[32 + j] = w + kp2;
+      __syncthreads();
+      __syncthreads();
+      wp = lds[96 + j];
     }
-    __syncthreads();
-    // rounds 44..63 and the key | idle
-    if (rounds_wave) {
-      read_part(2, qa);
-#pragma unroll
-      for (int t = 44; t < 48; ++t) pair_round(s0, s1, s2, s3, qb[t - 32], r1c, r2c, r3c, m, e_side);
-#pragma unroll
-      for (int t = 48; t < 64; ++t) pair_round(s0, s1, s2, s3, qa[t - 48], r1c, r2c, r3c, m, e_side);
-      const uint32_t o0 = h0.x + s0, o1 = h0.y + s1, o2 = h0.z + s2, o3 = h0.w + s3;
-      if (lane < 2) {
-        uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k + (e_side ? 16 : 0));
-        *out = make_uint4(__builtin_bswap32(o0), __builtin_bswap32(o1), __builtin_bswap32(o2),
-                          __builtin_bswap32(o3));
-        key4[e_side ? 1 : 0] = make_uint4(o0, o1, o2, o3);
-      }
-      const uint32_t a0 = dpp_from<kPermFromA>(o0), a2 = dpp_from<kPermFromA>(o2);
-      const uint32_t e1 = dpp_from<kPermFromE>(o1), e3 = dpp_from<kPermFromE>(o3);
-      x[0] = e_side ? a0 : o1;
-      x[1] = e_side ? a2 : o3;
-      x[2] = e_side ? o0 : e1;
-      x[3] = e_side ? o2 : e3;
-    }
-    __syncthreads();
-    if (!rounds_wave) {
-      const uint4 ka = key4[0], kb = key4[1];
-      prev[0] = ka.x; prev[1] = ka.y; prev[2] = ka.z; prev[3] = ka.w;
-      prev[4] = kb.x; prev[5] = kb.y; prev[6] = kb.z; prev[7] = kb.w;
-    }
+    if (k0 < k1 && lane < 8)
+      reinterpret_cast<uint32_t *>(keys + 32 * (k1 - 1))[lane] = __builtin_bswap32(wp);
   }
 }
 

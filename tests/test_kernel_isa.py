@@ -80,8 +80,8 @@ def test_no_scratch_and_lds_only_where_waves_share(assembly, src):
     assert set(scratch) >= set(bodies)
     for name in bodies:
         assert scratch[name] == 0, name
-        if "split" in name:
-            assert 0 < lds[name] <= 1024, (name, lds[name])
+        if "split" in name:  # the schedule hand-over (and the chain's key slots)
+            assert 0 < lds[name] <= 2048, (name, lds[name])
         elif "hash_offsets" in name:  # the key-offset scan's 256 run totals
             assert 0 < lds[name] <= 2048 + 64, (name, lds[name])
         else:
