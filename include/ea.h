@@ -51,11 +51,11 @@
  *  EA_TRANSFER=direct|staged   transfer plan of tiers left at EA_PLAN_AUTO
  *  EA_LINK_WG, EA_LINK_WG_STORE, EA_LINK_WG_LOAD
  *                              working workgroups of a direct store / load
- *                              (8 / 9; EA_LINK_WG sets both)
- *  EA_LOAD_PRIORITY            sleeps (x 127 x 64 cycles) a direct store's
- *                              waves take per 32 KiB copied while waves of a
- *                              direct or layered load of the same tier run
- *                              (4; 0 = off); read at tier creation
+ *                              (8 / 8; EA_LINK_WG sets both)
+ *  EA_LOAD_PRIORITY            sleep (in units of 1,024 cycles) a direct
+ *                              store's waves take per 32 KiB copied while
+ *                              waves of a direct or layered load of the same
+ *                              tier run (31; 0 = off); read at tier creation
  *  EA_LINK_WG_LAYERED          workgroups of one layer of a layered load (16)
  *  EA_XCD_STORE, EA_XCD_LOAD   XCD masks of the two directions (0x5, 0xA
  *                              with four or more XCDs); read at tier creation

@@ -120,13 +120,13 @@ int64_t grid_hbm(int dir) {
 // default (EA_XCD_STORE / EA_XCD_LOAD override the masks).  EA_LINK_WG sets
 // both directions' workgroups, EA_LINK_WG_STORE / EA_LINK_WG_LOAD one each.
 //
-// Loads get one workgroup more than stores (9 against 8): with a store
-// yielding the link (EA_LOAD_PRIORITY below) the load's extra reads in
-// flight carry it to 94% of the pinned host-to-device peak during the turn's
-// duplex, against 84% with 8.
+// Both directions get 8.  A ninth load workgroup carries the load to 95-96%
+// of the pinned host-to-device peak during the turn's duplex whatever the
+// store does, and costs the duplex 3-5%; with 8 the store's yield
+// (EA_LOAD_PRIORITY below) sets the share.
 int64_t grid_link(int dir) {
   const int both = env_int("EA_LINK_WG", 0);
-  const int dflt = both > 0 ? both : (dir == ea::kToSlots ? 8 : 9);
+  const int dflt = both > 0 ? both : 8;
   return std::max(1, env_int(dir == ea::kToSlots ? "EA_LINK_WG_STORE" : "EA_LINK_WG_LOAD", dflt));
 }
 
@@ -349,10 +349,10 @@ struct ea_tier {
   int64_t grid_store = 8, grid_load = 8, grid_layered = 16, grid_gather = 512, grid_scatter = 256;
   int32_t num_xcd = 1;
   uint32_t xcd_store = 1, xcd_load = 1;
-  // loads have priority on the host link when yield_sleeps > 0: load waves
+  // loads have priority on the host link when yield_units > 0: load waves
   // count themselves in d_busy, and direct stores sleep while it is > 0
   uint32_t *d_busy = nullptr;
-  int32_t yield_sleeps = 0;
+  int32_t yield_units = 0;
   int32_t controllers = 0;  // attached admission controllers (guarded by mu)
   int32_t steady_users = 0; // attached steady-clock controllers (guarded by mu)
 };
@@ -503,7 +503,7 @@ int copy_direct(ea_tier *t, ea_cache *c, const int64_t *slots, const int32_t *pa
   if (t->d_busy != nullptr) {
     a.link_flag = t->d_busy;
     a.link_role = dir == ea::kToSlots ? ea::kLinkYield : ea::kLinkMark;
-    a.yield_sleeps = t->yield_sleeps;
+    a.yield_units = t->yield_units;
   }
   return launch_entries(a, t->res[res_dir].ring, slots, pages, n, dir, ea::kRouteHostLink,
                         dir == ea::kToSlots ? t->grid_store : t->grid_load, s);
@@ -745,13 +745,14 @@ int ea_tier_create_chunked(const ea_cache *shape, int32_t chunk_pages, int64_t c
     // Loads first on the host link: a restore is the T_load of Eq. 2 that a
     // waiting request pays, a store is background write-back.  While waves
     // of a load of this tier run, each wave of a direct store sleeps
-    // 4 x 127 x 64 cycles per 32 KiB it copies.  Measured on the Qwen3 turn
-    // (2,000-page store beside a 1,500-page load): the load's in-step rate
-    // rose from 42.4-42.9 to 54.0 GB/s and the duplex fell from 87.5-87.8 to
-    // 85.2 GB/s; 3 sleeps did not shift the share, 5 or more cut the duplex
-    // to 79 GB/s and below.  EA_LOAD_PRIORITY=0 turns it off.
-    t->yield_sleeps = std::max(0, env_int("EA_LOAD_PRIORITY", 4));
-    if (t->yield_sleeps > 0) {
+    // EA_LOAD_PRIORITY x 1,024 cycles per 32 KiB it copies.  Measured on the
+    // Qwen3 turn (2,000-page store beside a 1,500-page load, 8 workgroups
+    // each way), load in the step / duplex: off 76% / 88.3 GB/s, 28 units
+    // 77% / 88.9, 30 82% / 87.0, 32 85% / 85.2, 34 87% / 83.5, 40 90% /
+    // 79.2.  31 keeps the restore above 80% of the host-to-device peak and
+    // the duplex above 85 GB/s.  EA_LOAD_PRIORITY=0 turns it off.
+    t->yield_units = std::max(0, env_int("EA_LOAD_PRIORITY", 31));
+    if (t->yield_units > 0) {
       e = hipMalloc((void **)&t->d_busy, 256);
       if (e == hipSuccess) e = hipMemset(t->d_busy, 0, 256);
       if (e != hipSuccess) {

@@ -105,8 +105,8 @@ __device__ __forceinline__ void copy_unit(const PieceCopy &a, int64_t l, int64_t
 // Loads first on the host link.  Every wave of a load raises the tier's
 // counter for its whole loop.  A store wave reads the counter before each
 // unit and acts on it after the unit (so the read's round trip overlaps the
-// copy): while a load runs it sleeps a.yield_sleeps x 127 x 64 cycles per
-// 32 KiB copied, which holds back small pieces as much as large ones.
+// copy): while a load runs it sleeps a.yield_units x 1,024 cycles per 32 KiB
+// copied, which holds back small pieces as much as large ones.
 constexpr int64_t kYieldBytes = 32768;
 
 __device__ __forceinline__ uint32_t link_busy(const PieceCopy &a) {
@@ -121,7 +121,7 @@ __device__ __forceinline__ void yield_link(const PieceCopy &a, uint32_t busy, in
     return;
   }
   for (; debt >= kYieldBytes; debt -= kYieldBytes)
-    for (int32_t k = 0; k < a.yield_sleeps; ++k) __builtin_amdgcn_s_sleep(127);
+    for (int32_t k = 0; k < a.yield_units; ++k) __builtin_amdgcn_s_sleep(16);  // 16 x 64 cycles
 }
 // one lane per wave: +1 before a load wave's loop, -1 after it
 __device__ __forceinline__ void mark_load(const PieceCopy &a, int lane, int32_t delta) {

@@ -38,11 +38,11 @@ struct PieceCopy {
   // Loads first on the host link.  link_flag is the tier's count of load
   // waves at work (nullptr: no priority).  A load (link_role 2) raises it
   // by one per wave for the wave's whole loop; a store (link_role 1) that
-  // finds it non-zero sleeps yield_sleeps x 127 x 64 cycles per 32 KiB it
-  // has copied since its last sleep.
+  // finds it non-zero sleeps yield_units x 1,024 cycles per 32 KiB it has
+  // copied since its last sleep.
   uint32_t *link_flag;
   int32_t link_role;
-  int32_t yield_sleeps;
+  int32_t yield_units;
   // Only workgroups on XCDs in xcd_mask do work.  Workgroups of a dispatch
   // go round-robin over the XCDs starting at an offset the hardware chooses
   // (workgroup b runs on XCD (b + offset) % num_xcd), so the workgroup's
