@@ -1447,6 +1447,7 @@ def summarize_plans(d):
              "-- python3 bench.py --workload plans --plan P",
              "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d bench_out/plans_P/write -o write "
              "-- python3 bench.py --workload plans --plan P",
+             "    python3 bench.py --workload plans --plan P > bench_out/plans_P/line.json",
              "    python3 bench.py --summarize-plans bench_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
              "Each process runs one plan over every size class: stores and loads alone, to "
@@ -1458,6 +1459,8 @@ def summarize_plans(d):
     both = {plan: json.load(open(os.path.join(d, f"plans_{plan}", "line.json")))["plans"]
             for plan in ("direct", "staged")}
     lines += ["## Rates per size class (HIP events, GB/s; store / load)", "",
+              "From the run without the profiler (the last command before the summary): the "
+              "copy trace adds its own cost to each of the staged plan's many small copies.", "",
               "| case | slot bytes | slots per call (store / load) | direct, consecutive | "
               "staged, consecutive | direct, random | staged, random |", "|---|---|---|---|---|---|---|"]
     for case, v in both["direct"].items():
