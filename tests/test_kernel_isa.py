@@ -3,7 +3,8 @@ keeps to the rules its kernels are written under: no scalar-cache writes
 (every store is a vector store), no packed two-wide FP32 instructions (the
 build turns them off), no scratch (private) memory, and LDS only in the
 kernels that hand data between waves (the two-wave hash forms and the
-one-workgroup scan of key offsets)."""
+one-workgroup scan of key offsets), and every DPP instruction written as
+inline asm keeps the wait states the hardware needs before it."""
 import os
 import re
 import shutil
@@ -86,3 +87,102 @@ def test_no_scratch_and_lds_only_where_waves_share(assembly, src):
             assert 0 < lds[name] <= 2048 + 64, (name, lds[name])
         else:
             assert lds[name] == 0, (name, lds[name])
+
+
+# ---------------------------------------------------------------- DPP hazards
+# A DPP instruction needs every VGPR it reads to have been written by a
+# VALU instruction at least two wait states earlier, and an EXEC write at
+# least five earlier (each instruction is one wait state, s_nop N is N + 1).
+# The compiler inserts those waits for its own code, not inside inline asm,
+# so the asm rounds of the hash chain are checked here.
+VGPR = re.compile(r"\bv(\d+)\b|\bv\[(\d+):(\d+)\]")
+
+
+def _vgprs(text):
+    out = set()
+    for m in VGPR.finditer(text):
+        if m.group(1) is not None:
+            out.add(int(m.group(1)))
+        else:
+            out.update(range(int(m.group(2)), int(m.group(3)) + 1))
+    return out
+
+
+def _instructions(body):
+    """(mnemonic, operand text, in_asm) per instruction, labels as ('LABEL', '', in_asm)."""
+    res, in_asm = [], False
+    for line in body:
+        s = line.split(";")[0].strip() if "ASM" not in line else line.strip()
+        if "ASMSTART" in s:
+            in_asm = True
+            continue
+        if "ASMEND" in s:
+            in_asm = False
+            continue
+        if not s or s.startswith("."):
+            if s.startswith(".LBB"):
+                res.append(("LABEL", "", in_asm))
+            continue
+        op, _, rest = s.partition(" ")
+        res.append((op, rest, in_asm))
+    return res
+
+
+def _valu_dst(op, rest):
+    if not op.startswith("v_") or op.startswith("v_cmp") or op.startswith("v_readlane") \
+            or op.startswith("v_readfirstlane"):
+        return set()
+    first = rest.split(",")[0]
+    return _vgprs(first)
+
+
+def _writes_exec(op, rest):
+    return ("saveexec" in op or op.startswith("v_cmpx")
+            or (op.startswith("s_") and rest.split(",")[0].strip() == "exec"))
+
+
+def _dpp_hazards(instrs):
+    bad = []
+    for k, (op, rest, in_asm) in enumerate(instrs):
+        if not in_asm or ("_dpp" not in op and "quad_perm" not in rest and "row_" not in rest):
+            continue
+        reads = _vgprs(rest.partition(",")[2])
+        waits = 0
+        for j in range(k - 1, -1, -1):
+            pop, prest, _ = instrs[j]
+            if pop == "LABEL":
+                bad.append((k, op, rest, "window crosses a label"))
+                break
+            if waits < 2 and reads & _valu_dst(pop, prest):
+                bad.append((k, op, rest, f"reads a VGPR written {waits} wait states before"))
+                break
+            if waits < 5 and _writes_exec(pop, prest):
+                bad.append((k, op, rest, f"EXEC written {waits} wait states before"))
+                break
+            waits += int(prest.split()[0]) + 1 if pop == "s_nop" else 1
+            if waits >= 5:
+                break
+    return bad
+
+
+def test_dpp_checker_catches_a_short_window():
+    # a planted hazard: the DPP add reads v3 right after a VALU wrote it
+    body = [";;#ASMSTART", "v_add_u32 v3, v1, v2",
+            "v_add_u32_dpp v4, v3, v3 row_shl:12 row_mask:0xf bank_mask:0xf bound_ctrl:1",
+            ";;#ASMEND"]
+    assert _dpp_hazards(_instructions(body))
+    ok = [";;#ASMSTART", "v_add_u32 v3, v1, v2", "v_add_u32 v5, v1, v2", "v_add_u32 v6, v1, v2",
+          "v_add_u32_dpp v4, v3, v3 row_shl:12 row_mask:0xf bank_mask:0xf bound_ctrl:1",
+          ";;#ASMEND"]
+    assert not _dpp_hazards(_instructions(ok))
+
+
+def test_asm_dpp_reads_keep_their_wait_states(assembly):
+    bodies, _, _ = kernels(assembly["ea_sha256_kernels.hip"])
+    checked = 0
+    for name, body in bodies.items():
+        instrs = _instructions(body)
+        checked += sum(1 for op, rest, in_asm in instrs if in_asm and "_dpp" in op)
+        bad = _dpp_hazards(instrs)
+        assert not bad, (name, bad[:3])
+    assert checked > 0, "no DPP instruction inside asm found"
