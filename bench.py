@@ -1645,7 +1645,7 @@ def run_hash(args):
         log(f"hash {name}: {out[name]}")
     b = out["batch_65536x256"]
     achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
-    roof = {"bound": "alu", "kernel": "hash key-offset scan + sha256_fused_lane "
+    roof = {"bound": "alu", "kernel": "hash_offsets_partials + sha256_fused_scan "
                                       "(65,536 x 256 tokens, offsets in HBM)",
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),

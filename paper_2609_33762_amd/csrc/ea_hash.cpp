@@ -391,6 +391,12 @@ extern "C" int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_
     HS_HIP(ea::launch_hash_scan_reset(w.d_scan, stream));  // a fresh ticket counter
   }
   if ((rc = ensure_mid(w, &w.d_mid, &w.cap_mid, std::max<int64_t>(bound, 1))) != EA_OK) return rc;
+  if (bound > 0 && ea::hash_fused(n_seqs)) {  // offsets and keys in two kernels
+    HS_HIP(ea::launch_hash_fused_offsets(d_tokens, d_seq_offsets, n_seqs, n_tokens, block_tokens,
+                                         bound, d_key_offsets_out, d_parents, d_keys_out,
+                                         w.d_scan, stream));
+    return release(w, stream);
+  }
   uint8_t *d_koff = w.d_off;
   uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
   HS_HIP(ea::launch_hash_key_offsets(d_seq_offsets, n_seqs, n_tokens, block_tokens, bound,
@@ -416,6 +422,12 @@ extern "C" int ea_hash_blocks_device_offsets_noalloc(
   HS_HIP(ea::hash_scratch(stream, &scratch));
   uint8_t *base = static_cast<uint8_t *>(scratch);
   const bool wide = n_tokens > INT32_MAX || bound > INT32_MAX || force_wide();
+  if (bound > 0 && ea::hash_fused(n_seqs)) {  // offsets and keys in two kernels
+    HS_HIP(ea::launch_hash_fused_offsets(d_tokens, d_seq_offsets, n_seqs, n_tokens, block_tokens,
+                                         bound, d_key_offsets_out, d_parents, d_keys_out,
+                                         base + ea::kScratchState, stream));
+    return EA_OK;
+  }
   uint8_t *d_koff = base + ea::kScratchOffsets;
   uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
   HS_HIP(ea::launch_hash_key_offsets(d_seq_offsets, n_seqs, n_tokens, block_tokens, bound,

@@ -131,6 +131,15 @@ hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
                                    int64_t n_tokens, int32_t block_tokens, int64_t keys_cap,
                                    int64_t *d_key_offsets_out, bool wide, void *d_koff,
                                    void *d_toff, void *d_state, hipStream_t stream);
+// The same offsets and the keys for batches that take the fused form
+// (hash_fused): the scan's first kernel, then one kernel that scans each
+// workgroup's sequences from its prefix, writes d_key_offsets_out and
+// hashes.  Same failure contract; d_state as above.
+hipError_t launch_hash_fused_offsets(const int32_t *d_tokens, const int64_t *d_seq_offsets,
+                                     int32_t n_seqs, int64_t n_tokens, int32_t block_tokens,
+                                     int64_t keys_cap, int64_t *d_key_offsets_out,
+                                     const uint8_t *d_parents, uint8_t *d_keys, void *d_state,
+                                     hipStream_t stream);
 int64_t hash_scan_groups(int32_t n_seqs);
 // Zero the first 8 bytes of a scan state on `stream` (a fill kernel).
 hipError_t launch_hash_scan_reset(void *d_state, hipStream_t stream);
@@ -143,13 +152,24 @@ constexpr int64_t kScratchKeys = int64_t(1) << 20;
 constexpr int64_t kScratchSeqs = int64_t(1) << 20;
 constexpr int64_t kScratchOffsets = 32 * kScratchKeys;  // byte offsets in the scratch
 constexpr int64_t kScratchState = kScratchOffsets + (8 * (2 * kScratchSeqs + 1) + 255) / 256 * 256;
-constexpr int64_t kScratchBytes = kScratchState + 64 + 16 * ((kScratchSeqs + 2047) / 2048);
+// Sequences per workgroup of the key-offset scan, and per sub-block of it
+// (the fused hash kernel's workgroups, one sequence per work-item).  The
+// scan state holds 64 bytes, two words per group and one per sub-block.
+constexpr int64_t kHashScanSeqs = 2048;
+constexpr int64_t kHashScanSub = 256;
+constexpr int64_t hash_scan_state_for(int64_t groups) {
+  return 64 + 16 * groups + 8 * groups * (kHashScanSeqs / kHashScanSub);
+}
+constexpr int64_t kScratchBytes =
+    kScratchState + hash_scan_state_for((kScratchSeqs + kHashScanSeqs - 1) / kHashScanSeqs);
 // The scratch's address on the current device: resolved with
 // hipGetSymbolAddress the first time a device asks (that device current),
 // then kept; the first resolution also zeroes the scan's ticket counter
 // with a fill kernel on `stream`.
 hipError_t hash_scratch(hipStream_t stream, void **ptr);
-inline int64_t hash_scan_state_bytes(int32_t n_seqs) { return 64 + 16 * hash_scan_groups(n_seqs); }
+inline int64_t hash_scan_state_bytes(int32_t n_seqs) {
+  return hash_scan_state_for(hash_scan_groups(n_seqs));
+}
 
 
 }  // namespace ea

@@ -683,7 +683,10 @@ __global__ __launch_bounds__(256) void sha256_chain_lane(
 
 // Key offsets from device-resident sequence offsets, in two kernels.  A
 // workgroup owns kScanSeqs consecutive sequences, kScanRun per thread
-// (thread t the t-th run), so its loads cover one contiguous range.
+// (thread t the t-th run), so its loads cover one contiguous range.  Each
+// group also records where each of its sub-blocks of kSubSeqs sequences
+// starts inside it, for the fused hash kernel, whose workgroups are those
+// sub-blocks (one sequence per lane).
 //   hash_offsets_partials: each workgroup counts the full blocks of its
 //     sequences and checks them; the last workgroup to finish (a ticket
 //     counter, reset by that workgroup) turns the per-workgroup totals into
@@ -697,16 +700,23 @@ __global__ __launch_bounds__(256) void sha256_chain_lane(
 constexpr int kScanThreads = 256;
 constexpr int kScanRun = 8;
 constexpr int64_t kScanSeqs = (int64_t)kScanThreads * kScanRun;
+constexpr int kSubSeqs = 256;
+constexpr int kSubThreads = kSubSeqs / kScanRun;  // scan threads per sub-block
+constexpr int kSubsPerGroup = (int)(kScanSeqs / kSubSeqs);
+static_assert(kScanSeqs == kHashScanSeqs && kSubSeqs == kHashScanSub,
+              "scan groups and the scratch's scan state agree");
 
 // Scan state in device memory: [0] ticket counter (zero between calls),
 // [1] grand total, [2] error flag, then per workgroup its total and, after
-// the last workgroup's pass, its exclusive prefix.
+// the last workgroup's pass, its exclusive prefix, then per sub-block its
+// exclusive prefix inside its group.
 struct ScanState {
   uint64_t *ticket;
   int64_t *total;
   int64_t *bad;
   int64_t *part;    // [groups]
   int64_t *prefix;  // [groups]
+  int64_t *subex;   // [groups * kSubsPerGroup]
 };
 
 __device__ __forceinline__ int64_t full_blocks(int64_t len, int32_t block_tokens, int32_t shift) {
@@ -776,7 +786,10 @@ __global__ __launch_bounds__(kScanThreads) void hash_offsets_partials(
       ok = ok && e >= a && e <= n_tokens;
       count += ok ? full_blocks(e - a, block_tokens, shift) : 0;
     }
-  const int64_t sum = group_sum(count, lds);
+  int64_t sum;
+  const int64_t before = group_scan(count, lds, &sum) - count;
+  if (threadIdx.x % kSubThreads == 0)  // where this thread's sub-block starts
+    st.subex[(int64_t)blockIdx.x * kSubsPerGroup + threadIdx.x / kSubThreads] = before;
   const int64_t nbad = group_sum(ok ? 0 : 1, lds);
   if (threadIdx.x == 0) {
     st.part[blockIdx.x] = nbad ? -1 : sum;
@@ -912,6 +925,77 @@ __global__ __launch_bounds__(256) void sha256_fused_lane(
                         __builtin_bswap32(st[6]), __builtin_bswap32(st[7]));
 #pragma unroll
     for (int j = 0; j < 8; ++j) prev[j] = st[j];
+  }
+}
+
+// The fused form with the key offsets derived in the same kernel: workgroup
+// b holds the scan's sub-block b (one sequence per lane), so it turns its
+// counts of full blocks into key offsets from the prefixes the scan's first
+// kernel left for the group and the sub-block, writes them for the caller
+// and hashes.  The first token block is requested before the scan, so the
+// scan runs while it arrives.  On a failed scan (invalid offsets, too many
+// keys) it writes key_off_out[0] = -1 and nothing else.
+__global__ __launch_bounds__(kSubSeqs) void sha256_fused_scan(
+    const int32_t *__restrict__ tokens, const int64_t *__restrict__ seq_off, int32_t n_seqs,
+    int32_t block_tokens, int32_t shift, int64_t keys_cap, uint32_t len_bits, ScanState st,
+    int64_t *__restrict__ key_off_out, const uint8_t *__restrict__ parents,
+    uint8_t *__restrict__ keys) {
+  __shared__ int64_t lds[kScanWaves];
+  const int64_t total = *st.total;
+  if (*st.bad != 0 || total > keys_cap) {  // the same for every work-item
+    if (blockIdx.x == 0 && threadIdx.x == 0) key_off_out[0] = -1;
+    return;
+  }
+  const int32_t s = blockIdx.x * kSubSeqs + threadIdx.x;
+  const bool live = s < n_seqs;
+  const int64_t a = live ? seq_off[s] : 0;
+  const int64_t cnt = live ? full_blocks(seq_off[s + 1] - a, block_tokens, shift) : 0;
+  const int32_t *tok = tokens + a;
+  uint32_t nx[16];
+  if (cnt > 0)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) nx[j] = (uint32_t)tok[j];
+  int64_t sub_total;
+  const int64_t k0 = st.prefix[blockIdx.x / kSubsPerGroup] + st.subex[blockIdx.x] +
+                     group_scan(cnt, lds, &sub_total) - cnt;
+  if (!live) return;
+  key_off_out[s] = k0;
+  if (s == n_seqs - 1) key_off_out[n_seqs] = total;
+  if (cnt == 0) return;
+  uint32_t prev[8];
+  parent_words(parents, s, prev);
+  const int32_t blocks = block_tokens / 16;
+  const int64_t nblk = cnt * blocks;  // token blocks of the sequence
+  int64_t q = 0;  // token blocks consumed
+  for (int64_t k = k0; k < k0 + cnt; ++k) {
+    uint32_t st8[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) st8[j] = kInit[j];
+    for (int32_t c = 0; c < blocks; ++c, ++q) {
+      uint32_t w[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)  // LE32 token bytes read as a big-endian word
+        w[j] = __builtin_bswap32(nx[j]);
+      if (q + 1 < nblk)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) nx[j] = (uint32_t)tok[16 * (q + 1) + j];
+      compress(st8, w);
+    }
+    uint32_t w[16];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = prev[j];
+    w[8] = 0x80000000u;
+#pragma unroll
+    for (int j = 9; j < 15; ++j) w[j] = 0u;
+    w[15] = len_bits;
+    compress(st8, w);
+    uint4 *out = reinterpret_cast<uint4 *>(keys + 32 * k);
+    out[0] = make_uint4(__builtin_bswap32(st8[0]), __builtin_bswap32(st8[1]),
+                        __builtin_bswap32(st8[2]), __builtin_bswap32(st8[3]));
+    out[1] = make_uint4(__builtin_bswap32(st8[4]), __builtin_bswap32(st8[5]),
+                        __builtin_bswap32(st8[6]), __builtin_bswap32(st8[7]));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) prev[j] = st8[j];
   }
 }
 
@@ -1078,16 +1162,26 @@ int64_t hash_scan_groups(int32_t n_seqs) {
   return std::max<int64_t>(1, ((int64_t)n_seqs + kScanSeqs - 1) / kScanSeqs);
 }
 
+// The scan state's fields inside d_state (see ScanState).
+ScanState scan_state(void *d_state, int64_t groups) {
+  uint8_t *base = static_cast<uint8_t *>(d_state);
+  int64_t *words = reinterpret_cast<int64_t *>(base + 64);
+  return ScanState{reinterpret_cast<uint64_t *>(base), reinterpret_cast<int64_t *>(base + 8),
+                   reinterpret_cast<int64_t *>(base + 16), words, words + groups,
+                   words + 2 * groups};
+}
+
+int block_shift(int32_t block_tokens) {
+  return (block_tokens & (block_tokens - 1)) == 0 ? __builtin_ctz(block_tokens) : -1;
+}
+
 hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
                                    int64_t n_tokens, int32_t block_tokens, int64_t keys_cap,
                                    int64_t *d_key_offsets_out, bool wide, void *d_koff,
                                    void *d_toff, void *d_state, hipStream_t stream) {
-  const int shift = (block_tokens & (block_tokens - 1)) == 0 ? __builtin_ctz(block_tokens) : -1;
+  const int shift = block_shift(block_tokens);
   const int64_t groups = hash_scan_groups(n_seqs);
-  uint8_t *base = static_cast<uint8_t *>(d_state);
-  ScanState st{reinterpret_cast<uint64_t *>(base), reinterpret_cast<int64_t *>(base + 8),
-               reinterpret_cast<int64_t *>(base + 16), reinterpret_cast<int64_t *>(base + 64),
-               reinterpret_cast<int64_t *>(base + 64) + groups};
+  const ScanState st = scan_state(d_state, groups);
   (void)hipGetLastError();  // report this launch's status only
   hipLaunchKernelGGL(hash_offsets_partials, dim3((unsigned)groups), dim3(kScanThreads), 0, stream,
                      d_seq_offsets, n_seqs, n_tokens, block_tokens, shift, st);
@@ -1101,6 +1195,25 @@ hipError_t launch_hash_key_offsets(const int64_t *d_seq_offsets, int32_t n_seqs,
                        stream, d_seq_offsets, n_seqs, block_tokens, shift, keys_cap, st,
                        d_key_offsets_out, static_cast<int32_t *>(d_koff),
                        static_cast<int32_t *>(d_toff));
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_fused_offsets(const int32_t *d_tokens, const int64_t *d_seq_offsets,
+                                     int32_t n_seqs, int64_t n_tokens, int32_t block_tokens,
+                                     int64_t keys_cap, int64_t *d_key_offsets_out,
+                                     const uint8_t *d_parents, uint8_t *d_keys, void *d_state,
+                                     hipStream_t stream) {
+  const int shift = block_shift(block_tokens);
+  const int64_t groups = hash_scan_groups(n_seqs);
+  const ScanState st = scan_state(d_state, groups);
+  const uint32_t len_bits = (uint32_t)(8u * (4u * (uint32_t)block_tokens + 32u));
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(hash_offsets_partials, dim3((unsigned)groups), dim3(kScanThreads), 0, stream,
+                     d_seq_offsets, n_seqs, n_tokens, block_tokens, shift, st);
+  const int64_t subs = ((int64_t)n_seqs + kSubSeqs - 1) / kSubSeqs;
+  hipLaunchKernelGGL(sha256_fused_scan, dim3((unsigned)subs), dim3(kSubSeqs), 0, stream,
+                     d_tokens, d_seq_offsets, n_seqs, block_tokens, shift, keys_cap, len_bits, st,
+                     d_key_offsets_out, d_parents, d_keys);
   return hipGetLastError();
 }
 
