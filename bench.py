@@ -1012,10 +1012,14 @@ def summarize_profiles(d):
         c, a = stats.get(k, (0, float("nan")))
         lines.append(f"| {k} | {len(ds)} | {avg:.4f} | {ev[k]:.4f} | "
                      f"{alg[k] / (avg * 1e-3) / GB:.1f} | {c}, {a:.4f} |")
+    # the hash kernels of the turn's own calls (one chain per call); the
+    # line's hash block calls the same kernels afterwards
+    n_turn = plan.get("hash_calls_of_turn")
     for k in ("sha256_midstates", "sha256_chain_split", "sha256_chain", "sha256_chain_lane"):
         if k in stats:
             c, a = stats[k]
-            lines.append(f"| {k} | {c} | {a:.4f} | - | - | {c}, {a:.4f} |")
+            ds = disp.get(k, [])[:n_turn] if n_turn else disp.get(k, [])
+            lines.append(f"| {k} | {len(ds)} | {float(np.mean(ds)):.4f} | - | - | {c}, {a:.4f} |")
     open(TRACE_SUMMARY, "w").write("\n".join(lines) + "\n")
 
     counters = {}
@@ -1598,64 +1602,78 @@ def run_hash(args):
     1,024 waves); every run checked against the host entry point's keys.
     The roofline is taken on the last."""
     import torch
-    from paper_2609_33762_amd import api, workloads as W
     torch.cuda.set_device(0)
-    cur = torch.cuda.current_stream()
     out = {}
     for name, lengths, b in (("turn_56k_prompt", [56000], 16),
                              ("turn_56k_prompt_1024_token_chunks", [56000], 1024),
                              ("one_64k", [65536], 16), ("pool_64x64k", [65536] * 64, 16),
                              ("batch_16384x1k", [1024] * 16384, 16),
                              ("batch_65536x256", [256] * 65536, 16)):
-        toks, offs = W.sequences(W.SEED_TOKENS, lengths)
-        d_tok = torch.as_tensor(toks, device="cuda")
-        d_offs = torch.as_tensor(offs, device="cuda")
-        d_koffs = torch.empty(len(offs), dtype=torch.int64, device="cuda")
-        nk = int(sum(n // b for n in lengths))
-        d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
-        host, _ = api.hash_blocks(toks, offs, b)
-        # tokens and offsets resident in HBM (the key offsets from the scan
-        # kernel), and for comparison host offsets uploaded by each call
-        calls = {"device_offsets": lambda: api.hash_blocks_device_offsets(  # noqa: E731
-                     d_tok, d_offs, b, d_keys, d_koffs, stream=cur),
-                 "host_offsets": lambda: api.hash_blocks_device(  # noqa: E731
-                     d_tok, offs, b, d_keys, stream=cur)}
-        res, counts = {}, {}
-        for kind, call in calls.items():
-            # untimed calls for 0.3 s first: a GPU left idle or lightly loaded
-            # runs at lower clocks and takes a while to rise (successive single
-            # chains measured 2.8 down to 2.1 us per key)
-            t_warm = time.perf_counter() + 0.3
-            n_warm = 0
-            while time.perf_counter() < t_warm:
-                call()
-                torch.cuda.synchronize()
-                n_warm += 1
-            d_keys.zero_()
-            ms = event_ms(torch, call, cur, 20, warm=2)
-            assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32)), (name, kind)
-            res[kind] = ms
-            # calls in launch order (untimed, timed): a kernel trace of the
-            # run is cut into calls with these counts
-            counts[kind] = [n_warm + 2, 20]
-        ms = res["device_offsets"]
-        out[name] = {"ms": round(ms, 4), "ms_host_offsets": round(res["host_offsets"], 4),
-                     "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
-                     "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1), "calls": counts}
+        out[name] = hash_case(torch, lengths, b)
         log(f"hash {name}: {out[name]}")
     b = out["batch_65536x256"]
-    achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
-    roof = {"bound": "alu", "kernel": "hash_offsets_partials + sha256_fused_scan "
-                                      "(65,536 x 256 tokens, offsets in HBM)",
-            "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
-            "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
-            "traffic": None}
+    roof = hash_roofline(b)
     extra = {"hash": out, "roofline": roof}
     if not args.no_cpu_baseline:
+        from paper_2609_33762_amd import workloads as W
         extra["cpu_baseline"] = _hash_cpu_baseline(W)
         log(f"cpu baseline: {extra['cpu_baseline']}")
     return _line("hash: chained SHA-256 keys of 16-token blocks, tokens in HBM",
                  round(b["tokens_per_s"] / 1e9, 3), "G tokens/s", b["ms"], 20, extra)
+
+
+def hash_roofline(b):
+    """The hash roofline on the 65,536 x 256-token case b (device offsets)."""
+    achieved = b["keys"] * HASH_INSTR_PER_KEY / (b["ms"] * 1e-3)
+    return {"bound": "alu", "kernel": "hash_offsets_partials + sha256_fused_scan "
+                                      "(65,536 x 256 tokens, offsets in HBM)",
+            "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
+            "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
+            "traffic": None}
+
+
+def hash_case(torch, lengths, b):
+    """One hash case: sequences of the given lengths, keys of b-token blocks,
+    tokens already in HBM, checked against the host entry point's keys, then
+    timed with device offsets and with host offsets (20 calls each between
+    one pair of HIP events after 0.3 s of untimed calls)."""
+    from paper_2609_33762_amd import api, workloads as W
+    cur = torch.cuda.current_stream()
+    toks, offs = W.sequences(W.SEED_TOKENS, lengths)
+    d_tok = torch.as_tensor(toks, device="cuda")
+    d_offs = torch.as_tensor(offs, device="cuda")
+    d_koffs = torch.empty(len(offs), dtype=torch.int64, device="cuda")
+    nk = int(sum(n // b for n in lengths))
+    d_keys = torch.empty(nk * 32, dtype=torch.uint8, device="cuda")
+    host, _ = api.hash_blocks(toks, offs, b)
+    # tokens and offsets resident in HBM (the key offsets from the scan
+    # kernel), and for comparison host offsets uploaded by each call
+    calls = {"device_offsets": lambda: api.hash_blocks_device_offsets(  # noqa: E731
+                 d_tok, d_offs, b, d_keys, d_koffs, stream=cur),
+             "host_offsets": lambda: api.hash_blocks_device(  # noqa: E731
+                 d_tok, offs, b, d_keys, stream=cur)}
+    res, counts = {}, {}
+    for kind, call in calls.items():
+        # untimed calls for 0.3 s first: a GPU left idle or lightly loaded
+        # runs at lower clocks and takes a while to rise (successive single
+        # chains measured 2.8 down to 2.1 us per key)
+        t_warm = time.perf_counter() + 0.3
+        n_warm = 0
+        while time.perf_counter() < t_warm:
+            call()
+            torch.cuda.synchronize()
+            n_warm += 1
+        d_keys.zero_()
+        ms = event_ms(torch, call, cur, 20, warm=2)
+        assert np.array_equal(host, d_keys.cpu().numpy().reshape(-1, 32)), (lengths[:2], kind)
+        res[kind] = ms
+        # calls in launch order (untimed, timed): a kernel trace of the
+        # run is cut into calls with these counts
+        counts[kind] = [n_warm + 2, 20]
+    ms = res["device_offsets"]
+    return {"ms": round(ms, 4), "ms_host_offsets": round(res["host_offsets"], 4),
+            "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
+            "tokens_per_s": round(sum(lengths) / (ms * 1e-3), 1), "calls": counts}
 
 
 def _hash_cpu_baseline(W):
@@ -1742,6 +1760,17 @@ def main():
         return
 
     steps = run_steps(ctx, args)
+    # the hash on its own, after the steps (before the isolated series, whose
+    # last device copy calibrates the byte counters): the turn's prompt as one chain
+    # (the step's serial part) and the batch case that the hash line's
+    # roofline is taken on
+    log("hash cases ...")
+    hash_block = {"turn_56k_prompt": hash_case(ctx["torch"], [56000], 16),
+                  "batch_65536x256": hash_case(ctx["torch"], [256] * 65536, 16)}
+    hash_block["roofline"] = hash_roofline(hash_block["batch_65536x256"])
+    for c in ("turn_56k_prompt", "batch_65536x256"):
+        hash_block[c].pop("calls")
+    log(f"hash: {hash_block}")
     iso = isolated(ctx)
     tier = ctx["tier"]
     plan_name = {N.EA_PLAN_DIRECT: "direct", N.EA_PLAN_STAGED: "staged"}
@@ -1813,6 +1842,7 @@ def main():
                       "duplex_step_gbs": round(steps["gbs"], 2),
                       "frac_duplex_of_bidir": round(steps["gbs"] / peak["bidir"], 4)},
         "restore_fit": fit,
+        "hash": hash_block,
         "cpu_baseline": cpu,
     }
     # launch order of each copy kernel in this run, for the profile summary:
@@ -1825,6 +1855,9 @@ def main():
         "load": {"before": args.warmup, "timed": args.steps,
                  "after": 1 + 3 + 1 + N_ISO["load"] + RESTORE_FIT_LOADS},
     }
+    # hash calls of the turn itself (the set-up's prefix, warmup and timed
+    # steps); the hash block's calls follow them
+    dispatches["hash_calls_of_turn"] = 1 + args.warmup + args.steps
     json.dump({"line": out, "steps": steps, "isolated": iso, "peak": peak,
                "dispatches": dispatches, "argv": sys.argv[1:]}, open(args.detail, "w"),
               indent=1, default=float)
