@@ -259,10 +259,14 @@ def test_device_offsets_batch_workload_size():
     assert np.array_equal(out.cpu().numpy(), okeys)
 
 
-def test_device_offsets_errors_are_reported_on_the_device():
+@pytest.mark.parametrize("form", [None, "fused"])
+def test_device_offsets_errors_are_reported_on_the_device(form, monkeypatch):
     # malformed device offsets or too small an output: key_offsets[0] = -1
-    # and no key is written; a later good call on the same stream works
+    # and no key is written; a later good call on the same stream works;
+    # also with the fused form, which derives the offsets in its own kernel
     torch = need_gpu()
+    if form:
+        monkeypatch.setenv("EA_HASH_CHAIN", form)
     cases = [
         ([0, 32, 16, 48], 64, None),     # a decrease
         ([-16, 0, 32], 64, None),        # a negative start

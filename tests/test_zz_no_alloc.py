@@ -36,9 +36,14 @@ def call(name, torch, toks, offs, b, parents, cap):
     return out.cpu().numpy(), d_koffs.cpu().numpy()
 
 
+@pytest.mark.parametrize("form", [None, "fused"])
 @pytest.mark.parametrize("b", [16, 1024])
-def test_no_alloc_matches_the_allocating_entry_point(b):
+def test_no_alloc_matches_the_allocating_entry_point(b, form, monkeypatch):
+    # also with the fused form forced: its key offsets come from its own
+    # kernel and the scan state in the fixed memory
     torch = need_gpu()
+    if form:
+        monkeypatch.setenv("EA_HASH_CHAIN", form)
     r = W.rng(900 + b)
     cases = [list(r.integers(0, 40 * b, size=3000)), list(r.integers(0, 9 * b, size=37))]
     for k, lengths in enumerate(cases):          # the second call is smaller
