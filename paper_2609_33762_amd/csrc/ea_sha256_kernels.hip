@@ -1101,15 +1101,18 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   }
   if (form == kChainSplit && n_seqs > kMaxSplitGroups) form = kChainPair;  // grid bound
   if (form < 0) {
-    // Up to one sequence per compute unit: the split form (a workgroup per
-    // sequence, 20% less time per key for a lone chain).  Up to 32
-    // sequences per SIMD (four per compute unit): two lanes per sequence.
-    // Beyond: one lane per sequence.
+    // Up to four sequences per compute unit (one per SIMD): the split form,
+    // a workgroup per sequence, 20-30% less time per key than two lanes per
+    // sequence, and no slower at four per compute unit for chains of 16 to
+    // 1,024 keys.  From six per compute unit the two-lane form wins (its
+    // waves hold 32 chains each), and beyond 128 per compute unit one lane
+    // per sequence does.
     int cus = 0;
     const hipError_t e = device_cus(&cus);
     if (e != hipSuccess) return e;
-    form = n_seqs <= cus ? kChainSplit
-                         : ((int64_t)n_seqs > 128 * (int64_t)cus ? kChainLane : kChainPair);
+    form = (int64_t)n_seqs <= 4 * (int64_t)cus
+               ? kChainSplit
+               : ((int64_t)n_seqs > 128 * (int64_t)cus ? kChainLane : kChainPair);
   }
   (void)hipGetLastError();  // report this launch's status only
   if (wide)

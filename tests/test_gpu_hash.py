@@ -113,7 +113,7 @@ def test_device_calls_back_to_back():
 def test_every_chain_form(form, monkeypatch):
     # the chained compression runs two lanes per sequence, one lane per
     # sequence (large batches), a workgroup of two waves per sequence (up to
-    # one sequence per compute unit), or, for the largest batches, one lane
+    # four sequences per compute unit), or, for the largest batches, one lane
     # per sequence for token blocks and chain alike (fused); each form forced
     # on ragged chains, parents, chunk-sized blocks, a long chain and the
     # extreme token values
@@ -162,12 +162,24 @@ def test_64_bit_offsets(form, monkeypatch):
 
 
 def test_few_long_chains_take_the_split_form():
-    # up to one sequence per compute unit the library picks the two-wave form
-    # by itself: ragged long chains with parents, a chain of one key, empty
-    # sequences
+    # up to four sequences per compute unit the library picks the two-wave
+    # form by itself: ragged long chains with parents, a chain of one key,
+    # empty sequences
     r = W.rng(101)
     lengths = [int(x) for x in r.integers(0, 20000, size=40)] + [16, 0, 15]
     check(lengths, 16, parents=True, seed=101)
+
+
+@pytest.mark.parametrize("extra", [0, 1])
+def test_split_form_threshold(extra):
+    # four sequences per compute unit (the last batch of the two-wave form)
+    # and one more (the first of the two-lane form), ragged chains of up to
+    # 40 keys with parents
+    torch = need_gpu()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    r = W.rng(102 + extra)
+    lengths = [int(x) for x in r.integers(0, 640, size=4 * cus + extra)]
+    check(lengths, 16, parents=True, seed=102 + extra)
 
 
 @pytest.mark.parametrize("form", ["lane", "split"])
