@@ -79,12 +79,17 @@ def copy_streams(torch):
 def event_ms(torch, fn, stream, reps, warm=1):
     """Average duration of one fn() call: `reps` back-to-back calls between
     one pair of HIP events on `stream`, after `warm` untimed calls (events
-    between the calls would add their own cost to every launch)."""
+    between the calls would add their own cost to every launch).  One more
+    untimed call goes onto the stream right before the start event, so the
+    GPU is still busy with it while the host enqueues the first timed call:
+    the interval holds the calls' GPU time and the spacing between their
+    launches, not the host's latency to the first launch."""
     for _ in range(warm):
         fn()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    fn()
     e0.record(stream)
     for _ in range(reps):
         fn()
@@ -1384,8 +1389,9 @@ def run_plans(args):
     2 MiB; each first to consecutive slots, then to random ones.  Direct:
     one kernel between the cache and the mapped pinned slots.  Staged: a
     paged gather or scatter through an HBM staging buffer plus
-    hipMemcpyAsync of each run of consecutive slots.  Each operation is one
-    untimed call and then the timed ones between HIP events.  Caches are
+    hipMemcpyAsync of each run of consecutive slots.  Each operation is two
+    untimed calls (the second right before the start event) and then the
+    timed ones between HIP events.  Caches are
     left unfilled (contents do not change the timing), so the only copy
     kernels in the process are the plan's own: a rocprofv3 run of this
     command attributes its kernels and byte counters to the plan."""
@@ -1421,7 +1427,7 @@ def run_plans(args):
             res[slots_name] = {"store_ms": round(st, 4),
                                "store_gbs": round(n_s * page / st / 1e6, 2),
                                "load_ms": round(ld, 4), "load_gbs": round(n_l * page / ld / 1e6, 2)}
-            link += (1 + reps) * (n_s + n_l) * page
+            link += (2 + reps) * (n_s + n_l) * page
         out[name] = {"slot_bytes": page, "store_slots": n_s, "load_slots": n_l, **res}
         log(f"plan {plan_name}, {name}: {res}")
         torch.cuda.synchronize()
@@ -1455,7 +1461,7 @@ def summarize_plans(d):
              "    python3 bench.py --summarize-plans bench_out", "",
              f"kernel_source_sha256: {kernel_source_hash()}", "",
              "Each process runs one plan over every size class: stores and loads alone, to "
-             "consecutive slots and then to random ones, one untimed call and then the timed "
+             "consecutive slots and then to random ones, two untimed calls and then the timed "
              "ones.  Every copy kernel in a process belongs to its plan, apart from the few "
              "bytes the library's one-time XCD probe copies back.  Byte counters are "
              f"scaled as in the piece-copy summary (FETCH_SIZE x{cal_f:.3f}, WRITE_SIZE "
@@ -1669,7 +1675,7 @@ def hash_case(torch, lengths, b):
         res[kind] = ms
         # calls in launch order (untimed, timed): a kernel trace of the
         # run is cut into calls with these counts
-        counts[kind] = [n_warm + 2, 20]
+        counts[kind] = [n_warm + 3, 20]
     ms = res["device_offsets"]
     return {"ms": round(ms, 4), "ms_host_offsets": round(res["host_offsets"], 4),
             "keys": nk, "us_per_key": round(ms * 1e3 / nk, 4),
@@ -1847,13 +1853,14 @@ def main():
     }
     # launch order of each copy kernel in this run, for the profile summary:
     # the setup's prefix store, the warmup and timed steps, then the
-    # isolated series (one untimed call before each)
+    # isolated series (two untimed calls before each: a warm call and the
+    # lead call right before the start event)
     # (then the restore fit's one store and its loads)
     dispatches = {
         "store": {"before": 1 + args.warmup, "timed": args.steps,
-                  "after": 1 + 3 + 1 + N_ISO["store"] + 1},
+                  "after": 2 + 3 + 2 + N_ISO["store"] + 1},
         "load": {"before": args.warmup, "timed": args.steps,
-                 "after": 1 + 3 + 1 + N_ISO["load"] + RESTORE_FIT_LOADS},
+                 "after": 2 + 3 + 2 + N_ISO["load"] + RESTORE_FIT_LOADS},
     }
     # hash calls of the turn itself (the set-up's prefix, warmup and timed
     # steps); the hash block's calls follow them

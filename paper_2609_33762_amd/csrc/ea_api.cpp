@@ -204,7 +204,8 @@ bool all_distinct(const T *v, int64_t n) {
 // each call's indices into a device twin first.  Region r is rewritten only
 // after the event recorded behind its last consumer has fired, so
 // back-to-back calls never wait on each other unless kRegions calls are
-// still in flight.
+// still in flight.  The events only tell the host that the kernels have
+// finished reading, so they skip the system-scope release.
 class IndexRing {
  public:
   static constexpr int kRegions = 4;
@@ -261,7 +262,7 @@ class IndexRing {
       EA_HIP(hipHostMalloc((void **)&h_[r], (size_t)cap * 12,
                            hipHostMallocMapped | hipHostMallocCoherent));
       EA_HIP(hipHostGetDevicePointer((void **)&d_[r], h_[r], 0));
-      if (!ev_[r]) EA_HIP(hipEventCreateWithFlags(&ev_[r], hipEventDisableTiming));
+      if (!ev_[r]) EA_HIP(hipEventCreateWithFlags(&ev_[r], ea::kDeviceEventFlags));
     }
     cap_ = cap;
     return EA_OK;

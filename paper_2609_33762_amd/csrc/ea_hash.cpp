@@ -45,8 +45,15 @@ struct DevSlot {
 struct HashWs {
   int device = -1;
   hipStream_t stream = nullptr;
-  std::mutex mu;              // one call at a time on this workspace
-  hipEvent_t done = nullptr;  // end of the last call's use of the buffers
+  std::mutex mu;  // one call at a time on this workspace
+  // End of a call's use of the buffers.  `done` ends a call whose results
+  // the host reads (its record carries the system-scope release that makes
+  // them visible there); `done_dev` ends a call whose results stay on the
+  // device, and skips that release (it only orders later work and buffer
+  // reuse).  `last` is whichever event the last call recorded.
+  hipEvent_t done = nullptr;
+  hipEvent_t done_dev = nullptr;
+  hipEvent_t last = nullptr;
   bool used = false;
   // ea_hash_blocks: pinned host staging
   uint8_t *h_tok = nullptr;  int64_t cap_tok = 0;   // bytes
@@ -82,6 +89,7 @@ int workspace(hipStream_t stream, HashWs **out) {
   w->device = dev;
   w->stream = stream;
   HS_HIP(hipEventCreateWithFlags(&w->done, hipEventDisableTiming));
+  HS_HIP(hipEventCreateWithFlags(&w->done_dev, ea::kDeviceEventFlags));
   *out = w.get();
   g_ws.push_back(std::move(w));
   return EA_OK;
@@ -91,12 +99,16 @@ int workspace(hipStream_t stream, HashWs **out) {
 // ordered already; this covers a stream handle that a destroyed stream's
 // successor reuses.
 int after_last_use(HashWs &w, hipStream_t stream) {
-  if (w.used) HS_HIP(hipStreamWaitEvent(stream, w.done, 0));
+  if (w.used) HS_HIP(hipStreamWaitEvent(stream, w.last, 0));
   return EA_OK;
 }
 
-int release(HashWs &w, hipStream_t stream) {
-  HS_HIP(hipEventRecord(w.done, stream));
+// Mark the end of this call's use of the buffers on `stream`; host_reads:
+// the host reads what the call wrote once the event has fired.
+int release(HashWs &w, hipStream_t stream, bool host_reads) {
+  hipEvent_t e = host_reads ? w.done : w.done_dev;
+  HS_HIP(hipEventRecord(e, stream));
+  w.last = e;
   w.used = true;
   return EA_OK;
 }
@@ -105,7 +117,7 @@ int release(HashWs &w, hipStream_t stream) {
 // old buffers may still be read by the stream's earlier work: wait for it.
 int grow_pair(HashWs &w, uint8_t **h, uint8_t **d, int64_t *cap, int64_t need) {
   if (need <= *cap) return EA_OK;
-  if (w.used) HS_HIP(hipEventSynchronize(w.done));
+  if (w.used) HS_HIP(hipEventSynchronize(w.last));
   if (*h) (void)hipHostFree(*h);
   if (d && *d) (void)hipFree(*d);
   *h = nullptr;
@@ -120,7 +132,7 @@ int grow_pair(HashWs &w, uint8_t **h, uint8_t **d, int64_t *cap, int64_t need) {
 
 int grow_device(HashWs &w, uint8_t **d, int64_t *cap, int64_t need) {
   if (need <= *cap) return EA_OK;
-  if (w.used) HS_HIP(hipEventSynchronize(w.done));
+  if (w.used) HS_HIP(hipEventSynchronize(w.last));
   if (*d) (void)hipFree(*d);
   *d = nullptr;
   *cap = 0;
@@ -132,7 +144,7 @@ int grow_device(HashWs &w, uint8_t **d, int64_t *cap, int64_t need) {
 
 int ensure_mid(HashWs &w, uint32_t **mid, int64_t *cap, int64_t keys) {
   if (keys <= *cap) return EA_OK;
-  if (w.used) HS_HIP(hipEventSynchronize(w.done));
+  if (w.used) HS_HIP(hipEventSynchronize(w.last));
   if (*mid) (void)hipFree(*mid);
   *mid = nullptr;
   *cap = 0;
@@ -252,7 +264,7 @@ extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
   std::lock_guard<std::mutex> lk(w.mu);
   // the previous call on this stream has returned its keys already, but a
   // reused stream handle may not be ordered after it
-  if (w.used) HS_HIP(hipEventSynchronize(w.done));
+  if (w.used) HS_HIP(hipEventSynchronize(w.last));
   // pack the full-block tokens of every sequence contiguously
   const int64_t tok_bytes = total * block_tokens * 4;
   const bool wide = total * block_tokens > INT32_MAX || force_wide();
@@ -280,7 +292,7 @@ extern "C" int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
                         n_seqs, total, block_tokens, w.d_mid, d_par, w.d_keys, stream)) != EA_OK)
     return rc;
   HS_HIP(hipMemcpyAsync(w.h_keys, w.d_keys, (size_t)total * 32, hipMemcpyDeviceToHost, stream));
-  if ((rc = release(w, stream)) != EA_OK) return rc;
+  if ((rc = release(w, stream, true)) != EA_OK) return rc;
   HS_HIP(hipEventSynchronize(w.done));  // this workspace's lock only
   std::memcpy(keys_out, w.h_keys, (size_t)total * 32);
   return EA_OK;
@@ -308,7 +320,7 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, int64_t n_tokens,
   w.next ^= 1;
   // the call two back on this stream still reads this slot's host offsets
   if (d.used) HS_HIP(hipEventSynchronize(d.done));
-  if (!d.done) HS_HIP(hipEventCreateWithFlags(&d.done, hipEventDisableTiming));
+  if (!d.done) HS_HIP(hipEventCreateWithFlags(&d.done, ea::kDeviceEventFlags));
   if ((rc = after_last_use(w, stream)) != EA_OK) return rc;
   // token offsets are the caller's sequence starts, all at most seq_offsets[n]
   const bool wide = seq_offsets[n_seqs] > INT32_MAX || total > INT32_MAX || force_wide();
@@ -339,9 +351,12 @@ extern "C" int ea_hash_blocks_device(const int32_t *d_tokens, int64_t n_tokens,
   if ((rc = run_kernels(d_tokens, d_koff, d_toff, wide, n_seqs, total, block_tokens, d.d_mid,
                         d_parents, d_keys_out, stream)) != EA_OK)
     return rc;
+  // one event ends both the slot's use and the workspace's
   HS_HIP(hipEventRecord(d.done, stream));
   d.used = true;
-  return release(w, stream);
+  w.last = d.done;
+  w.used = true;
+  return EA_OK;
 }
 
 namespace {
@@ -395,7 +410,7 @@ extern "C" int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_
     HS_HIP(ea::launch_hash_fused_offsets(d_tokens, d_seq_offsets, n_seqs, n_tokens, block_tokens,
                                          bound, d_key_offsets_out, d_parents, d_keys_out,
                                          w.d_scan, stream));
-    return release(w, stream);
+    return release(w, stream, false);
   }
   uint8_t *d_koff = w.d_off;
   uint8_t *d_toff = d_koff + (n_seqs + 1) * (wide ? 8 : 4);
@@ -405,7 +420,7 @@ extern "C" int ea_hash_blocks_device_offsets(const int32_t *d_tokens, int64_t n_
       (rc = run_kernels(d_tokens, d_koff, d_toff, wide, n_seqs, bound, block_tokens, w.d_mid,
                         d_parents, d_keys_out, stream)) != EA_OK)
     return rc;
-  return release(w, stream);
+  return release(w, stream, false);
 }
 
 extern "C" int ea_hash_blocks_device_offsets_noalloc(

@@ -14,6 +14,12 @@ enum CopyDir : int { kToSlots = 0, kToPages = 1 };
 // device index array (the small-batch latency path).
 constexpr int kInlineMax = 32;
 
+// Flags of events that only order later device work, or tell the host that
+// the GPU has finished reading a host buffer: nothing the host reads
+// depends on them, so they skip the system-scope release on completion
+// (1.4 us added per record between 86 us kernels, against 3.2 us with it).
+constexpr unsigned kDeviceEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+
 // A slot holds a chunk of `chunk` (C) pages laid out [L][C][piece], then the
 // [L][C][8]-byte scale trailer.  Entry i is one page: it goes to chunk
 // position i % C of its slot.
