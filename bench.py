@@ -854,6 +854,7 @@ def _tiny_cpu_baseline(sh, W, src, dst, slots, toks, offs):
 def _short(name):
     for key, short in (("copy_host_link<0", "store"), ("copy_host_link<1", "load"),
                        ("copy_hbm<0", "gather"), ("copy_hbm<1", "scatter"),
+                       ("copy_hbm_args<0", "gather"), ("copy_hbm_args<1", "scatter"),
                        ("sha256_chain_lane", "sha256_chain_lane"),
                        ("sha256_chain_split", "sha256_chain_split"),
                        ("sha256_chain", "sha256_chain"), ("sha256_midstates", "sha256_midstates"),

@@ -67,6 +67,10 @@
  *                              unit order of the HBM gather / scatter: each
  *                              page's layers in turn (entry, the default) or
  *                              one layer of every page at a time
+ *  EA_HBM_INDEX=ring           page ids of an HBM gather / scatter (and of
+ *                              the staged plan's) through the mapped index
+ *                              ring even for 33-2,048 pages, which by default
+ *                              travel in the kernel arguments
  *  EA_STAGING_MB               HBM staging of the staged plan per direction (512)
  *  EA_HOST_COHERENT=0          non-coherent pinned memory for new tiers
  *  EA_HOST_ALLOC_WAIT_MS       how long a tier's failed pinned allocation is

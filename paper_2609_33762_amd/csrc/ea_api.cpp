@@ -103,6 +103,13 @@ int32_t hbm_layer_major(int dir) {
   return v && std::strcmp(v, "layer") == 0 ? 1 : 0;
 }
 
+// Page ids of HBM copies with identity slots in the kernel arguments
+// (default), or through the index ring (EA_HBM_INDEX=ring).
+bool hbm_arg_pages() {
+  const char *v = std::getenv("EA_HBM_INDEX");
+  return !(v && std::strcmp(v, "ring") == 0);
+}
+
 int64_t grid_hbm(int dir) {
   const int both = env_int("EA_GRID_HBM", 0);
   if (dir == ea::kToSlots) return std::max(1, env_int("EA_GRID_GATHER", both ? both : 512));
@@ -472,7 +479,9 @@ ea::PieceCopy base_copy(const ea_cache *c, int64_t slot_bytes, int32_t chunk) {
 
 // Launch a piece copy for n (slot, page) entries, one per page (slots null:
 // entry i goes to slot i / a.chunk): small batches carry their indices in
-// the kernel arguments, larger ones go through the index ring.
+// the kernel arguments, and so do the page ids of HBM copies of up to
+// kArgPagesMax pages with identity slots; larger ones go through the index
+// ring.
 int launch_entries(ea::PieceCopy a, IndexRing &ring, const int64_t *slots,
                    const int32_t *pages, int64_t n, int dir, int route, int64_t grid,
                    hipStream_t s) {
@@ -483,13 +492,23 @@ int launch_entries(ea::PieceCopy a, IndexRing &ring, const int64_t *slots,
       inl.pages[i] = pages[i];
       inl.slots[i] = slots ? slots[i] : i / a.chunk;
     }
-    EA_HIP(ea::launch_piece_copy(a, &inl, dir, route, grid, s));
+    EA_HIP(ea::launch_piece_copy(a, &inl, nullptr, dir, route, grid, s));
+    return EA_OK;
+  }
+  if (route == ea::kRouteHbm && !slots && n <= ea::kArgPagesMax && hbm_arg_pages()) {
+    ea::ArgPages ids;
+    std::memcpy(ids.pages, pages, (size_t)n * 4);
+    std::memset(ids.pages + n, 0, (size_t)(ea::kArgPagesMax - n) * 4);
+    a.identity_slots = 1;
+    a.pages = nullptr;
+    a.slot_idx = nullptr;
+    EA_HIP(ea::launch_piece_copy(a, nullptr, &ids, dir, route, grid, s));
     return EA_OK;
   }
   int region;
   EA_TRY(ring.upload(slots, pages, n, &a.slot_idx, &a.pages, &region));
   a.identity_slots = slots ? 0 : 1;
-  EA_HIP(ea::launch_piece_copy(a, nullptr, dir, route, grid, s));
+  EA_HIP(ea::launch_piece_copy(a, nullptr, nullptr, dir, route, grid, s));
   return ring.release(region, s);
 }
 
@@ -1066,8 +1085,8 @@ int ea_load_blocks_layered(ea_tier *t, ea_cache *c, const int64_t *host_slots,
     hipError_t e = hipSuccess;
     for (int32_t l = 0; l < c->d.num_layers && e == hipSuccess; ++l) {
       a.layer_begin = l;
-      e = ea::launch_piece_copy(a, pin, ea::kToPages, ea::kRouteHostLink, t->grid_layered,
-                                copy_stream);
+      e = ea::launch_piece_copy(a, pin, nullptr, ea::kToPages, ea::kRouteHostLink,
+                                t->grid_layered, copy_stream);
       if (e == hipSuccess) e = hipEventRecord(layer_done[l], copy_stream);
     }
     EA_HIP(e);

@@ -133,7 +133,7 @@ __device__ __forceinline__ void mark_load(const PieceCopy &a, int lane, int32_t 
 template <int DIR, bool INLINE, int VEC>
 __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__restrict__ pages,
                                            const int64_t *__restrict__ slot_idx,
-                                           const InlineIdx &inl) {
+                                           const InlineIdx *inl) {
   const int64_t units = a.n * a.layer_count;
   const int lane = threadIdx.x & (kWave - 1);
   const int xcd = this_xcd(a);
@@ -152,14 +152,15 @@ __device__ __forceinline__ void piece_copy(const PieceCopy &a, const int32_t *__
     for (int64_t u = first; u < units; u += waves) {
       const int64_t i = unit_entry(a, u);
       const uint32_t busy = link_busy(a);
-      copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, inl.pages[i], inl.slots[i], lane);
+      copy_unit<DIR, INLINE, VEC>(a, unit_layer(a, u, i), i, inl->pages[i], inl->slots[i], lane);
       yield_link(a, busy, debt);
     }
   } else {
     // The index arrays live in pinned host memory that the kernel reads
-    // over the link.  Lane k fetches the page and slot of the wave's k-th
-    // next unit in one vector load per 64 units, and the loop broadcasts
-    // them with readlane, so a unit's copy never waits on an index fetch.
+    // over the link, or in the kernel arguments.  Lane k fetches the page
+    // and slot of the wave's k-th next unit in one vector load per 64
+    // units, and the loop broadcasts them with readlane, so a unit's copy
+    // never waits on an index fetch.
     for (int64_t k0 = 0;; k0 += kWave) {
       const int64_t u0 = first + k0 * waves;
       if (u0 >= units) break;
@@ -195,13 +196,21 @@ __global__ __launch_bounds__(kThreads) void copy_host_link(PieceCopy a,
                                                            const int32_t *__restrict__ pages,
                                                            const int64_t *__restrict__ slot_idx,
                                                            InlineIdx inl) {
-  piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, inl);
+  piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, &inl);
 }
 template <int DIR, bool INLINE, int VEC>
 __global__ __launch_bounds__(kThreads) void copy_hbm(PieceCopy a, const int32_t *__restrict__ pages,
                                                      const int64_t *__restrict__ slot_idx,
                                                      InlineIdx inl) {
-  piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, inl);
+  piece_copy<DIR, INLINE, VEC>(a, pages, slot_idx, &inl);
+}
+// The HBM gather/scatter with the page ids of up to kArgPagesMax entries in
+// the kernel arguments (slot of entry i is i): the same loop reads them as
+// it reads an index array, and the call needs no index buffer whose reuse
+// the host would have to track.
+template <int DIR, int VEC>
+__global__ __launch_bounds__(kThreads) void copy_hbm_args(PieceCopy a, ArgPages ids) {
+  piece_copy<DIR, false, VEC>(a, ids.pages, nullptr, nullptr);
 }
 
 // Consumer stand-in of the layered load: wave w of the grid folds the
@@ -247,8 +256,11 @@ __global__ __launch_bounds__(64) void xcd_probe(int32_t *__restrict__ out) {
 }
 
 template <int DIR, bool INLINE, int VEC>
-void launch_route(const PieceCopy &a, const InlineIdx &inl, int route, dim3 g, hipStream_t stream) {
-  if (route == kRouteHostLink)
+void launch_route(const PieceCopy &a, const InlineIdx &inl, const ArgPages *ids, int route, dim3 g,
+                  hipStream_t stream) {
+  if (ids != nullptr)
+    hipLaunchKernelGGL((copy_hbm_args<DIR, VEC>), g, dim3(kThreads), 0, stream, a, *ids);
+  else if (route == kRouteHostLink)
     hipLaunchKernelGGL((copy_host_link<DIR, INLINE, VEC>), g, dim3(kThreads), 0, stream, a,
                        a.pages, a.slot_idx, inl);
   else
@@ -257,15 +269,15 @@ void launch_route(const PieceCopy &a, const InlineIdx &inl, int route, dim3 g, h
 }
 
 template <int DIR, bool INLINE>
-void launch_dir(const PieceCopy &a, const InlineIdx &inl, int route, int64_t grid,
-                hipStream_t stream) {
+void launch_dir(const PieceCopy &a, const InlineIdx &inl, const ArgPages *ids, int route,
+                int64_t grid, hipStream_t stream) {
   const dim3 g((unsigned)grid);
   const int64_t nvec = a.piece_bytes >> 4;
   // four vectors per lane per round measured best for 8-64 KiB pieces; a
   // piece smaller than one round uses fewer
-  if (nvec >= 4 * kWave) launch_route<DIR, INLINE, 4>(a, inl, route, g, stream);
-  else if (nvec >= 2 * kWave) launch_route<DIR, INLINE, 2>(a, inl, route, g, stream);
-  else launch_route<DIR, INLINE, 1>(a, inl, route, g, stream);
+  if (nvec >= 4 * kWave) launch_route<DIR, INLINE, 4>(a, inl, ids, route, g, stream);
+  else if (nvec >= 2 * kWave) launch_route<DIR, INLINE, 2>(a, inl, ids, route, g, stream);
+  else launch_route<DIR, INLINE, 1>(a, inl, ids, route, g, stream);
 }
 
 }  // namespace
@@ -321,8 +333,8 @@ hipError_t launch_layer_checksum(const uint8_t *cache, const uint8_t *scales, in
   return hipGetLastError();
 }
 
-hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
-                             int64_t workgroups, hipStream_t stream) {
+hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, const ArgPages *ids,
+                             int dir, int route, int64_t workgroups, hipStream_t stream) {
   const int64_t units = a.n * a.layer_count;
   if (units <= 0) return hipSuccess;
   if (a.num_xcd < 1 || a.num_xcd > 32 || a.xcd_mask == 0 ||
@@ -330,6 +342,10 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
     return hipErrorInvalidValue;
   // entry indices and chunk positions are computed in 32 bits
   if (a.chunk < 1 || a.n > INT32_MAX) return hipErrorInvalidValue;
+  // page ids in the arguments: HBM route, identity slots, all ids there
+  if (ids != nullptr && (inl != nullptr || route != kRouteHbm || !a.identity_slots ||
+                         a.n > kArgPagesMax))
+    return hipErrorInvalidValue;
   const int64_t waves_per_group = kThreads / kWave;
   const int64_t needed = (units + waves_per_group - 1) / waves_per_group;
   const int64_t work = needed < workgroups ? needed : workgroups;
@@ -341,11 +357,11 @@ hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, 
   // left recorded on this thread (hipGetLastError returns and clears it)
   (void)hipGetLastError();
   if (inl != nullptr) {
-    if (dir == kToSlots) launch_dir<kToSlots, true>(a, *inl, route, grid, stream);
-    else launch_dir<kToPages, true>(a, *inl, route, grid, stream);
+    if (dir == kToSlots) launch_dir<kToSlots, true>(a, *inl, nullptr, route, grid, stream);
+    else launch_dir<kToPages, true>(a, *inl, nullptr, route, grid, stream);
   } else {
-    if (dir == kToSlots) launch_dir<kToSlots, false>(a, kEmpty, route, grid, stream);
-    else launch_dir<kToPages, false>(a, kEmpty, route, grid, stream);
+    if (dir == kToSlots) launch_dir<kToSlots, false>(a, kEmpty, ids, route, grid, stream);
+    else launch_dir<kToPages, false>(a, kEmpty, ids, route, grid, stream);
   }
   return hipGetLastError();
 }

@@ -60,6 +60,15 @@ struct PieceCopy {
   int32_t hw_xcd;
 };
 
+// HBM gather/scatter calls of up to kArgPagesMax pages carry their page ids
+// in the kernel arguments (8 KiB) instead of a mapped index buffer: with
+// nothing to release after the kernel, back-to-back calls launch with no
+// event between them.
+constexpr int kArgPagesMax = 2048;
+struct ArgPages {
+  int32_t pages[kArgPagesMax];
+};
+
 struct InlineIdx {
   int32_t pages[kInlineMax];
   int64_t slots[kInlineMax];
@@ -93,8 +102,12 @@ hipError_t probe_xcd_round_robin(int num_xcd, bool *ok);
 
 // Launch one piece-copy kernel with at most `workgroups` (> 0) working
 // workgroups, placed on the XCDs of a.xcd_mask.
-hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, int dir, int route,
-                             int64_t workgroups, hipStream_t stream);
+// The entries' indices come from inl (at most kInlineMax, in the arguments),
+// ids (page ids of at most kArgPagesMax entries of an HBM copy with
+// identity slots, in the arguments) or, with both null, a.pages and
+// a.slot_idx.
+hipError_t launch_piece_copy(const PieceCopy &a, const InlineIdx *inl, const ArgPages *ids,
+                             int dir, int route, int64_t workgroups, hipStream_t stream);
 
 // Add delta to a tier's load counter on `stream` (a one-lane kernel).
 

@@ -194,8 +194,13 @@ def test_layered_load_events_mark_finished_layers(n):
     p.close()
 
 
+@pytest.mark.parametrize("index", [None, "ring"])
 @pytest.mark.parametrize("n", [7, 150])
-def test_gather_scatter_through_device_buffer(n):
+def test_gather_scatter_through_device_buffer(n, index, monkeypatch):
+    # page ids in the kernel arguments (the default for 33-2,048 pages) or
+    # through the mapped index ring
+    if index:
+        monkeypatch.setenv("EA_HBM_INDEX", index)
     torch = need_gpu()
     p = Pair(256, 4, 16, 2, 64, 2, 8, scales=True, seed=41)
     slot = p.sizes["slot"]
@@ -205,6 +210,30 @@ def test_gather_scatter_through_device_buffer(n):
     buf = torch.full((n * slot,), 0x5A, dtype=torch.uint8, device="cuda")
     p.cache.gather(src, buf)
     # oracle: the gather buffer is a tier whose slot i holds entry i
+    want = np.full((n, slot), 0x5A, np.uint8)
+    oracle.store_blocks(p.oshape, p.o_cache, p.o_sc, want, src, np.arange(n))
+    torch.cuda.synchronize()
+    assert np.array_equal(buf.cpu().numpy().reshape(n, slot), want)
+    p.cache.scatter(buf, dst)
+    oracle.load_blocks(p.oshape, want, p.o_cache, p.o_sc, np.arange(n), dst)
+    p.assert_equal("scatter")
+    p.close()
+
+
+@pytest.mark.parametrize("n", [2048, 2049])
+def test_gather_scatter_at_the_argument_limit(n):
+    # up to 2,048 page ids travel in the kernel arguments, one more goes
+    # through the index ring: both sides of the limit, every gathered slot
+    # and every page of the cache against the oracle
+    torch = need_gpu()
+    P = 4200
+    p = Pair(P, 2, 16, 2, 64, 2, 8, scales=True, seed=47)
+    slot = p.sizes["slot"]
+    r = W.rng(47)
+    src = W.distinct(r, P, n)
+    dst = W.distinct(r, P, n, exclude=src)
+    buf = torch.full((n * slot,), 0x5A, dtype=torch.uint8, device="cuda")
+    p.cache.gather(src, buf)
     want = np.full((n, slot), 0x5A, np.uint8)
     oracle.store_blocks(p.oshape, p.o_cache, p.o_sc, want, src, np.arange(n))
     torch.cuda.synchronize()
@@ -265,13 +294,17 @@ def test_any_xcd_masks_copy_every_piece(masks, placement, monkeypatch):
     p.close()
 
 
+@pytest.mark.parametrize("hbm_index", [None, "ring"])
 @pytest.mark.parametrize("placement", ["hardware", "index"])
-def test_one_workgroup_runs_many_index_batches(placement, monkeypatch):
+def test_one_workgroup_runs_many_index_batches(placement, hbm_index, monkeypatch):
     # Kernels fetch page and slot indices 64 units per wave at a time.  With
     # one working workgroup (four waves) on one XCD, 600 pages of 4 layers
     # give each wave about 600 units: ten index batches, the last one
-    # partial.  Store, load, layered load, gather and scatter, full images
-    # against the oracle.
+    # partial.  Store, load, layered load, gather and scatter (page ids in
+    # the kernel arguments or through the index ring), full images against
+    # the oracle.
+    if hbm_index:
+        monkeypatch.setenv("EA_HBM_INDEX", hbm_index)
     torch = need_gpu()
     for k, v in {"EA_LINK_WG": "1", "EA_LINK_WG_LAYERED": "1", "EA_XCD_STORE": "0x1",
                  "EA_XCD_LOAD": "0x1", "EA_GRID_GATHER": "1", "EA_GRID_SCATTER": "1",

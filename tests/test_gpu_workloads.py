@@ -106,12 +106,16 @@ def test_qwen3_turn_full_size(plan):
     release(torch)
 
 
-def test_hbm_gather_and_scatter_full_size():
+@pytest.mark.parametrize("index", [None, "ring"])
+def test_hbm_gather_and_scatter_full_size(index, monkeypatch):
     # The measured HBM launches: one gather of 2,000 random pages of the
     # 20,000-page Qwen3 cache into a slot-layout device buffer, one scatter of
-    # that buffer into 2,000 other pages (the default grids).  Every gathered
-    # slot is the oracle's store of its page, every scattered page the
-    # oracle's load of that slot, and no other page changes.
+    # that buffer into 2,000 other pages (the default grids), with the page
+    # ids in the kernel arguments (the default) or through the index ring.
+    # Every gathered slot is the oracle's store of its page, every scattered
+    # page the oracle's load of that slot, and no other page changes.
+    if index:
+        monkeypatch.setenv("EA_HBM_INDEX", index)
     torch = need_gpu()
     sh = W.QWEN3
     L, P, piece = sh.num_layers, sh.num_pages, sh.piece_bytes
