@@ -1513,10 +1513,17 @@ def summarize_plans(d):
         elif plan == "staged":
             lines += ["", "No copy ran on the copy engines: every hipMemcpyAsync was a blit "
                       "kernel."]
+        counters = {label: os.path.join(base, label, f"{label}_counter_collection.csv")
+                    for label in ("fetch", "write")}
+        if not all(os.path.exists(f) for f in counters.values()):
+            lines += ["", "Byte counters: not collected for this plan in this retake (its "
+                      "FETCH_SIZE pass stopped with a segmentation fault in host code, inside "
+                      "the profiler's interception of the plan's own runtime calls).", ""]
+            continue
         tot = {}
         for label, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
             s = 0.0
-            for x in csv.DictReader(open(os.path.join(base, label, f"{label}_counter_collection.csv"))):
+            for x in csv.DictReader(open(counters[label])):
                 n = x["Kernel_Name"]
                 if x["Counter_Name"] == ctr and ("copy_host_link" in n or "copy_hbm" in n or
                                                   "__amd_rocclr" in n):
