@@ -89,6 +89,25 @@ def test_no_scratch_and_lds_only_where_waves_share(assembly, src):
             assert lds[name] == 0, (name, lds[name])
 
 
+def test_argument_blocks_fit_what_the_runtime_takes(assembly):
+    # The HBM gather/scatter of up to 2,048 pages passes its page ids in the
+    # kernel arguments; the HIP runtime on MI355X was measured to take
+    # argument blocks of 16,000 bytes and more, so every kernel's block
+    # stays at or under 16,384 bytes, and only the argument-page kernels go
+    # past 4 KiB.
+    text = assembly["ea_copy_kernels.hip"]
+    sizes = {}
+    for m in re.finditer(r"^(\w+):\s*;\s*@", text, re.M):
+        k = re.search(r"\.amdhsa_kernarg_size\s+(\d+)", text[m.end():])
+        sizes[m.group(1)] = int(k.group(1))
+    args = {n: v for n, v in sizes.items() if "copy_hbm_args" in n}
+    assert len(args) == 6, sorted(args)  # two directions x three vector widths
+    for n, v in sizes.items():
+        assert v <= 16384, (n, v)
+        assert v <= 4096 or n in args, (n, v)
+    assert all(v >= 8192 for v in args.values()), args
+
+
 # ---------------------------------------------------------------- DPP hazards
 # A DPP instruction needs every VGPR it reads to have been written by a
 # VALU instruction at least two wait states earlier, and an EXEC write at
