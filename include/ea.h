@@ -206,9 +206,9 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  * `stream` completes.
  *
  * Both entry points run the chained compression in one of three forms (the
- * keys are the same): a workgroup of two waves per sequence while there are
- * at most four sequences per compute unit, two lanes per sequence up to 32
- * sequences per SIMD, one lane per sequence beyond; EA_HASH_CHAIN=split,
+ * keys are the same): a workgroup of two waves per four sequences while
+ * there are at most eight sequences per compute unit, two lanes per sequence
+ * up to 32 sequences per SIMD, one lane per sequence beyond; EA_HASH_CHAIN=split,
  * pair or lane forces a form.
  * Sequence and key offsets travel to the kernels as 32-bit values when all
  * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter.

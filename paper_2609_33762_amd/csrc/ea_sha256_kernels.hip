@@ -15,8 +15,9 @@
 //   sha256_chain_lane: the same with one lane per sequence, for batches of
 //                     sequences large enough to give every SIMD more than
 //                     one wave of the two-lane form;
-//   sha256_chain_split: the same for up to one sequence per compute unit,
-//                     with the message schedule moved to a second wave.
+//   sha256_chain_split: the same for few long chains, a workgroup of two
+//                     waves per four sequences (one per 16-lane row), with
+//                     the message schedule moved to the second wave.
 // A lone chain runs at the issue rate of one wave, so the instructions per
 // compression set its speed: rotations are v_alignbit_b32, every
 // three-input XOR and Ch/Maj one v_bitop3_b32 (gfx950's three-input logic
@@ -512,30 +513,64 @@ __device__ __forceinline__ uint32_t split_schedule16(uint32_t wp) {
   return w;
 }
 
+// LDS of the two-wave chain form, in 32-bit words.  Row r of both waves
+// (16 lanes) carries the chain of sequence 4 * block + r: its K_t + W_t
+// (t = 16..63) at kSpKw + 48 r, its last key and the 8 padding words of the
+// chained block at kSpKey + 16 r; the 48 ones (the a-lanes' K + W) are
+// shared; then a 4-word store slot for each lane that holds nothing
+// (lanes 4..11 of each row).
+constexpr int kSpRows = 4;
+constexpr int kSpKw = 0;
+constexpr int kSpOnes = kSpKw + 48 * kSpRows;
+constexpr int kSpKey = kSpOnes + 48;
+constexpr int kSpJunk = kSpKey + 16 * kSpRows;
+constexpr int kSpWords = kSpJunk + 4 * 8 * kSpRows;
+
 template <typename Off>
 __global__ __launch_bounds__(128) void sha256_chain_split(
     const uint32_t *__restrict__ mid, const Off *__restrict__ key_off, int32_t n_seqs,
     uint32_t len_bits, const uint8_t *__restrict__ parents, uint8_t *__restrict__ keys) {
-  // words 0..47: K_t + W_t (t = 16..63); 48..95: ones (the a-lanes' K +
-  // W); 96..103 the last key, 104..111 the padding words; 112..367: the
-  // stores of lanes that hold nothing
-  __shared__ __align__(16) uint32_t lds[112 + 4 * 64];
-  const int32_t s = blockIdx.x;
-  if (s >= n_seqs) return;  // the whole workgroup
+  __shared__ __align__(16) uint32_t lds[kSpWords];
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int j = lane & 15;
+  const int row = lane >> 4;
   const bool e_lane = j >= 12;
   const bool a_lane = j < 4;
-  const int64_t k0 = key_off[s], k1 = key_off[s + 1];
-  uint32_t prev[8];
-  parent_words(parents, s, prev);
+  // this row's sequence; rows past the last sequence carry an empty chain
+  const int32_t s = (int32_t)blockIdx.x * kSpRows + row;
+  int64_t k0 = 0, k1 = 0;
+  if (s < n_seqs) {
+    k0 = key_off[s];
+    k1 = key_off[s + 1];
+  }
+  // Key counts in the offsets' width: with 32-bit offsets the loop and its
+  // bounds stay 32-bit (scalar compares, one-instruction clamps).
+  const Off len = (Off)(k1 - k0);
+  // Every row of both waves runs the longest row's number of keys, so the
+  // two waves meet at the same barriers; a row past its own end computes
+  // keys that are never stored.
+  Off kmax = 0;
+#pragma unroll
+  for (int r = 0; r < kSpRows; ++r) {
+    Off l;
+    if constexpr (sizeof(Off) == 4) {
+      l = (Off)__builtin_amdgcn_readlane((int)len, 16 * r);
+    } else {
+      const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)len, 16 * r);
+      const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)len >> 32), 16 * r);
+      l = (Off)(((uint64_t)hi << 32) | lo);
+    }
+    kmax = l > kmax ? l : kmax;
+  }
   if (wave == 1) {
-    if (lane < 48) lds[48 + lane] = 1u;
-    if (lane < 8) lds[104 + lane] = lane == 0 ? 0x80000000u : (lane == 7 ? len_bits : 0u);
+    if (lane < 48) lds[kSpOnes + lane] = 1u;
+    if (j >= 8) lds[kSpKey + 16 * row + j] = j == 8 ? 0x80000000u : (j == 15 ? len_bits : 0u);
   }
   __syncthreads();
   if (wave == 0) {
+    uint32_t prev[8];
+    parent_words(s < n_seqs ? parents : nullptr, s, prev);
     SplitLane c;
     c.c1 = e_lane ? 6 : 2;
     c.c2 = e_lane ? 11 : 13;
@@ -553,22 +588,28 @@ __global__ __launch_bounds__(128) void sha256_chain_split(
     uint32_t o[4];  // the previous key, this lane's half (a: H0..3, e: H4..7)
 #pragma unroll
     for (int i = 0; i < 4; ++i) o[i] = e_lane ? prev[4 + i] : prev[i];
-    const uint4 *mh = reinterpret_cast<const uint4 *>(mid);
     const int half = j >= 8 ? 1 : 0;
+    // midstate of this row's key k0 + kk, held at the row's last key past
+    // its end (key 0 for an empty row: some key exists whenever this runs)
+    const uint4 *mbase = reinterpret_cast<const uint4 *>(mid) + 2 * (len > 0 ? k0 : 0) + half;
+    const Off last = len > 0 ? len - 1 : 0;
+    auto mid_at = [&](Off kk) { return mbase[2 * (int64_t)(kk < last ? kk : last)]; };
     uint4 nx = make_uint4(0, 0, 0, 0);
-    if (k0 < k1) nx = mh[2 * k0 + half];
+    if (kmax > 0) nx = mid_at(0);
     // The word offsets of the K + W reads and of the key store differ per
     // lane; hiding them keeps the compiler from reading both arrays and
     // selecting.
-    uint32_t kbase = e_lane ? 0u : 48u;
+    uint32_t kbase = e_lane ? (uint32_t)(kSpKw + 48 * row) : (uint32_t)kSpOnes;
     asm volatile("" : "+v"(kbase));
     const uint4 *kw4 = reinterpret_cast<const uint4 *>(lds + kbase);
-    uint32_t kst = a_lane ? 96u : (e_lane ? 100u : 112u + 4u * lane);
+    uint32_t kst = a_lane ? (uint32_t)(kSpKey + 16 * row)
+                          : (e_lane ? (uint32_t)(kSpKey + 16 * row + 4)
+                                    : (uint32_t)(kSpJunk + 4 * (8 * row + j - 4)));
     asm volatile("" : "+v"(kst));
     uint4 *key_dst = reinterpret_cast<uint4 *>(lds + kst);
-    for (int64_t k = k0; k < k1; ++k) {
+    for (Off kk = 0; kk < kmax; ++kk) {
       const uint4 h0 = nx;
-      if (k + 1 < k1) nx = mh[2 * (k + 1) + half];
+      if (kk + 1 < kmax) nx = mid_at(kk + 1);
       SplitState q{h0.x, h0.y, h0.z, h0.w, 0u};
       uint32_t kw[8];  // K + W of rounds 0..7: the previous key
 #pragma unroll
@@ -609,29 +650,32 @@ __global__ __launch_bounds__(128) void sha256_chain_split(
     // read per lane rather than from prev[j], which a per-lane index would
     // move out of registers
     uint32_t wp = j == 8 ? 0x80000000u : (j == 15 ? len_bits : 0u);
-    if (j < 8 && parents != nullptr) {
+    if (j < 8 && parents != nullptr && s < n_seqs) {
       const uint8_t *pw = parents + 32 * (int64_t)s + 4 * j;
       wp = ((uint32_t)pw[0] << 24) | ((uint32_t)pw[1] << 16) | ((uint32_t)pw[2] << 8) | pw[3];
     }
     const uint32_t kp0 = kRound[16 + j], kp1 = kRound[32 + j], kp2 = kRound[48 + j];
-    for (int64_t k = k0; k < k1; ++k) {
-      const uint32_t key_prev = wp;  // lanes 0..7: key k - 1
+    uint32_t *kw_row = lds + kSpKw + 48 * row;
+    for (Off kk = 0; kk < kmax; ++kk) {
+      const uint32_t key_prev = wp;  // lanes 0..7: key kk - 1 of this row
       uint32_t w = split_schedule16(wp);
-      lds[j] = w + kp0;
+      kw_row[j] = w + kp0;
       __syncthreads();
-      if (k > k0 && lane < 8)
-        reinterpret_cast<uint32_t *>(keys + 32 * (k - 1))[lane] = __builtin_bswap32(key_prev);
+      if (kk > 0 && kk <= len && j < 8)
+        reinterpret_cast<uint32_t *>(keys + 32 * (k0 + (int64_t)kk - 1))[j] = __builtin_bswap32(key_prev);
       w = split_schedule16(w);
-      lds[16 + j] = w + kp1;
+      kw_row[16 + j] = w + kp1;
       __syncthreads();
       w = split_schedule16(w);
-      lds[32 + j] = w + kp2;
+      kw_row[32 + j] = w + kp2;
       __syncthreads();
       __syncthreads();
-      wp = lds[96 + j];
+      wp = lds[kSpKey + 16 * row + j];
     }
-    if (k0 < k1 && lane < 8)
-      reinterpret_cast<uint32_t *>(keys + 32 * (k1 - 1))[lane] = __builtin_bswap32(wp);
+    // a row as long as the longest stores its last key here; shorter rows
+    // stored theirs in the loop
+    if (len > 0 && len == kmax && j < 8)
+      reinterpret_cast<uint32_t *>(keys + 32 * (k1 - 1))[j] = __builtin_bswap32(wp);
   }
 }
 
@@ -1078,8 +1122,8 @@ void launch_chain(int form, const uint32_t *d_mid, const Off *d_koff, int32_t n_
     hipLaunchKernelGGL(sha256_chain_lane<Off>, dim3((n_seqs + 255) / 256), dim3(256), 0, stream,
                        d_mid, d_koff, n_seqs, len_bits, d_parents, d_keys);
   else if (form == kChainSplit)
-    hipLaunchKernelGGL(sha256_chain_split<Off>, dim3(n_seqs), dim3(128), 0, stream, d_mid,
-                       d_koff, n_seqs, len_bits, d_parents, d_keys);
+    hipLaunchKernelGGL(sha256_chain_split<Off>, dim3((n_seqs + kSpRows - 1) / kSpRows),
+                       dim3(128), 0, stream, d_mid, d_koff, n_seqs, len_bits, d_parents, d_keys);
   else
     hipLaunchKernelGGL(sha256_chain<Off>, dim3((n_seqs + 31) / 32), dim3(64), 0, stream, d_mid,
                        d_koff, n_seqs, len_bits, d_parents, d_keys);
@@ -1101,16 +1145,16 @@ hipError_t launch_sha256_chain(const uint32_t *d_mid, const void *d_key_offsets,
   }
   if (form == kChainSplit && n_seqs > kMaxSplitGroups) form = kChainPair;  // grid bound
   if (form < 0) {
-    // Up to four sequences per compute unit (one per SIMD): the split form,
-    // a workgroup per sequence, 20-30% less time per key than two lanes per
-    // sequence, and no slower at four per compute unit for chains of 16 to
-    // 1,024 keys.  From six per compute unit the two-lane form wins (its
-    // waves hold 32 chains each), and beyond 128 per compute unit one lane
-    // per sequence does.
+    // Up to eight sequences per compute unit (two workgroups of four rows):
+    // the split form, 4-30% less time per call than two lanes per sequence
+    // for chains of 16 to 1,024 keys (1,024 chains of 1,024 keys: 1.55
+    // against 2.15 ms).  At sixteen per compute unit the two-lane form wins
+    // for long chains (its waves hold 32 chains each), beyond for all, and
+    // beyond 128 per compute unit one lane per sequence does.
     int cus = 0;
     const hipError_t e = device_cus(&cus);
     if (e != hipSuccess) return e;
-    form = (int64_t)n_seqs <= 4 * (int64_t)cus
+    form = (int64_t)n_seqs <= 8 * (int64_t)cus
                ? kChainSplit
                : ((int64_t)n_seqs > 128 * (int64_t)cus ? kChainLane : kChainPair);
   }

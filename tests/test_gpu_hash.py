@@ -112,8 +112,8 @@ def test_device_calls_back_to_back():
 @pytest.mark.parametrize("form", ["pair", "lane", "split", "fused"])
 def test_every_chain_form(form, monkeypatch):
     # the chained compression runs two lanes per sequence, one lane per
-    # sequence (large batches), a workgroup of two waves per sequence (up to
-    # four sequences per compute unit), or, for the largest batches, one lane
+    # sequence (large batches), a workgroup of two waves per four sequences
+    # (up to eight sequences per compute unit), or, for the largest batches, one lane
     # per sequence for token blocks and chain alike (fused); each form forced
     # on ragged chains, parents, chunk-sized blocks, a long chain and the
     # extreme token values
@@ -162,7 +162,7 @@ def test_64_bit_offsets(form, monkeypatch):
 
 
 def test_few_long_chains_take_the_split_form():
-    # up to four sequences per compute unit the library picks the two-wave
+    # up to eight sequences per compute unit the library picks the two-wave
     # form by itself: ragged long chains with parents, a chain of one key,
     # empty sequences
     r = W.rng(101)
@@ -170,15 +170,30 @@ def test_few_long_chains_take_the_split_form():
     check(lengths, 16, parents=True, seed=101)
 
 
+@pytest.mark.parametrize("lengths", [
+    [16 * 40, 0, 16 * 3, 16 * 7 + 5],         # the longest chain in row 0, an empty row
+    [16, 16 * 2, 0, 16 * 50 + 3],             # the longest in row 3
+    [16 * 9, 16 * 9, 16 * 9, 16 * 9, 16 * 2],  # a second workgroup with one row
+    [0, 0, 0, 15, 16 * 12, 0, 16],            # rows without a key, two workgroups
+])
+def test_split_rows_of_unequal_length(lengths, monkeypatch):
+    # the two-wave form carries four sequences per workgroup, one per row of
+    # 16 lanes, each row running as many keys as the longest: every key of
+    # every row, with parents, equals the oracle's
+    monkeypatch.setenv("EA_HASH_CHAIN", "split")
+    check(lengths, 16, parents=True, seed=120 + len(lengths))
+    check(lengths, 16, seed=130 + len(lengths))
+
+
 @pytest.mark.parametrize("extra", [0, 1])
 def test_split_form_threshold(extra):
-    # four sequences per compute unit (the last batch of the two-wave form)
+    # eight sequences per compute unit (the last batch of the two-wave form)
     # and one more (the first of the two-lane form), ragged chains of up to
     # 40 keys with parents
     torch = need_gpu()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     r = W.rng(102 + extra)
-    lengths = [int(x) for x in r.integers(0, 640, size=4 * cus + extra)]
+    lengths = [int(x) for x in r.integers(0, 640, size=8 * cus + extra)]
     check(lengths, 16, parents=True, seed=102 + extra)
 
 
