@@ -514,7 +514,11 @@ int ea_load_blocks_layered(ea_tier *tier, ea_cache *cache,
  * scatter writes d_src + i*slot_bytes into page dst_pages[i] (destinations
  * distinct).  slot_bytes is that of a tier of the same shape with C = 1;
  * dst_bytes / src_bytes give the device buffer's size, which must hold n
- * slots (EA_EINVAL otherwise, nothing launched). */
+ * slots (EA_EINVAL otherwise, nothing launched).  block_ids / dst_pages are
+ * HOST arrays the call has copied by the time it returns (up to 2,048 ids
+ * into the kernel arguments, more into the library's mapped index ring), so
+ * the caller may reuse them at once; the copy itself is asynchronous on
+ * `stream`. */
 int ea_gather_blocks(ea_cache *cache, const int32_t *block_ids, int32_t n,
                      void *d_dst, int64_t dst_bytes, hipStream_t stream);
 int ea_scatter_blocks(ea_cache *cache, const void *d_src, int64_t src_bytes,
