@@ -1179,6 +1179,37 @@ def summarize_hbm_counters(d):
 
 
 HASH_SUMMARY = os.path.join(ROOT, "profiles", "sha256_hash_workloads_kernel_trace.md")
+HASH_BYTES_SUMMARY = os.path.join(ROOT, "profiles", "sha256_hash_batch_hbm_bytes.md")
+HASH_SOURCE = os.path.join(ROOT, "paper_2609_33762_amd", "csrc", "ea_sha256_kernels.hip")
+# the hash line's roofline case: 65,536 sequences of 256 tokens, 16-token blocks
+HASH_BATCH = (65536, 256, 16)
+
+
+def hash_source_hash():
+    return hashlib.sha256(open(HASH_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def hash_batch_bytes():
+    """Algorithmic bytes of one call of the batch case with offsets in HBM:
+    the tokens and the sequence offsets read once, the key offsets and the
+    keys written once."""
+    n, t, b = HASH_BATCH
+    return n * t * 4 + (n + 1) * 8 + (n + 1) * 8 + n * (t // b) * 32
+
+
+def hash_traffic():
+    """HBM bytes per call of the batch case from the committed counter
+    summary, or None when it is missing or was taken from other hash kernel
+    sources."""
+    if not os.path.exists(HASH_BYTES_SUMMARY):
+        return None
+    src = val = None
+    for line in open(HASH_BYTES_SUMMARY):
+        if line.startswith("hash_kernel_source_sha256:"):
+            src = line.split(":", 1)[1].strip()
+        if line.startswith("traffic_bytes_per_call:"):
+            val = int(line.split(":", 1)[1])
+    return val if src == hash_source_hash() else None
 HASH_CASE_NOTES = {
     "turn_56k_prompt": "the turn's 56,000-token prompt as one chain",
     "turn_56k_prompt_1024_token_chunks": "the same prompt in 1,024-token chunks (64 token "
@@ -1193,6 +1224,90 @@ HASH_CASE_NOTES = {
 def _hash_role(name):
     n = _plain_name(name)
     return n if ("sha256" in n or "hash_" in n) else None
+
+
+def _hash_counter_calls(path, ctr):
+    """Per-call counter values of the hash kernels in a counter-collection
+    CSV, in dispatch order: each call ends with its chain or fused kernel."""
+    rows = [x for x in csv.DictReader(open(path)) if x["Counter_Name"] == ctr]
+    rows.sort(key=lambda x: int(x["Dispatch_Id"]))
+    calls, cur = [], []
+    for x in rows:
+        role = _hash_role(x["Kernel_Name"])
+        if role is None:
+            continue
+        cur.append((role, float(x["Counter_Value"])))
+        if "chain" in role or "fused" in role:
+            calls.append(cur)
+            cur = []
+    return calls
+
+
+def _hash_series(line, calls, case_name, kind):
+    """The timed calls of one series, located with the counts the line
+    records (each case: the host entry point's check call, then each
+    series' untimed and timed calls)."""
+    want = sum(1 + sum(sum(c) for c in case["calls"].values()) for case in line["hash"].values())
+    if len(calls) != want:
+        raise SystemExit(f"{len(calls)} calls in the counters, the run made {want}")
+    i = 0
+    for name, case in line["hash"].items():
+        i += 1
+        for k, (n_untimed, n_timed) in case["calls"].items():
+            if name == case_name and k == kind:
+                return calls[i + n_untimed:i + n_untimed + n_timed]
+            i += n_untimed + n_timed
+    raise SystemExit(f"no series {case_name}/{kind} in the line")
+
+
+def summarize_hash_bytes(d):
+    """Write the HBM byte summary of the hash line's roofline case from two
+    rocprofv3 counter runs of `bench.py --workload hash` under d (FETCH_SIZE
+    in d/prof_hash_fetch, WRITE_SIZE in d/prof_hash_write, each beside the
+    line its run printed), scaled like the piece-copy counters."""
+    import re
+    m = re.search(r"FETCH_SIZE is scaled by ([0-9.]+) and WRITE_SIZE by ([0-9]+\.[0-9]+)",
+                  open(TRAFFIC_SUMMARY).read())
+    cal = {"FETCH_SIZE": float(m.group(1)), "WRITE_SIZE": float(m.group(2))}
+    per = {}
+    for label, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        base = os.path.join(d, f"prof_hash_{label}")
+        line = json.load(open(os.path.join(base, "hash.json")))
+        calls = _hash_counter_calls(os.path.join(base, f"{label}_counter_collection.csv"), ctr)
+        series = _hash_series(line, calls, "batch_65536x256", "device_offsets")
+        kernels = {}
+        for call in series:
+            for role, v in call:
+                kernels.setdefault(role, []).append(v)
+        per[ctr] = {k: float(np.median(v)) for k, v in kernels.items()}
+    roles = sorted(set(per["FETCH_SIZE"]) | set(per["WRITE_SIZE"]))
+    total = sum((per["FETCH_SIZE"].get(k, 0.0) * cal["FETCH_SIZE"] +
+                 per["WRITE_SIZE"].get(k, 0.0) * cal["WRITE_SIZE"]) * 1024 for k in roles)
+    alg = hash_batch_bytes()
+    n, t, b = HASH_BATCH
+    cmd = ("rocprofv3 --pmc {c} --output-format csv -d bench_out/prof_hash_{l} -o {l} -- "
+           "python3 -u bench.py --workload hash > bench_out/prof_hash_{l}/hash.json")
+    lines = [f"# HBM bytes per call: chained keys of {n:,} sequences of {t} tokens "
+             f"({b}-token blocks, offsets in HBM)", "",
+             "Commands (from the repository root on the MI355X):", "",
+             "    " + cmd.format(c="FETCH_SIZE", l="fetch"),
+             "    " + cmd.format(c="WRITE_SIZE", l="write"),
+             "    python3 bench.py --summarize-hash-bytes bench_out", "",
+             f"hash_kernel_source_sha256: {hash_source_hash()}", "",
+             "The 20 timed calls of the batch case with device offsets (the hash line's "
+             "roofline case), median per kernel over the calls.  Counters are scaled as in "
+             f"the piece-copy summary (FETCH_SIZE x{cal['FETCH_SIZE']:.3f}, WRITE_SIZE "
+             f"x{cal['WRITE_SIZE']:.3f}).", "",
+             "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes |", "|---|---|---|---|"]
+    for k in roles:
+        f, w = per["FETCH_SIZE"].get(k, 0.0), per["WRITE_SIZE"].get(k, 0.0)
+        lines.append(f"| {k} | {f:.0f} | {w:.0f} | "
+                     f"{(f * cal['FETCH_SIZE'] + w * cal['WRITE_SIZE']) * 1024:.0f} |")
+    lines += ["", f"Per call: {total:.0f} bytes against {alg} algorithmic (tokens and sequence "
+              f"offsets read once, key offsets and keys written once): ratio "
+              f"{total / alg:.4f}.", "", f"traffic_bytes_per_call: {total:.0f}"]
+    open(HASH_BYTES_SUMMARY, "w").write("\n".join(lines) + "\n")
+    print(open(HASH_BYTES_SUMMARY).read())
 
 
 def summarize_hash(d):
@@ -1643,7 +1758,7 @@ def hash_roofline(b):
                                       "(65,536 x 256 tokens, offsets in HBM)",
             "achieved": round(achieved / 1e12, 3), "peak": round(VALU_INT_PEAK / 1e12, 2),
             "unit": "T lane-instructions/s", "frac": round(achieved / VALU_INT_PEAK, 4),
-            "traffic": None}
+            "traffic": hash_traffic(), "traffic_algorithmic": hash_batch_bytes()}
 
 
 def hash_case(torch, lengths, b):
@@ -1727,6 +1842,7 @@ def main():
     ap.add_argument("--summarize-workloads", metavar="DIR")
     ap.add_argument("--summarize-hbm-counters", metavar="DIR")
     ap.add_argument("--summarize-hash", metavar="DIR")
+    ap.add_argument("--summarize-hash-bytes", metavar="DIR")
     ap.add_argument("--workload", default="qwen3_turn",
                     choices=["qwen3_turn", "agent_pool", "dense_scattered", "layered_fp8", "tiny",
                              "load_cost", "tp8_shard", "hash", "agent_pool_chunked", "plans"])
@@ -1747,6 +1863,9 @@ def main():
         return
     if args.summarize_hash:
         summarize_hash(args.summarize_hash)
+        return
+    if args.summarize_hash_bytes:
+        summarize_hash_bytes(args.summarize_hash_bytes)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the offload path shards per tensor-parallel rank with "
