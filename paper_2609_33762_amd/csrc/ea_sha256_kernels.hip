@@ -1043,8 +1043,9 @@ __global__ __launch_bounds__(kSubSeqs) void sha256_fused_scan(
   }
 }
 
-// The split forms launch one workgroup per sequence or key; forcing them on
-// more than this many falls back to the other forms.
+// The split forms launch one workgroup per key (midstates) or per four
+// sequences (chain); forcing them on more than this many keys or sequences
+// falls back to the other forms.
 constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
 
 // Compute units of the current device, cached per device.
