@@ -5,8 +5,10 @@ free pages, fitted to T_load(n) = n beta / B_eff + tau_load by least squares
 (App. "Offload Cost and Prefix-Survival Model", Eq. 2).
 
 * The oracle's Eq. 2 with the fitted B_eff and tau_load reproduces every
-  measured point within 15% (the smallest loads take about 20 us, where a
-  microsecond or two of launch jitter is 5-10%).
+  measured point within 15% plus 5 us.  A point's device time starts at an
+  event recorded on an idle GPU right before the call, so it includes the
+  host's enqueue of that call: the smallest loads take about 20 us, and a
+  few microseconds of host jitter there is 10-25%.
 * B_eff cannot exceed the measured pinned-copy peak of the host link.
 * The loads in the sweep move the right bytes (a load after the sweep is
   compared with the oracle)."""
@@ -20,7 +22,8 @@ from gpu_common import need_gpu, oracle_pages, oracle_slots, pages_to_host
 
 pytestmark = pytest.mark.gpu
 
-TOLERANCE = 0.15
+TOLERANCE = 0.15   # relative to the measured time
+JITTER_S = 5e-6    # plus this much: host enqueue and launch jitter
 
 
 def test_restore_fit_on_one_tp8_rank():
@@ -52,7 +55,7 @@ def test_restore_fit_on_one_tp8_rank():
           f"{beta / B * 1e6:.3f} us per token, peak {peak:.2f} GB/s, residual {resid:.3f}")
     for n, s in zip(tok, sec):
         pred = oracle.restore_time(float(n), float(beta), float(B), float(tau))
-        assert abs(pred - s) / s <= TOLERANCE, (n, s, pred)
+        assert abs(pred - s) <= TOLERANCE * s + JITTER_S, (n, s, pred)
     assert 0 < B <= peak * 1e9 * 1.01
     assert tau > 0
     # the sweep's loads move the right bytes
