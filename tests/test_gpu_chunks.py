@@ -30,8 +30,12 @@ def chunk_pair(C, slots, scales=False, seed=0):
 @pytest.mark.parametrize("plan", list(PLANS))
 @pytest.mark.parametrize("C,n,scales", [(4, 1, False), (4, 8, True), (4, 9, False),
                                          (4, 30, True), (16, 5, True), (64, 2, False)])
-def test_chunked_store_and_load(plan, C, n, scales):
-    # n*C <= 32 page entries travel in kernel arguments, more through the ring
+def test_chunked_store_and_load(plan, C, n, scales, monkeypatch, hbm_index=None):
+    # n*C <= 32 page entries travel in kernel arguments; more go through the
+    # index ring, except for the staged plan's HBM halves, whose page ids
+    # travel in an argument block (through the ring with EA_HBM_INDEX=ring)
+    if hbm_index:
+        monkeypatch.setenv("EA_HBM_INDEX", hbm_index)
     p = chunk_pair(C, max(2 * n, 8), scales=scales, seed=100 + C + n)
     assert p.tier.chunk_pages == C and p.tier.slot_bytes == p.sizes["slot"]
     p.tier.set_plan(N.EA_DIR_BOTH, PLANS[plan])
@@ -46,6 +50,12 @@ def test_chunked_store_and_load(plan, C, n, scales):
     p.o_load(slots, dst)
     p.assert_equal("load")
     p.close()
+
+
+@pytest.mark.parametrize("C,n,scales", [(4, 30, True), (16, 5, True)])
+def test_chunked_staged_halves_through_the_ring(C, n, scales, monkeypatch):
+    # the staged plan with its HBM halves' page ids through the index ring
+    test_chunked_store_and_load("staged", C, n, scales, monkeypatch, hbm_index="ring")
 
 
 def test_chunked_mask_and_repeated_sources():
