@@ -8,7 +8,8 @@
 //   sha256_midstates: one lane per key, compresses the b/16 token blocks
 //                     from the initial hash value (fully parallel);
 //   sha256_midstates_split: the same for few keys of several blocks, a
-//                     workgroup of two waves per key;
+//                     workgroup of two waves per four keys (one per
+//                     16-lane row), the schedules on the second wave;
 //   sha256_chain:     two lanes per sequence, run the final compression of
 //                     each key in order, feeding key_{i-1} in as message
 //                     words 0..7 (the serial part: one compression per key);
@@ -264,104 +265,6 @@ __global__ __launch_bounds__(64) void sha256_chain(
     x[2] = e_side ? o0 : e1;
     x[3] = e_side ? o2 : e3;
   }
-}
-
-// One round of the two-lane form with W_t + K_t given (both lanes).
-__device__ __forceinline__ void pair_round(uint32_t &s0, uint32_t &s1, uint32_t &s2,
-                                           uint32_t &s3, uint32_t wk, uint32_t r1c,
-                                           uint32_t r2c, uint32_t r3c, uint32_t m,
-                                           bool e_side) {
-  const uint32_t S = bitop3<kXor3>(__builtin_amdgcn_alignbit(s0, s0, r1c),
-                                   __builtin_amdgcn_alignbit(s0, s0, r2c),
-                                   __builtin_amdgcn_alignbit(s0, s0, r3c));
-  const uint32_t F = bitop3<kCh>(bitop3<kXorAnd>(s0, s2, m), s1, s2);
-  const uint32_t U = S + F;
-  const uint32_t T1 = U + s3 + wk;
-  const uint32_t dA = dpp_from<kPermFromA>(s3);
-  const uint32_t Q = e_side ? dA : U;
-  const uint32_t nw = dpp_from<kPermFromE>(T1) + Q;
-  s3 = s2; s2 = s1; s1 = s0; s0 = nw;
-}
-
-// W_T0 .. W_T0+15 of the rolling schedule w, each stored as W_t + K_t.
-template <int T0>
-__device__ __forceinline__ void schedule16(uint32_t w[16], uint32_t out[16]) {
-#pragma unroll
-  for (int t = T0; t < T0 + 16; ++t) {
-    const uint32_t a = w[(t - 2) & 15], b = w[(t - 15) & 15];
-    const uint32_t s1 = bitop3<kXor3>(rotr(a, 17), rotr(a, 19), a >> 10);
-    const uint32_t s0 = bitop3<kXor3>(rotr(b, 7), rotr(b, 18), b >> 3);
-    const uint32_t wt = s1 + w[(t - 7) & 15] + s0 + w[t & 15];
-    w[t & 15] = wt;
-    out[t - T0] = wt + kRound[t];
-  }
-}
-
-// Midstates of few keys with several token blocks each: one key per
-// workgroup of two waves.  The token blocks of a key are compressed one
-// after the other, but their message schedules depend on the tokens alone,
-// so wave 1 prepares block c + 1's 64 words (W_t + K_t) in one half of an
-// LDS double buffer while wave 0 runs block c's 64 rounds in the two-lane
-// form from the other half; one barrier per block.  Both waves run the
-// same loop over the key's blocks, so every barrier is reached by both.
-template <typename Off>
-__global__ __launch_bounds__(128) void sha256_midstates_split(
-    const int32_t *__restrict__ tokens, const Off *__restrict__ key_off,
-    const Off *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys, int32_t block_tokens,
-    uint32_t *__restrict__ mid) {
-  __shared__ uint4 wk4[2][16];  // W_t + K_t of two blocks
-  const int64_t g = blockIdx.x;
-  if (g >= n_keys || g >= (int64_t)key_off[n_seqs]) return;  // the whole workgroup
-  const bool rounds_wave = threadIdx.x < 64;
-  const int lane = threadIdx.x & 63;
-  const bool e_side = lane & 1;
-  const int32_t s = owner(key_off, n_seqs, g);
-  if (g < (int64_t)key_off[s] || g >= (int64_t)key_off[s + 1]) return;  // the whole workgroup
-  const int32_t *tok = tokens + (int64_t)tok_off[s] + (g - (int64_t)key_off[s]) * block_tokens;
-  const int32_t blocks = block_tokens / 16;
-  const uint32_t r1c = e_side ? 6 : 2, r2c = e_side ? 11 : 13, r3c = e_side ? 25 : 22;
-  const uint32_t m = e_side ? 0u : 0xffffffffu;
-  // schedule wave: block c's 64 words into half c & 1
-  auto prepare = [&](int32_t c) {
-    uint32_t w[16], o[64];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {  // LE32 token bytes read as a big-endian word
-      w[j] = __builtin_bswap32((uint32_t)tok[16 * c + j]);
-      o[j] = w[j] + kRound[j];
-    }
-    schedule16<16>(w, o + 16);
-    schedule16<32>(w, o + 32);
-    schedule16<48>(w, o + 48);
-    if (lane == 0)
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        wk4[c & 1][i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
-  };
-  if (!rounds_wave) prepare(0);
-  __syncthreads();
-  // rounds wave: this lane's half of the state (a..d on the a-lane, e..h on
-  // the e-lane)
-  uint32_t h0 = e_side ? kInit[4] : kInit[0], h1 = e_side ? kInit[5] : kInit[1];
-  uint32_t h2 = e_side ? kInit[6] : kInit[2], h3 = e_side ? kInit[7] : kInit[3];
-  for (int32_t c = 0; c < blocks; ++c) {
-    if (rounds_wave) {
-      uint32_t s0 = h0, s1 = h1, s2 = h2, s3 = h3;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const uint4 v = wk4[c & 1][i];
-        pair_round(s0, s1, s2, s3, v.x, r1c, r2c, r3c, m, e_side);
-        pair_round(s0, s1, s2, s3, v.y, r1c, r2c, r3c, m, e_side);
-        pair_round(s0, s1, s2, s3, v.z, r1c, r2c, r3c, m, e_side);
-        pair_round(s0, s1, s2, s3, v.w, r1c, r2c, r3c, m, e_side);
-      }
-      h0 += s0; h1 += s1; h2 += s2; h3 += s3;
-    } else if (c + 1 < blocks) {
-      prepare(c + 1);
-    }
-    __syncthreads();
-  }
-  if (rounds_wave && lane < 2)
-    reinterpret_cast<uint4 *>(mid + 8 * g)[e_side ? 1 : 0] = make_uint4(h0, h1, h2, h3);
 }
 
 // One sequence per workgroup of two waves: wave 0 runs the rounds, wave 1
@@ -676,6 +579,111 @@ __global__ __launch_bounds__(128) void sha256_chain_split(
     // stored theirs in the loop
     if (len > 0 && len == kmax && j < 8)
       reinterpret_cast<uint32_t *>(keys + 32 * (k1 - 1))[j] = __builtin_bswap32(wp);
+  }
+}
+
+// Midstates of few keys with several token blocks each: a workgroup of two
+// waves per four keys, row r (16 lanes) of both waves on key 4 * block + r.
+// The token blocks of a key are compressed one after the other, but their
+// message schedules depend on the tokens alone, so wave 1 prepares block
+// c + 1's 64 words (K_t + W_t) for every row in one half of an LDS double
+// buffer while wave 0 runs block c's 64 rounds in the split form of the
+// chain kernel above from the other half: one barrier per block, and every
+// key of a launch has the same number of blocks, so the rows stay in step.
+// Rows past the last key rerun row 0's tokens and store nothing.
+//
+// LDS in 32-bit words: two halves of kMsHalf words, row r's K_t + W_t at
+// 64 r of each, then the 64 ones the a-lanes read as their K + W.
+constexpr int kMsHalf = 64 * kSpRows;
+constexpr int kMsOnes = 2 * kMsHalf;
+constexpr int kMsWords = kMsOnes + 64;
+
+template <typename Off>
+__global__ __launch_bounds__(128) void sha256_midstates_split(
+    const int32_t *__restrict__ tokens, const Off *__restrict__ key_off,
+    const Off *__restrict__ tok_off, int32_t n_seqs, int64_t n_keys, int32_t block_tokens,
+    uint32_t *__restrict__ mid) {
+  __shared__ __align__(16) uint32_t lds[kMsWords];
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int j = lane & 15;
+  const int row = lane >> 4;
+  const bool e_lane = j >= 12;
+  const int64_t lim = n_keys < (int64_t)key_off[n_seqs] ? n_keys : (int64_t)key_off[n_seqs];
+  const int64_t g0 = (int64_t)blockIdx.x * kSpRows;
+  if (g0 >= lim) return;  // the whole workgroup
+  const int32_t s0 = owner(key_off, n_seqs, g0);
+  if (g0 < (int64_t)key_off[s0] || g0 >= (int64_t)key_off[s0 + 1]) return;  // the whole workgroup
+  const int32_t *tok =
+      tokens + (int64_t)tok_off[s0] + (g0 - (int64_t)key_off[s0]) * block_tokens;
+  const int64_t g = g0 + row;
+  bool ok = false;
+  if (row > 0 && g < lim) {
+    const int32_t s = owner(key_off, n_seqs, g);
+    if (g >= (int64_t)key_off[s] && g < (int64_t)key_off[s + 1]) {
+      ok = true;
+      tok = tokens + (int64_t)tok_off[s] + (g - (int64_t)key_off[s]) * block_tokens;
+    }
+  }
+  ok = ok || row == 0;
+  const int32_t blocks = block_tokens / 16;
+  if (wave == 1) {
+    // lane j of row r: word j of the row's current block, W_16+j, W_32+j and
+    // W_48+j in turn; the next block's token read one block ahead
+    lds[kMsOnes + lane] = 1u;
+    const uint32_t kp0 = kRound[j], kp1 = kRound[16 + j], kp2 = kRound[32 + j],
+                   kp3 = kRound[48 + j];
+    uint32_t nx = (uint32_t)tok[j];
+    for (int32_t c = 0; c < blocks; ++c) {
+      uint32_t w = __builtin_bswap32(nx);  // LE32 token bytes read as a big-endian word
+      if (c + 1 < blocks) nx = (uint32_t)tok[16 * (c + 1) + j];
+      uint32_t *kw_row = lds + (c & 1) * kMsHalf + 64 * row;
+      kw_row[j] = w + kp0;
+      w = split_schedule16(w);
+      kw_row[16 + j] = w + kp1;
+      w = split_schedule16(w);
+      kw_row[32 + j] = w + kp2;
+      w = split_schedule16(w);
+      kw_row[48 + j] = w + kp3;
+      __syncthreads();
+    }
+    __syncthreads();  // the rounds wave's last block
+  } else {
+    SplitLane c;
+    c.c1 = e_lane ? 6 : 2;
+    c.c2 = e_lane ? 11 : 13;
+    c.c3 = e_lane ? 25 : 22;
+    c.m = e_lane ? 0u : 0xffffffffu;
+    uint32_t h0 = e_lane ? kInit[4] : kInit[0], h1 = e_lane ? kInit[5] : kInit[1];
+    uint32_t h2 = e_lane ? kInit[6] : kInit[2], h3 = e_lane ? kInit[7] : kInit[3];
+    // e-lanes read their row's words in the current half, the other lanes
+    // the ones; hidden from the compiler, which would otherwise read both
+    // and select
+    uint32_t kbase = e_lane ? (uint32_t)(64 * row) : (uint32_t)kMsOnes;
+    uint32_t kstep = e_lane ? (uint32_t)kMsHalf : 0u;
+    asm volatile("" : "+v"(kbase), "+v"(kstep));
+    __syncthreads();  // block 0's words
+    for (int32_t cb = 0; cb < blocks; ++cb) {
+      const uint4 *kw4 = reinterpret_cast<const uint4 *>(lds + kbase + (cb & 1) * kstep);
+      uint32_t kw[64];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint4 v = kw4[i];
+        kw[4 * i] = v.x; kw[4 * i + 1] = v.y; kw[4 * i + 2] = v.z; kw[4 * i + 3] = v.w;
+      }
+      SplitState q{h0, h1, h2, h3, 0u};
+      q.v = (q.s3 ^ c.m) + (row_move<kRowShr12>(q.s3) + kw[0]);
+#pragma unroll
+      for (int t = 0; t < 56; t += 4)  // rounds 0..55
+        split_rounds4(q, kw[t + 1], kw[t + 2], kw[t + 3], kw[t + 4], c);
+      split_rounds3(q, kw[57], kw[58], kw[59], c);  // 56..58
+      split_rounds3(q, kw[60], kw[61], kw[62], c);  // 59..61
+      split_rounds_end(q, kw[63], c);               // 62, 63
+      h0 += q.s0; h1 += q.s1; h2 += q.s2; h3 += q.s3;
+      __syncthreads();
+    }
+    if (ok && (j == 0 || j == 12))
+      reinterpret_cast<uint4 *>(mid + 8 * g)[e_lane ? 1 : 0] = make_uint4(h0, h1, h2, h3);
   }
 }
 
@@ -1043,9 +1051,9 @@ __global__ __launch_bounds__(kSubSeqs) void sha256_fused_scan(
   }
 }
 
-// The split forms launch one workgroup per key (midstates) or per four
-// sequences (chain); forcing them on more than this many keys or sequences
-// falls back to the other forms.
+// The split forms launch one workgroup per four keys (midstates) or four
+// sequences (chain); forcing them on more than this many workgroups falls
+// back to the other forms.
 constexpr int64_t kMaxSplitGroups = int64_t(1) << 24;
 
 // Compute units of the current device, cached per device.
@@ -1073,28 +1081,30 @@ hipError_t launch_sha256_midstates(const int32_t *d_tokens, const void *d_key_of
                                    int64_t n_keys, int32_t block_tokens, uint32_t *d_mid,
                                    hipStream_t stream) {
   if (n_keys <= 0) return hipSuccess;
-  // Keys of several blocks, at most one per compute unit: a workgroup of
-  // two waves per key (the schedule on its own wave); otherwise one lane
-  // per key.  EA_HASH_MID=lane or split forces a form.
+  // Keys of several blocks, at most 16 per compute unit (8 for two-block
+  // keys, where the lane form catches up sooner): a workgroup of two waves
+  // per four keys (the schedules on their own wave); otherwise one lane per
+  // key.  EA_HASH_MID=lane or split forces a form.
+  const int64_t groups = (n_keys + kSpRows - 1) / kSpRows;
   bool split = false;
   const char *f = std::getenv("EA_HASH_MID");
   if (f && std::strcmp(f, "split") == 0) {
-    split = n_keys <= kMaxSplitGroups;
+    split = groups <= kMaxSplitGroups;
   } else if (!(f && std::strcmp(f, "lane") == 0) && block_tokens >= 32) {
     int cus = 0;
     const hipError_t e = device_cus(&cus);
     if (e != hipSuccess) return e;
-    split = n_keys <= cus;
+    split = n_keys <= (block_tokens >= 64 ? 16 : 8) * (int64_t)cus;
   }
   (void)hipGetLastError();  // report this launch's status only
   const int64_t blocks = (n_keys + 255) / 256;
   if (split && wide)
-    hipLaunchKernelGGL(sha256_midstates_split<int64_t>, dim3((unsigned)n_keys), dim3(128), 0,
+    hipLaunchKernelGGL(sha256_midstates_split<int64_t>, dim3((unsigned)groups), dim3(128), 0,
                        stream, d_tokens, static_cast<const int64_t *>(d_key_offsets),
                        static_cast<const int64_t *>(d_tok_offsets), n_seqs, n_keys,
                        block_tokens, d_mid);
   else if (split)
-    hipLaunchKernelGGL(sha256_midstates_split<int32_t>, dim3((unsigned)n_keys), dim3(128), 0,
+    hipLaunchKernelGGL(sha256_midstates_split<int32_t>, dim3((unsigned)groups), dim3(128), 0,
                        stream, d_tokens, static_cast<const int32_t *>(d_key_offsets),
                        static_cast<const int32_t *>(d_tok_offsets), n_seqs, n_keys,
                        block_tokens, d_mid);

@@ -201,13 +201,33 @@ def test_split_form_threshold(extra):
 @pytest.mark.parametrize("b", [32, 1024])
 def test_midstate_forms(form, b, monkeypatch):
     # the token blocks of a key are compressed by one lane, or for few keys
-    # of several blocks by a workgroup of two waves; each form forced on
-    # ragged sequences with parents, a single key, and many keys
+    # of several blocks by a workgroup of two waves per four keys; each form
+    # forced on ragged sequences with parents, a single key (three rows of
+    # its workgroup past the last key), and many keys
     monkeypatch.setenv("EA_HASH_MID", form)
     r = W.rng(110 + b)
     check([0, b - 1, b, b + 1, 7 * b + 3, 3 * b], b, parents=True, seed=111)
     check([b], b, seed=112)
     check(list(r.integers(0, 20 * b, size=30)), b, parents=True, seed=113)
+
+
+@pytest.mark.parametrize("b,per_cu", [(32, 8), (64, 16), (1024, 16)])
+@pytest.mark.parametrize("extra", [0, 1])
+def test_midstate_split_threshold(b, per_cu, extra):
+    # the last batch of keys the library gives the two-wave midstate form
+    # (8 keys per compute unit for two-block keys, 16 from four blocks) and
+    # one key more (the first of the one-lane form): ragged sequences with
+    # parents, so that the four rows of a workgroup span several sequences
+    torch = need_gpu()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    r = W.rng(140 + b + extra)
+    n_keys = per_cu * cus + extra
+    lengths, total = [], 0
+    while total < n_keys:  # 0..6 keys and a ragged tail per sequence
+        k = min(int(r.integers(0, 7)), n_keys - total)
+        lengths.append(k * b + int(r.integers(0, b)))
+        total += k
+    check(lengths, b, parents=True, seed=141 + extra)
 
 
 def test_longest_contexts():
