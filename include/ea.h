@@ -209,7 +209,10 @@ int ea_hash_blocks(const int32_t *tokens, const int64_t *seq_offsets,
  * keys are the same): a workgroup of two waves per four sequences while
  * there are at most eight sequences per compute unit, two lanes per sequence
  * up to 32 sequences per SIMD, one lane per sequence beyond; EA_HASH_CHAIN=split,
- * pair or lane forces a form.
+ * pair or lane forces a form.  The token blocks of keys of 32 tokens or more
+ * run in a workgroup of two waves per four keys while there are at most 16
+ * keys per compute unit (8 with 32-token keys), one lane per key beyond;
+ * EA_HASH_MID=split or lane forces a form.
  * Sequence and key offsets travel to the kernels as 32-bit values when all
  * fit, else as 64-bit values; EA_HASH_OFFSETS=64 forces the latter.
  * Buffers are kept per (device, stream): calls on different streams run
