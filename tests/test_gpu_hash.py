@@ -306,14 +306,17 @@ def test_device_offsets_batch_workload_size():
     assert np.array_equal(out.cpu().numpy(), okeys)
 
 
+@pytest.mark.parametrize("b", [16, 64])
 @pytest.mark.parametrize("form", [None, "fused"])
-def test_device_offsets_errors_are_reported_on_the_device(form, monkeypatch):
+def test_device_offsets_errors_are_reported_on_the_device(form, b, monkeypatch):
     # malformed device offsets or too small an output: key_offsets[0] = -1
     # and no key is written; a later good call on the same stream works;
-    # also with the fused form, which derives the offsets in its own kernel
+    # also with the fused form, which derives the offsets in its own kernel,
+    # and with keys of four blocks (the two-wave midstate form)
     torch = need_gpu()
     if form:
         monkeypatch.setenv("EA_HASH_CHAIN", form)
+    m = b // 16
     cases = [
         ([0, 32, 16, 48], 64, None),     # a decrease
         ([-16, 0, 32], 64, None),        # a negative start
@@ -321,17 +324,35 @@ def test_device_offsets_errors_are_reported_on_the_device(form, monkeypatch):
         ([0, 32, 64], 64, 3),            # 4 keys, room for 3
     ]
     for offs, n_tok, cap in cases:
-        d_tok = torch.zeros(n_tok, dtype=torch.int32, device="cuda")
+        offs = [m * o for o in offs]
+        d_tok = torch.zeros(m * n_tok, dtype=torch.int32, device="cuda")
         out = torch.full((cap or 8, 32), 0xEE, dtype=torch.uint8, device="cuda")
         d_koffs = torch.full((len(offs),), 5, dtype=torch.int64, device="cuda")
         api.hash_blocks_device_offsets(d_tok, torch.tensor(offs, dtype=torch.int64,
-                                                           device="cuda"), 16, out, d_koffs)
+                                                           device="cuda"), b, out, d_koffs)
         torch.cuda.synchronize()
         assert d_koffs[0].item() == -1, offs
         assert (out.cpu().numpy() == 0xEE).all(), offs
     okeys, okoffs, out, d_koffs = device_offsets_case(torch, [64, 48], 16, 74)
     torch.cuda.synchronize()
     assert np.array_equal(out.cpu().numpy(), okeys)
+
+
+@pytest.mark.parametrize("b", [64, 1024])
+def test_device_offsets_room_for_more_keys(b):
+    # device offsets with room for 37 keys more than the sequences hold: the
+    # kernels are sized for the room, and every key slot past the last key
+    # stays untouched
+    torch = need_gpu()
+    lengths = [3 * b + 5, 0, b, 7 * b - 1, 2 * b]
+    n = sum(x // b for x in lengths)
+    okeys, okoffs, out, d_koffs = device_offsets_case(torch, lengths, b, 80 + b, parents=True,
+                                                      keys_capacity=n + 37)
+    torch.cuda.synchronize()
+    assert np.array_equal(d_koffs.cpu().numpy(), okoffs)
+    got = out.cpu().numpy()
+    assert np.array_equal(got[:n], okeys)
+    assert (got[n:] == 0xEE).all()
 
 
 def test_device_offsets_no_sequences():
